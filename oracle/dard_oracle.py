@@ -1,0 +1,439 @@
+"""Plain CPU oracle for one Dependency-Aware Revocable Decoding (DARD) step.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
+execute this module: only the test suite, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the HIP
+library; both sides receive the same seeded inputs and nothing else.
+
+Everything here is written from the paper (arXiv 2608.26574) as plainly as
+possible: loops or whole-array numpy expressions in float64, with a matrix
+product (``@``) as the only library primitive.  No blocking, fusion or
+reordering beyond what the definitions state.
+
+Numeric conventions (the "storage rounding points").  The paper fixes no
+precision, so values are accumulated in float64 and rounded to the storage type
+(bfloat16, round-to-nearest-even, or float32 in the fp32 configuration) exactly
+where a real implementation stores them: the embedding output, every RMSNorm
+output, Q/K/V after RoPE (the KV cache), the attention output and the SwiGLU
+output.  The residual stream and the logits are float32.  Decisions that turn
+floats into integers (argmax, threshold tests of Eq. 8, logit mixing feeding an
+argmax) are taken on float32 values, the precision of the GPU kernels.
+
+Parity pins (see ``tests/test_oracle_*.py``):
+  * take_x / visible_keys   -- brute-force dense mask built from the per-state
+                               prose rules of Sec. 3.2, invariants of Eq. 2-4.
+  * masked_attention        -- dense textbook evaluation with -inf and torch's
+                               CPU scaled_dot_product_attention.
+  * rmsnorm, rope, swiglu   -- closed forms (unit RMS, norm preservation,
+                               relative-position property, silu identities).
+  * confidence              -- closed forms (uniform row, single spike, shift
+                               invariance), argmax tie rule.
+  * guidance_weights        -- closed forms of Eq. 5-6 (lambda^8 = 1/2, a
+                               hand-computed worked example, P4 of the tests).
+  * transition              -- exact inequalities of Eq. 8.
+  * step_logits / prefill   -- special cases P1 (all-M block), P2 (empty C) and
+                               P3 (one-layer independence from C tokens); the
+                               full multi-layer logits beyond these cases are
+                               "parity unpinned" (no published values exist).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+# Token state codes (Sec. 3.2): masked, candidate, unmasked.
+STATE_M, STATE_C, STATE_U = 0, 1, 2
+
+# Flags selecting the alternative readings of points the paper leaves open.
+F_XSELF_SHADOW = 1 << 0   # x-row of a U token does not see its own x key
+F_MKEYS_SHADOW = 1 << 1   # x-row of an M token sees M keys through s
+F_VERIFY_PCUR = 1 << 2    # C/U confidence = prob. of the current token
+
+LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # Sec. 4.1: lambda = 0.917, i.e. 0.5^(1/8)
+P0_DEFAULT = 0.1                      # Sec. 4.1: prior constant p_0
+
+
+# --------------------------------------------------------------------------
+# storage rounding
+# --------------------------------------------------------------------------
+def to_f32(x):
+    """Round to IEEE binary32 (round-to-nearest-even) and return float64."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def to_bf16(x):
+    """Round to bfloat16 (round-to-nearest-even on the binary32 bit pattern).
+
+    bfloat16 keeps the upper 16 bits of a binary32 number; ties go to the even
+    upper half.  The value is first rounded to binary32, as a kernel holding a
+    float32 accumulator does.
+    """
+    f = np.ascontiguousarray(np.asarray(x, dtype=np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    u = (u + np.uint64(0x7FFF) + lsb) & np.uint64(0xFFFF0000)
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def storage(x, dtype):
+    """Round to the activation storage type: 'bf16' or 'f32'."""
+    if dtype == "bf16":
+        return to_bf16(x)
+    if dtype == "f32":
+        return to_f32(x)
+    raise ValueError(dtype)
+
+
+# --------------------------------------------------------------------------
+# state-specific attention mask (Sec. 2 "parallelized inference", Eq. 2-3,
+# Sec. 3.2 paragraphs on U, C and M tokens)
+# --------------------------------------------------------------------------
+def take_x(state, conf, flags=0):
+    """Return X[r, j] (bool, shape [2B, B]): row r sees x^j (True) or s^j.
+
+    Rows 0..B-1 are the queries of the original block x, rows B..2B-1 those of
+    the shadow block s; row r belongs to position i = r mod B.  Eq. 2 demands
+    that each query sees exactly one of x^j and s^j, so one boolean per
+    (row, position) describes the whole block part of the mask; the prefix is
+    always visible.
+
+    Per query state (Sec. 3.2):
+      U  -- sees the U tokens in x, everything else in s; the shadow query s^i
+            never sees its own x^i (leakage block).  The x query uses the same
+            pattern; it keeps its own x^i unless F_XSELF_SHADOW.
+      C  -- sees U in x and, by Eq. 3, the C tokens j with c_i <= c_j in x
+            (itself included); the shadow query drops its own x^i (Eq. 4
+            conditions the k-th candidate on the k-1 more confident ones only).
+      M  -- the x query sees C and U in x; M keys are taken from x as well
+            (vanilla decoding of the x stream) unless F_MKEYS_SHADOW, which
+            takes them from s except its own position.  The shadow query sees
+            U in x and C in s ("C regarded as masked"); M keys from s.
+    """
+    state = np.asarray(state)
+    conf = np.asarray(conf, dtype=np.float32)
+    B = state.shape[0]
+    X = np.zeros((2 * B, B), dtype=bool)
+    for r in range(2 * B):
+        i = r % B
+        shadow = r >= B
+        si = state[i]
+        for j in range(B):
+            sj = state[j]
+            if si == STATE_U:
+                vis = sj == STATE_U
+                if j == i and (shadow or (flags & F_XSELF_SHADOW)):
+                    vis = False
+            elif si == STATE_C:
+                vis = sj == STATE_U or (sj == STATE_C and conf[i] <= conf[j])
+                if j == i and shadow:
+                    vis = False
+            elif si == STATE_M:
+                if shadow:
+                    vis = sj == STATE_U
+                elif flags & F_MKEYS_SHADOW:
+                    vis = sj in (STATE_C, STATE_U) or j == i
+                else:
+                    vis = True
+            else:
+                raise ValueError("state code out of range")
+            X[r, j] = vis
+    return X
+
+
+def visible_keys(state, conf, P, flags=0):
+    """Dense mask [2B, P + 2B]: prefix keys, then x^0..x^{B-1}, then s^0..s^{B-1}."""
+    X = take_x(state, conf, flags)
+    R, B = X.shape
+    vis = np.zeros((R, P + 2 * B), dtype=bool)
+    vis[:, :P] = True
+    vis[:, P:P + B] = X
+    vis[:, P + B:] = ~X
+    return vis
+
+
+# --------------------------------------------------------------------------
+# transformer pieces (the paper's models are LLaDA / MMaDA-like; the internals
+# used here are the common pre-norm RMSNorm / RoPE / SwiGLU block)
+# --------------------------------------------------------------------------
+def rmsnorm(h, gain, eps):
+    """y = h / sqrt(mean(h^2) + eps) * gain, over the last axis."""
+    h = np.asarray(h, dtype=np.float64)
+    ms = np.mean(h * h, axis=-1, keepdims=True)
+    return h / np.sqrt(ms + eps) * gain
+
+
+def rope(x, pos, theta):
+    """Rotate-half rotary embedding.  x: [..., rows, heads, dh], pos: [rows].
+
+    Dimension t < dh/2 is paired with t + dh/2 and both are rotated by the angle
+    pos * theta^(-2t/dh).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    dh = x.shape[-1]
+    half = dh // 2
+    t = np.arange(half, dtype=np.float64)
+    inv = theta ** (-2.0 * t / dh)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv[None, :]   # [rows, half]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    x1 = x[..., :half]
+    x2 = x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def masked_attention(q, k, v, visible, scale, n_kv_heads):
+    """Softmax attention restricted to the visible keys, in float64.
+
+    q: [R, Hq, dh]; k, v: [Nk, Hkv, dh]; visible: bool [R, Nk].
+    o[r, h] = sum_k softmax_k(q.k / sqrt(dh) over visible k) v_k.
+    Query head h reads KV head h // (Hq / Hkv).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    R, Hq, dh = q.shape
+    group = Hq // n_kv_heads
+    out = np.zeros((R, Hq, dh))
+    for h in range(Hq):
+        g = h // group
+        s = (q[:, h, :] @ k[:, g, :].T) * scale          # [R, Nk]
+        s = np.where(visible, s, -np.inf)
+        m = np.max(s, axis=1, keepdims=True)
+        p = np.exp(s - m)
+        p = p / np.sum(p, axis=1, keepdims=True)
+        out[:, h, :] = p @ v[:, g, :]
+    return out
+
+
+# --------------------------------------------------------------------------
+# forward passes
+# --------------------------------------------------------------------------
+def _layer(w, dims, h, pos, kv_prefix, visible_fn, scale):
+    """One pre-norm block over the rows of every sequence.
+
+    h: [b, R, d] residual (float32 values); pos: [R] absolute positions.
+    kv_prefix: (K, V) each [b, P, Hkv, dh] or None.  visible_fn(bi) -> bool
+    [R, P + R] mask over (prefix keys, the rows' own keys).
+    Returns the new residual and this layer's (K, V) of the rows.
+    """
+    dt = dims["dtype"]
+    Hq, Hkv, dh = dims["n_heads"], dims["n_kv_heads"], dims["head_dim"]
+    b, R, d = h.shape
+    xn = storage(rmsnorm(h, w["attn_norm"], dims["norm_eps"]), dt)
+    q = (xn @ w["wq"].T).reshape(b, R, Hq, dh)
+    k = (xn @ w["wk"].T).reshape(b, R, Hkv, dh)
+    v = (xn @ w["wv"].T).reshape(b, R, Hkv, dh)
+    q = storage(rope(q, pos, dims["rope_theta"]), dt)
+    k = storage(rope(k, pos, dims["rope_theta"]), dt)
+    v = storage(v, dt)
+    att = np.zeros((b, R, Hq, dh))
+    for bi in range(b):
+        if kv_prefix is not None:
+            kk = np.concatenate([kv_prefix[0][bi], k[bi]], axis=0)
+            vv = np.concatenate([kv_prefix[1][bi], v[bi]], axis=0)
+        else:
+            kk, vv = k[bi], v[bi]
+        att[bi] = masked_attention(q[bi], kk, vv, visible_fn(bi), scale, Hkv)
+    att = storage(att, dt).reshape(b, R, Hq * dh)
+    h = to_f32(h + att @ w["wo"].T)
+    xn = storage(rmsnorm(h, w["ffn_norm"], dims["norm_eps"]), dt)
+    act = storage(silu(xn @ w["w_gate"].T) * (xn @ w["w_up"].T), dt)
+    h = to_f32(h + act @ w["w_down"].T)
+    return h, (k, v)
+
+
+def embed_rows(weights, dims, ids, embeds=None):
+    """Token embedding lookup; ids < 0 take the row of ``embeds`` instead
+    (visual prefix positions of a multimodal prompt)."""
+    ids = np.asarray(ids)
+    out = np.zeros(ids.shape + (dims["d_model"],))
+    tok = ids >= 0
+    out[tok] = weights["embed"][ids[tok]]
+    if (~tok).any():
+        out[~tok] = np.asarray(embeds, dtype=np.float64)[~tok]
+    return storage(out, dims["dtype"])
+
+
+def prefill(weights, dims, ids, embeds=None):
+    """Prefix cache of block decoding (App. "attention overhead": prefix
+    caching).  The prefix tokens attend bidirectionally to each other only.
+
+    ids: [b, P] (negative = take ``embeds[b, p]``).  Returns a list over layers
+    of (K, V), each [b, P, Hkv, dh], rounded to the storage type.
+    """
+    ids = np.asarray(ids)
+    b, P = ids.shape
+    h = to_f32(embed_rows(weights, dims, ids, embeds))
+    pos = np.arange(P)
+    scale = 1.0 / math.sqrt(dims["head_dim"])
+    allvis = np.ones((P, P), dtype=bool)
+    cache = []
+    for layer in range(dims["n_layers"]):
+        h, kv = _layer(weights["layers"][layer], dims, h, pos, None,
+                       lambda bi: allvis, scale)
+        cache.append(kv)
+    return cache
+
+
+def step_logits(weights, dims, cache, tok, state, conf, mask_id, flags=0):
+    """Forward over the augmented block (x; s) of one DARD step (Alg. 1:
+    construct the augmented input, build the mask, run the model).
+
+    cache: per layer (K, V) of the prefix, each [b, P, Hkv, dh].
+    tok, state, conf: [b, B].  x^i embeds tok[i]; every s^i embeds [Mask].
+    x^i and s^i share the position P + i (Sec. 2).  Returns float32-valued
+    logits [b, 2B, V] (rows 0..B-1 from x, B..2B-1 from s) and the block's
+    per-layer (K, V).
+    """
+    tok = np.asarray(tok)
+    state = np.asarray(state)
+    conf = np.asarray(conf, dtype=np.float32)
+    b, B = tok.shape
+    P = cache[0][0].shape[1] if dims["n_layers"] > 0 else 0
+    ids = np.concatenate([tok, np.full((b, B), mask_id, dtype=tok.dtype)], axis=1)
+    h = to_f32(embed_rows(weights, dims, ids))
+    pos = P + np.concatenate([np.arange(B), np.arange(B)])
+    scale = 1.0 / math.sqrt(dims["head_dim"])
+    masks = [visible_keys(state[bi], conf[bi], P, flags) for bi in range(b)]
+    block_kv = []
+    for layer in range(dims["n_layers"]):
+        h, kv = _layer(weights["layers"][layer], dims, h, pos, cache[layer],
+                       lambda bi: masks[bi], scale)
+        block_kv.append(kv)
+    xn = storage(rmsnorm(h, weights["final_norm"], dims["norm_eps"]), dims["dtype"])
+    logits = to_f32(xn @ weights["lm_head"].T)
+    return logits, block_kv
+
+
+# --------------------------------------------------------------------------
+# confidence, guidance weight, transitions (Eq. 1, 5-8, Alg. 1)
+# --------------------------------------------------------------------------
+def confidence(row, cur_tok=None):
+    """Eq. 1: prediction = argmax of the distribution, confidence = its top-1
+    probability.  Returns (argmax, maxprob, prob of cur_tok) with the argmax
+    taken on the given (float32) logits, the lowest index winning ties, and
+    the probabilities in float64."""
+    row = np.asarray(row, dtype=np.float64)
+    a = int(np.argmax(row))                    # first maximal index
+    m = row[a]
+    z = np.sum(np.exp(row - m))
+    pc = math.exp(row[cur_tok] - m) / z if cur_tok is not None else float("nan")
+    return a, 1.0 / z, pc
+
+
+def mix_logits(lx, ls, w):
+    """Eq. 7: w * logit(x) + (1 - w) * logit(s), evaluated in float32 as
+    (w * lx) + ((1 - w) * ls), each operation rounded once."""
+    w = np.float32(w)
+    lx = np.asarray(lx, dtype=np.float32)
+    ls = np.asarray(ls, dtype=np.float32)
+    return (w * lx) + ((np.float32(1.0) - w) * ls)
+
+
+def guidance_weights(promoted, demoted, lam, p0):
+    """Eq. 5-6 for every position i of the block.
+
+    promoted, demoted: bool [B] (the sets P_t and D_t).  Returns float64
+    arrays (P^i, D^i, w^i) with P^i = sum_{j in P_t} lam^|i-j|, D^i likewise,
+    w^i = (P^i + p0) / (P^i + D^i + p0).
+    """
+    B = len(promoted)
+    Pi = np.zeros(B)
+    Di = np.zeros(B)
+    for i in range(B):
+        for j in range(B):
+            kern = lam ** abs(i - j)
+            if promoted[j]:
+                Pi[i] += kern
+            if demoted[j]:
+                Di[i] += kern
+    return Pi, Di, (Pi + p0) / (Pi + Di + p0)
+
+
+def transition(c, tau_c, tau_u):
+    """Eq. 8 on float32 values: c <= tau_c -> M, c <= tau_u -> C, else U."""
+    c = np.float32(c)
+    if c <= np.float32(tau_c):
+        return STATE_M
+    if c <= np.float32(tau_u):
+        return STATE_C
+    return STATE_U
+
+
+def decide(logits, tok, state, params):
+    """The decision part of one loop iteration of Alg. 1 for every sequence.
+
+    logits: [b, 2B, V] float32 values (x rows then s rows).
+    params: dict with tau_c, tau_u, lam, p0, mask_id, flags.
+    Returns a dict of per-position arrays: tok_out, state_out, conf_out,
+    block_done, w, and the intermediate argmax / confidences.
+    """
+    logits = np.asarray(logits, dtype=np.float32)
+    tok = np.asarray(tok)
+    state = np.asarray(state)
+    b, B = tok.shape
+    tc, tu = params["tau_c"], params["tau_u"]
+    flags = params.get("flags", 0)
+    out = {k: np.zeros((b, B), dtype=np.float64) for k in
+           ("w", "conf_out", "maxprob_s", "pcur_s", "maxprob_mix")}
+    out.update({k: np.zeros((b, B), dtype=np.int64) for k in
+                ("tok_out", "state_out", "argmax_s", "argmax_mix")})
+    out["block_done"] = np.zeros(b, dtype=np.int64)
+    for bi in range(b):
+        xhat = np.zeros(B, dtype=np.int64)
+        c = np.zeros(B)
+        nxt = np.zeros(B, dtype=np.int64)
+        # confidences of C and U tokens from the shadow stream
+        for i in range(B):
+            a, mp, pc = confidence(logits[bi, B + i], int(tok[bi, i]))
+            out["argmax_s"][bi, i] = a
+            out["maxprob_s"][bi, i] = np.float32(mp)
+            out["pcur_s"][bi, i] = np.float32(pc)
+            if state[bi, i] in (STATE_C, STATE_U):
+                xhat[i] = a
+                c[i] = np.float32(pc if flags & F_VERIFY_PCUR else mp)
+        # update the C tokens; collect promoted / demoted sets
+        promoted = np.zeros(B, dtype=bool)
+        demoted = np.zeros(B, dtype=bool)
+        for i in range(B):
+            if state[bi, i] == STATE_C:
+                nxt[i] = transition(c[i], tc, tu)
+                promoted[i] = nxt[i] == STATE_U
+                demoted[i] = nxt[i] == STATE_M
+        # decode the M tokens with logit mixing
+        _, _, w = guidance_weights(promoted, demoted, params["lam"], params["p0"])
+        for i in range(B):
+            if state[bi, i] == STATE_M:
+                wi = np.float32(w[i])
+                out["w"][bi, i] = wi
+                mixed = mix_logits(logits[bi, i], logits[bi, B + i], wi)
+                a, mp, _ = confidence(mixed)
+                out["argmax_mix"][bi, i] = a
+                out["maxprob_mix"][bi, i] = np.float32(mp)
+                xhat[i] = a
+                c[i] = np.float32(mp)
+        # update the M and U tokens
+        for i in range(B):
+            if state[bi, i] in (STATE_M, STATE_U):
+                nxt[i] = transition(c[i], tc, tu)
+        # fill: M -> [Mask], C/U -> prediction
+        for i in range(B):
+            out["state_out"][bi, i] = nxt[i]
+            out["tok_out"][bi, i] = params["mask_id"] if nxt[i] == STATE_M else xhat[i]
+            out["conf_out"][bi, i] = c[i]
+        out["block_done"][bi] = int(np.all(nxt == STATE_U))
+    return out
+
+
+def dard_step(weights, dims, cache, tok, state, conf, params):
+    """One DARD step (one iteration of the loop of Alg. 1)."""
+    logits, _ = step_logits(weights, dims, cache, tok, state, conf,
+                            params["mask_id"], params.get("flags", 0))
+    out = decide(logits, tok, state, params)
+    out["logits"] = logits
+    return out

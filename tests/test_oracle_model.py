@@ -1,0 +1,238 @@
+"""Pins of the oracle's attention, transformer pieces and step forward.
+
+Attention is checked against a textbook per-row evaluation and against
+torch's CPU scaled_dot_product_attention; RMSNorm / RoPE / SwiGLU against
+closed forms; the forward of a DARD step against the special cases the paper's
+rules fix exactly (P1 all-M block, P2 empty candidate set, P3 one-layer
+independence from candidate tokens, and a uniform-attention closed form that
+exposes which keys each row reads).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dard_oracle as O
+from paper_2608_26574_amd import synth
+
+
+# ---------------------------------------------------------------- rounding
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.01171875, 3.0e38, -1e-40]])
+    ref = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(O.to_bf16(x), ref)
+
+
+def test_bf16_ties_to_even():
+    # 1 + 2^-8 lies exactly between bf16 neighbours 1 and 1 + 2^-7: goes to 1.
+    assert O.to_bf16(1.0 + 2 ** -8) == 1.0
+    # 1 + 3*2^-8 lies between 1 + 2^-7 and 1 + 2^-6: goes to the even 1 + 2^-6.
+    assert O.to_bf16(1.0 + 3 * 2 ** -8) == 1.0 + 2 ** -6
+
+
+# ---------------------------------------------------------------- attention
+def _textbook_attention(q, k, v, vis, scale, n_kv):
+    R, Hq, dh = q.shape
+    out = np.zeros((R, Hq, dh))
+    for r in range(R):
+        for h in range(Hq):
+            g = h // (Hq // n_kv)
+            keys = [j for j in range(k.shape[0]) if vis[r, j]]
+            logits = [sum(q[r, h, e] * k[j, g, e] for e in range(dh)) * scale for j in keys]
+            mx = max(logits)
+            ws = [math.exp(a - mx) for a in logits]
+            z = sum(ws)
+            for w_, j in zip(ws, keys):
+                out[r, h] += (w_ / z) * v[j, g]
+    return out
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 2), (3, 1)])
+def test_attention_textbook(Hq, Hkv):
+    rng = np.random.default_rng(Hq * 10 + Hkv)
+    B, P, dh = 5, 3, 8
+    state = rng.integers(0, 3, B).astype(np.uint8)
+    conf = rng.permutation(np.linspace(0.1, 0.9, B)).astype(np.float32)
+    vis = O.visible_keys(state, conf, P)
+    q = rng.standard_normal((2 * B, Hq, dh))
+    k = rng.standard_normal((P + 2 * B, Hkv, dh))
+    v = rng.standard_normal((P + 2 * B, Hkv, dh))
+    got = O.masked_attention(q, k, v, vis, 1 / math.sqrt(dh), Hkv)
+    ref = _textbook_attention(q, k, v, vis, 1 / math.sqrt(dh), Hkv)
+    assert np.allclose(got, ref, rtol=0, atol=1e-12)
+
+
+def test_attention_matches_torch_sdpa():
+    rng = np.random.default_rng(3)
+    B, P, dh, H = 16, 40, 32, 4
+    state = rng.integers(0, 3, B).astype(np.uint8)
+    conf = rng.permutation(np.linspace(0.1, 0.9, B)).astype(np.float32)
+    vis = O.visible_keys(state, conf, P)
+    q = rng.standard_normal((2 * B, H, dh))
+    k = rng.standard_normal((P + 2 * B, H, dh))
+    v = rng.standard_normal((P + 2 * B, H, dh))
+    got = O.masked_attention(q, k, v, vis, 1 / math.sqrt(dh), H)
+    tq = torch.tensor(q).permute(1, 0, 2)
+    tk = torch.tensor(k).permute(1, 0, 2)
+    tv = torch.tensor(v).permute(1, 0, 2)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        tq, tk, tv, attn_mask=torch.tensor(vis)).permute(1, 0, 2).numpy()
+    assert np.allclose(got, ref, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- layer pieces
+def test_rmsnorm_unit_rms():
+    rng = np.random.default_rng(1)
+    h = rng.standard_normal((7, 64)) * 3
+    y = O.rmsnorm(h, np.ones(64), 0.0)
+    assert np.allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, atol=1e-14)
+    g = rng.standard_normal(64)
+    assert np.allclose(O.rmsnorm(h, g, 0.0), y * g, atol=1e-14)
+
+
+def test_rope_properties():
+    rng = np.random.default_rng(2)
+    dh, theta = 16, 10000.0
+    x = rng.standard_normal((5, 1, dh))
+    pos = np.array([0, 1, 7, 100, 3000])
+    y = O.rope(x, pos, theta)
+    # position 0 is the identity
+    assert np.allclose(y[0], x[0], atol=1e-15)
+    # each rotated pair (t, t + dh/2) keeps its length
+    half = dh // 2
+    n_in = x[..., :half] ** 2 + x[..., half:] ** 2
+    n_out = y[..., :half] ** 2 + y[..., half:] ** 2
+    assert np.allclose(n_in, n_out, atol=1e-12)
+    # q(a) . k(b) depends only on a - b
+    q = rng.standard_normal((1, 1, dh))
+    k = rng.standard_normal((1, 1, dh))
+    def dot(a, b):
+        return float(np.sum(O.rope(q, np.array([a]), theta) * O.rope(k, np.array([b]), theta)))
+    assert abs(dot(10, 3) - dot(107, 100)) < 1e-10
+    assert abs(dot(5, 5) - float(np.sum(q * k))) < 1e-12
+    # dimension 0 turns by exactly pos radians (frequency theta^0 = 1)
+    e = np.zeros((1, 1, dh)); e[0, 0, 0] = 1.0
+    r = O.rope(e, np.array([2]), theta)
+    assert abs(r[0, 0, 0] - math.cos(2)) < 1e-15 and abs(r[0, 0, half] - math.sin(2)) < 1e-15
+
+
+def test_silu_closed_forms():
+    x = np.linspace(-8, 8, 33)
+    assert O.silu(np.array(0.0)) == 0.0
+    assert np.allclose(O.silu(x) - O.silu(-x), x, atol=1e-14)
+    assert abs(O.silu(np.array(1.0)) - 1 / (1 + math.exp(-1))) < 1e-15
+
+
+# ---------------------------------------------------------------- step forward
+def _tiny(n_layers=2, dtype="f32", d=64, H=2, Hkv=2, dh=32, F=96, V=97):
+    dims = synth.Dims(n_layers, d, H, Hkv, dh, F, V, 512, dtype).as_dict()
+    dims_obj = synth.Dims(**dims)
+    w = synth.OracleWeights(dims_obj, synth.make_weights(dims_obj, seed=11))
+    return dims, w
+
+
+def _block(B, V, kinds, seed=4):
+    rng = np.random.default_rng(seed)
+    state = np.array(kinds, dtype=np.uint8)[None, :]
+    tok = rng.integers(0, V - 1, (1, B)).astype(np.int32)
+    tok[state == O.STATE_M] = V - 1
+    conf = rng.permutation(np.linspace(0.45, 0.85, B)).astype(np.float32)[None, :]
+    conf[state == O.STATE_U] = 0.95
+    return tok, state, conf
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_p1_all_masked_block(dtype):
+    """P1: with every position masked the x and s streams are the same vanilla
+    forward, so their logits agree and the guidance weight is 1 (Eq. 6 with
+    empty P and D)."""
+    dims, w = _tiny(dtype=dtype)
+    B, P = 6, 5
+    V = dims["vocab"]
+    cache = O.prefill(w, dims, synth.prompt_ids(1, P, V, seed=3))
+    tok = np.full((1, B), V - 1, dtype=np.int32)
+    state = np.zeros((1, B), dtype=np.uint8)
+    conf = np.zeros((1, B), dtype=np.float32)
+    logits, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    assert np.allclose(logits[0, :B], logits[0, B:], rtol=0, atol=1e-6)
+    params = dict(tau_c=0.4, tau_u=0.9, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=V - 1)
+    out = O.decide(logits, tok, state, params)
+    assert np.all(out["w"] == 1.0)
+
+
+@pytest.mark.parametrize("flags", [0, O.F_MKEYS_SHADOW])
+def test_p2_no_candidates(flags):
+    """P2: with C empty, x^i and s^i of every M position stay identical through
+    all layers (they hold the same [Mask] token and read the same keys), so
+    their logits agree."""
+    dims, w = _tiny(n_layers=3)
+    kinds = [0, 2, 0, 0, 2, 2, 0, 2]
+    B = len(kinds)
+    V = dims["vocab"]
+    cache = O.prefill(w, dims, synth.prompt_ids(1, 7, V, seed=3))
+    tok, state, conf = _block(B, V, kinds)
+    logits, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1, flags)
+    for i in range(B):
+        if kinds[i] == O.STATE_M:
+            assert np.allclose(logits[0, i], logits[0, B + i], rtol=0, atol=1e-6)
+
+
+def test_p3_one_layer_ignores_candidate_tokens():
+    """P3: in a one-layer model, U queries (x and s) and M shadow queries never
+    read a candidate's x key, so changing candidate token ids leaves their
+    logits unchanged, while the M x queries do change."""
+    dims, w = _tiny(n_layers=1)
+    kinds = [1, 2, 0, 1, 2, 0, 1, 0]
+    B = len(kinds)
+    V = dims["vocab"]
+    cache = O.prefill(w, dims, synth.prompt_ids(1, 4, V, seed=3))
+    tok, state, conf = _block(B, V, kinds)
+    l1, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    tok2 = tok.copy()
+    for i in range(B):
+        if kinds[i] == O.STATE_C:
+            tok2[0, i] = (tok2[0, i] + 17) % (V - 1)
+    l2, _ = O.step_logits(w, dims, cache, tok2, state, conf, V - 1)
+    for i in range(B):
+        if kinds[i] == O.STATE_U:
+            assert np.array_equal(l1[0, i], l2[0, i])
+        if kinds[i] in (O.STATE_U, O.STATE_M):
+            assert np.array_equal(l1[0, B + i], l2[0, B + i])
+    m_rows = [i for i in range(B) if kinds[i] == O.STATE_M]
+    assert not np.allclose(l1[0, m_rows], l2[0, m_rows])
+
+
+def test_uniform_attention_closed_form():
+    """With zero query/key projections every visible key gets the same weight,
+    so the attention output of a row is the plain mean of the values it reads.
+    With W_o = identity and a zero FFN, the first layer's residual update is
+    that mean: this exposes exactly which keys each row of the step reads."""
+    d = H = 0
+    dims = dict(n_layers=1, d_model=32, n_heads=2, n_kv_heads=2, head_dim=16,
+                ffn_dim=8, vocab=50, max_pos=64, dtype="f32", norm_eps=1e-5,
+                rope_theta=10000.0)
+    rng = np.random.default_rng(9)
+    d = dims["d_model"]
+    lay = dict(attn_norm=np.ones(d), wq=np.zeros((d, d)), wk=np.zeros((d, d)),
+               wv=rng.standard_normal((d, d)) * 0.1, wo=np.eye(d), ffn_norm=np.ones(d),
+               w_gate=np.zeros((8, d)), w_up=np.zeros((8, d)), w_down=np.zeros((d, 8)))
+    w = dict(embed=rng.standard_normal((50, d)), layers=[lay], final_norm=np.ones(d),
+             lm_head=np.eye(50, d))
+    w["embed"] = O.to_f32(w["embed"])
+    kinds = [2, 1, 0, 1, 2, 0]
+    B, P = len(kinds), 3
+    tok, state, conf = _block(B, 50, kinds)
+    pre_ids = np.array([[5, 6, 7]])
+    cache = O.prefill(w, dims, pre_ids)
+    # expected: h1 = h0 + mean of visible V rows (V = rmsnorm(h0) wv^T)
+    ids = np.concatenate([pre_ids[0], tok[0], np.full(B, 49)])
+    h0 = w["embed"][ids]
+    vals = O.to_f32(O.rmsnorm(h0, np.ones(d), 1e-5) @ lay["wv"].T)
+    vis = O.visible_keys(state[0], conf[0], P)
+    expect_h1 = h0[P:] + np.stack([vals[vis[r]].mean(axis=0) for r in range(2 * B)])
+    expect_logits = O.to_f32(O.rmsnorm(O.to_f32(expect_h1), np.ones(d), 1e-5) @ w["lm_head"].T)
+    logits, _ = O.step_logits(w, dims, cache, tok, state, conf, 49)
+    assert np.allclose(logits[0], expect_logits, rtol=0, atol=1e-5)
