@@ -1,0 +1,244 @@
+"""Throughput of the DARD hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Workload: the 8B-shape DARD step -- a random-init LLaDA-8B-like model
+(32 layers, d 4096, 32 x 128 MHA, SwiGLU FFN 12288, vocab 126464, bf16),
+batch 1, prompt 512, generation 256 in blocks of 32, prefix KV cache, per-step
+token states drawn at candidate fraction 0.25, thresholds (0.4, 0.9).
+
+A step is one dard_step call: the augmented-block forward through all 32
+layers, the LM head, both confidence passes and both decision phases.  The
+timed region runs K steps with inputs resident in HBM, cycling the prefix
+length over the 8 blocks of the generation.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DARD decode steps/sec and tokens committed/sec at 8B shape; attention % MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+TOKENS_PER_STEP = 6.0          # mean tokens decoded per DARD step on LLaDA (paper, Sec. on ordering)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=24)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=32, help=argparse.SUPPRESS)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the DARD step is data-parallel "
+              f"over sequences and is measured on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+
+    dims = synth.LLADA8B if args.layers == 32 else synth.truncated(synth.LLADA8B, args.layers)
+    b, B, prompt, gen, frac = 1, 32, 512, 256, 0.25
+    nblocks = gen // B
+    cap = prompt + gen + B
+    V = dims.vocab
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log(f"[bench] weights: {dims}")
+    t0 = time.time()
+    w = synth.make_weights(dims, seed=1, device="cuda")
+    eng = dard.Engine(dims, w, b, B, cap)
+    del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    log(f"[bench] packed weights in {time.time() - t0:.1f}s; workspace {eng.ws.numel() / 2**20:.0f} MiB")
+
+    # prefix cache for the longest prefix; step t reads the prefix of its block
+    P_max = prompt + gen - B
+    ids = torch.from_numpy(synth.prompt_ids(b, P_max, V, seed=2)).cuda()
+    eng.dard_prefill(ids)
+    torch.cuda.synchronize()
+
+    total = args.warmup + args.steps
+    S_b = math.ceil(B / TOKENS_PER_STEP)
+    inputs = []
+    for t in range(total):
+        tok, state, conf = synth.workload_block(b, B, frac, V, seed=1000 + t)
+        inputs.append(tuple(torch.from_numpy(a).cuda() for a in (tok, state, conf)))
+    Ps = [prompt + B * ((t // S_b) % nblocks) for t in range(total)]
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, 0)
+    t_out = torch.empty(b, B, dtype=torch.int32, device=dev)
+    s_out = torch.empty(b, B, dtype=torch.uint8, device=dev)
+    c_out = torch.empty(b, B, device=dev)
+    done = torch.empty(b, dtype=torch.int32, device=dev)
+
+    def step(t):
+        tok, state, conf = inputs[t]
+        eng.dard_step(Ps[t], params, tok, state, conf, t_out, s_out, c_out, done)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K steps; the dominant kernel class is bracketed by HIP events
+    dard.dard_trace_reset()
+    dard.dard_trace_enable(1 << dard.K_GEMM_GU)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    tw = time.perf_counter()
+    for t in range(args.warmup, total):
+        step(t)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - tw
+    ms_total = ev0.elapsed_time(ev1)
+    dard.dard_trace_enable(0)
+    n_gu, ms_gu = dard.dard_trace_read(dard.K_GEMM_GU)
+    ms_per_step = ms_total / args.steps
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})")
+
+    # ---- per-kernel-class breakdown (a separate traced pass over the same steps)
+    dard.dard_trace_reset()
+    dard.dard_trace_enable((1 << dard.K_COUNT) - 1)
+    for t in range(args.warmup, total):
+        step(t)
+    torch.cuda.synchronize()
+    dard.dard_trace_enable(0)
+    names = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "attention", "confidence",
+             "decide", "norm"]
+    breakdown = {}
+    for k, nm in enumerate(names):
+        n, ms = dard.dard_trace_read(k)
+        breakdown[nm] = {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+    dard.dard_trace_reset()
+
+    # ---- roofline of the dominant kernel: gate/up projection with SwiGLU epilogue
+    rows = b * 2 * B
+    d, F = dims.d_model, dims.ffn_dim
+    gu_bytes = 2 * F * d * 2 + rows * d * 2 + rows * F * 2          # weights + X + act
+    gu_ms = ms_gu / max(n_gu, 1)
+    gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9
+    roofline = {"kernel": "gemm_skinny_bf16 (gate/up + SwiGLU), per launch", "bound": "hbm",
+                "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic_bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_ms * 1e3, 2)}
+
+    # all weight-streaming GEMMs of a step together
+    qd, kd = dims.n_heads * dims.head_dim, dims.n_kv_heads * dims.head_dim
+    per_layer = (qd + 2 * kd) * d + d * qd + 2 * F * d + d * F
+    weight_bytes = 2 * (dims.n_layers * per_layer + V * d)
+    gemm_ms = sum(breakdown[k]["ms_per_step"] for k in names[:5])
+
+    # attention: algorithmic flops / bytes per step (each row sees P + B keys)
+    P_avg = sum(Ps[args.warmup:]) / args.steps
+    att_flops = 4 * dims.head_dim * dims.n_heads * rows * (P_avg + B) * dims.n_layers
+    att_bytes = dims.n_layers * b * dims.n_kv_heads * (P_avg + 2 * B) * dims.head_dim * 2 * 2
+    att_ms = breakdown["attention"]["ms_per_step"]
+    attention = {"tflops": round(att_flops / (att_ms * 1e-3) / 1e12, 2),
+                 "mfma_frac": round(att_flops / (att_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                 "kv_gbs": round(att_bytes / (att_ms * 1e-3) / 1e9, 1),
+                 "hbm_frac": round(att_bytes / (att_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "ms_per_step": round(att_ms, 4)}
+
+    # ---- tokens committed / s: 8 blocks of prefill + ceil(B / 6) steps each
+    def generation():
+        for k in range(nblocks):
+            eng.dard_prefill(ids[:, : prompt + B * k])
+            for j in range(S_b):
+                step(args.warmup + (k * S_b + j) % args.steps)
+    generation()
+    torch.cuda.synchronize()
+    g0 = time.perf_counter()
+    generation()
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - g0
+    tokens_per_s = b * gen / gen_s
+
+    out = {
+        "metric": METRIC, "value": round(1e3 / ms_per_step, 2), "unit": "steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded random-init weights N(0, 0.02), uniform prompt ids, drawn token states",
+        "config": {"workload": "llada8b-like full DARD step: 32 layers, d 4096, 32x128 MHA, FFN 12288, "
+                               "vocab 126464, bf16; batch 1, prompt 512, generation 256, block 32, "
+                               "candidate fraction 0.25, prefix KV cache",
+                   "batch": b, "block": B, "prompt": prompt, "gen_len": gen, "cand_frac": frac,
+                   "layers": dims.n_layers},
+        "tokens_committed_per_s": round(tokens_per_s, 1),
+        "tokens_committed_note": f"{nblocks} blocks x (prefill + {S_b} steps), 6.0 tokens/step as reported",
+        "roofline": roofline,
+        "weight_stream": {"gb_per_step": round(weight_bytes / 1e9, 3), "gemm_ms_per_step": round(gemm_ms, 4),
+                          "gbs": round(weight_bytes / (gemm_ms * 1e-3) / 1e9, 1)},
+        "attention": attention,
+        "breakdown_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in breakdown.items()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(dims, b, B, P, frac, layers_sampled=2):
+    """The CPU oracle on a bounded sample of the same step: embedding, two of
+    the 32 layers, final norm, LM head and the decisions, timed and scaled to
+    32 layers.  Inputs are seeded and synthetic (the prefix KV cache is random
+    of the right shape)."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import dard_oracle as O
+    from paper_2608_26574_amd import synth
+
+    sub = synth.truncated(dims, layers_sampled)
+    w = synth.make_weights(sub, seed=1, device="cuda")
+    ow = synth.OracleWeights(sub, w)
+    dd = sub.as_dict()
+    g = torch.Generator(device="cuda").manual_seed(7)
+    cache = []
+    for _ in range(layers_sampled):
+        k = torch.randn(b, P, sub.n_kv_heads, sub.head_dim, generator=g, device="cuda").bfloat16()
+        v = torch.randn(b, P, sub.n_kv_heads, sub.head_dim, generator=g, device="cuda").bfloat16()
+        cache.append((k.double().cpu().numpy(), v.double().cpu().numpy()))
+    tok, state, conf = synth.workload_block(b, B, frac, sub.vocab, seed=1000)
+    params = dict(tau_c=0.4, tau_u=0.9, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=sub.mask_id)
+    # warm the converted weights once (conversion is not the oracle's work)
+    layers = [ow.layers[i] for i in range(layers_sampled)]
+    wd = {"embed": ow["embed"], "final_norm": ow["final_norm"], "lm_head": ow["lm_head"], "layers": layers}
+    t0 = time.perf_counter()
+    out = O.dard_step(wd, dd, cache, tok, state, conf, params)
+    t_sample = time.perf_counter() - t0
+    # time the layers alone to scale them to the full depth
+    t1 = time.perf_counter()
+    O.step_logits({**wd, "layers": layers[:1]}, {**dd, "n_layers": 1}, cache[:1], tok, state, conf, sub.mask_id)
+    t_one = time.perf_counter() - t1
+    t_zero0 = time.perf_counter()
+    O.step_logits({**wd, "layers": []}, {**dd, "n_layers": 0}, [], tok, state, conf, sub.mask_id)
+    t_zero = time.perf_counter() - t_zero0
+    per_layer = max(t_one - t_zero, 1e-9)
+    t_step = t_sample + (dims.n_layers - layers_sampled) * per_layer
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": round(1.0 / t_step, 5), "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one DARD step with {layers_sampled} of {dims.n_layers} layers, LM head and decisions "
+                      f"({t_sample:.1f} s), per-layer time {per_layer:.2f} s scaled to {dims.n_layers} layers",
+            "host_cpus": os.cpu_count()}
+
+
+if __name__ == "__main__":
+    main()

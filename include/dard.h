@@ -1,0 +1,267 @@
+/*
+ * dard.h -- C ABI of libdard.so, the gfx950 (MI355X) hot path of
+ * Dependency-Aware Revocable Decoding (DARD, arXiv 2608.26574).
+ *
+ * One DARD step (Algorithm 1, one iteration of its loop) runs a bidirectional
+ * transformer over the augmented block (x; s): the current block x of B
+ * positions and its all-[Mask] shadow copy s, both at positions P..P+B-1 after
+ * a cached prefix of P tokens.  Attention uses the state-specific mask of
+ * Sec. 3.2, built from every position's state (M / C / U) and its previous
+ * confidence.  The logits then drive the vocab-wide confidence reduction
+ * (Eq. 1), the verification of candidates, the guidance weight of masked
+ * tokens (Eq. 5-6), logit mixing (Eq. 7) and the state transition (Eq. 8).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers owned by the caller, row-major,
+ *     naturally aligned (16-byte aligned for bf16/f32 tensors).  The library
+ *     never frees them and, on the hot calls, allocates nothing: scratch space
+ *     comes from the caller's workspace `ws` of `ws_bytes` bytes, sized by the
+ *     matching *_workspace_bytes() query.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *     enqueues work on it and returns at once; results are valid once the
+ *     stream has run.
+ *   - Every call returns a dard_status.  Arguments are validated on the host
+ *     first; on any violation nothing is enqueued and the call returns
+ *     DARD_ERR_ARG / DARD_ERR_SHAPE / DARD_ERR_UNSUPPORTED.  A failing HIP call
+ *     returns DARD_ERR_HIP.  dard_last_error() gives a thread-local message.
+ *   - Token state codes outside {0,1,2} in device arrays are not checked and
+ *     give unspecified (but memory-safe) results.
+ */
+#ifndef DARD_H
+#define DARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+typedef int dard_status;
+#define DARD_OK               0
+#define DARD_ERR_ARG        (-1)  /* null pointer, bad flag, bad parameter     */
+#define DARD_ERR_SHAPE      (-2)  /* sizes outside the supported ranges        */
+#define DARD_ERR_UNSUPPORTED (-3) /* valid but not implemented on this path     */
+#define DARD_ERR_HIP        (-4)  /* a HIP runtime call failed                 */
+#define DARD_ERR_WORKSPACE  (-5)  /* ws smaller than the size query asked for  */
+
+/* Token states (Sec. 3.2; Eq. 8): masked, candidate, unmasked. */
+#define DARD_STATE_M 0
+#define DARD_STATE_C 1
+#define DARD_STATE_U 2
+
+/* Storage types of weights / activations / KV cache.  Logits, confidences
+ * and the residual stream are always float32. */
+#define DARD_DTYPE_F32  0
+#define DARD_DTYPE_BF16 1
+
+/* Flags selecting alternative readings where the paper leaves a choice open
+ * (the default, 0, is the reading the library documents as primary):
+ *   XSELF_SHADOW  the x query of a U token does not see its own x key
+ *                 (default: it does; only shadow queries are blocked from
+ *                 their own position, Sec. 3.2 "Verification of U tokens");
+ *   MKEYS_SHADOW  the x query of an M token reads the other M positions from
+ *                 s (default: from x, i.e. the x stream is vanilla decoding);
+ *   VERIFY_PCUR   C/U confidence = probability of the current token instead of
+ *                 the top-1 probability of Eq. 1 (default). */
+#define DARD_F_XSELF_SHADOW (1u << 0)
+#define DARD_F_MKEYS_SHADOW (1u << 1)
+#define DARD_F_VERIFY_PCUR  (1u << 2)
+#define DARD_F_ALL          (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR)
+
+/* Decoding hyper-parameters (Alg. 1 inputs; Sec. 4.1 uses lambda = 0.5^(1/8),
+ * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0. */
+typedef struct {
+    float tau_c;      /* c <= tau_c -> M                                   */
+    float tau_u;      /* tau_c < c <= tau_u -> C, tau_u < c -> U (Eq. 8)    */
+    double lambda;    /* geometric kernel K(i,j) = lambda^|i-j| (Eq. 5)     */
+    double p0;        /* prior constant of the guidance weight (Eq. 6)     */
+    int32_t mask_id;  /* token id of [Mask]                                */
+    uint32_t flags;   /* DARD_F_* bits                                     */
+} dard_params;
+
+/* Transformer shape.  Pre-norm blocks: RMSNorm (norm_eps), rotary position
+ * embedding of the rotate-half form (rope_theta), multi-head / grouped-query
+ * attention, SwiGLU feed-forward, no biases, untied LM head.
+ * Supported: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ * d_model == n_heads * head_dim; bf16 needs d_model, ffn_dim % 64 == 0 and
+ * vocab % 16 == 0; max_pos bounds prefix + block positions. */
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, max_pos;
+    int32_t dtype;    /* DARD_DTYPE_F32 or DARD_DTYPE_BF16 */
+    float norm_eps, rope_theta;
+} dard_dims;
+
+/* ------------------------------------------------------------ library */
+const char* dard_last_error(void);
+int dard_version(void);
+
+/* ------------------------------------------------------------ a1: mask
+ * State-specific attention mask of Sec. 3.2 (Eq. 2-4) for b sequences of
+ * block length B (1 <= B <= 128).  By Eq. 2 every query row sees exactly one
+ * of x^j and s^j, so the block part of the mask is one bit per (row, j):
+ *   sel[s][r][w] (uint64, W = ceil(B/64) words per row), bit j%64 of word j/64
+ *   = 1 if row r reads x^j, 0 if it reads s^j.
+ * Rows r < B are the x queries of position r, rows B..2B-1 the s queries of
+ * position r-B.  The prefix is always visible and not encoded.
+ *   state [b][B] uint8, conf [b][B] float32 (c_{t-1}, the ordering key of
+ *   Eq. 3), sel [b][2B][W] uint64. */
+dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
+                                  uint32_t flags, uint64_t* sel, void* stream);
+
+/* ------------------------------------------------------------ a3: attention
+ * State-masked attention over the augmented block (Sec. 2 "parallelized
+ * inference over distinct decoding contexts", Sec. 3.2 masks):
+ *   out[s][r][h] = sum_k softmax_k(scale * q[s][r][h] . k_k) v_k
+ * over the visible keys of row r: the prefix keys 0..P-1, and for every block
+ * position j either x^j (cache index P+j) or s^j (cache index P+B+j) as the
+ * mask of dard_build_state_mask says.
+ *   q   [b][2B][Hq][dh]     dtype
+ *   k,v [b][Hkv][cap][dh]   dtype; keys P..P+2B-1 hold the block (x then s)
+ *   out [b][2B][Hq][dh]     dtype
+ * Query head h reads KV head h / (Hq/Hkv).  Any permutation of the head_dim
+ * axis applied to both q and k gives the same result.  Needs P >= 0,
+ * P + 2B <= cap, dh in {64, 128}. */
+size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P);
+dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v,
+                                  int P, int cap, const uint8_t* state, const float* conf,
+                                  int b, int B, int Hq, int Hkv, int dh, float scale,
+                                  uint32_t flags, void* out, void* ws, size_t ws_bytes,
+                                  void* stream);
+
+/* ------------------------------------------------------------ a5/a7: confidence
+ * Vocab-wide confidence reduction (Eq. 1), with the optional logit mixing of
+ * Eq. 7.  For each row r:
+ *   l_v = logits_s[r][v]                                  if logits_x == NULL
+ *   l_v = (w[r] * logits_x[r][v]) + ((1 - w[r]) * logits_s[r][v])   otherwise,
+ *         each product, the difference 1 - w and the sum rounded once in fp32
+ *   argmax[r]  = first index of the largest l_v
+ *   maxprob[r] = 1 / sum_v exp(l_v - l_max)              (top-1 probability)
+ *   pcur[r]    = exp(l_cur - l_max) * maxprob[r], l_cur = l at cur_tok[r]
+ *                (only if pcur != NULL; needs cur_tok, no mixing)
+ * logits_* rows have leading dimension ld >= V (elements, multiple of 4).
+ * Outputs: argmax int32 [rows], maxprob float32 [rows], pcur float32 [rows]. */
+size_t dard_confidence_workspace_bytes(int rows, int V);
+dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w,
+                            const int32_t* cur_tok, int rows, int V, int64_t ld,
+                            int32_t* argmax, float* maxprob, float* pcur,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------ a6/a8: decisions
+ * Decision part of Algorithm 1 for b sequences of block length B.
+ * phase DARD_PHASE_VERIFY (after the shadow confidences of the candidates):
+ *   for C positions, the transition of Eq. 8 on c (maxprob_s, or pcur_s with
+ *   VERIFY_PCUR) gives the promoted set P_t (-> U) and demoted set D_t (-> M);
+ *   for every M position i:  P^i = sum_{j in P_t} lambda^|i-j|,
+ *   D^i likewise (Eq. 5), w_out[i] = (P^i + p0) / (P^i + D^i + p0) (Eq. 6);
+ *   w_out = 0 at C and U positions.  Reads state_in, maxprob_s / pcur_s.
+ * phase DARD_PHASE_FINAL (after the mixed confidences of the M positions):
+ *   c_i = maxprob_s (or pcur_s) for C/U positions, maxprob_mix for M;
+ *   prediction x_i = argmax_s for C/U, argmax_mix for M;
+ *   state_out by Eq. 8; tok_out = mask_id for next-M, x_i otherwise;
+ *   conf_out = c_i; block_done[s] = 1 iff every position is next-U.
+ * All per-position arrays are [b][B]; block_done is [b] int32.  Arrays not
+ * read or written by a phase may be NULL. */
+#define DARD_PHASE_VERIFY 0
+#define DARD_PHASE_FINAL  1
+dard_status dard_commit_remask(int phase, const dard_params* params, int b, int B,
+                               const uint8_t* state_in, const float* maxprob_s,
+                               const float* pcur_s, const int32_t* argmax_s,
+                               const float* maxprob_mix, const int32_t* argmax_mix,
+                               float* w_out, uint8_t* state_out, int32_t* tok_out,
+                               float* conf_out, int32_t* block_done, void* stream);
+
+/* ------------------------------------------------------------ weights and KV cache
+ * The library runs on its own packed weight image.  dard_pack_weights() copies
+ * the logical weights into it once (not a hot call; synchronous on `stream`).
+ * src: 3 + 9 * n_layers device pointers of the storage dtype, in this order:
+ *   embed [V][d];
+ *   per layer: attn_norm [d], wq [Hq*dh][d], wk [Hkv*dh][d], wv [Hkv*dh][d],
+ *              wo [d][Hq*dh], ffn_norm [d], w_gate [F][d], w_up [F][d],
+ *              w_down [d][F];
+ *   final_norm [d], lm_head [V][d].
+ * The packed image also holds the rotary cos/sin table (float32).  Inside it
+ * the rows of wq/wk are reordered per head so that each rotary pair (t, t+dh/2)
+ * is adjacent, and the rows of w_gate/w_up interleave; the Q and K caches
+ * therefore hold each head's dims in the order (0, dh/2, 1, dh/2+1, ...),
+ * which leaves every attention score unchanged.
+ *
+ * KV cache: [n_layers][2 (K, V)][b][Hkv][cap][dh] of the storage dtype,
+ * sized by dard_kv_bytes().  Keys 0..P-1 hold the prefix (dard_prefill);
+ * a step writes its block keys at P..P+2B-1. */
+size_t dard_packed_weight_bytes(const dard_dims* dims);
+dard_status dard_pack_weights(const dard_dims* dims, const void* const* src, int n_src,
+                              void* packed, size_t packed_bytes, void* stream);
+size_t dard_kv_bytes(const dard_dims* dims, int b, int cap);
+
+/* ------------------------------------------------------------ a9: prefill
+ * Prefix KV cache of block decoding (appendix on attention overhead: prefix
+ * caching of system, visual and text-prompt tokens).  Runs the model over the
+ * P prefix positions of each sequence with bidirectional attention among them
+ * and writes K/V[0..P-1] of every layer.
+ *   ids    [b][P] int32; an id < 0 takes row [s][p] of `embeds` instead
+ *   embeds [b][P][d] dtype or NULL (visual tokens of a multimodal prompt). */
+size_t dard_workspace_bytes(const dard_dims* dims, int b, int B, int cap);
+dard_status dard_prefill(const dard_dims* dims, const void* packed, void* kv, int cap,
+                         int b, int P, const int32_t* ids, const void* embeds,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------ a1-a8: one step
+ * One DARD step (one loop iteration of Algorithm 1) for b sequences whose
+ * current block has B positions after a prefix of P cached keys:
+ *   build the augmented block (x = tok_in, s = [Mask] at the same positions),
+ *   run the model under the state-specific mask (state_in, conf_in as the
+ *   ordering key), take the shadow confidences of C and U tokens, verify the
+ *   candidates, mix the two logit rows of every M token with its guidance
+ *   weight, apply the transitions and fill the tokens.
+ *   tok_in/tok_out [b][B] int32, state_in/state_out [b][B] uint8,
+ *   conf_in/conf_out [b][B] float32, block_done [b] int32.
+ * Outputs may alias the matching inputs.  `dbg`, when not NULL, receives
+ * copies of intermediate results (any member may be NULL). */
+typedef struct {
+    float* logits;       /* [b][2B][V]: x rows then s rows                  */
+    float* w;            /* [b][B] guidance weights (0 at C/U)              */
+    float* maxprob_s;    /* [b][B] shadow top-1 prob. (C/U positions)       */
+    int32_t* argmax_s;   /* [b][B]                                          */
+    float* pcur_s;       /* [b][B] shadow prob. of the current token (C/U)  */
+    float* maxprob_mix;  /* [b][B] mixed top-1 prob. (M positions)          */
+    int32_t* argmax_mix; /* [b][B]                                          */
+} dard_step_debug;
+
+dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int cap, int P,
+                      const dard_params* params, int b, int B, const int32_t* tok_in,
+                      const uint8_t* state_in, const float* conf_in, int32_t* tok_out,
+                      uint8_t* state_out, float* conf_out, int32_t* block_done,
+                      const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------ plain linear layer
+ * Y[m][n] = sum_k X[m][k] * W[n][k] in float32 (the projection GEMM of every
+ * layer and the LM head, exposed for testing and measurement).
+ * X [M][K], W [N][K] of `dtype`, Y [M][N] float32. */
+dard_status dard_linear(int dtype, const void* X, int M, int K, const void* W, int N,
+                        float* Y, void* stream);
+
+/* ------------------------------------------------------------ tracing
+ * When enabled, the library brackets each launch of the kernel classes in
+ * `class_mask` with HIP events on the launch stream.  dard_trace_read()
+ * synchronises with those events and returns, for one class, the number of
+ * launches seen and their summed duration since the last reset. */
+#define DARD_K_GEMM_QKV   0
+#define DARD_K_GEMM_O     1
+#define DARD_K_GEMM_GU    2
+#define DARD_K_GEMM_DOWN  3
+#define DARD_K_GEMM_HEAD  4
+#define DARD_K_ATTENTION  5
+#define DARD_K_CONFIDENCE 6
+#define DARD_K_DECIDE     7
+#define DARD_K_NORM       8
+#define DARD_K_COUNT      9
+dard_status dard_trace_enable(uint32_t class_mask);
+dard_status dard_trace_read(int kernel_class, int64_t* launches, double* total_ms);
+dard_status dard_trace_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DARD_H */

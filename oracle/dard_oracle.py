@@ -365,6 +365,34 @@ def transition(c, tau_c, tau_u):
     return STATE_U
 
 
+def verify_candidates(state, c, params):
+    """Update of the C tokens in Alg. 1 and the guidance weights of the M
+    tokens (Eq. 5-6).  state, c: [B] (c = confidence of the C tokens, float32
+    values).  Returns (next state of C tokens or -1, promoted, demoted, w) with
+    w = 0 at C and U positions and w rounded to float32."""
+    B = len(state)
+    nxt = np.full(B, -1, dtype=np.int64)
+    promoted = np.zeros(B, dtype=bool)
+    demoted = np.zeros(B, dtype=bool)
+    for i in range(B):
+        if state[i] == STATE_C:
+            nxt[i] = transition(c[i], params["tau_c"], params["tau_u"])
+            promoted[i] = nxt[i] == STATE_U
+            demoted[i] = nxt[i] == STATE_M
+    _, _, w = guidance_weights(promoted, demoted, params["lam"], params["p0"])
+    w = np.where(np.asarray(state) == STATE_M, w, 0.0).astype(np.float32).astype(np.float64)
+    return nxt, promoted, demoted, w
+
+
+def finalize(c, xhat, params):
+    """Transition of every position by Eq. 8 and the fill rule: next-M
+    positions hold [Mask], the others their prediction.  c, xhat: [B]."""
+    B = len(c)
+    st = np.array([transition(c[i], params["tau_c"], params["tau_u"]) for i in range(B)], dtype=np.int64)
+    tok = np.where(st == STATE_M, params["mask_id"], np.asarray(xhat, dtype=np.int64))
+    return st, tok, np.asarray(c, dtype=np.float64), int(np.all(st == STATE_U))
+
+
 def decide(logits, tok, state, params):
     """The decision part of one loop iteration of Alg. 1 for every sequence.
 
@@ -377,7 +405,6 @@ def decide(logits, tok, state, params):
     tok = np.asarray(tok)
     state = np.asarray(state)
     b, B = tok.shape
-    tc, tu = params["tau_c"], params["tau_u"]
     flags = params.get("flags", 0)
     out = {k: np.zeros((b, B), dtype=np.float64) for k in
            ("w", "conf_out", "maxprob_s", "pcur_s", "maxprob_mix")}
@@ -387,7 +414,6 @@ def decide(logits, tok, state, params):
     for bi in range(b):
         xhat = np.zeros(B, dtype=np.int64)
         c = np.zeros(B)
-        nxt = np.zeros(B, dtype=np.int64)
         # confidences of C and U tokens from the shadow stream
         for i in range(B):
             a, mp, pc = confidence(logits[bi, B + i], int(tok[bi, i]))
@@ -397,36 +423,24 @@ def decide(logits, tok, state, params):
             if state[bi, i] in (STATE_C, STATE_U):
                 xhat[i] = a
                 c[i] = np.float32(pc if flags & F_VERIFY_PCUR else mp)
-        # update the C tokens; collect promoted / demoted sets
-        promoted = np.zeros(B, dtype=bool)
-        demoted = np.zeros(B, dtype=bool)
-        for i in range(B):
-            if state[bi, i] == STATE_C:
-                nxt[i] = transition(c[i], tc, tu)
-                promoted[i] = nxt[i] == STATE_U
-                demoted[i] = nxt[i] == STATE_M
+        # update the C tokens; promoted / demoted sets; weights of M tokens
+        _, _, _, w = verify_candidates(state[bi], c, params)
+        out["w"][bi] = w
         # decode the M tokens with logit mixing
-        _, _, w = guidance_weights(promoted, demoted, params["lam"], params["p0"])
         for i in range(B):
             if state[bi, i] == STATE_M:
-                wi = np.float32(w[i])
-                out["w"][bi, i] = wi
-                mixed = mix_logits(logits[bi, i], logits[bi, B + i], wi)
+                mixed = mix_logits(logits[bi, i], logits[bi, B + i], w[i])
                 a, mp, _ = confidence(mixed)
                 out["argmax_mix"][bi, i] = a
                 out["maxprob_mix"][bi, i] = np.float32(mp)
                 xhat[i] = a
                 c[i] = np.float32(mp)
-        # update the M and U tokens
-        for i in range(B):
-            if state[bi, i] in (STATE_M, STATE_U):
-                nxt[i] = transition(c[i], tc, tu)
-        # fill: M -> [Mask], C/U -> prediction
-        for i in range(B):
-            out["state_out"][bi, i] = nxt[i]
-            out["tok_out"][bi, i] = params["mask_id"] if nxt[i] == STATE_M else xhat[i]
-            out["conf_out"][bi, i] = c[i]
-        out["block_done"][bi] = int(np.all(nxt == STATE_U))
+        # transitions of all tokens (C ones repeat the rule above) and fill
+        st, tk, cf, done = finalize(c, xhat, params)
+        out["state_out"][bi] = st
+        out["tok_out"][bi] = tk
+        out["conf_out"][bi] = cf
+        out["block_done"][bi] = done
     return out
 
 

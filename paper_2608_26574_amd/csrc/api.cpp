@@ -1,0 +1,551 @@
+// C ABI of libdard (include/dard.h): argument validation, the packed weight
+// image, workspace layout and the stream-ordered orchestration of a DARD step
+// and of the prefix prefill.  No entry point synchronises the stream except
+// dard_pack_weights (a one-off) and dard_trace_read.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/dard.h"
+#include "launch.h"
+
+namespace dard {
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIPOK(expr)                                                                        \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess) return fail(DARD_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t esize(int dtype) { return dtype == DARD_DTYPE_BF16 ? 2 : 4; }
+
+int check_dims(const dard_dims* d) {
+    if (!d) return fail(DARD_ERR_ARG, "dims is NULL");
+    if (d->dtype != DARD_DTYPE_F32 && d->dtype != DARD_DTYPE_BF16)
+        return fail(DARD_ERR_ARG, "unknown dtype %d", d->dtype);
+    if (d->n_layers < 0 || d->d_model <= 0 || d->n_heads <= 0 || d->n_kv_heads <= 0 || d->ffn_dim <= 0 ||
+        d->vocab <= 1 || d->max_pos <= 0)
+        return fail(DARD_ERR_SHAPE, "non-positive model dimension");
+    if (d->head_dim != 64 && d->head_dim != 128) return fail(DARD_ERR_SHAPE, "head_dim must be 64 or 128");
+    if (d->n_heads % d->n_kv_heads) return fail(DARD_ERR_SHAPE, "n_heads %% n_kv_heads != 0");
+    if (d->n_heads * d->head_dim != d->d_model) return fail(DARD_ERR_SHAPE, "d_model != n_heads * head_dim");
+    if (d->dtype == DARD_DTYPE_BF16 && (d->d_model % 64 || d->ffn_dim % 64 || d->vocab % 16))
+        return fail(DARD_ERR_SHAPE, "bf16 needs d_model, ffn_dim %% 64 == 0 and vocab %% 16 == 0");
+    if (d->dtype == DARD_DTYPE_F32 && (d->d_model % 4 || d->ffn_dim % 4 || d->vocab % 4))
+        return fail(DARD_ERR_SHAPE, "f32 needs d_model, ffn_dim, vocab %% 4 == 0");
+    if (!(d->norm_eps >= 0.f) || !(d->rope_theta > 0.f)) return fail(DARD_ERR_ARG, "bad norm_eps / rope_theta");
+    return DARD_OK;
+}
+
+// Byte offsets of the packed weight image.
+struct Layout {
+    size_t embed, lm_head, final_norm, rope, layer0, layer_stride;
+    size_t attn_norm, wqkv, wo, ffn_norm, wgu, wdown;   // relative to the layer
+    size_t total;
+};
+
+Layout layout_of(const dard_dims* d) {
+    const size_t es = esize(d->dtype);
+    const size_t D = d->d_model, F = d->ffn_dim, V = d->vocab;
+    const size_t qd = (size_t)d->n_heads * d->head_dim, kd = (size_t)d->n_kv_heads * d->head_dim;
+    Layout L{};
+    size_t o = 0;
+    L.embed = o; o = align256(o + V * D * es);
+    L.lm_head = o; o = align256(o + V * D * es);
+    L.final_norm = o; o = align256(o + D * es);
+    L.rope = o; o = align256(o + (size_t)d->max_pos * (d->head_dim / 2) * 2 * sizeof(float));
+    L.layer0 = o;
+    size_t l = 0;
+    L.attn_norm = l; l = align256(l + D * es);
+    L.wqkv = l; l = align256(l + (qd + 2 * kd) * D * es);
+    L.wo = l; l = align256(l + D * qd * es);
+    L.ffn_norm = l; l = align256(l + D * es);
+    L.wgu = l; l = align256(l + 2 * F * D * es);
+    L.wdown = l; l = align256(l + D * F * es);
+    L.layer_stride = l;
+    L.total = o + l * d->n_layers;
+    return L;
+}
+
+// Workspace of dard_step / dard_prefill.
+struct WsLayout {
+    size_t h, xn, q, attn, act, part, part_ml, part_slots, logits, cpart_v, cpart_m, w, total;
+};
+
+WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
+    const size_t es = esize(d->dtype);
+    const size_t rows = (size_t)b * (2 * B > cap ? 2 * B : cap);
+    const size_t qd = (size_t)d->n_heads * d->head_dim;
+    const size_t step_rows = (size_t)b * 2 * B;
+    const size_t nch = conf_chunks(d->vocab);
+    WsLayout W{};
+    size_t o = 0;
+    W.h = o; o = align256(o + rows * d->d_model * 4);
+    W.xn = o; o = align256(o + rows * d->d_model * es);
+    W.q = o; o = align256(o + rows * qd * es);
+    W.attn = o; o = align256(o + rows * qd * es);
+    W.act = o; o = align256(o + rows * d->ffn_dim * es);
+    // split-key partials: room for the step's largest split (16 ways); the
+    // prefill splits only as far as this room allows
+    const size_t slots = (size_t)16 * b * 2 * B * d->n_heads;
+    W.part_slots = d->dtype == DARD_DTYPE_BF16 ? slots : 0;
+    W.part = o; o = align256(o + W.part_slots * d->head_dim * 4);
+    W.part_ml = o; o = align256(o + W.part_slots * 2 * 4);
+    W.logits = o; o = align256(o + step_rows * d->vocab * 4);
+    W.cpart_v = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
+    W.cpart_m = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
+    W.w = o; o = align256(o + (size_t)b * B * 4);
+    W.total = o;
+    return W;
+}
+
+int check_params(const dard_params* p) {
+    if (!p) return fail(DARD_ERR_ARG, "params is NULL");
+    if (!(p->tau_c >= 0.f) || !(p->tau_c <= p->tau_u) || !(p->tau_u <= 1.f))
+        return fail(DARD_ERR_ARG, "need 0 <= tau_c <= tau_u <= 1");
+    if (!(p->lambda > 0.0) || !(p->lambda < 1.0)) return fail(DARD_ERR_ARG, "need 0 < lambda < 1");
+    if (!(p->p0 > 0.0)) return fail(DARD_ERR_ARG, "need p0 > 0");
+    if (p->flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", p->flags);
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- tracing
+struct TraceRec {
+    hipEvent_t a, b;
+};
+std::mutex g_trace_mu;
+uint32_t g_trace_mask = 0;
+std::vector<TraceRec> g_trace[DARD_K_COUNT];
+
+}  // namespace
+
+TraceScope::TraceScope(int kernel_class, hipStream_t s) : cls(kernel_class), st(s), ev0(nullptr) {
+    if (!(g_trace_mask & (1u << cls))) return;
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    hipEventRecord(e, st);
+    ev0 = e;
+}
+
+TraceScope::~TraceScope() {
+    if (!ev0) return;
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    hipEventRecord(e, st);
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    g_trace[cls].push_back({(hipEvent_t)ev0, e});
+}
+
+}  // namespace dard
+
+using namespace dard;
+
+extern "C" {
+
+const char* dard_last_error(void) { return g_err.c_str(); }
+int dard_version(void) { return 1; }
+
+// ---------------------------------------------------------------- mask
+dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b, int B, uint32_t flags,
+                                  uint64_t* sel, void* stream) {
+    if (!state || !conf || !sel) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
+    if (flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", flags);
+    HIPOK(launch_build_state_mask(state, conf, b, B, flags, sel, (hipStream_t)stream));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- attention
+size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P) {
+    if (b < 1 || B < 1 || Hq < 1 || P < 0) return 0;
+    const size_t slots = attention_partial_slots(dtype, b, 2 * B, Hq, P + 2 * B);
+    if (slots == 0) return 0;
+    // + 64 slots of slack for the alignment of the (m, l) array
+    return (slots + 64) * ((size_t)dh * 4 + 8);
+}
+
+dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v, int P, int cap,
+                                  const uint8_t* state, const float* conf, int b, int B, int Hq, int Hkv, int dh,
+                                  float scale, uint32_t flags, void* out, void* ws, size_t ws_bytes,
+                                  void* stream) {
+    if (!q || !k || !v || !state || !conf || !out) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
+    if (flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", flags);
+    if (b < 1 || B < 1 || B > 128 || P < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || P + 2 * B > cap)
+        return fail(DARD_ERR_SHAPE, "bad attention shape (b=%d B=%d P=%d cap=%d Hq=%d Hkv=%d)", b, B, P, cap, Hq, Hkv);
+    if (dh != 64 && dh != 128) return fail(DARD_ERR_SHAPE, "dh must be 64 or 128");
+    const size_t need = dard_attention_workspace_bytes(dtype, b, B, Hq, dh, P);
+    if (need && (!ws || ws_bytes < need)) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", need);
+    AttnArgs a{};
+    a.q = q; a.k = k; a.v = v; a.out = out; a.state = state; a.conf = conf;
+    a.b = b; a.R = 2 * B; a.Hq = Hq; a.Hkv = Hkv; a.dh = dh; a.cap = cap;
+    a.P = P; a.B = B; a.nkeys = P + 2 * B; a.masked = 1; a.scale = scale; a.flags = flags;
+    // as many partial slots as the given workspace holds
+    const size_t slots = ws ? ws_bytes / ((size_t)dh * 4 + 8) : 0;
+    a.part_slots = slots > 64 ? slots - 64 : 0;
+    a.part = (float*)ws;
+    a.part_ml = ws ? (float*)((char*)ws + align256(a.part_slots * dh * 4)) : nullptr;
+    TraceScope ts(DARD_K_ATTENTION, (hipStream_t)stream);
+    HIPOK(launch_attention(dtype, a, (hipStream_t)stream));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- confidence
+size_t dard_confidence_workspace_bytes(int rows, int V) {
+    if (rows < 1 || V < 1) return 0;
+    return align256((size_t)rows * conf_chunks(V) * 3 * 4);
+}
+
+dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w, const int32_t* cur_tok,
+                            int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur, void* ws,
+                            size_t ws_bytes, void* stream) {
+    if (!logits_s || !argmax || !maxprob) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (logits_x && !w) return fail(DARD_ERR_ARG, "mixing needs w");
+    if (pcur && (!cur_tok || logits_x)) return fail(DARD_ERR_ARG, "pcur needs cur_tok and no mixing");
+    if (rows < 1 || V < 1 || ld < V || ld % 4) return fail(DARD_ERR_SHAPE, "need rows, V >= 1, ld >= V, ld %% 4 == 0");
+    const size_t need = dard_confidence_workspace_bytes(rows, V);
+    if (!ws || ws_bytes < need) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", need);
+    ConfArgs a{};
+    a.ls = logits_s; a.lx = logits_x; a.w = w; a.ld_s = ld; a.ld_x = ld;
+    a.rows = rows; a.V = V; a.part = (float*)ws; a.state = nullptr; a.phase = 0; a.step_B = 0;
+    hipStream_t s = (hipStream_t)stream;
+    HIPOK(launch_conf_partial(a, s));
+    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), logits_s, ld, cur_tok, argmax, maxprob, pcur, s));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- decisions
+dard_status dard_commit_remask(int phase, const dard_params* params, int b, int B, const uint8_t* state_in,
+                               const float* maxprob_s, const float* pcur_s, const int32_t* argmax_s,
+                               const float* maxprob_mix, const int32_t* argmax_mix, float* w_out,
+                               uint8_t* state_out, int32_t* tok_out, float* conf_out, int32_t* block_done,
+                               void* stream) {
+    int rc = check_params(params);
+    if (rc) return rc;
+    if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
+    const bool pcur_mode = params->flags & DARD_F_VERIFY_PCUR;
+    if (!state_in) return fail(DARD_ERR_ARG, "NULL state_in");
+    if (phase == DARD_PHASE_VERIFY) {
+        if (!w_out || (pcur_mode ? !pcur_s : !maxprob_s)) return fail(DARD_ERR_ARG, "VERIFY needs w_out and c");
+    } else if (phase == DARD_PHASE_FINAL) {
+        if (!maxprob_s || !argmax_s || !maxprob_mix || !argmax_mix || !state_out || !tok_out || !conf_out ||
+            (pcur_mode && !pcur_s))
+            return fail(DARD_ERR_ARG, "FINAL needs confidences, predictions and outputs");
+    } else {
+        return fail(DARD_ERR_ARG, "unknown phase %d", phase);
+    }
+    DecideArgs a{};
+    a.phase = phase; a.b = b; a.B = B;
+    a.tau_c = params->tau_c; a.tau_u = params->tau_u; a.lambda = params->lambda; a.p0 = params->p0;
+    a.mask_id = params->mask_id; a.flags = params->flags;
+    a.state_in = state_in;
+    a.maxprob_s = maxprob_s; a.pcur_s = pcur_s; a.argmax_s = argmax_s;
+    a.maxprob_mix = maxprob_mix; a.argmax_mix = argmax_mix;
+    a.w_out = w_out; a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out;
+    a.block_done = block_done;
+    HIPOK(launch_decide(a, (hipStream_t)stream));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- weights / KV
+size_t dard_packed_weight_bytes(const dard_dims* dims) {
+    if (check_dims(dims)) return 0;
+    return layout_of(dims).total;
+}
+
+size_t dard_kv_bytes(const dard_dims* d, int b, int cap) {
+    if (check_dims(d) || b < 1 || cap < 1) return 0;
+    return (size_t)d->n_layers * 2 * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+}
+
+dard_status dard_pack_weights(const dard_dims* d, const void* const* src, int n_src, void* packed,
+                              size_t packed_bytes, void* stream) {
+    int rc = check_dims(d);
+    if (rc) return rc;
+    if (!src || !packed) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (n_src != 3 + 9 * d->n_layers) return fail(DARD_ERR_ARG, "expected %d weight pointers", 3 + 9 * d->n_layers);
+    for (int i = 0; i < n_src; ++i)
+        if (!src[i]) return fail(DARD_ERR_ARG, "weight pointer %d is NULL", i);
+    const Layout L = layout_of(d);
+    if (packed_bytes < L.total) return fail(DARD_ERR_WORKSPACE, "packed image needs %zu bytes", L.total);
+    hipStream_t s = (hipStream_t)stream;
+    const size_t es = esize(d->dtype);
+    const int D = d->d_model, F = d->ffn_dim, V = d->vocab, dh = d->head_dim;
+    const int qd = d->n_heads * dh, kd = d->n_kv_heads * dh;
+    char* P = (char*)packed;
+    const int rowD = (int)(D * es), rowF = (int)(F * es);
+    if (rowD % 16 || rowF % 16) return fail(DARD_ERR_SHAPE, "weight rows must be multiples of 16 bytes");
+    HIPOK(launch_pack_rows(src[0], nullptr, P + L.embed, V, rowD, 0, dh, s));
+    for (int l = 0; l < d->n_layers; ++l) {
+        const void* const* w = src + 1 + 9 * l;
+        char* base = P + L.layer0 + L.layer_stride * l;
+        HIPOK(launch_copy_rows(w[0], base + L.attn_norm, D * es, s));
+        HIPOK(launch_pack_rows(w[1], nullptr, base + L.wqkv, qd, rowD, 1, dh, s));
+        HIPOK(launch_pack_rows(w[2], nullptr, base + L.wqkv + (size_t)qd * rowD, kd, rowD, 1, dh, s));
+        HIPOK(launch_pack_rows(w[3], nullptr, base + L.wqkv + (size_t)(qd + kd) * rowD, kd, rowD, 0, dh, s));
+        HIPOK(launch_pack_rows(w[4], nullptr, base + L.wo, D, (int)(qd * es), 0, dh, s));
+        HIPOK(launch_copy_rows(w[5], base + L.ffn_norm, D * es, s));
+        HIPOK(launch_pack_rows(w[6], w[7], base + L.wgu, 2 * F, rowD, 2, dh, s));
+        HIPOK(launch_pack_rows(w[8], nullptr, base + L.wdown, D, rowF, 0, dh, s));
+    }
+    HIPOK(launch_copy_rows(src[1 + 9 * d->n_layers], P + L.final_norm, D * es, s));
+    HIPOK(launch_pack_rows(src[2 + 9 * d->n_layers], nullptr, P + L.lm_head, V, rowD, 0, dh, s));
+    // small norm vectors may not be a multiple of 16 bytes: copy the tail
+    if ((D * es) % 16) {
+        const size_t tail = (D * es) % 16, off = D * es - tail;
+        for (int l = 0; l < d->n_layers; ++l) {
+            const void* const* w = src + 1 + 9 * l;
+            char* base = P + L.layer0 + L.layer_stride * l;
+            HIPOK(hipMemcpyAsync(base + L.attn_norm + off, (const char*)w[0] + off, tail, hipMemcpyDeviceToDevice, s));
+            HIPOK(hipMemcpyAsync(base + L.ffn_norm + off, (const char*)w[5] + off, tail, hipMemcpyDeviceToDevice, s));
+        }
+        HIPOK(hipMemcpyAsync(P + L.final_norm + off, (const char*)src[1 + 9 * d->n_layers] + off, tail,
+                             hipMemcpyDeviceToDevice, s));
+    }
+    // rotary table: cos / sin of pos * theta^(-2t/dh), built in double precision
+    std::vector<float> rope((size_t)d->max_pos * (dh / 2) * 2);
+    for (int pos = 0; pos < d->max_pos; ++pos)
+        for (int t = 0; t < dh / 2; ++t) {
+            const double ang = (double)pos * std::pow((double)d->rope_theta, -2.0 * t / dh);
+            rope[((size_t)pos * (dh / 2) + t) * 2] = (float)std::cos(ang);
+            rope[((size_t)pos * (dh / 2) + t) * 2 + 1] = (float)std::sin(ang);
+        }
+    HIPOK(hipMemcpyAsync(P + L.rope, rope.data(), rope.size() * sizeof(float), hipMemcpyHostToDevice, s));
+    HIPOK(hipStreamSynchronize(s));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- forward
+size_t dard_workspace_bytes(const dard_dims* d, int b, int B, int cap) {
+    if (check_dims(d) || b < 1 || B < 1 || B > 128 || cap < 2 * B) return 0;
+    return ws_layout(d, b, B, cap).total;
+}
+
+namespace {
+
+struct Fwd {
+    const dard_dims* d;
+    Layout L;
+    WsLayout W;
+    const char* pk;
+    char* kv;
+    char* ws;
+    int b, cap;
+    hipStream_t s;
+
+    const void* layer(int l, size_t off) const { return pk + L.layer0 + L.layer_stride * l + off; }
+    void* kc(int l) const {
+        return kv + (size_t)(2 * l) * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+    }
+    void* vc(int l) const {
+        return kv + (size_t)(2 * l + 1) * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+    }
+};
+
+// The transformer layers over `rows` token rows (R per sequence).  step != 0:
+// the rows are the augmented block (x then s) of block length B after P
+// cached keys, attention under the state mask; step == 0: the rows are the P
+// prefix tokens, attention bidirectional among them.
+int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state, const float* conf,
+               uint32_t flags) {
+    const dard_dims* d = f.d;
+    const int dt = d->dtype;
+    const int rows = f.b * R;
+    const int D = d->d_model, F = d->ffn_dim, dh = d->head_dim;
+    const int qd = d->n_heads * dh, kd = d->n_kv_heads * dh;
+    float* h = (float*)(f.ws + f.W.h);
+    void* xn = f.ws + f.W.xn;
+    void* q = f.ws + f.W.q;
+    void* at = f.ws + f.W.attn;
+    void* act = f.ws + f.W.act;
+    for (int l = 0; l < d->n_layers; ++l) {
+        EpiArgs e{};
+        e.kind = EPI_QKV; e.q = q; e.ldq = qd; e.kc = f.kc(l); e.vc = f.vc(l);
+        e.rope = (const float*)(f.pk + f.L.rope);
+        e.rows_per_seq = R; e.P = P; e.B = B; e.cap = f.cap; e.Hq = d->n_heads; e.Hkv = d->n_kv_heads; e.dh = dh;
+        e.step = step;
+        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wqkv), qd + 2 * kd, e, DARD_K_GEMM_QKV, f.s));
+
+        AttnArgs a{};
+        a.q = q; a.k = f.kc(l); a.v = f.vc(l); a.out = at; a.state = state; a.conf = conf;
+        a.b = f.b; a.R = R; a.Hq = d->n_heads; a.Hkv = d->n_kv_heads; a.dh = dh; a.cap = f.cap;
+        a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step; a.scale = 1.f / std::sqrt((float)dh);
+        a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
+        a.part_slots = f.W.part_slots;
+        {
+            TraceScope ts(DARD_K_ATTENTION, f.s);
+            HIPOK(launch_attention(dt, a, f.s));
+        }
+        EpiArgs r{};
+        r.kind = EPI_RESID; r.y = h; r.ldy = D;
+        HIPOK(launch_gemm(dt, at, rows, qd, qd, f.layer(l, f.L.wo), D, r, DARD_K_GEMM_O, f.s));
+        HIPOK(launch_rmsnorm(dt, h, f.layer(l, f.L.ffn_norm), rows, D, d->norm_eps, xn, f.s));
+        EpiArgs g{};
+        g.kind = EPI_SWIGLU; g.act = act; g.ld_act = F;
+        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wgu), 2 * F, g, DARD_K_GEMM_GU, f.s));
+        HIPOK(launch_gemm(dt, act, rows, F, F, f.layer(l, f.L.wdown), D, r, DARD_K_GEMM_DOWN, f.s));
+        const void* gain = l + 1 < d->n_layers ? f.layer(l + 1, f.L.attn_norm) : f.pk + f.L.final_norm;
+        HIPOK(launch_rmsnorm(dt, h, gain, rows, D, d->norm_eps, xn, f.s));
+    }
+    return DARD_OK;
+}
+
+int fwd_setup(Fwd& f, const dard_dims* d, const void* packed, void* kv, int cap, int b, int B, void* ws,
+              size_t ws_bytes, void* stream) {
+    int rc = check_dims(d);
+    if (rc) return rc;
+    if (!packed || !kv || !ws) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (b < 1 || B < 1 || B > 128 || cap < 2 * B) return fail(DARD_ERR_SHAPE, "need b >= 1, 1 <= B <= 128, cap >= 2B");
+    f.d = d; f.L = layout_of(d); f.W = ws_layout(d, b, B, cap);
+    if (ws_bytes < f.W.total) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", f.W.total);
+    f.pk = (const char*)packed; f.kv = (char*)kv; f.ws = (char*)ws; f.b = b; f.cap = cap;
+    f.s = (hipStream_t)stream;
+    return DARD_OK;
+}
+
+}  // namespace
+
+dard_status dard_prefill(const dard_dims* d, const void* packed, void* kv, int cap, int b, int P, const int32_t* ids,
+                         const void* embeds, void* ws, size_t ws_bytes, void* stream) {
+    Fwd f;
+    // the workspace is sized for (b, B, cap); prefill rows b*P fit because P <= cap
+    int rc = check_dims(d);
+    if (rc) return rc;
+    if (!ids) return fail(DARD_ERR_ARG, "NULL ids");
+    if (P < 1 || P > cap || P > d->max_pos) return fail(DARD_ERR_SHAPE, "need 1 <= P <= min(cap, max_pos)");
+    rc = fwd_setup(f, d, packed, kv, cap, b, 1, ws, ws_bytes, stream);
+    if (rc) return rc;
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    HIPOK(launch_embed_norm(d->dtype, ids, embeds, f.pk + f.L.embed, gain0, b * P, d->d_model, d->vocab, d->norm_eps, 0, 0,
+                            (float*)(f.ws + f.W.h), f.ws + f.W.xn, f.s));
+    return run_layers(f, P, P, 0, 0, nullptr, nullptr, 0);
+}
+
+dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap, int P, const dard_params* params,
+                      int b, int B, const int32_t* tok_in, const uint8_t* state_in, const float* conf_in,
+                      int32_t* tok_out, uint8_t* state_out, float* conf_out, int32_t* block_done,
+                      const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
+    if (rc) return rc;
+    rc = check_params(params);
+    if (rc) return rc;
+    if (!tok_in || !state_in || !conf_in || !tok_out || !state_out || !conf_out)
+        return fail(DARD_ERR_ARG, "NULL pointer");
+    if (P < 0 || P + 2 * B > cap || P + B > d->max_pos)
+        return fail(DARD_ERR_SHAPE, "need P >= 0, P + 2B <= cap, P + B <= max_pos");
+    if (params->mask_id < 0 || params->mask_id >= d->vocab) return fail(DARD_ERR_ARG, "mask_id outside the vocab");
+    const int R = 2 * B, rows = b * R, V = d->vocab;
+    float* logits = (float*)(f.ws + f.W.logits);
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
+                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, f.s));
+    rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags);
+    if (rc) return rc;
+    EpiArgs e{};
+    e.kind = EPI_STORE_F32; e.y = logits; e.ldy = V;
+    HIPOK(launch_gemm(d->dtype, f.ws + f.W.xn, rows, d->d_model, d->d_model, f.pk + f.L.lm_head, V, e,
+                      DARD_K_GEMM_HEAD, f.s));
+
+    ConfArgs c{};
+    c.ls = logits; c.ld_s = V; c.ld_x = V; c.rows = b * B; c.V = V; c.state = state_in; c.step_B = B;
+    c.phase = 0; c.part = (float*)(f.ws + f.W.cpart_v);
+    HIPOK(launch_conf_partial(c, f.s));
+
+    DecideArgs a{};
+    a.b = b; a.B = B; a.tau_c = params->tau_c; a.tau_u = params->tau_u; a.lambda = params->lambda;
+    a.p0 = params->p0; a.mask_id = params->mask_id; a.flags = params->flags;
+    a.state_in = state_in; a.tok_in = tok_in;
+    a.part_v = (const float*)(f.ws + f.W.cpart_v); a.part_m = (const float*)(f.ws + f.W.cpart_m);
+    a.logits = logits; a.ld = V; a.nchunk = conf_chunks(V);
+    a.w_out = (float*)(f.ws + f.W.w);
+    a.phase = DARD_PHASE_VERIFY;
+    HIPOK(launch_decide(a, f.s));
+
+    c.phase = 1; c.w = (const float*)(f.ws + f.W.w); c.part = (float*)(f.ws + f.W.cpart_m);
+    HIPOK(launch_conf_partial(c, f.s));
+
+    a.phase = DARD_PHASE_FINAL;
+    a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out; a.block_done = block_done;
+    if (dbg) {
+        a.dbg_maxprob_s = dbg->maxprob_s; a.dbg_argmax_s = dbg->argmax_s; a.dbg_pcur_s = dbg->pcur_s;
+        a.dbg_maxprob_mix = dbg->maxprob_mix; a.dbg_argmax_mix = dbg->argmax_mix;
+    }
+    HIPOK(launch_decide(a, f.s));
+    if (dbg && dbg->logits)
+        HIPOK(hipMemcpyAsync(dbg->logits, logits, (size_t)rows * V * 4, hipMemcpyDeviceToDevice, f.s));
+    if (dbg && dbg->w)
+        HIPOK(hipMemcpyAsync(dbg->w, f.ws + f.W.w, (size_t)b * B * 4, hipMemcpyDeviceToDevice, f.s));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- linear
+dard_status dard_linear(int dtype, const void* X, int M, int K, const void* W, int N, float* Y, void* stream) {
+    if (!X || !W || !Y) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
+    if (M < 1 || N < 1 || K < 1) return fail(DARD_ERR_SHAPE, "need M, N, K >= 1");
+    if (dtype == DARD_DTYPE_BF16 && (K % 64 || N % 16)) return fail(DARD_ERR_SHAPE, "bf16 needs K %% 64 == 0, N %% 16 == 0");
+    if (dtype == DARD_DTYPE_F32 && N % 4) return fail(DARD_ERR_SHAPE, "f32 needs N %% 4 == 0");
+    EpiArgs e{};
+    e.kind = EPI_STORE_F32; e.y = Y; e.ldy = N;
+    HIPOK(launch_gemm(dtype, X, M, K, K, W, N, e, DARD_K_GEMM_HEAD, (hipStream_t)stream));
+    return DARD_OK;
+}
+
+// ---------------------------------------------------------------- tracing
+dard_status dard_trace_enable(uint32_t class_mask) {
+    g_trace_mask = class_mask;
+    return DARD_OK;
+}
+
+dard_status dard_trace_read(int cls, int64_t* launches, double* total_ms) {
+    if (cls < 0 || cls >= DARD_K_COUNT || !launches || !total_ms) return fail(DARD_ERR_ARG, "bad trace query");
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    double sum = 0.0;
+    for (auto& r : g_trace[cls]) {
+        HIPOK(hipEventSynchronize(r.b));
+        float ms = 0.f;
+        HIPOK(hipEventElapsedTime(&ms, r.a, r.b));
+        sum += ms;
+    }
+    *launches = (int64_t)g_trace[cls].size();
+    *total_ms = sum;
+    return DARD_OK;
+}
+
+dard_status dard_trace_reset(void) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    for (auto& v : g_trace) {
+        for (auto& r : v) {
+            hipEventSynchronize(r.b);
+            hipEventDestroy(r.a);
+            hipEventDestroy(r.b);
+        }
+        v.clear();
+    }
+    return DARD_OK;
+}
+
+}  // extern "C"

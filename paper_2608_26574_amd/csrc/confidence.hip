@@ -1,0 +1,169 @@
+// Vocab-wide confidence reduction (Eq. 1) with optional logit mixing (Eq. 7).
+//
+// A row of V float32 logits is cut into chunks of 8192; one 256-thread
+// workgroup reduces one chunk with 16-byte loads into a partial
+// (max, first argmax, sum of exp(l - max)), so that even a single step's few
+// rows fill the chip.  Partials are merged in chunk order, which keeps the
+// result independent of scheduling.  Mixed rows are formed on the fly,
+// (w * l_x) + ((1 - w) * l_s) with every operation rounded once in fp32.
+#include "common.h"
+#include "launch.h"
+
+namespace dard {
+
+namespace {
+
+constexpr int kChunk = 8192;
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct Acc {
+    float m;
+    int a;
+    float s;
+};
+
+// Merge two partials; the larger maximum wins, ties go to the lower index.
+__device__ __forceinline__ Acc merge(Acc x, Acc y) {
+    Acc r;
+    const bool take_y = (y.m > x.m) || (y.m == x.m && y.a < x.a);
+    r.a = take_y ? y.a : x.a;
+    r.m = fmaxf(x.m, y.m);
+    const float sx = x.m == -INFINITY ? 0.f : x.s * exp2f((x.m - r.m) * kLog2e);
+    const float sy = y.m == -INFINITY ? 0.f : y.s * exp2f((y.m - r.m) * kLog2e);
+    r.s = sx + sy;
+    return r;
+}
+
+__device__ __forceinline__ float mixv(float x, float s, float w, float omw) {
+    return __fadd_rn(__fmul_rn(w, x), __fmul_rn(omw, s));
+}
+
+__global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_B) {
+    const int row = blockIdx.x, ch = blockIdx.y;
+    const float* ls;
+    const float* lx = nullptr;
+    float w = 0.f;
+    if (step_B > 0) {
+        // rows are block positions; logits hold [b][2B][V] (x rows then s rows)
+        const int st = a.state[row];
+        if (a.phase == 0 ? st != DARD_STATE_C : st == DARD_STATE_C) return;
+        const int s = row / step_B, i = row % step_B;
+        ls = a.ls + ((size_t)s * 2 * step_B + step_B + i) * a.ld_s;
+        if (a.phase == 1 && st == DARD_STATE_M) {
+            lx = a.ls + ((size_t)s * 2 * step_B + i) * a.ld_s;
+            w = a.w[row];
+        }
+    } else {
+        ls = a.ls + (size_t)row * a.ld_s;
+        if (a.lx) {
+            lx = a.lx + (size_t)row * a.ld_x;
+            w = a.w[row];
+        }
+    }
+    const float omw = __fsub_rn(1.f, w);
+    const bool use_x = lx != nullptr && w != 0.f;
+    const bool use_s = !(lx != nullptr && w == 1.f);
+
+    const int begin = ch * a.chunk;
+    const int end = min(a.V, begin + a.chunk);
+    Acc acc{-INFINITY, 0x7fffffff, 0.f};
+    for (int i = begin + 4 * threadIdx.x; i < end; i += 4 * 256) {
+        float v[4];
+        if (i + 4 <= end) {
+            const float4 sv = use_s ? *reinterpret_cast<const float4*>(ls + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            if (use_x) {
+                const float4 xv = *reinterpret_cast<const float4*>(lx + i);
+                if (use_s) {
+                    v[0] = mixv(xv.x, sv.x, w, omw); v[1] = mixv(xv.y, sv.y, w, omw);
+                    v[2] = mixv(xv.z, sv.z, w, omw); v[3] = mixv(xv.w, sv.w, w, omw);
+                } else {
+                    v[0] = xv.x; v[1] = xv.y; v[2] = xv.z; v[3] = xv.w;
+                }
+            } else {
+                v[0] = sv.x; v[1] = sv.y; v[2] = sv.z; v[3] = sv.w;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if (i + k < end) {
+                    const float sv = use_s ? ls[i + k] : 0.f;
+                    v[k] = use_x ? (use_s ? mixv(lx[i + k], sv, w, omw) : lx[i + k]) : sv;
+                } else {
+                    v[k] = -INFINITY;
+                }
+            }
+        }
+        float lm = v[0];
+        int li = 0;
+#pragma unroll
+        for (int k = 1; k < 4; ++k)
+            if (v[k] > lm) { lm = v[k]; li = k; }
+        if (lm > acc.m) {
+            acc.s = acc.m == -INFINITY ? 0.f : acc.s * exp2f((acc.m - lm) * kLog2e);
+            acc.m = lm;
+            acc.a = i + li;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc.s += exp2f((v[k] - acc.m) * kLog2e);
+    }
+    // wave reduction then across the 4 waves, fixed order
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        Acc y{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.a, o, 64), __shfl_xor(acc.s, o, 64)};
+        acc = merge(acc, y);
+    }
+    __shared__ Acc red[4];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) red[wave] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        Acc t = red[0];
+        for (int k = 1; k < 4; ++k) t = merge(t, red[k]);
+        float* p = a.part + ((size_t)row * a.nchunk + ch) * 3;
+        p[0] = t.m;
+        p[1] = __int_as_float(t.a);
+        p[2] = t.s;
+    }
+}
+
+__global__ void conf_combine_kernel(const float* __restrict__ part, int rows, int nchunk,
+                                    const float* __restrict__ ls, int64_t ld, const int32_t* __restrict__ cur,
+                                    int32_t* __restrict__ argmax, float* __restrict__ maxprob,
+                                    float* __restrict__ pcur) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    const float* p = part + (size_t)r * nchunk * 3;
+    Acc t{p[0], __float_as_int(p[1]), p[2]};
+    for (int c = 1; c < nchunk; ++c) t = merge(t, Acc{p[3 * c], __float_as_int(p[3 * c + 1]), p[3 * c + 2]});
+    argmax[r] = t.a;
+    maxprob[r] = 1.f / t.s;
+    if (pcur) {
+        const float lc = ls[(size_t)r * ld + cur[r]];
+        pcur[r] = exp2f((lc - t.m) * kLog2e) / t.s;
+    }
+}
+
+}  // namespace
+
+int conf_chunks(int V) { return (V + kChunk - 1) / kChunk; }
+
+hipError_t launch_conf_partial(const ConfArgs& a, hipStream_t s) {
+    TraceScope ts(DARD_K_CONFIDENCE, s);
+    ConfArgs b = a;
+    b.chunk = kChunk;
+    b.nchunk = conf_chunks(a.V);
+    const int step_B = a.step_B;
+    hipLaunchKernelGGL(conf_partial_kernel, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
+    return hipGetLastError();
+}
+
+hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls, int64_t ld,
+                               const int32_t* cur_tok, int32_t* argmax, float* maxprob, float* pcur,
+                               hipStream_t s) {
+    TraceScope ts(DARD_K_CONFIDENCE, s);
+    hipLaunchKernelGGL(conf_combine_kernel, dim3((rows + 127) / 128), dim3(128), 0, s, part, rows, nchunk, ls,
+                       ld, cur_tok, argmax, maxprob, pcur);
+    return hipGetLastError();
+}
+
+}  // namespace dard

@@ -1,0 +1,134 @@
+// Row-wise kernels: embedding gather of the augmented block / prefix with the
+// first RMSNorm fused, the RMSNorm between sub-layers, and the row copies
+// used to pack the weight image.
+#include "common.h"
+#include "launch.h"
+
+namespace dard {
+
+namespace {
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float t = 0.f;
+    const int nw = blockDim.x >> 6;
+    for (int i = 0; i < nw; ++i) t += red[i];
+    __syncthreads();
+    return t;
+}
+
+// y = h / sqrt(mean(h^2) + eps) * gain, rounded to T.
+template <typename T>
+__device__ void norm_row(const float* h, const T* gain, int d, float eps, T* out, float* red) {
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) ss += h[c] * h[c];
+    ss = block_sum(ss, red);
+    const float inv = rsqrtf(ss / (float)d + eps);
+    for (int c = threadIdx.x; c < d; c += blockDim.x) St<T>::st(out + c, h[c] * inv * St<T>::ld(gain + c));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_norm_kernel(const int32_t* __restrict__ ids, const T* __restrict__ embeds,
+                                                         const T* __restrict__ table, const T* __restrict__ gain,
+                                                         int d, int vocab, float eps, int step_B, int mask_id,
+                                                         float* __restrict__ h, T* __restrict__ xn) {
+    __shared__ float red[8];
+    const size_t row = blockIdx.x;
+    int id;
+    if (step_B > 0) {
+        const int s = row / (2 * step_B), r = row % (2 * step_B);
+        id = r < step_B ? ids[(size_t)s * step_B + r] : mask_id;
+    } else {
+        id = ids[row];
+    }
+    // ids are device data: keep every read inside its table
+    if (id >= vocab || (id < 0 && embeds == nullptr)) id = id < 0 ? 0 : vocab - 1;
+    const T* src = id >= 0 ? table + (size_t)id * d : embeds + row * d;
+    float* hr = h + row * d;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) hr[c] = St<T>::ld(src + c);
+    __syncthreads();
+    norm_row<T>(hr, gain, d, eps, xn + row * d, red);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, const T* __restrict__ gain, int d,
+                                                      float eps, T* __restrict__ xn) {
+    __shared__ float red[8];
+    const size_t row = blockIdx.x;
+    norm_row<T>(h + row * d, gain, d, eps, xn + row * d, red);
+}
+
+__global__ void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t n16) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+// Packed weight rows.  mode 0: identity; mode 1: per head of `dh` rows, packed
+// row 2t <- row t and 2t+1 <- row t + dh/2 (rotary pairs adjacent); mode 2:
+// packed row 2t <- row t of src0 (gate), 2t+1 <- row t of src1 (up).
+__global__ void pack_rows_kernel(const uint8_t* __restrict__ src0, const uint8_t* __restrict__ src1,
+                                 uint8_t* __restrict__ dst, int nrows, int rowbytes, int mode, int dh) {
+    const int rd = blockIdx.x;
+    if (rd >= nrows) return;
+    const uint8_t* src;
+    if (mode == 1) {
+        const int head = rd / dh, e = rd % dh, t = e / 2;
+        src = src0 + (size_t)(head * dh + ((e & 1) ? t + dh / 2 : t)) * rowbytes;
+    } else if (mode == 2) {
+        src = ((rd & 1) ? src1 : src0) + (size_t)(rd / 2) * rowbytes;
+    } else {
+        src = src0 + (size_t)rd * rowbytes;
+    }
+    const uint4* s4 = reinterpret_cast<const uint4*>(src);
+    uint4* d4 = reinterpret_cast<uint4*>(dst + (size_t)rd * rowbytes);
+    for (int i = threadIdx.x; i < rowbytes / 16; i += blockDim.x) d4[i] = s4[i];
+}
+
+}  // namespace
+
+hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
+                            int dh, hipStream_t s) {
+    hipLaunchKernelGGL(pack_rows_kernel, dim3(nrows), dim3(128), 0, s, (const uint8_t*)src0,
+                       (const uint8_t*)src1, (uint8_t*)dst, nrows, rowbytes, mode, dh);
+    return hipGetLastError();
+}
+
+hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds, const void* table,
+                             const void* gain, int rows, int d, int vocab, float eps, int step_B,
+                             int mask_id, float* h, void* xn, hipStream_t s) {
+    TraceScope ts(DARD_K_NORM, s);
+    if (dtype == DARD_DTYPE_BF16)
+        hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, ids,
+                           (const bf16_t*)embeds, (const bf16_t*)table, (const bf16_t*)gain, d, vocab, eps, step_B,
+                           mask_id, h, (bf16_t*)xn);
+    else
+        hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, ids, (const float*)embeds,
+                           (const float*)table, (const float*)gain, d, vocab, eps, step_B, mask_id, h, (float*)xn);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, int rows, int d, float eps, void* xn,
+                          hipStream_t s) {
+    TraceScope ts(DARD_K_NORM, s);
+    if (dtype == DARD_DTYPE_BF16)
+        hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, (const bf16_t*)gain, d, eps,
+                           (bf16_t*)xn);
+    else
+        hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, h, (const float*)gain, d, eps,
+                           (float*)xn);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_t s) {
+    const size_t n16 = bytes / 16;
+    if (n16 == 0) return hipSuccess;
+    const size_t blocks = (n16 + 255) / 256;
+    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s,
+                       (const uint4*)src, (uint4*)dst, n16);
+    return hipGetLastError();
+}
+
+}  // namespace dard

@@ -1,0 +1,126 @@
+// Host-side launchers of the libdard kernels (internal interface between the
+// C ABI in api.cpp and the kernel translation units).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dard {
+
+// ---- mask.hip
+hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
+                                   uint32_t flags, uint64_t* sel, hipStream_t s);
+
+// ---- attention.hip
+struct AttnArgs {
+    const void* q;      // [b][R][Hq][dh]
+    const void* k;      // [b][Hkv][cap][dh]
+    const void* v;
+    void* out;          // [b][R][Hq][dh]
+    const uint8_t* state;  // [b][B] (masked mode)
+    const float* conf;     // [b][B]
+    int b, R, Hq, Hkv, dh, cap;
+    int P;              // prefix keys (always visible)
+    int B;              // block length (masked mode); keys = P + 2B
+    int nkeys;          // total keys per sequence
+    int masked;         // 1: state-specific mask on keys >= P; 0: all visible
+    float scale;
+    uint32_t flags;
+    float* part;        // split partials [nsplit][b][R][Hq][dh] fp32
+    float* part_ml;     // [nsplit][b][R][Hq][2]
+    size_t part_slots;  // capacity of part / part_ml in (split, row, head) slots
+};
+// Key splits the launcher uses for these sizes with `slots` partial slots.
+int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots);
+// Partial slots the launcher would like (0 = no split).
+size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys);
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
+
+// ---- gemm.hip
+enum EpiKind { EPI_STORE_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+struct EpiArgs {
+    int kind;
+    float* y;  int ldy;             // STORE_F32 / RESID (fp32, RESID adds)
+    void* act; int ld_act;          // SWIGLU output (dtype), columns N/2
+    // QKV
+    void* q; int ldq;               // [rows][Hq*dh]
+    void* kc; void* vc;             // cache base of this layer: [b][Hkv][cap][dh]
+    const float* rope;              // [max_pos][dh/2][2] (cos, sin)
+    int rows_per_seq;               // R
+    int P, B, cap, Hq, Hkv, dh;
+    int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r
+};
+// Y = X * W^T with X [M][K] (leading dim ldx), W [N][K]; epilogue per `e`.
+hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
+                       const EpiArgs& e, int kernel_class, hipStream_t s);
+
+// ---- elementwise.hip
+// h[row] = embedding of ids[row] (or embeds[row] when ids[row] < 0), then
+// xn[row] = RMSNorm(h[row]) * gain.  When step_B > 0 the rows are the
+// augmented block: row r of sequence s embeds tok[s][r] for r < B and mask_id
+// for r >= B.
+hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds,
+                             const void* table, const void* gain, int rows, int d, int vocab,
+                             float eps, int step_B, int mask_id, float* h, void* xn,
+                             hipStream_t s);
+hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, int rows, int d,
+                          float eps, void* xn, hipStream_t s);
+hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
+                            int dh, hipStream_t s);
+
+// ---- confidence.hip
+struct ConfArgs {
+    const float* ls;       // shadow / plain rows
+    const float* lx;       // x rows or NULL
+    const float* w;        // per-row weight or NULL
+    int64_t ld_s, ld_x;    // row strides (elements)
+    int rows, V, nchunk, chunk;
+    float* part;           // [rows][nchunk][3]: max, argmax (as int bits), sum
+    // step mode: skip rows by state (phase 0: only C rows; phase 1: only M/U)
+    const uint8_t* state;  // [rows] or NULL
+    int phase;
+    int step_B;            // >0: rows are block positions of [b][2B][V] logits
+};
+int conf_chunks(int V);
+hipError_t launch_conf_partial(const ConfArgs& a, hipStream_t s);
+hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls,
+                               int64_t ld, const int32_t* cur_tok, int32_t* argmax,
+                               float* maxprob, float* pcur, hipStream_t s);
+
+// ---- decide.hip
+struct DecideArgs {
+    int phase;
+    int b, B;
+    float tau_c, tau_u;
+    double lambda, p0;
+    int32_t mask_id;
+    uint32_t flags;
+    const uint8_t* state_in;
+    const int32_t* tok_in;
+    // combined per-position inputs
+    const float* maxprob_s; const float* pcur_s; const int32_t* argmax_s;
+    const float* maxprob_mix; const int32_t* argmax_mix;
+    // chunk partials (step mode; used when the per-position arrays are NULL)
+    const float* part_v;     // [b*B][nchunk][3] shadow rows (phase VERIFY)
+    const float* part_m;     // [b*B][nchunk][3] mixed / shadow rows (phase FINAL)
+    const float* logits;     // [b][2B][V] (step mode, for pcur)
+    int64_t ld;
+    int nchunk;
+    float* w_out;
+    uint8_t* state_out; int32_t* tok_out; float* conf_out; int32_t* block_done;
+    // optional debug copies
+    float* dbg_maxprob_s; int32_t* dbg_argmax_s; float* dbg_pcur_s;
+    float* dbg_maxprob_mix; int32_t* dbg_argmax_mix;
+};
+hipError_t launch_decide(const DecideArgs& a, hipStream_t s);
+
+// ---- tracing (api.cpp)
+struct TraceScope {
+    TraceScope(int kernel_class, hipStream_t s);
+    ~TraceScope();
+    int cls; hipStream_t st; void* ev0;
+};
+
+}  // namespace dard

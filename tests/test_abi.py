@@ -1,0 +1,110 @@
+"""CPU-side checks of the C ABI: the library loads, exports every entry point
+that include/dard.h declares, validates arguments on the host (error codes
+without touching a GPU) and sizes its buffers as documented."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_26574_amd import dard, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dard.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dard_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("dard_build_state_mask", "dard_masked_attention", "dard_confidence",
+                     "dard_commit_remask", "dard_step"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = dard.lib()
+    missing = [n for n in declared_functions() if not hasattr(L, n)]
+    assert not missing
+    assert sorted(dard.EXPORTS) == declared_functions()
+
+
+def test_version():
+    assert dard.lib().dard_version() == 1
+
+
+def _params(**kw):
+    p = dict(tau_c=0.4, tau_u=0.9, lam=0.5 ** 0.125, p0=0.1, mask_id=5, flags=0)
+    p.update(kw)
+    return dard.make_params(**p)
+
+
+def test_host_validation_errors():
+    L = dard.lib()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+    # NULL pointers
+    assert L.dard_build_state_mask(None, fake, 1, 4, 0, fake, None) == -1
+    # B outside [1, 128]
+    assert L.dard_build_state_mask(fake, fake, 1, 0, 0, fake, None) == -2
+    assert L.dard_build_state_mask(fake, fake, 1, 129, 0, fake, None) == -2
+    # unknown flag bits
+    assert L.dard_build_state_mask(fake, fake, 1, 4, 1 << 7, fake, None) == -1
+    assert b"flag" in L.dard_last_error()
+    # attention: P + 2B > cap, bad dh, GQA ratio
+    args = [1, fake, fake, fake]
+    assert L.dard_masked_attention(*args, 10, 11, fake, fake, 1, 1, 4, 4, 128, 0.1, 0, fake, None, 0, None) == -2
+    assert L.dard_masked_attention(*args, 0, 64, fake, fake, 1, 8, 4, 4, 96, 0.1, 0, fake, None, 0, None) == -2
+    assert L.dard_masked_attention(*args, 0, 64, fake, fake, 1, 8, 6, 4, 128, 0.1, 0, fake, None, 0, None) == -2
+    # confidence: mixing without w, ld not a multiple of 4
+    assert L.dard_confidence(fake, fake, None, None, 2, 10, 12, fake, fake, None, fake, 1 << 20, None) == -1
+    assert L.dard_confidence(fake, None, None, None, 2, 10, 10, fake, fake, None, fake, 1 << 20, None) == -2
+    # confidence: workspace too small
+    assert L.dard_confidence(fake, None, None, None, 2, 16, 16, fake, fake, None, fake, 4, None) == -5
+    # commit/remask: thresholds out of order, lambda outside (0, 1), unknown phase
+    bad = _params(tau_c=0.95, tau_u=0.9)
+    assert L.dard_commit_remask(0, ctypes.byref(bad), 1, 4, fake, fake, None, None, None, None, fake,
+                                None, None, None, None, None) == -1
+    bad = _params(lam=1.0)
+    assert L.dard_commit_remask(0, ctypes.byref(bad), 1, 4, fake, fake, None, None, None, None, fake,
+                                None, None, None, None, None) == -1
+    good = _params()
+    assert L.dard_commit_remask(7, ctypes.byref(good), 1, 4, fake, fake, None, None, None, None, fake,
+                                None, None, None, None, None) == -1
+
+
+def test_dims_validation_and_sizes():
+    L = dard.lib()
+    d = dard.make_dims(synth.LLADA8B)
+    # packed image: weights + rotary table, each region 256-byte aligned
+    n = L.dard_packed_weight_bytes(ctypes.byref(d))
+    D, F, V, Lr = 4096, 12288, 126464, 32
+    weights = 2 * (2 * V * D + Lr * (4 * D * D + 3 * D * F + 2 * D) + D)
+    assert weights <= n <= weights + 256 * (4 + 6 * Lr) + 4096 * 64 * 2 * 4 + 256
+    # KV cache [L][2][b][Hkv][cap][dh] bf16
+    assert L.dard_kv_bytes(ctypes.byref(d), 1, 768) == 32 * 2 * 32 * 768 * 128 * 2
+    # workspace holds at least the step's logits
+    assert L.dard_workspace_bytes(ctypes.byref(d), 1, 32, 768) >= 64 * V * 4
+    # cap smaller than the augmented block
+    assert L.dard_workspace_bytes(ctypes.byref(d), 1, 32, 63) == 0
+    bad = dard.make_dims(synth.Dims(2, 256, 4, 4, 96, 1024, 2048, 64, "f32"))
+    assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
+    assert b"head_dim" in L.dard_last_error()
+    bad = dard.make_dims(synth.Dims(2, 256, 4, 3, 64, 1024, 2048, 64, "f32"))
+    assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
+    bad = dard.make_dims(synth.Dims(2, 4096, 32, 32, 128, 12288, 126460, 64, "bf16"))
+    assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
+
+
+def test_attention_workspace_sizing():
+    L = dard.lib()
+    # batch 1, 32 heads, 64 rows: the key range is split across workgroups
+    n = L.dard_attention_workspace_bytes(1, 1, 32, 32, 128, 512)
+    assert n > 0
+    # many sequences fill the chip without splitting: no workspace needed
+    assert L.dard_attention_workspace_bytes(1, 64, 32, 32, 128, 512) == 0
+    # the fp32 path never splits
+    assert L.dard_attention_workspace_bytes(0, 1, 32, 4, 64, 64) == 0

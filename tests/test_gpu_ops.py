@@ -1,0 +1,234 @@
+"""GPU parity of the individual entry points against the oracle (and, for the
+plain linear layer, against the definition of the product).
+
+Every case prints its name and sizes before touching the GPU."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dard_oracle as O
+from paper_2608_26574_amd import dard, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+# ---------------------------------------------------------------- linear
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("M,N,K", [(1, 16, 64), (17, 48, 192), (64, 4096, 4096), (40, 1024, 12288),
+                                   (130, 272, 320), (300, 512, 256)])
+def test_linear(dtype, M, N, K):
+    announce("linear", dtype, M, N, K)
+    g = torch.Generator().manual_seed(M * 7 + N)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    X = torch.randn(M, K, generator=g).to(td)
+    W = torch.randn(N, K, generator=g).to(td)
+    Y = torch.empty(M, N, device="cuda")
+    dard.dard_linear(X.cuda(), W.cuda(), Y)
+    torch.cuda.synchronize()
+    ref = X.double().numpy() @ W.double().numpy().T
+    scale = np.abs(X.double().numpy()) @ np.abs(W.double().numpy()).T
+    err = np.abs(Y.cpu().double().numpy() - ref) / (scale + 1e-30)
+    assert err.max() < 2e-6, err.max()
+
+
+# ---------------------------------------------------------------- mask
+@pytest.mark.parametrize("B", [1, 5, 32, 63, 64, 65, 128])
+@pytest.mark.parametrize("flags", [0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW])
+def test_state_mask_bit_exact(B, flags):
+    announce("mask", B, flags)
+    b = 3
+    rng = np.random.default_rng(B * 3 + flags)
+    state = rng.integers(0, 3, (b, B)).astype(np.uint8)
+    conf = rng.choice(np.linspace(0.41, 0.89, 7).astype(np.float32), (b, B))   # with ties
+    W = (B + 63) // 64
+    sel = torch.zeros(b, 2 * B, W, dtype=torch.int64, device="cuda")
+    dard.dard_build_state_mask(dev(state), dev(conf), flags, sel)
+    torch.cuda.synchronize()
+    got = sel.cpu().numpy().view(np.uint64)
+    for s in range(b):
+        X = O.take_x(state[s], conf[s], flags)
+        for r in range(2 * B):
+            for j in range(B):
+                bit = (int(got[s, r, j // 64]) >> (j % 64)) & 1
+                assert bit == int(X[r, j]), (s, r, j)
+            for j in range(B, 64 * W):   # unused bits stay clear
+                assert ((int(got[s, r, j // 64]) >> (j % 64)) & 1) == 0
+
+
+# ---------------------------------------------------------------- attention
+def _attn_case(b, B, P, Hq, Hkv, dh, dtype, cand_frac, seed, flags=0, cap_extra=3):
+    cap = P + 2 * B + cap_extra
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, k, v = synth.qkv(b, 2 * B, Hq, Hkv, dh, cap, seed=seed, dtype=td)
+    if cand_frac is None:
+        _, state, conf = synth.tiny_block(b, B, 100, seed=seed)
+    else:
+        _, state, conf = synth.workload_block(b, B, cand_frac, 100, seed=seed)
+    out = torch.empty_like(q).cuda()
+    scale = 1.0 / math.sqrt(dh)
+    nws = dard.dard_attention_workspace_bytes(1 if dtype == "bf16" else 0, b, B, Hq, dh, P)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
+    dard.dard_masked_attention(q.cuda(), k.cuda(), v.cuda(), P, dev(state), dev(conf), scale, flags, out, ws)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    qn, kn, vn = q.double().numpy(), k.double().numpy(), v.double().numpy()
+    worst = 0.0
+    for s in range(b):
+        vis = O.visible_keys(state[s], conf[s], P, flags)
+        ref = O.masked_attention(qn[s], kn[s, :, :P + 2 * B].transpose(1, 0, 2),
+                                 vn[s, :, :P + 2 * B].transpose(1, 0, 2), vis, scale, Hkv)
+        worst = max(worst, float(np.max(np.abs(got[s] - ref))))
+    return worst
+
+
+@pytest.mark.parametrize("b", [1, 4, 16])
+@pytest.mark.parametrize("frac", [0.1, 0.25, 0.5])
+def test_attention_llada_shape(b, frac):
+    """The isolated attention workload: 32 heads x 128, prompt 512, block 32."""
+    announce("attention 8B-shape", b, frac)
+    err = _attn_case(b, 32, 512, 32, 32, 128, "bf16", frac, seed=b * 10 + int(frac * 100))
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("case", [
+    dict(b=1, B=1, P=0, Hq=2, Hkv=2, dh=128),       # smallest block, no prefix
+    dict(b=2, B=5, P=70, Hq=4, Hkv=2, dh=128),      # ragged block, ragged prefix, GQA
+    dict(b=1, B=64, P=1024, Hq=7, Hkv=1, dh=128),   # two row tiles, 7:1 GQA
+    dict(b=1, B=128, P=33, Hq=2, Hkv=2, dh=128),    # maximum block: 4 row tiles, 2 mask words
+    dict(b=3, B=32, P=100, Hq=4, Hkv=4, dh=64),     # head_dim 64
+    dict(b=1, B=32, P=4000, Hq=2, Hkv=1, dh=128),   # long prefix: many key splits
+])
+def test_attention_edges_bf16(case):
+    announce("attention edge bf16", case)
+    err = _attn_case(case["b"], case["B"], case["P"], case["Hq"], case["Hkv"], case["dh"], "bf16", None, seed=7)
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("flags", [O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW])
+def test_attention_flags_bf16(flags):
+    announce("attention flags", flags)
+    err = _attn_case(2, 16, 40, 4, 4, 128, "bf16", None, seed=9, flags=flags)
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("case", [dict(b=1, B=32, P=64, Hq=4, Hkv=4, dh=64),
+                                  dict(b=2, B=7, P=9, Hq=4, Hkv=2, dh=128),
+                                  dict(b=1, B=3, P=0, Hq=1, Hkv=1, dh=64)])
+def test_attention_f32(case):
+    announce("attention f32", case)
+    err = _attn_case(case["b"], case["B"], case["P"], case["Hq"], case["Hkv"], case["dh"], "f32", None, seed=3)
+    assert err < 1e-4, err
+
+
+# ---------------------------------------------------------------- confidence
+def _conf_ref(ls, lx=None, w=None, cur=None):
+    rows = ls.shape[0]
+    am = np.zeros(rows, dtype=np.int64)
+    mp = np.zeros(rows)
+    pc = np.zeros(rows)
+    for r in range(rows):
+        row = ls[r] if lx is None else O.mix_logits(lx[r], ls[r], w[r])
+        am[r], mp[r], pc[r] = O.confidence(row, None if cur is None else int(cur[r]))
+    return am, mp, pc
+
+
+@pytest.mark.parametrize("rows,V", [(5, 126464), (3, 152064), (7, 2048), (4, 10), (2, 8195), (1, 1)])
+def test_confidence_plain(rows, V):
+    announce("confidence", rows, V)
+    g = torch.Generator().manual_seed(V + rows)
+    ld = (V + 3) // 4 * 4
+    ls = (torch.randn(rows, ld, generator=g) * 3).float()
+    # plant equal maxima in different chunks: the lower index must win
+    if V > 9000:
+        ls[0, 9000] = 50.0
+        ls[0, 100] = 50.0
+    cur = torch.randint(0, V, (rows,), generator=g, dtype=torch.int32)
+    am = torch.empty(rows, dtype=torch.int32, device="cuda")
+    mp = torch.empty(rows, device="cuda")
+    pc = torch.empty(rows, device="cuda")
+    ws = torch.empty(dard.dard_confidence_workspace_bytes(rows, V), dtype=torch.uint8, device="cuda")
+    ls_d = ls.cuda()
+    L = dard.lib()
+    dard._check(L.dard_confidence(ls_d.data_ptr(), None, None, cur.cuda().data_ptr(), rows, V, ld,
+                                  am.data_ptr(), mp.data_ptr(), pc.data_ptr(), ws.data_ptr(), ws.numel(),
+                                  torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    ram, rmp, rpc = _conf_ref(ls[:, :V].numpy(), cur=cur.numpy())
+    assert np.array_equal(am.cpu().numpy(), ram)
+    assert np.max(np.abs(mp.cpu().numpy() - rmp) / rmp) < 1e-5
+    assert np.max(np.abs(pc.cpu().numpy() - rpc) / np.maximum(rpc, 1e-30)) < 1e-4
+    if V > 9000:
+        assert am[0].item() == 100
+
+
+@pytest.mark.parametrize("wvals", [[0.0, 0.3, 1.0, 0.97, 0.05]])
+def test_confidence_mixed(wvals):
+    announce("confidence mixed", wvals)
+    rows, V = len(wvals), 126464
+    g = torch.Generator().manual_seed(11)
+    ls = torch.randn(rows, V, generator=g) * 2
+    lx = torch.randn(rows, V, generator=g) * 2
+    w = torch.tensor(wvals, dtype=torch.float32)
+    am = torch.empty(rows, dtype=torch.int32, device="cuda")
+    mp = torch.empty(rows, device="cuda")
+    ws = torch.empty(dard.dard_confidence_workspace_bytes(rows, V), dtype=torch.uint8, device="cuda")
+    dard.dard_confidence(ls.cuda(), am, mp, logits_x=lx.cuda(), w=w.cuda(), ws=ws)
+    torch.cuda.synchronize()
+    ram, rmp, _ = _conf_ref(ls.numpy(), lx.numpy(), w.numpy())
+    assert np.array_equal(am.cpu().numpy(), ram)
+    assert np.max(np.abs(mp.cpu().numpy() - rmp) / rmp) < 1e-5
+
+
+# ---------------------------------------------------------------- decisions
+def _params(flags=0, tc=0.4, tu=0.9):
+    return dict(tau_c=tc, tau_u=tu, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=999, flags=flags)
+
+
+@pytest.mark.parametrize("B", [1, 7, 32, 128])
+@pytest.mark.parametrize("flags,tc,tu", [(0, 0.4, 0.9), (O.F_VERIFY_PCUR, 0.3, 0.7), (0, 0.9, 0.9)])
+def test_commit_remask_bit_exact(B, flags, tc, tu):
+    announce("commit/remask", B, flags, tc, tu)
+    b = 4
+    rng = np.random.default_rng(B + int(tc * 10))
+    p = _params(flags, tc, tu)
+    state = rng.integers(0, 3, (b, B)).astype(np.uint8)
+    # confidences including the exact threshold values and their neighbours
+    pool = np.array([0.0, tc, np.nextafter(np.float32(tc), np.float32(1)), 0.5, tu,
+                     np.nextafter(np.float32(tu), np.float32(1)), 0.99, 1.0], dtype=np.float32)
+    mp_s = rng.choice(pool, (b, B)).astype(np.float32)
+    pc_s = rng.choice(pool, (b, B)).astype(np.float32)
+    mp_mix = rng.choice(pool, (b, B)).astype(np.float32)
+    am_s = rng.integers(0, 998, (b, B)).astype(np.int32)
+    am_mix = rng.integers(0, 998, (b, B)).astype(np.int32)
+    cp = dard.make_params(tc, tu, O.LAMBDA_DEFAULT, 0.1, 999, flags)
+    w = torch.empty(b, B, device="cuda")
+    dard.dard_commit_remask(dard.PHASE_VERIFY, cp, dev(state), maxprob_s=dev(mp_s), pcur_s=dev(pc_s), w_out=w)
+    so = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    to = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    co = torch.empty(b, B, device="cuda")
+    bd = torch.empty(b, dtype=torch.int32, device="cuda")
+    dard.dard_commit_remask(dard.PHASE_FINAL, cp, dev(state), dev(mp_s), dev(pc_s), dev(am_s), dev(mp_mix),
+                            dev(am_mix), None, so, to, co, bd)
+    torch.cuda.synchronize()
+    c_sh = pc_s if flags & O.F_VERIFY_PCUR else mp_s
+    for s in range(b):
+        _, _, _, rw = O.verify_candidates(state[s], c_sh[s], p)
+        assert np.array_equal(w[s].cpu().numpy().astype(np.float64), rw), s
+        c = np.where(state[s] == O.STATE_M, mp_mix[s], c_sh[s])
+        xh = np.where(state[s] == O.STATE_M, am_mix[s], am_s[s])
+        st, tk, cf, done = O.finalize(c, xh, p)
+        assert np.array_equal(so[s].cpu().numpy(), st)
+        assert np.array_equal(to[s].cpu().numpy(), tk)
+        assert np.array_equal(co[s].cpu().numpy(), cf.astype(np.float32))
+        assert bd[s].item() == done
