@@ -238,8 +238,13 @@ dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int c
 /* ------------------------------------------------------------ plain linear layer
  * Y[m][n] = sum_k X[m][k] * W[n][k] in float32 (the projection GEMM of every
  * layer and the LM head, exposed for testing and measurement).
- * X [M][K], W [N][K] of `dtype`, Y [M][N] float32. */
-dard_status dard_linear(int dtype, const void* X, int M, int K, const void* W, int N,
+ * dard_pack_matrix() converts a row-major W [N][K] of `dtype` into the
+ * library's weight layout Wp (same size; bf16: 16 x 64 blocks stored in the
+ * order the matrix cores consume them, needs K % 64 == 0 and N % 16 == 0;
+ * fp32: row-major copy, needs K % 4 == 0).  dard_linear() takes X [M][K] of
+ * `dtype`, the packed Wp, and writes Y [M][N] float32. */
+dard_status dard_pack_matrix(int dtype, const void* W, int N, int K, void* Wp, void* stream);
+dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, int N,
                         float* Y, void* stream);
 
 /* ------------------------------------------------------------ tracing

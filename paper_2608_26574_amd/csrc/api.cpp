@@ -53,6 +53,7 @@ int check_dims(const dard_dims* d) {
     if (d->n_heads * d->head_dim != d->d_model) return fail(DARD_ERR_SHAPE, "d_model != n_heads * head_dim");
     if (d->dtype == DARD_DTYPE_BF16 && (d->d_model % 64 || d->ffn_dim % 64 || d->vocab % 16))
         return fail(DARD_ERR_SHAPE, "bf16 needs d_model, ffn_dim %% 64 == 0 and vocab %% 16 == 0");
+    if (d->d_model > 8192) return fail(DARD_ERR_SHAPE, "d_model must be <= 8192");
     if (d->dtype == DARD_DTYPE_F32 && (d->d_model % 4 || d->ffn_dim % 4 || d->vocab % 4))
         return fail(DARD_ERR_SHAPE, "f32 needs d_model, ffn_dim, vocab %% 4 == 0");
     if (!(d->norm_eps >= 0.f) || !(d->rope_theta > 0.f)) return fail(DARD_ERR_ARG, "bad norm_eps / rope_theta");
@@ -91,7 +92,7 @@ Layout layout_of(const dard_dims* d) {
 
 // Workspace of dard_step / dard_prefill.
 struct WsLayout {
-    size_t h, xn, q, attn, act, part, part_ml, part_slots, logits, cpart_v, cpart_m, w, total;
+    size_t h, xn, q, attn, act, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, total;
 };
 
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
@@ -117,6 +118,8 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.cpart_v = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
     W.cpart_m = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
     W.w = o; o = align256(o + (size_t)b * B * 4);
+    // split-K partials of the O and down projections (64-row tiles only)
+    W.gpart = o; o = align256(o + (size_t)8 * 64 * d->d_model * 4);
     W.total = o;
     return W;
 }
@@ -298,20 +301,26 @@ dard_status dard_pack_weights(const dard_dims* d, const void* const* src, int n_
     const int rowD = (int)(D * es), rowF = (int)(F * es);
     if (rowD % 16 || rowF % 16) return fail(DARD_ERR_SHAPE, "weight rows must be multiples of 16 bytes");
     HIPOK(launch_pack_rows(src[0], nullptr, P + L.embed, V, rowD, 0, dh, s));
+    const bool frag = d->dtype == DARD_DTYPE_BF16;
+    // projection matrices: bf16 fragment-major, fp32 row-major (same row order)
+    auto pack = [&](const void* a, const void* b2, char* dst, int N, int K, int mode) -> hipError_t {
+        return frag ? launch_pack_frag(a, b2, dst, N, K, mode, dh, s)
+                    : launch_pack_rows(a, b2, dst, N, (int)(K * es), mode, dh, s);
+    };
     for (int l = 0; l < d->n_layers; ++l) {
         const void* const* w = src + 1 + 9 * l;
         char* base = P + L.layer0 + L.layer_stride * l;
         HIPOK(launch_copy_rows(w[0], base + L.attn_norm, D * es, s));
-        HIPOK(launch_pack_rows(w[1], nullptr, base + L.wqkv, qd, rowD, 1, dh, s));
-        HIPOK(launch_pack_rows(w[2], nullptr, base + L.wqkv + (size_t)qd * rowD, kd, rowD, 1, dh, s));
-        HIPOK(launch_pack_rows(w[3], nullptr, base + L.wqkv + (size_t)(qd + kd) * rowD, kd, rowD, 0, dh, s));
-        HIPOK(launch_pack_rows(w[4], nullptr, base + L.wo, D, (int)(qd * es), 0, dh, s));
+        HIPOK(pack(w[1], nullptr, base + L.wqkv, qd, D, 1));
+        HIPOK(pack(w[2], nullptr, base + L.wqkv + (size_t)qd * rowD, kd, D, 1));
+        HIPOK(pack(w[3], nullptr, base + L.wqkv + (size_t)(qd + kd) * rowD, kd, D, 0));
+        HIPOK(pack(w[4], nullptr, base + L.wo, D, qd, 0));
         HIPOK(launch_copy_rows(w[5], base + L.ffn_norm, D * es, s));
-        HIPOK(launch_pack_rows(w[6], w[7], base + L.wgu, 2 * F, rowD, 2, dh, s));
-        HIPOK(launch_pack_rows(w[8], nullptr, base + L.wdown, D, rowF, 0, dh, s));
+        HIPOK(pack(w[6], w[7], base + L.wgu, 2 * F, D, 2));
+        HIPOK(pack(w[8], nullptr, base + L.wdown, D, F, 0));
     }
     HIPOK(launch_copy_rows(src[1 + 9 * d->n_layers], P + L.final_norm, D * es, s));
-    HIPOK(launch_pack_rows(src[2 + 9 * d->n_layers], nullptr, P + L.lm_head, V, rowD, 0, dh, s));
+    HIPOK(pack(src[2 + 9 * d->n_layers], nullptr, P + L.lm_head, V, D, 0));
     // small norm vectors may not be a multiple of 16 bytes: copy the tail
     if ((D * es) % 16) {
         const size_t tail = (D * es) % 16, off = D * es - tail;
@@ -400,14 +409,21 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         }
         EpiArgs r{};
         r.kind = EPI_RESID; r.y = h; r.ldy = D;
-        HIPOK(launch_gemm(dt, at, rows, qd, qd, f.layer(l, f.L.wo), D, r, DARD_K_GEMM_O, f.s));
-        HIPOK(launch_rmsnorm(dt, h, f.layer(l, f.L.ffn_norm), rows, D, d->norm_eps, xn, f.s));
+        // O projection: residual add in the epilogue, or split-K partials that
+        // the residual-norm kernel adds in a fixed order
+        const int so = gemm_split(dt, rows, D, qd);
+        float* gp = (float*)(f.ws + f.W.gpart);
+        EpiArgs po{};
+        po.kind = EPI_PARTIAL; po.y = gp; po.ldy = D;
+        HIPOK(launch_gemm(dt, at, rows, qd, qd, f.layer(l, f.L.wo), D, so > 1 ? po : r, DARD_K_GEMM_O, f.s));
+        HIPOK(launch_resid_norm(dt, h, gp, so > 1 ? so : 0, rows, D, f.layer(l, f.L.ffn_norm), d->norm_eps, xn, f.s));
         EpiArgs g{};
         g.kind = EPI_SWIGLU; g.act = act; g.ld_act = F;
         HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wgu), 2 * F, g, DARD_K_GEMM_GU, f.s));
-        HIPOK(launch_gemm(dt, act, rows, F, F, f.layer(l, f.L.wdown), D, r, DARD_K_GEMM_DOWN, f.s));
+        const int sd = gemm_split(dt, rows, D, F);
+        HIPOK(launch_gemm(dt, act, rows, F, F, f.layer(l, f.L.wdown), D, sd > 1 ? po : r, DARD_K_GEMM_DOWN, f.s));
         const void* gain = l + 1 < d->n_layers ? f.layer(l + 1, f.L.attn_norm) : f.pk + f.L.final_norm;
-        HIPOK(launch_rmsnorm(dt, h, gain, rows, D, d->norm_eps, xn, f.s));
+        HIPOK(launch_resid_norm(dt, h, gp, sd > 1 ? sd : 0, rows, D, gain, d->norm_eps, xn, f.s));
     }
     return DARD_OK;
 }
@@ -502,15 +518,29 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
 }
 
 // ---------------------------------------------------------------- linear
-dard_status dard_linear(int dtype, const void* X, int M, int K, const void* W, int N, float* Y, void* stream) {
-    if (!X || !W || !Y) return fail(DARD_ERR_ARG, "NULL pointer");
+dard_status dard_pack_matrix(int dtype, const void* W, int N, int K, void* Wp, void* stream) {
+    if (!W || !Wp) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
+    if (N < 1 || K < 1) return fail(DARD_ERR_SHAPE, "need N, K >= 1");
+    if (dtype == DARD_DTYPE_BF16 && (K % 64 || N % 16)) return fail(DARD_ERR_SHAPE, "bf16 needs K %% 64 == 0, N %% 16 == 0");
+    if (dtype == DARD_DTYPE_F32 && K % 4) return fail(DARD_ERR_SHAPE, "f32 needs K %% 4 == 0");
+    hipStream_t s = (hipStream_t)stream;
+    if (dtype == DARD_DTYPE_BF16)
+        HIPOK(launch_pack_frag(W, nullptr, Wp, N, K, 0, 64, s));
+    else
+        HIPOK(launch_copy_rows(W, Wp, (size_t)N * K * 4, s));
+    return DARD_OK;
+}
+
+dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, int N, float* Y, void* stream) {
+    if (!X || !Wp || !Y) return fail(DARD_ERR_ARG, "NULL pointer");
     if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
     if (M < 1 || N < 1 || K < 1) return fail(DARD_ERR_SHAPE, "need M, N, K >= 1");
     if (dtype == DARD_DTYPE_BF16 && (K % 64 || N % 16)) return fail(DARD_ERR_SHAPE, "bf16 needs K %% 64 == 0, N %% 16 == 0");
-    if (dtype == DARD_DTYPE_F32 && N % 4) return fail(DARD_ERR_SHAPE, "f32 needs N %% 4 == 0");
+    if (dtype == DARD_DTYPE_F32 && (N % 4 || K % 4)) return fail(DARD_ERR_SHAPE, "f32 needs N, K %% 4 == 0");
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.y = Y; e.ldy = N;
-    HIPOK(launch_gemm(dtype, X, M, K, K, W, N, e, DARD_K_GEMM_HEAD, (hipStream_t)stream));
+    HIPOK(launch_gemm(dtype, X, M, K, K, Wp, N, e, DARD_K_GEMM_HEAD, (hipStream_t)stream));
     return DARD_OK;
 }
 

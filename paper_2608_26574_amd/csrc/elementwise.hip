@@ -53,12 +53,51 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(const int32_t* __restri
     norm_row<T>(hr, gain, d, eps, xn + row * d, red);
 }
 
+// h[row] += sum_s part[s][row] (split-K partials of the preceding projection,
+// added in split order), then xn[row] = RMSNorm(h[row]) * gain.  One
+// workgroup per row, each thread holding up to kVec float4 of the row.
+constexpr int kVec = 8;   // d <= 256 * 4 * kVec
+
 template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h, const T* __restrict__ gain, int d,
-                                                      float eps, T* __restrict__ xn) {
-    __shared__ float red[8];
+__global__ __launch_bounds__(256) void resid_norm_kernel(float* __restrict__ h, const float* __restrict__ part,
+                                                         int nsplit, size_t split_stride, const T* __restrict__ gain,
+                                                         int d, float eps, T* __restrict__ xn) {
+    __shared__ float red[4];
     const size_t row = blockIdx.x;
-    norm_row<T>(h + row * d, gain, d, eps, xn + row * d, red);
+    float4* hr = reinterpret_cast<float4*>(h + row * d);
+    const int n4 = d / 4;
+    float4 v[kVec];
+    float ss = 0.f;
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) {
+        const int c4 = threadIdx.x + 256 * q;
+        if (c4 < n4) {
+            float4 x = hr[c4];
+            for (int s = 0; s < nsplit; ++s) {
+                const float4 p = reinterpret_cast<const float4*>(part + s * split_stride + row * d)[c4];
+                x.x += p.x; x.y += p.y; x.z += p.z; x.w += p.w;
+            }
+            if (nsplit > 0) hr[c4] = x;
+            v[q] = x;
+            ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+        }
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float inv = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+    T* out = xn + row * d;
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) {
+        const int c4 = threadIdx.x + 256 * q;
+        if (c4 < n4) {
+            const int c = 4 * c4;
+            St<T>::st(out + c, v[q].x * inv * St<T>::ld(gain + c));
+            St<T>::st(out + c + 1, v[q].y * inv * St<T>::ld(gain + c + 1));
+            St<T>::st(out + c + 2, v[q].z * inv * St<T>::ld(gain + c + 2));
+            St<T>::st(out + c + 3, v[q].w * inv * St<T>::ld(gain + c + 3));
+        }
+    }
 }
 
 __global__ void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t n16) {
@@ -110,15 +149,16 @@ hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds, 
     return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, int rows, int d, float eps, void* xn,
-                          hipStream_t s) {
+hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit, int rows, int d,
+                             const void* gain, float eps, void* xn, hipStream_t s) {
     TraceScope ts(DARD_K_NORM, s);
+    const size_t stride = (size_t)rows * d;
     if (dtype == DARD_DTYPE_BF16)
-        hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, (const bf16_t*)gain, d, eps,
-                           (bf16_t*)xn);
+        hipLaunchKernelGGL(resid_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, part, nsplit, stride,
+                           (const bf16_t*)gain, d, eps, (bf16_t*)xn);
     else
-        hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, h, (const float*)gain, d, eps,
-                           (float*)xn);
+        hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(rows), dim3(256), 0, s, h, part, nsplit, stride,
+                           (const float*)gain, d, eps, (float*)xn);
     return hipGetLastError();
 }
 

@@ -1,20 +1,27 @@
-// Projection GEMMs Y = X * W^T (X [M][K] activations, W [N][K] weights, both
-// K-contiguous) with fused epilogues:
+// Projection GEMMs Y = X * W^T (X [M][K] activations, W [N][K] weights) with
+// fused epilogues:
 //   STORE_F32  plain fp32 store (LM head logits, dard_linear)
 //   RESID      fp32 residual add into the residual stream (O and down proj.)
 //   SWIGLU     silu(gate) * up on interleaved gate/up rows, stored as dtype
 //   QKV        rotary embedding on adjacent (t, t + dh/2) pairs, Q to its
 //              buffer, K and V straight into the KV cache at the rows' keys
+//   PARTIAL    fp32 split-K partial [split][M][N], reduced by the consumer
 //
-// bf16 kernels use v_mfma_f32_16x16x32_bf16 with W as the A operand (16 output
-// columns) and X as the B operand (16 tokens), so that each lane ends with 4
-// consecutive output columns of one token -- exactly what the epilogues need.
-//   gemm_skinny: M <= 64 tokens (a decoding step).  The weight matrix streams
-//     from HBM straight into registers, 16-byte loads, each 4-lane group reads
-//     128 contiguous bytes of a weight row; the few activation rows are re-read
-//     from L2.  The waves of a workgroup split K and are summed in LDS in a
-//     fixed order (deterministic).
-//   gemm_tiled: 128x128 tiles through LDS for large M (prefill, big batches).
+// bf16 weights are packed fragment-major: the 16 x 64 block (row block nb,
+// k unit u) is stored contiguously at element ((nb * K/64 + u) * 1024), as two
+// halves of 512 (k 8h..8h+7 of each 16-wide group) in which lane l of a wave
+// finds its 8 values at 8*l.  One 16-byte load per lane then reads exactly the
+// A operand of v_mfma_f32_16x16x32_bf16 and a wave load is 1 KB contiguous;
+// a wave streaming a row block over K reads one contiguous region.
+//
+// W is the A operand (16 output columns), X the B operand (16 tokens), so each
+// lane ends with 4 consecutive output columns of one token.
+//   gemm_stream: M <= 64 tokens (a decoding step).  Each wave owns 16*NW
+//     columns; the KSPLIT waves of a workgroup take interleaved k units and are
+//     summed in LDS in a fixed order; DEPTH units per wave are in flight in a
+//     register ring.  Weights are read with non-temporal loads (streamed once).
+//     Optional split of K across SPLIT workgroups writes fp32 partials.
+//   gemm_tiled: 128 x 128 tiles through LDS for large M (prefill, big batches).
 #include "common.h"
 #include "launch.h"
 
@@ -42,6 +49,7 @@ template <typename T>
 __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4 v) {
     switch (e.kind) {
     case EPI_STORE_F32:
+    case EPI_PARTIAL:
         *reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n) = make_float4(v[0], v[1], v[2], v[3]);
         break;
     case EPI_RESID: {
@@ -53,10 +61,8 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4
     }
     case EPI_SWIGLU: {
         T* a = reinterpret_cast<T*>(e.act) + (size_t)m * e.ld_act + n / 2;
-        const float r0 = silu(v[0]) * v[1];
-        const float r1 = silu(v[2]) * v[3];
-        St<T>::st(a, r0);
-        St<T>::st(a + 1, r1);
+        St<T>::st(a, silu(v[0]) * v[1]);
+        St<T>::st(a + 1, silu(v[2]) * v[3]);
         break;
     }
     case EPI_QKV: {
@@ -89,22 +95,21 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4
     }
 }
 
-// ---------------------------------------------------------------- skinny
-template <int NW, int KSPLIT>
-__global__ __launch_bounds__(64 * KSPLIT) void gemm_skinny_bf16(const bf16_t* __restrict__ X, int M, int K,
-                                                              int ldx, const bf16_t* __restrict__ W, int N,
-                                                              EpiArgs e) {
+__device__ __forceinline__ bf16x8 ld_nt(const bf16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
+}
+
+// ---------------------------------------------------------------- streaming
+template <int NW, int KSPLIT, int DEPTH>
+__global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __restrict__ X, int M, int K, int ldx,
+                                                               const bf16_t* __restrict__ W, int N, EpiArgs e) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lr = lane & 15, g = lane >> 4;
-    const int n0 = blockIdx.x * 16 * NW;
-    const int m0 = blockIdx.y * 64;
-
-    const bf16_t* wp[NW];
-#pragma unroll
-    for (int j = 0; j < NW; ++j) wp[j] = W + (size_t)min(n0 + 16 * j + lr, N - 1) * K + 16 * g;
-    const bf16_t* xp[4];
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) xp[mb] = X + (size_t)min(m0 + 16 * mb + lr, M - 1) * ldx + 16 * g;
+    const int nb0 = blockIdx.x * NW;
+    const int KU = K / 64;
+    // this workgroup's k units: [u_begin, u_end) of split blockIdx.y
+    const int split = blockIdx.y, nsplit = gridDim.y;
+    const int u_begin = (int)((long)KU * split / nsplit), u_end = (int)((long)KU * (split + 1) / nsplit);
 
     floatx4 acc[NW][4];
 #pragma unroll
@@ -112,37 +117,44 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_skinny_bf16(const bf16_t* __
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb) acc[j][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    const int nu = K / 64;
-    bf16x8 wa[2][NW], xb[2][4];
-    int u = wave;
-    if (u < nu) {
+    const bf16_t* wp[NW];
 #pragma unroll
-        for (int j = 0; j < NW; ++j) { wa[0][j] = ld_bf16x8(wp[j] + u * 64); wa[1][j] = ld_bf16x8(wp[j] + u * 64 + 8); }
+    for (int j = 0; j < NW; ++j) wp[j] = W + (size_t)min(nb0 + j, N / 16 - 1) * KU * 1024 + 8 * lane;
+    const bf16_t* xp[4];
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb) { xb[0][mb] = ld_bf16x8(xp[mb] + u * 64); xb[1][mb] = ld_bf16x8(xp[mb] + u * 64 + 8); }
-    }
-    for (; u < nu; u += KSPLIT) {
-        bf16x8 wn[2][NW], xn[2][4];
-        const int un = u + KSPLIT;
-        if (un < nu) {
+    for (int mb = 0; mb < 4; ++mb) xp[mb] = X + (size_t)min(16 * mb + lr, M - 1) * ldx + 16 * g;
+
+    bf16x8 wb[DEPTH][NW][2], xb[DEPTH][4][2];
+    auto load = [&](int s, int u) {
 #pragma unroll
-            for (int j = 0; j < NW; ++j) { wn[0][j] = ld_bf16x8(wp[j] + un * 64); wn[1][j] = ld_bf16x8(wp[j] + un * 64 + 8); }
-#pragma unroll
-            for (int mb = 0; mb < 4; ++mb) { xn[0][mb] = ld_bf16x8(xp[mb] + un * 64); xn[1][mb] = ld_bf16x8(xp[mb] + un * 64 + 8); }
+        for (int j = 0; j < NW; ++j) {
+            wb[s][j][0] = ld_nt(wp[j] + (size_t)u * 1024);
+            wb[s][j][1] = ld_nt(wp[j] + (size_t)u * 1024 + 512);
         }
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
+        for (int mb = 0; mb < 4; ++mb) {
+            xb[s][mb][0] = ld_bf16x8(xp[mb] + 64 * u);
+            xb[s][mb][1] = ld_bf16x8(xp[mb] + 64 * u + 8);
+        }
+    };
 #pragma unroll
-            for (int j = 0; j < NW; ++j)
+    for (int s = 0; s < DEPTH; ++s) {
+        const int u = u_begin + wave + s * KSPLIT;
+        if (u < u_end) load(s, u);
+    }
+    for (int base = u_begin + wave; base < u_end; base += DEPTH * KSPLIT) {
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) acc[j][mb] = mfma16x16x32(wa[hh][j], xb[hh][mb], acc[j][mb]);
-        if (un < nu) {
+        for (int s = 0; s < DEPTH; ++s) {
+            const int u = base + s * KSPLIT;
+            if (u < u_end) {
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
+                for (int h = 0; h < 2; ++h)
 #pragma unroll
-                for (int j = 0; j < NW; ++j) wa[hh][j] = wn[hh][j];
+                    for (int j = 0; j < NW; ++j)
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) xb[hh][mb] = xn[hh][mb];
+                        for (int mb = 0; mb < 4; ++mb) acc[j][mb] = mfma16x16x32(wb[s][j][h], xb[s][mb][h], acc[j][mb]);
+                const int un = u + DEPTH * KSPLIT;
+                if (un < u_end) load(s, un);
             }
         }
     }
@@ -164,13 +176,15 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_skinny_bf16(const bf16_t* __
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb) acc[j][mb] += red[w][j * 4 + mb][lane];
     }
+    EpiArgs ee = e;
+    if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
 #pragma unroll
     for (int j = 0; j < NW; ++j) {
-        const int n = n0 + 16 * j + 4 * g;
+        const int n = 16 * (nb0 + j) + 4 * g;
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
-            const int m = m0 + 16 * mb + lr;
-            if (m < M && n < N) epilogue<bf16_t>(e, m, n, acc[j][mb]);
+            const int m = 16 * mb + lr;
+            if (m < M && n < N) epilogue<bf16_t>(ee, m, n, acc[j][mb]);
         }
     }
 }
@@ -181,7 +195,7 @@ constexpr int TBM = 128, TBN = 128, TBK = 64, TPAD = TBK + 8;
 __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict__ X, int M, int K, int ldx,
                                                        const bf16_t* __restrict__ W, int N, EpiArgs e,
                                                        int tiles_m, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) bf16_t Ws[TBN * TPAD];
+    __shared__ __attribute__((aligned(16))) bf16_t Ws[8 * 1024];      // 8 fragment blocks of one k unit
     __shared__ __attribute__((aligned(16))) bf16_t Xs[TBM * TPAD];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lr = lane & 15, g = lane >> 4;
@@ -192,8 +206,9 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
     int bid = blockIdx.x;
     if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
     const int tm = bid % tiles_m, tn = bid / tiles_m;
-    const int n0 = tn * TBN, m0 = tm * TBM;
+    const int nb_base = tn * (TBN / 16), m0 = tm * TBM;
     const int wn = wave & 1, wm = wave >> 1;
+    const int KU = K / 64, NB = N / 16;
 
     floatx4 acc[4][4];
 #pragma unroll
@@ -202,40 +217,40 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
         for (int i = 0; i < 4; ++i) acc[j][i] = floatx4{0.f, 0.f, 0.f, 0.f};
 
     bf16x8 wr[4], xr[4];
-    auto gload = [&](int k0) {
+    auto gload = [&](int u) {
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
-            const int c = threadIdx.x + 256 * it;
+            const int c = threadIdx.x + 256 * it;      // 16-byte chunk of the 16 KB tile
+            const int nbl = c >> 7, off = c & 127;
+            wr[it] = ld_bf16x8(W + ((size_t)min(nb_base + nbl, NB - 1) * KU + u) * 1024 + off * 8);
             const int row = c >> 3, c8 = c & 7;
-            wr[it] = ld_bf16x8(W + (size_t)min(n0 + row, N - 1) * K + k0 + c8 * 8);
-            xr[it] = ld_bf16x8(X + (size_t)min(m0 + row, M - 1) * ldx + k0 + c8 * 8);
+            xr[it] = ld_bf16x8(X + (size_t)min(m0 + row, M - 1) * ldx + u * 64 + c8 * 8);
         }
     };
     auto sstore = [&]() {
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
             const int c = threadIdx.x + 256 * it;
+            *reinterpret_cast<bf16x8*>(&Ws[c * 8]) = wr[it];
             const int row = c >> 3, c8 = c & 7;
-            *reinterpret_cast<bf16x8*>(&Ws[row * TPAD + c8 * 8]) = wr[it];
             *reinterpret_cast<bf16x8*>(&Xs[row * TPAD + c8 * 8]) = xr[it];
         }
     };
-    const int nk = K / TBK;
     gload(0);
-    for (int kt = 0; kt < nk; ++kt) {
+    for (int u = 0; u < KU; ++u) {
         __syncthreads();
         sstore();
         __syncthreads();
-        if (kt + 1 < nk) gload((kt + 1) * TBK);
+        if (u + 1 < KU) gload(u + 1);
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
             bf16x8 af[4], bfr[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                af[j] = *reinterpret_cast<const bf16x8*>(&Ws[(wn * 64 + 16 * j + lr) * TPAD + 32 * hh + 8 * g]);
+                af[j] = *reinterpret_cast<const bf16x8*>(&Ws[(wn * 4 + j) * 1024 + hh * 512 + lane * 8]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                bfr[i] = *reinterpret_cast<const bf16x8*>(&Xs[(wm * 64 + 16 * i + lr) * TPAD + 32 * hh + 8 * g]);
+                bfr[i] = *reinterpret_cast<const bf16x8*>(&Xs[(wm * 64 + 16 * i + lr) * TPAD + 16 * g + 8 * hh]);
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -244,7 +259,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const int n = n0 + wn * 64 + 16 * j + 4 * g;
+        const int n = 16 * (nb_base + wn * 4 + j) + 4 * g;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int m = m0 + wm * 64 + 16 * i + lr;
@@ -255,7 +270,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
 
 // ---------------------------------------------------------------- fp32
 // One thread per (token, 4 output columns); 16 tokens x 16 column-quads per
-// workgroup with the K loop staged through LDS in 32-wide slices.
+// workgroup with the K loop staged through LDS in 32-wide slices.  Row-major W.
 __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int M, int K, int ldx,
                                                 const float* __restrict__ W, int N, EpiArgs e) {
     __shared__ float xs[16][33];
@@ -286,7 +301,55 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
     if (m < M && n < N) epilogue<float>(e, m, n, floatx4{acc[0], acc[1], acc[2], acc[3]});
 }
 
+// Fragment-major packing of a bf16 weight matrix (see the file comment), with
+// an optional row permutation: mode 1 puts rotary pairs (t, t + dh/2) of each
+// head on adjacent rows, mode 2 interleaves the rows of src0 (gate) and src1
+// (up).  One thread per 16-byte piece.
+__global__ void pack_frag_kernel(const bf16_t* __restrict__ src0, const bf16_t* __restrict__ src1,
+                                 bf16_t* __restrict__ dst, int N, int K, int mode, int dh) {
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)N * K / 8;
+    if (t >= total) return;
+    const int KU = K / 64;
+    const int lane = t & 63;
+    const int h = (t >> 6) & 1;
+    const size_t blk = t >> 7;                // (nb, u)
+    const int u = blk % KU, nb = blk / KU;
+    const int row = 16 * nb + (lane & 15);
+    const int k0 = 64 * u + 16 * (lane >> 4) + 8 * h;
+    const bf16_t* src;
+    if (mode == 1) {
+        const int head = row / dh, e = row % dh, tt = e / 2;
+        src = src0 + (size_t)(head * dh + ((e & 1) ? tt + dh / 2 : tt)) * K;
+    } else if (mode == 2) {
+        src = ((row & 1) ? src1 : src0) + (size_t)(row / 2) * K;
+    } else {
+        src = src0 + (size_t)row * K;
+    }
+    *reinterpret_cast<bf16x8*>(dst + t * 8) = *reinterpret_cast<const bf16x8*>(src + k0);
+}
+
 }  // namespace
+
+hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
+                            hipStream_t s) {
+    const size_t total = (size_t)N * K / 8;
+    hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                       (const bf16_t*)src0, (const bf16_t*)src1, (bf16_t*)dst, N, K, mode, dh);
+    return hipGetLastError();
+}
+
+int gemm_split(int dtype, int M, int N, int K) {
+    // the 64-token streaming kernel needs >= ~256 workgroups: split K across
+    // workgroups when the output has few 64-column tiles
+    if (dtype != DARD_DTYPE_BF16 || M > 64) return 1;
+    const int tiles = N / 64;
+    if (tiles >= 192) return 1;
+    int s = (256 + tiles - 1) / tiles;
+    const int KU = K / 64;
+    if (s > KU / 4) s = KU / 4 > 1 ? KU / 4 : 1;
+    return s > 8 ? 8 : s;
+}
 
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
                        const EpiArgs& e, int kernel_class, hipStream_t s) {
@@ -300,13 +363,11 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
     const bf16_t* x = reinterpret_cast<const bf16_t*>(X);
     const bf16_t* w = reinterpret_cast<const bf16_t*>(W);
     if (M <= 64) {
-        // enough workgroups to cover 256 CUs at least twice
-        if (N / 64 >= 512) {
-            hipLaunchKernelGGL((gemm_skinny_bf16<4, 4>), dim3((N + 63) / 64, 1), dim3(256), 0, s, x, M, K, ldx, w, N, e);
-        } else if (N / 32 >= 512) {
-            hipLaunchKernelGGL((gemm_skinny_bf16<2, 4>), dim3((N + 31) / 32, 1), dim3(256), 0, s, x, M, K, ldx, w, N, e);
+        const int split = e.kind == EPI_PARTIAL ? gemm_split(dtype, M, N, K) : 1;
+        if (N % 64 == 0) {
+            hipLaunchKernelGGL((gemm_stream_bf16<4, 2, 2>), dim3(N / 64, split), dim3(128), 0, s, x, M, K, ldx, w, N, e);
         } else {
-            hipLaunchKernelGGL((gemm_skinny_bf16<1, 8>), dim3((N + 15) / 16, 1), dim3(512), 0, s, x, M, K, ldx, w, N, e);
+            hipLaunchKernelGGL((gemm_stream_bf16<1, 4, 2>), dim3(N / 16, split), dim3(256), 0, s, x, M, K, ldx, w, N, e);
         }
         return hipGetLastError();
     }

@@ -38,7 +38,7 @@ size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys);
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---- gemm.hip
-enum EpiKind { EPI_STORE_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+enum EpiKind { EPI_STORE_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PARTIAL = 4 };
 struct EpiArgs {
     int kind;
     float* y;  int ldy;             // STORE_F32 / RESID (fp32, RESID adds)
@@ -51,9 +51,15 @@ struct EpiArgs {
     int P, B, cap, Hq, Hkv, dh;
     int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r
 };
-// Y = X * W^T with X [M][K] (leading dim ldx), W [N][K]; epilogue per `e`.
+// Y = X * W^T with X [M][K] (leading dim ldx), W [N][K] packed (bf16:
+// fragment-major, fp32: row-major); epilogue per `e`.  With EPI_PARTIAL the
+// output is gemm_split(...) fp32 partials [split][M][ldy] at e.y.
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
                        const EpiArgs& e, int kernel_class, hipStream_t s);
+int gemm_split(int dtype, int M, int N, int K);
+// bf16 fragment-major packing (mode 0 plain, 1 rotary-pair rows, 2 gate/up interleave)
+hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
+                            hipStream_t s);
 
 // ---- elementwise.hip
 // h[row] = embedding of ids[row] (or embeds[row] when ids[row] < 0), then
@@ -64,8 +70,10 @@ hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds,
                              const void* table, const void* gain, int rows, int d, int vocab,
                              float eps, int step_B, int mask_id, float* h, void* xn,
                              hipStream_t s);
-hipError_t launch_rmsnorm(int dtype, const float* h, const void* gain, int rows, int d,
-                          float eps, void* xn, hipStream_t s);
+// h[row] += sum of the nsplit fp32 partials part[s][row] (nsplit may be 0),
+// then xn[row] = RMSNorm(h[row]) * gain.  Needs d % 4 == 0, d <= 8192.
+hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit, int rows, int d,
+                             const void* gain, float eps, void* xn, hipStream_t s);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
                             int dh, hipStream_t s);

@@ -27,7 +27,7 @@ EXPORTS = [
     "dard_last_error", "dard_version", "dard_build_state_mask", "dard_attention_workspace_bytes",
     "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
-    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_linear", "dard_trace_enable",
+    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_pack_matrix", "dard_linear", "dard_trace_enable",
     "dard_trace_read", "dard_trace_reset",
 ]
 
@@ -82,6 +82,7 @@ def lib():
             "dard_workspace_bytes": (sz, [vp, i32, i32, i32]),
             "dard_prefill": (i32, [vp, vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]),
             "dard_step": (i32, [vp, vp, vp, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "dard_pack_matrix": (i32, [i32, vp, i32, i32, vp, vp]),
             "dard_linear": (i32, [i32, vp, i32, i32, vp, i32, vp, vp]),
             "dard_trace_enable": (i32, [u32]),
             "dard_trace_read": (i32, [i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]),
@@ -181,10 +182,15 @@ def dard_commit_remask(phase, params, state_in, maxprob_s=None, pcur_s=None, arg
                                     _p(tok_out), _p(conf_out), _p(block_done), _stream(stream)))
 
 
-def dard_linear(X, W, Y, stream=None):
+def dard_pack_matrix(W, Wp, stream=None):
+    N, K = W.shape
+    _check(lib().dard_pack_matrix(_dt(W), _p(W), N, K, _p(Wp), _stream(stream)))
+
+
+def dard_linear(X, Wp, N, Y, stream=None):
+    """Y = X W^T with W packed by dard_pack_matrix (Wp has N*K elements)."""
     M, K = X.shape
-    N = W.shape[0]
-    _check(lib().dard_linear(_dt(X), _p(X), M, K, _p(W), N, _p(Y), _stream(stream)))
+    _check(lib().dard_linear(_dt(X), _p(X), M, K, _p(Wp), N, _p(Y), _stream(stream)))
 
 
 def dard_trace_enable(mask):

@@ -34,7 +34,9 @@ def test_linear(dtype, M, N, K):
     X = torch.randn(M, K, generator=g).to(td)
     W = torch.randn(N, K, generator=g).to(td)
     Y = torch.empty(M, N, device="cuda")
-    dard.dard_linear(X.cuda(), W.cuda(), Y)
+    Wp = torch.empty_like(W).cuda()
+    dard.dard_pack_matrix(W.cuda(), Wp)
+    dard.dard_linear(X.cuda(), Wp, N, Y)
     torch.cuda.synchronize()
     ref = X.double().numpy() @ W.double().numpy().T
     scale = np.abs(X.double().numpy()) @ np.abs(W.double().numpy()).T
