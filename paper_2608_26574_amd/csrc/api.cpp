@@ -208,10 +208,13 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
     // as many partial slots as the given workspace holds
     const size_t slots = ws ? ws_bytes / ((size_t)dh * 4 + 8) : 0;
     a.part_slots = slots > 64 ? slots - 64 : 0;
-    a.part = (float*)ws;
-    a.part_ml = ws ? (float*)((char*)ws + align256(a.part_slots * dh * 4)) : nullptr;
-    TraceScope ts(DARD_K_ATTENTION, (hipStream_t)stream);
-    HIPOK(launch_attention(dtype, a, (hipStream_t)stream));
+    if (a.part_slots > 0) {
+        a.part = (float*)ws;
+        a.part_ml = (float*)((char*)ws + align256(a.part_slots * dh * 4));
+    }
+    hipStream_t s = (hipStream_t)stream;
+    TraceScope ts(DARD_K_ATTENTION, s);
+    HIPOK(launch_attention(dtype, a, s));
     return DARD_OK;
 }
 

@@ -1,17 +1,21 @@
 // State-masked attention over the augmented block (Sec. 2, Sec. 3.2).
 //
-// bf16 path: flash-style, one workgroup = 64 query rows of one (sequence,
-// query head), 4 waves of 16 rows.  K tiles of 64 keys are staged in LDS
-// row-major, V tiles transposed (key-contiguous), so that both products run on
-// v_mfma_f32_16x16x32_bf16:
+// bf16 path: flash-style.  A workgroup serves 64 query rows of one (sequence,
+// query head) with G groups of 4 waves (16 rows per wave); the groups take
+// interleaved 64-key tiles of the workgroup's key range and are merged
+// through LDS at the end, so a short key range costs few serial steps
+// without any cross-workgroup synchronisation.  Per group, K tiles are staged
+// in LDS row-major and V tiles transposed (key-contiguous), so that both
+// products run on v_mfma_f32_16x16x32_bf16:
 //   S^T = K * Q^T   (A = K rows from LDS, B = this wave's Q rows in registers)
 //   O^T += V^T P^T  (A = V^T from LDS, B = probabilities straight from the
 //                    S^T accumulators; the MFMA k index is permuted so that a
 //                    lane's 8 probabilities are its own score values)
-// The mask is built in-kernel: each row's "take x" bits (Eq. 2-3) live in LDS;
-// prefix keys are always visible, block key P+j is x^j, P+B+j is s^j.
-// Long key ranges are split across workgroups (flash-decoding) and merged by
-// a log-sum-exp combine.
+// The mask is built in-kernel: each wave derives its rows' "take x" bits (Eq. 2-3) with ballots;
+// prefix keys are always visible, block key P+j is x^j, P+B+j is s^j.  Tiles
+// that hold only prefix keys skip the per-key visibility test entirely.
+// Very long key ranges are additionally split across workgroups and merged
+// by a log-sum-exp combine kernel.
 //
 // fp32 path: one thread per (row, head), plain online softmax.
 #include "common.h"
@@ -21,69 +25,97 @@ namespace dard {
 
 namespace {
 
-constexpr int kRows = 64;   // query rows per workgroup
-constexpr int kKeys = 64;   // keys per tile
+constexpr int kRows = 64;      // query rows per workgroup
+constexpr int kKeys = 64;      // keys per tile
+// tiles in flight per group: two, or one when four groups share the registers
+constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 
-struct MaskSmem {
-    uint64_t sel[kRows][2];
+template <int DH>
+struct Lds {
+    static constexpr int KPAD = DH + 8;       // K row stride (bf16): 16-byte bank shift per row
+    static constexpr int VPAD = kKeys + 4;    // V^T row stride (bf16)
+    static constexpr int TILE_BYTES = (kKeys * KPAD + DH * VPAD) * 2;
+    static constexpr int MERGE_BYTES = (DH / 4 + 2) * 256 * 4;   // o, m, l of every lane
+    static constexpr int GROUP_BYTES = ((TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 15) / 16 * 16;
 };
 
-// Row visibility bits for the rows [r0, r0 + 64) of sequence s.
-__device__ void build_row_bits(const AttnArgs& a, int s, int r0, uint8_t* st, float* cf,
-                               uint64_t (*sel)[2]) {
-    for (int j = threadIdx.x; j < a.B; j += blockDim.x) {
-        st[j] = a.state[(size_t)s * a.B + j];
-        cf[j] = a.conf[(size_t)s * a.B + j];
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < kRows * 2; t += blockDim.x) {
-        const int rl = t >> 1, w = t & 1;
-        const int r = r0 + rl;
-        uint64_t word = 0;
-        if (r < a.R) {
-            const int i = r % a.B;
-            const bool shadow = r >= a.B;
-            const int j0 = w * 64, j1 = min(a.B, j0 + 64);
-            for (int j = j0; j < j1; ++j)
-                if (take_x(st[i], st[j], cf[i], cf[j], shadow, i == j, a.flags))
-                    word |= 1ull << (j - j0);
-        }
-        sel[rl][w] = word;
-    }
-    __syncthreads();
-}
+template <int DH, int G, int RING>
+__global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
+    using L = Lds<DH>;
+    constexpr int KPAD = L::KPAD, VPAD = L::VPAD;
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    __shared__ __attribute__((aligned(16))) char smem[G * L::GROUP_BYTES];
 
-template <int DH>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
-    constexpr int KPAD = DH + 8;      // K row stride (bf16): 16-byte bank shift per row
-    constexpr int VPAD = kKeys + 4;   // V^T row stride (bf16)
-    __shared__ __attribute__((aligned(16))) bf16_t Ks[kKeys * KPAD];
-    __shared__ __attribute__((aligned(16))) bf16_t Vt[DH * VPAD];
-    __shared__ uint64_t sel[kRows][2];
-    __shared__ uint8_t st[128];
-    __shared__ float cf[128];
-
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int grp = threadIdx.x >> 8, tid = threadIdx.x & 255;
+    const int lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, g = lane >> 4;
+    bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + grp * L::GROUP_BYTES);
+    bf16_t* Vt = Ks + kKeys * KPAD;
     int bid = blockIdx.x;
     const int rt = bid % rowtiles; bid /= rowtiles;
     const int h = bid % a.Hq;
     const int s = bid / a.Hq;
     const int kvh = h / (a.Hq / a.Hkv);
     const int r0 = rt * kRows;
-    const int split = blockIdx.y;
+    const int split = blockIdx.y, nsplit = gridDim.y;
 
     const int ntiles = (a.nkeys + kKeys - 1) / kKeys;
     const int t_begin = split * tiles_per_split;
     const int t_end = min(ntiles, t_begin + tiles_per_split);
     const int key_end = min(a.nkeys, t_end * kKeys);
-
-    if (a.masked) build_row_bits(a, s, r0, st, cf, sel);
+    const int iters = (t_end - t_begin + G - 1) / G;   // tile steps of every group
 
     const bf16_t* q = reinterpret_cast<const bf16_t*>(a.q);
     const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
     const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
+
+    // ---- issue the loads of this group's first RING tiles before anything else
+    constexpr int KCH = kKeys * DH / 8 / 256;  // 16-byte K chunks per thread
+    constexpr int VUNITS = (kKeys / 4) * (DH / 8);
+    bf16x8 kreg[RING][KCH];
+    bf16x8 vreg[RING][4];
+    auto load_tile = [&](int slot, int tile) {
+        const int kb0 = tile * kKeys;
+#pragma unroll
+        for (int it = 0; it < KCH; ++it) {
+            const int qd = tid + 256 * it;
+            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
+            const int kabs = kb0 + key;
+            bf16x8 z = {};
+            kreg[slot][it] = kabs < key_end ? ld_bf16x8(kbase + (size_t)kabs * DH + c8 * 8) : z;
+        }
+        if (tid < VUNITS) {
+            const int kg = tid / (DH / 8), dg = tid % (DH / 8);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int kabs = kb0 + 4 * kg + e;
+                bf16x8 z = {};
+                vreg[slot][e] = kabs < key_end ? ld_bf16x8(vbase + (size_t)kabs * DH + dg * 8) : z;
+            }
+        }
+    };
+    auto store_tile = [&](int slot) {
+#pragma unroll
+        for (int it = 0; it < KCH; ++it) {
+            const int qd = tid + 256 * it;
+            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
+            *reinterpret_cast<bf16x8*>(&Ks[key * KPAD + c8 * 8]) = kreg[slot][it];
+        }
+        if (tid < VUNITS) {
+            const int kg = tid / (DH / 8), dg = tid % (DH / 8);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                bf16x4 t4 = {vreg[slot][0][e], vreg[slot][1][e], vreg[slot][2][e], vreg[slot][3][e]};
+                *reinterpret_cast<bf16x4*>(&Vt[(dg * 8 + e) * VPAD + 4 * kg]) = t4;
+            }
+        }
+    };
+#pragma unroll
+    for (int sl = 0; sl < RING; ++sl) {
+        const int tile = t_begin + grp + G * sl;
+        if (sl < iters && tile < t_end) load_tile(sl, tile);
+    }
 
     // this lane's query row and its Q fragments (B operand of S^T = K Q^T)
     const int my_row = r0 + wave * 16 + lr;
@@ -97,8 +129,18 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles
             qf[c] = row_ok ? ld_bf16x8(qp + 32 * c + 8 * g) : z;
         }
     }
-    const uint64_t sel0 = a.masked ? sel[wave * 16 + lr][0] : 0;
-    const uint64_t sel1 = a.masked ? sel[wave * 16 + lr][1] : 0;
+    // this lane's row of the state mask, built by its wave with ballots
+    uint64_t sel0 = 0, sel1 = 0;
+    if (a.masked) {
+        const BlockView bv = load_block_view(a.state + (size_t)s * a.B, a.conf + (size_t)s * a.B, a.B);
+        for (int k = 0; k < 16; ++k) {
+            const int r = r0 + wave * 16 + k;      // the same on every lane of the wave
+            if (r >= a.R) break;
+            uint64_t x0, x1;
+            row_take_x(bv, r, a.B, a.flags, x0, x1);
+            if (lr == k) { sel0 = x0; sel1 = x1; }
+        }
+    }
     const float sl2 = a.scale * kLog2e;
 
     floatx4 o[DH / 16];
@@ -106,56 +148,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles
     for (int d = 0; d < DH / 16; ++d) o[d] = floatx4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    // cooperative tile loads: K 4 chunks of 16 B per thread, V 4 rows x 16 B
-    constexpr int KCH = kKeys * DH / 8 / 256;  // 16-byte K chunks per thread
-    constexpr int VUNITS = (kKeys / 4) * (DH / 8);
-    bf16x8 kreg[KCH];
-    bf16x8 vreg[4];
-    auto load_tile = [&](int tile) {
-        const int kb0 = tile * kKeys;
-#pragma unroll
-        for (int it = 0; it < KCH; ++it) {
-            const int qd = threadIdx.x + 256 * it;
-            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
-            const int kabs = kb0 + key;
-            bf16x8 z = {};
-            kreg[it] = kabs < key_end ? ld_bf16x8(kbase + (size_t)kabs * DH + c8 * 8) : z;
-        }
-        if (threadIdx.x < VUNITS) {
-            const int kg = threadIdx.x / (DH / 8), dg = threadIdx.x % (DH / 8);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int kabs = kb0 + 4 * kg + e;
-                bf16x8 z = {};
-                vreg[e] = kabs < key_end ? ld_bf16x8(vbase + (size_t)kabs * DH + dg * 8) : z;
-            }
-        }
-    };
-    auto store_tile = [&]() {
-#pragma unroll
-        for (int it = 0; it < KCH; ++it) {
-            const int qd = threadIdx.x + 256 * it;
-            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
-            *reinterpret_cast<bf16x8*>(&Ks[key * KPAD + c8 * 8]) = kreg[it];
-        }
-        if (threadIdx.x < VUNITS) {
-            const int kg = threadIdx.x / (DH / 8), dg = threadIdx.x % (DH / 8);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-                bf16x4 t4 = {vreg[0][e], vreg[1][e], vreg[2][e], vreg[3][e]};
-                *reinterpret_cast<bf16x4*>(&Vt[(dg * 8 + e) * VPAD + 4 * kg]) = t4;
-            }
-        }
-    };
-
-    if (t_begin < t_end) load_tile(t_begin);
-    for (int tile = t_begin; tile < t_end; ++tile) {
-        __syncthreads();   // previous tile fully consumed
-        store_tile();
-        __syncthreads();
-        if (tile + 1 < t_end) load_tile(tile + 1);
-
+    auto compute_tile = [&](int tile) {
         // ---- S^T = K * Q^T for this wave's 16 rows: 4 blocks of 16 keys
         floatx4 sc[4];
 #pragma unroll
@@ -168,25 +161,36 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles
             }
             sc[kb] = acc;
         }
-        // ---- scale, mask, tile max
+        // ---- scale; visibility only where the tile has block keys or a tail
         const int kb0 = tile * kKeys;
+        const bool all_visible = kb0 + kKeys <= key_end && (!a.masked || kb0 + kKeys <= a.P);
         float mt = -INFINITY;
+        if (all_visible) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+            for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = kb0 + 16 * kb + 4 * g + i;
-                bool vis = key < key_end;
-                if (a.masked && key >= a.P) {
-                    const int j = key - a.P;
-                    const int jj = j < a.B ? j : j - a.B;
-                    const uint64_t word = jj < 64 ? sel0 : sel1;
-                    const bool bx = (word >> (jj & 63)) & 1ull;
-                    vis = vis && (j < a.B ? bx : !bx);
+                for (int i = 0; i < 4; ++i) {
+                    sc[kb][i] *= sl2;
+                    mt = fmaxf(mt, sc[kb][i]);
                 }
-                const float v = vis ? sc[kb][i] * sl2 : -INFINITY;
-                sc[kb][i] = v;
-                mt = fmaxf(mt, v);
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = kb0 + 16 * kb + 4 * g + i;
+                    bool vis = key < key_end;
+                    if (a.masked && key >= a.P) {
+                        const int j = key - a.P;
+                        const int jj = j < a.B ? j : j - a.B;
+                        const uint64_t word = jj < 64 ? sel0 : sel1;
+                        const bool bx = (word >> (jj & 63)) & 1ull;
+                        vis = vis && (j < a.B ? bx : !bx);
+                    }
+                    const float v = vis ? sc[kb][i] * sl2 : -INFINITY;
+                    sc[kb][i] = v;
+                    mt = fmaxf(mt, v);
+                }
             }
         }
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
@@ -208,13 +212,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles
         m_run = m_new;
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
-
         // ---- O^T += V^T * P^T
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) {
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
-                typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
                 const bf16_t* vp = &Vt[(16 * d + lr) * VPAD + 32 * c + 4 * g];
                 const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vp);
                 const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vp + 16);
@@ -222,59 +224,132 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, int rowtiles
                 o[d] = mfma16x16x32(vf, pb[c], o[d]);
             }
         }
+    };
+
+    for (int base = 0; base < iters; base += RING) {
+#pragma unroll
+        for (int sl = 0; sl < RING; ++sl) {
+            const int it = base + sl;
+            if (it < iters) {                     // uniform across the workgroup
+                const int tile = t_begin + grp + G * it;
+                const bool mine = tile < t_end;
+                __syncthreads();                  // the previous tiles are fully consumed
+                if (mine) store_tile(sl);
+                __syncthreads();
+                if (mine) {
+                    const int next = tile + G * RING;
+                    if (next < t_end) load_tile(sl, next);
+                    compute_tile(tile);
+                }
+            }
+        }
+    }
+
+    // ---- merge the groups through LDS (group 0 keeps the result)
+    if constexpr (G > 1) {
+        __syncthreads();
+        float* mb = reinterpret_cast<float*>(smem + grp * L::GROUP_BYTES);
+        if (grp > 0) {
+#pragma unroll
+            for (int d = 0; d < DH / 16; ++d)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mb[(4 * d + i) * 256 + tid] = o[d][i];
+            mb[(DH / 4) * 256 + tid] = m_run;
+            mb[(DH / 4 + 1) * 256 + tid] = l_run;
+        }
+        __syncthreads();
+        if (grp > 0) return;
+        float M = m_run;
+#pragma unroll
+        for (int gg = 1; gg < G; ++gg)
+            M = fmaxf(M, reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES)[(DH / 4) * 256 + tid]);
+        const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
+        float lsum = l_run * f0;
+#pragma unroll
+        for (int d = 0; d < DH / 16; ++d) o[d] *= f0;
+#pragma unroll
+        for (int gg = 1; gg < G; ++gg) {
+            const float* ob = reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES);
+            const float mg = ob[(DH / 4) * 256 + tid];
+            const float f = mg == -INFINITY ? 0.f : exp2f(mg - M);
+            lsum += ob[(DH / 4 + 1) * 256 + tid] * f;
+#pragma unroll
+            for (int d = 0; d < DH / 16; ++d)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[d][i] += ob[(4 * d + i) * 256 + tid] * f;
+        }
+        m_run = M;
+        l_run = lsum;
     }
 
     // ---- epilogue: row sum over the 4 lanes sharing a row
     float l_tot = l_run + __shfl_xor(l_run, 16, 64);
     l_tot += __shfl_xor(l_tot, 32, 64);
     if (!row_ok) return;
+    const size_t nrow = (size_t)a.b * a.R * a.Hq;
     const size_t orow = ((size_t)s * a.R + my_row) * a.Hq + h;
-    if (gridDim.y == 1) {
+    if (nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
         bf16_t* out = reinterpret_cast<bf16_t*>(a.out) + orow * DH;
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) {
-            uint32_t w0 = (uint32_t)f2bf(o[d][0] * inv) | ((uint32_t)f2bf(o[d][1] * inv) << 16);
-            uint32_t w1 = (uint32_t)f2bf(o[d][2] * inv) | ((uint32_t)f2bf(o[d][3] * inv) << 16);
+            const uint32_t w0 = (uint32_t)f2bf(o[d][0] * inv) | ((uint32_t)f2bf(o[d][1] * inv) << 16);
+            const uint32_t w1 = (uint32_t)f2bf(o[d][2] * inv) | ((uint32_t)f2bf(o[d][3] * inv) << 16);
             *reinterpret_cast<uint2*>(out + 16 * d + 4 * g) = make_uint2(w0, w1);
         }
-    } else {
-        const size_t nrow = (size_t)a.b * a.R * a.Hq;
-        float* po = a.part + ((size_t)split * nrow + orow) * DH;
+        return;
+    }
+    float* po = a.part + ((size_t)split * nrow + orow) * DH;
 #pragma unroll
-        for (int d = 0; d < DH / 16; ++d)
-            *reinterpret_cast<float4*>(po + 16 * d + 4 * g) = make_float4(o[d][0], o[d][1], o[d][2], o[d][3]);
-        if (g == 0) {
-            float* pm = a.part_ml + ((size_t)split * nrow + orow) * 2;
-            pm[0] = m_run;
-            pm[1] = l_tot;
-        }
+    for (int d = 0; d < DH / 16; ++d)
+        *reinterpret_cast<float4*>(po + 16 * d + 4 * g) = make_float4(o[d][0], o[d][1], o[d][2], o[d][3]);
+    if (g == 0) {
+        float* pm = a.part_ml + ((size_t)split * nrow + orow) * 2;
+        pm[0] = m_run;
+        pm[1] = l_tot;
     }
 }
 
-// Merge split partials: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).
-template <typename T>
-__global__ __launch_bounds__(128) void attn_combine_kernel(const float* __restrict__ part,
-                                                           const float* __restrict__ part_ml,
-                                                           int nsplit, size_t nrow, int dh,
-                                                           T* __restrict__ out) {
-    const size_t row = blockIdx.x;
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, part_ml[(sp * nrow + row) * 2]);
-    float L = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) {
-        const float m = part_ml[(sp * nrow + row) * 2];
-        if (m != -INFINITY) L += part_ml[(sp * nrow + row) * 2 + 1] * exp2f(m - M);
-    }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    for (int e = threadIdx.x; e < dh; e += blockDim.x) {
-        float acc = 0.f;
-        for (int sp = 0; sp < nsplit; ++sp) {
-            const float m = part_ml[(sp * nrow + row) * 2];
-            if (m != -INFINITY) acc += part[(sp * nrow + row) * dh + e] * exp2f(m - M);
+// Merge key splits: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).  One
+// thread per (row, head, 4 dims); every load of a thread is issued up front.
+template <int DH>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
+                                                           const float* __restrict__ part_ml, int ns,
+                                                           size_t nrow, bf16_t* __restrict__ out) {
+    const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t row = t / (DH / 4);
+    const int q4 = t % (DH / 4);
+    if (row >= nrow) return;
+    float m[kMaxSplit], l[kMaxSplit];
+    float4 ov[kMaxSplit];
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp) {
+        if (sp < ns) {
+            m[sp] = part_ml[(sp * nrow + row) * 2];
+            l[sp] = part_ml[(sp * nrow + row) * 2 + 1];
+            ov[sp] = reinterpret_cast<const float4*>(part + (sp * nrow + row) * DH)[q4];
+        } else {
+            m[sp] = -INFINITY;
+            l[sp] = 0.f;
+            ov[sp] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        St<T>::st(out + row * dh + e, acc * inv);
     }
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp) M = fmaxf(M, m[sp]);
+    float Lsum = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp) {
+        if (m[sp] == -INFINITY) continue;
+        const float f = exp2f(m[sp] - M);
+        Lsum += l[sp] * f;
+        acc.x += ov[sp].x * f; acc.y += ov[sp].y * f; acc.z += ov[sp].z * f; acc.w += ov[sp].w * f;
+    }
+    const float inv = Lsum > 0.f ? 1.f / Lsum : 0.f;
+    const uint32_t w0 = (uint32_t)f2bf(acc.x * inv) | ((uint32_t)f2bf(acc.y * inv) << 16);
+    const uint32_t w1 = (uint32_t)f2bf(acc.z * inv) | ((uint32_t)f2bf(acc.w * inv) << 16);
+    *reinterpret_cast<uint2*>(out + row * DH + 4 * q4) = make_uint2(w0, w1);
 }
 
 // fp32 path: one thread per (sequence, row, head).
@@ -319,6 +394,17 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     for (int e = 0; e < DH; ++e) out[e] = o[e] * inv;
 }
 
+// Groups per workgroup: aim at >= 1024 waves over the chip.  Four groups
+// leave 128 registers per lane, enough only for head_dim 64.
+int attention_groups(int b, int R, int Hq, int dh, int ntiles) {
+    const int wgs = b * Hq * ((R + kRows - 1) / kRows);
+    int G = (1024 + 4 * wgs - 1) / (4 * wgs);
+    G = G >= 4 ? 4 : (G >= 2 ? 2 : 1);
+    if (dh == 128 && G > 2) G = 2;
+    while (G > 1 && G > ntiles) G >>= 1;
+    return G;
+}
+
 }  // namespace
 
 int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots) {
@@ -326,13 +412,14 @@ int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots) {
     const int rowtiles = (R + kRows - 1) / kRows;
     const int ntiles = (nkeys + kKeys - 1) / kKeys;
     const int wgs = b * Hq * rowtiles;
-    int ns = (512 + wgs - 1) / wgs;       // aim at >= 512 workgroups
-    ns = ns < 1 ? 1 : (ns > ntiles ? ntiles : ns);
-    if (ns > 16) ns = 16;
-    // never more partial slots (split, row, head) than the workspace holds
+    const int G = attention_groups(b, R, Hq, 128, ntiles);   // the head_dim 128 grouping
+    // split across workgroups only while the chip is not yet covered and
+    // every group would still walk more than 3 tiles
+    int ns = 1;
+    while (ns < kMaxSplit && wgs * ns * G * 4 < 1024 && ntiles / (ns * G) > 3) ns *= 2;
     const size_t per_split = (size_t)b * R * Hq;
     while (ns > 1 && (size_t)ns * per_split > slots) --ns;
-    if (ns <= 1 || ntiles == 0) return 1;
+    if (ns <= 1) return 1;
     const int tps = (ntiles + ns - 1) / ns;
     return (ntiles + tps - 1) / tps;      // no empty split
 }
@@ -342,22 +429,35 @@ size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys) {
     return ns <= 1 ? 0 : (size_t)ns * b * R * Hq;
 }
 
-hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStream_t s) {
     if (dtype == DARD_DTYPE_BF16) {
         const int rowtiles = (a.R + kRows - 1) / kRows;
         const int ntiles = (a.nkeys + kKeys - 1) / kKeys;
-        const int ns = (a.part && a.part_ml) ? attention_splits(dtype, a.b, a.R, a.Hq, a.nkeys, a.part_slots) : 1;
+        const bool can_split = a.part && a.part_ml;
+        if (!can_split || ns < 1 || ns > kMaxSplit || (size_t)ns * a.b * a.R * a.Hq > a.part_slots) ns = 1;
+        if (ns > ntiles) ns = ntiles > 0 ? ntiles : 1;
         const int tps = (ntiles + ns - 1) / ns;
+        ns = ntiles > 0 ? (ntiles + tps - 1) / tps : 1;
+        const int G = attention_groups(a.b, a.R, a.Hq, a.dh, tps);
         dim3 grid(a.b * a.Hq * rowtiles, ns);
-        if (a.dh == 128)
-            hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, dim3(256), 0, s, a, rowtiles, tps);
-        else
-            hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, dim3(256), 0, s, a, rowtiles, tps);
+#define DARD_ATT(DHV, GV) \
+    hipLaunchKernelGGL((attn_bf16_kernel<DHV, GV, GV == 4 ? 1 : 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
+        if (a.dh == 128) {
+            if (G == 4) DARD_ATT(128, 4); else if (G == 2) DARD_ATT(128, 2); else DARD_ATT(128, 1);
+        } else {
+            if (G == 4) DARD_ATT(64, 4); else if (G == 2) DARD_ATT(64, 2); else DARD_ATT(64, 1);
+        }
+#undef DARD_ATT
         hipError_t e = hipGetLastError();
         if (e != hipSuccess || ns == 1) return e;
         const size_t nrow = (size_t)a.b * a.R * a.Hq;
-        hipLaunchKernelGGL(attn_combine_kernel<bf16_t>, dim3(nrow), dim3(128), 0, s, a.part,
-                           a.part_ml, ns, nrow, a.dh, reinterpret_cast<bf16_t*>(a.out));
+        const size_t threads = nrow * (a.dh / 4);
+        if (a.dh == 128)
+            hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
+                               a.part_ml, ns, nrow, reinterpret_cast<bf16_t*>(a.out));
+        else
+            hipLaunchKernelGGL(attn_combine_kernel<64>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
+                               a.part_ml, ns, nrow, reinterpret_cast<bf16_t*>(a.out));
         return hipGetLastError();
     }
     const size_t total = (size_t)a.b * a.R * a.Hq;
@@ -367,6 +467,12 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     else
         hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, s, a);
     return hipGetLastError();
+}
+
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
+    const bool can_split = a.part && a.part_ml;
+    const int ns = can_split ? attention_splits(dtype, a.b, a.R, a.Hq, a.nkeys, a.part_slots) : 1;
+    return launch_attention_splits(dtype, a, ns, s);
 }
 
 }  // namespace dard

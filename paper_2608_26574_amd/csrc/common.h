@@ -82,4 +82,57 @@ __device__ __forceinline__ bool take_x(int si, int sj, float ci, float cj, bool 
     return true;
 }
 
+// The same rule for whole rows, one wave at a time: lane l holds positions l
+// and l + 64 of the block (B <= 128), ballots give the U and C sets as bit
+// masks, and a candidate row's set {j in C : c_i <= c_j} (Eq. 3) is one more
+// ballot.  Every lane of the wave must call these with the same arguments.
+struct BlockView {
+    int s0, s1;        // states of positions lane, lane + 64 (-1 beyond B)
+    float c0, c1;      // their confidences
+    uint64_t U0, U1, C0, C1;
+};
+
+__device__ __forceinline__ BlockView load_block_view(const uint8_t* state, const float* conf, int B) {
+    const int lane = threadIdx.x & 63;
+    BlockView v;
+    v.s0 = lane < B ? (int)state[lane] : -1;
+    v.s1 = lane + 64 < B ? (int)state[lane + 64] : -1;
+    v.c0 = lane < B ? conf[lane] : 0.f;
+    v.c1 = lane + 64 < B ? conf[lane + 64] : 0.f;
+    v.U0 = __ballot(v.s0 == DARD_STATE_U);
+    v.U1 = __ballot(v.s1 == DARD_STATE_U);
+    v.C0 = __ballot(v.s0 == DARD_STATE_C);
+    v.C1 = __ballot(v.s1 == DARD_STATE_C);
+    return v;
+}
+
+// "Take x" words (positions 0..63, 64..127) of query row r (x rows r < B,
+// shadow rows r >= B); r must be the same on every lane.
+__device__ __forceinline__ void row_take_x(const BlockView& v, int r, int B, uint32_t flags, uint64_t& x0,
+                                           uint64_t& x1) {
+    const int i = r % B;
+    const bool shadow = r >= B;
+    const int sa = __shfl(v.s0, i & 63, 64), sb = __shfl(v.s1, i & 63, 64);
+    const float ca = __shfl(v.c0, i & 63, 64), cb = __shfl(v.c1, i & 63, 64);
+    const int si = i < 64 ? sa : sb;
+    const float ci = i < 64 ? ca : cb;
+    const uint64_t self0 = i < 64 ? 1ull << i : 0ull, self1 = i < 64 ? 0ull : 1ull << (i - 64);
+    const uint64_t all0 = B >= 64 ? ~0ull : (1ull << B) - 1;
+    const uint64_t all1 = B >= 128 ? ~0ull : (B > 64 ? (1ull << (B - 64)) - 1 : 0ull);
+    if (si == DARD_STATE_U) {
+        x0 = v.U0; x1 = v.U1;
+        if (shadow || (flags & DARD_F_XSELF_SHADOW)) { x0 &= ~self0; x1 &= ~self1; }
+    } else if (si == DARD_STATE_C) {
+        x0 = v.U0 | __ballot(v.s0 == DARD_STATE_C && ci <= v.c0);
+        x1 = v.U1 | __ballot(v.s1 == DARD_STATE_C && ci <= v.c1);
+        if (shadow) { x0 &= ~self0; x1 &= ~self1; }
+    } else if (shadow) {
+        x0 = v.U0; x1 = v.U1;
+    } else if (flags & DARD_F_MKEYS_SHADOW) {
+        x0 = v.U0 | v.C0 | self0; x1 = v.U1 | v.C1 | self1;
+    } else {
+        x0 = all0; x1 = all1;
+    }
+}
+
 }  // namespace dard

@@ -64,15 +64,28 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
     const bool use_x = lx != nullptr && w != 0.f;
     const bool use_s = !(lx != nullptr && w == 1.f);
 
-    const int begin = ch * a.chunk;
-    const int end = min(a.V, begin + a.chunk);
+    const int begin = ch * kChunk;
+    const int end = min(a.V, begin + kChunk);
     Acc acc{-INFINITY, 0x7fffffff, 0.f};
-    for (int i = begin + 4 * threadIdx.x; i < end; i += 4 * 256) {
+    // every full float4 of this thread is loaded before any arithmetic
+    constexpr int kIt = kChunk / (4 * 256);
+    float4 sv4[kIt], xv4[kIt];
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        const int i = begin + 4 * threadIdx.x + 4 * 256 * it;
+        const bool full = i + 4 <= end;
+        sv4[it] = (use_s && full) ? *reinterpret_cast<const float4*>(ls + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        xv4[it] = (use_x && full) ? *reinterpret_cast<const float4*>(lx + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int it = 0; it < kIt; ++it) {
+        const int i = begin + 4 * threadIdx.x + 4 * 256 * it;
+        if (i >= end) break;
         float v[4];
         if (i + 4 <= end) {
-            const float4 sv = use_s ? *reinterpret_cast<const float4*>(ls + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 sv = sv4[it];
             if (use_x) {
-                const float4 xv = *reinterpret_cast<const float4*>(lx + i);
+                const float4 xv = xv4[it];
                 if (use_s) {
                     v[0] = mixv(xv.x, sv.x, w, omw); v[1] = mixv(xv.y, sv.y, w, omw);
                     v[2] = mixv(xv.z, sv.z, w, omw); v[3] = mixv(xv.w, sv.w, w, omw);

@@ -2,7 +2,9 @@
 // promotion / demotion sets, the guidance weight of masked tokens (Eq. 5-6)
 // and the three-state transition with token fill (Eq. 8).  One workgroup per
 // sequence, one thread per block position.  Distance-weighted sums are formed
-// in float64 in position order.
+// in float64 in position order from a table of lambda^k.  In step mode the
+// vocab-chunk partials of the confidence reduction are first copied to LDS
+// in one coalesced pass and merged there in chunk order.
 #include "common.h"
 #include "launch.h"
 
@@ -41,18 +43,36 @@ __device__ Red combine(const float* p, int nchunk) {
     return t;
 }
 
-// Confidence, prediction and current-token probability of one position from
-// either the per-position arrays or (step mode) the chunk partials.
+// Copy n floats from global to LDS with all of a thread's loads in flight.
+__device__ void stage(float* dst, const float* src, int n) {
+    constexpr int U = 8;
+    for (int base = 0; base < n; base += U * 128) {
+        float v[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int t = base + k * 128 + threadIdx.x;
+            v[k] = t < n ? src[t] : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int t = base + k * 128 + threadIdx.x;
+            if (t < n) dst[t] = v[k];
+        }
+    }
+}
+
 struct PosConf {
     float maxprob, pcur;
     int argmax;
 };
 
+// Shadow-row confidence of position i: from staged chunk partials (step mode)
+// or from the per-position arrays.
 __device__ PosConf shadow_conf(const DecideArgs& a, const float* part, int s, int i, int tok) {
     PosConf r;
     const int pos = s * a.B + i;
     if (part) {
-        const Red t = combine(part + (size_t)pos * a.nchunk * 3, a.nchunk);
+        const Red t = combine(part + (size_t)i * a.nchunk * 3, a.nchunk);
         r.maxprob = 1.f / t.s;
         r.argmax = t.a;
         tok = min(max(tok, 0), (int)a.ld - 1);   // stay inside the row whatever the id
@@ -67,20 +87,29 @@ __device__ PosConf shadow_conf(const DecideArgs& a, const float* part, int s, in
 }
 
 __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
+    extern __shared__ float staged[];            // [2][B][nchunk][3] in step mode
     __shared__ uint8_t promoted[128], demoted[128];
+    __shared__ double lam_pow[128];
     __shared__ int all_u;
     const int s = blockIdx.x, i = threadIdx.x;
     const bool live = i < a.B;
     const int pos = s * a.B + i;
     const int st = live ? a.state_in[pos] : DARD_STATE_U;
     const bool pcur_mode = (a.flags & DARD_F_VERIFY_PCUR) != 0;
+    const int per_seq = a.B * a.nchunk * 3;
+    float* sv = staged;
+    float* sm = staged + per_seq;
+    if (a.part_v) stage(sv, a.part_v + (size_t)s * per_seq, per_seq);
+    if (a.part_m && a.phase == DARD_PHASE_FINAL) stage(sm, a.part_m + (size_t)s * per_seq, per_seq);
 
     if (a.phase == DARD_PHASE_VERIFY) {
         promoted[i] = 0;
         demoted[i] = 0;
+        if (live) lam_pow[i] = pow(a.lambda, (double)i);
+        __syncthreads();
         if (live && st == DARD_STATE_C) {
             const int tok = a.tok_in ? a.tok_in[pos] : 0;
-            const PosConf pc = shadow_conf(a, a.part_v, s, i, tok);
+            const PosConf pc = shadow_conf(a, a.part_v ? sv : nullptr, s, i, tok);
             const float c = pcur_mode ? pc.pcur : pc.maxprob;
             const int nxt = transition(c, a.tau_c, a.tau_u);
             promoted[i] = nxt == DARD_STATE_U;
@@ -92,8 +121,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         if (st == DARD_STATE_M) {
             double P = 0.0, D = 0.0;
             for (int j = 0; j < a.B; ++j) {
-                if (!(promoted[j] | demoted[j])) continue;
-                const double k = pow(a.lambda, (double)abs(i - j));
+                const double k = lam_pow[abs(i - j)];
                 if (promoted[j]) P += k;
                 if (demoted[j]) D += k;
             }
@@ -114,7 +142,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         int am_s = -1, am_mix = -1;
         if (st == DARD_STATE_M) {
             if (a.part_m) {
-                const Red t = combine(a.part_m + (size_t)pos * a.nchunk * 3, a.nchunk);
+                const Red t = combine(sm + (size_t)i * a.nchunk * 3, a.nchunk);
                 mp_mix = 1.f / t.s;
                 am_mix = t.a;
             } else {
@@ -124,7 +152,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
             c = mp_mix;
             xhat = am_mix;
         } else {
-            const float* part = a.part_m ? (st == DARD_STATE_C ? a.part_v : a.part_m) : nullptr;
+            const float* part = a.part_m ? (st == DARD_STATE_C ? sv : sm) : nullptr;
             const PosConf pc = shadow_conf(a, part, s, i, tok);
             mp_s = pc.maxprob; pc_s = pc.pcur; am_s = pc.argmax;
             c = pcur_mode ? pc.pcur : pc.maxprob;
@@ -149,7 +177,9 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
 
 hipError_t launch_decide(const DecideArgs& a, hipStream_t s) {
     TraceScope ts(DARD_K_DECIDE, s);
-    hipLaunchKernelGGL(decide_kernel, dim3(a.b), dim3(128), 0, s, a);
+    const size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * 3 * sizeof(float) : 0;
+    if (lds > 96 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(decide_kernel, dim3(a.b), dim3(128), lds, s, a);
     return hipGetLastError();
 }
 

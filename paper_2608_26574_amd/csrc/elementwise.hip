@@ -55,41 +55,52 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(const int32_t* __restri
 
 // h[row] += sum_s part[s][row] (split-K partials of the preceding projection,
 // added in split order), then xn[row] = RMSNorm(h[row]) * gain.  One
-// workgroup per row, each thread holding up to kVec float4 of the row.
-constexpr int kVec = 8;   // d <= 256 * 4 * kVec
+// workgroup of 512 threads per row, each thread holding up to kVec float4 of the row.
+constexpr int kVec = 4;   // d <= 512 * 4 * kVec
 
-template <typename T>
-__global__ __launch_bounds__(256) void resid_norm_kernel(float* __restrict__ h, const float* __restrict__ part,
-                                                         int nsplit, size_t split_stride, const T* __restrict__ gain,
+// NS is the split count (0 = no partials); all loads of a thread are issued
+// before the first add so that the row costs one memory round trip.
+template <typename T, int NS>
+__global__ __launch_bounds__(512) void resid_norm_kernel(float* __restrict__ h, const float* __restrict__ part,
+                                                         size_t split_stride, const T* __restrict__ gain,
                                                          int d, float eps, T* __restrict__ xn) {
-    __shared__ float red[4];
+    __shared__ float red[8];
     const size_t row = blockIdx.x;
     float4* hr = reinterpret_cast<float4*>(h + row * d);
     const int n4 = d / 4;
     float4 v[kVec];
+    float4 p[NS > 0 ? NS : 1][kVec];
+#pragma unroll
+    for (int q = 0; q < kVec; ++q) {
+        const int c4 = threadIdx.x + 512 * q;
+        v[q] = c4 < n4 ? hr[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            p[s][q] = c4 < n4 ? reinterpret_cast<const float4*>(part + s * split_stride + row * d)[c4]
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     float ss = 0.f;
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
-        const int c4 = threadIdx.x + 256 * q;
-        if (c4 < n4) {
-            float4 x = hr[c4];
-            for (int s = 0; s < nsplit; ++s) {
-                const float4 p = reinterpret_cast<const float4*>(part + s * split_stride + row * d)[c4];
-                x.x += p.x; x.y += p.y; x.z += p.z; x.w += p.w;
-            }
-            if (nsplit > 0) hr[c4] = x;
-            v[q] = x;
-            ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
-        }
+        const int c4 = threadIdx.x + 512 * q;
+        float4 x = v[q];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) { x.x += p[s][q].x; x.y += p[s][q].y; x.z += p[s][q].z; x.w += p[s][q].w; }
+        if (NS > 0 && c4 < n4) hr[c4] = x;
+        v[q] = x;
+        ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
     }
     ss = wave_sum(ss);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
     __syncthreads();
-    const float inv = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) tot += red[w];
+    const float inv = rsqrtf(tot / (float)d + eps);
     T* out = xn + row * d;
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
-        const int c4 = threadIdx.x + 256 * q;
+        const int c4 = threadIdx.x + 512 * q;
         if (c4 < n4) {
             const int c = 4 * c4;
             St<T>::st(out + c, v[q].x * inv * St<T>::ld(gain + c));
@@ -153,12 +164,23 @@ hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit,
                              const void* gain, float eps, void* xn, hipStream_t s) {
     TraceScope ts(DARD_K_NORM, s);
     const size_t stride = (size_t)rows * d;
-    if (dtype == DARD_DTYPE_BF16)
-        hipLaunchKernelGGL(resid_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, part, nsplit, stride,
-                           (const bf16_t*)gain, d, eps, (bf16_t*)xn);
-    else
-        hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(rows), dim3(256), 0, s, h, part, nsplit, stride,
-                           (const float*)gain, d, eps, (float*)xn);
+    if (nsplit < 0 || nsplit > 8 || d > 512 * 4 * kVec) return hipErrorInvalidValue;
+#define DARD_RN(T, NS)                                                                                 \
+    hipLaunchKernelGGL((resid_norm_kernel<T, NS>), dim3(rows), dim3(512), 0, s, h, part, stride,      \
+                       (const T*)gain, d, eps, (T*)xn)
+#define DARD_RN_ALL(T)                                                                                 \
+    switch (nsplit) {                                                                                  \
+    case 0: DARD_RN(T, 0); break; case 1: DARD_RN(T, 1); break; case 2: DARD_RN(T, 2); break;          \
+    case 3: DARD_RN(T, 3); break; case 4: DARD_RN(T, 4); break; case 5: DARD_RN(T, 5); break;          \
+    case 6: DARD_RN(T, 6); break; case 7: DARD_RN(T, 7); break; default: DARD_RN(T, 8); break;         \
+    }
+    if (dtype == DARD_DTYPE_BF16) {
+        DARD_RN_ALL(bf16_t)
+    } else {
+        DARD_RN_ALL(float)
+    }
+#undef DARD_RN_ALL
+#undef DARD_RN
     return hipGetLastError();
 }
 

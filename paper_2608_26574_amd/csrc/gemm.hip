@@ -339,16 +339,45 @@ hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N
     return hipGetLastError();
 }
 
-int gemm_split(int dtype, int M, int N, int K) {
-    // the 64-token streaming kernel needs >= ~256 workgroups: split K across
-    // workgroups when the output has few 64-column tiles
-    if (dtype != DARD_DTYPE_BF16 || M > 64) return 1;
-    const int tiles = N / 64;
-    if (tiles >= 192) return 1;
-    int s = (256 + tiles - 1) / tiles;
+// Configuration of the streaming kernel for one projection shape:
+//   nw     16-column blocks per wave (wave tile 16*nw columns)
+//   ks     waves per workgroup splitting K
+//   depth  k units in flight per wave
+//   split  workgroups splitting K (fp32 partials, reduced by the consumer)
+// Chosen from measurements on MI355X at 64 tokens: the widest wave tile whose
+// grid fills the 256 CUs most evenly, more waves per workgroup when there is
+// only one workgroup per CU, and a 4-way K split for the residual projections
+// whose 4096-wide output has too few column tiles.
+struct StreamCfg {
+    int nw, ks, depth, split;
+};
+
+StreamCfg stream_cfg(int N, int K, bool partial) {
     const int KU = K / 64;
-    if (s > KU / 4) s = KU / 4 > 1 ? KU / 4 : 1;
-    return s > 8 ? 8 : s;
+    if (partial) {
+        int S = 4;
+        while (S > 1 && KU / S < 8) S /= 2;
+        if (N % 64 == 0) return K > 4096 ? StreamCfg{4, 4, 2, S} : StreamCfg{4, 2, 3, S};
+        return StreamCfg{1, 4, 2, S};
+    }
+    int nw = 0;
+    double best = -1.0;
+    for (int c : {4, 3}) {
+        if (N % (16 * c)) continue;
+        const int grid = N / (16 * c);
+        const double eff = (double)grid / (((grid + 255) / 256) * 256);
+        if (eff > best + 1e-9) { best = eff; nw = c; }
+    }
+    if (nw == 0) nw = N % 32 == 0 ? 2 : 1;
+    const int grid = N / (16 * nw);
+    const int ks = grid <= 256 ? 4 : 2;
+    const int depth = (nw == 3 && ks == 4) ? 3 : 2;
+    return StreamCfg{nw, ks, depth, 1};
+}
+
+int gemm_split(int dtype, int M, int N, int K) {
+    if (dtype != DARD_DTYPE_BF16 || M > 64) return 1;
+    return stream_cfg(N, K, true).split;
 }
 
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
@@ -363,12 +392,17 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
     const bf16_t* x = reinterpret_cast<const bf16_t*>(X);
     const bf16_t* w = reinterpret_cast<const bf16_t*>(W);
     if (M <= 64) {
-        const int split = e.kind == EPI_PARTIAL ? gemm_split(dtype, M, N, K) : 1;
-        if (N % 64 == 0) {
-            hipLaunchKernelGGL((gemm_stream_bf16<4, 2, 2>), dim3(N / 64, split), dim3(128), 0, s, x, M, K, ldx, w, N, e);
-        } else {
-            hipLaunchKernelGGL((gemm_stream_bf16<1, 4, 2>), dim3(N / 16, split), dim3(256), 0, s, x, M, K, ldx, w, N, e);
-        }
+        const StreamCfg c = stream_cfg(N, K, e.kind == EPI_PARTIAL);
+        const dim3 grid(N / (16 * c.nw), c.split), block(64 * c.ks);
+#define DARD_GS(NW, KS, D) hipLaunchKernelGGL((gemm_stream_bf16<NW, KS, D>), grid, block, 0, s, x, M, K, ldx, w, N, e)
+        if (c.nw == 4 && c.ks == 4) DARD_GS(4, 4, 2);
+        else if (c.nw == 4 && c.depth == 3) DARD_GS(4, 2, 3);
+        else if (c.nw == 4) DARD_GS(4, 2, 2);
+        else if (c.nw == 3 && c.ks == 4) DARD_GS(3, 4, 3);
+        else if (c.nw == 3) DARD_GS(3, 2, 2);
+        else if (c.nw == 2) DARD_GS(2, 4, 2);
+        else DARD_GS(1, 4, 2);
+#undef DARD_GS
         return hipGetLastError();
     }
     const int tiles_m = (M + TBM - 1) / TBM, tiles_n = (N + TBN - 1) / TBN;

@@ -1,6 +1,7 @@
 // State-specific attention mask (Sec. 3.2, Eq. 2-3): one "take x" bit per
-// (query row, block position).  One workgroup per sequence; the block's states
-// and confidences are staged in LDS, each thread builds whole 64-bit words.
+// (query row, block position).  One workgroup of 4 waves per sequence; each
+// wave builds whole rows with ballots (row_take_x), so the kernel holds no
+// per-bit loops.
 #include "common.h"
 #include "launch.h"
 
@@ -10,25 +11,14 @@ __global__ __launch_bounds__(256) void build_state_mask_kernel(const uint8_t* __
                                                                const float* __restrict__ conf,
                                                                int B, uint32_t flags,
                                                                uint64_t* __restrict__ sel) {
-    __shared__ uint8_t st[128];
-    __shared__ float cf[128];
     const int s = blockIdx.x;
-    for (int j = threadIdx.x; j < B; j += blockDim.x) {
-        st[j] = state[(size_t)s * B + j];
-        cf[j] = conf[(size_t)s * B + j];
-    }
-    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int W = (B + 63) / 64;
-    for (int t = threadIdx.x; t < 2 * B * W; t += blockDim.x) {
-        const int r = t / W, w = t % W;
-        const int i = r % B;
-        const bool shadow = r >= B;
-        uint64_t word = 0;
-        const int j0 = w * 64, j1 = min(B, j0 + 64);
-        for (int j = j0; j < j1; ++j)
-            if (take_x(st[i], st[j], cf[i], cf[j], shadow, i == j, flags))
-                word |= 1ull << (j - j0);
-        sel[((size_t)s * 2 * B + r) * W + w] = word;
+    const BlockView v = load_block_view(state + (size_t)s * B, conf + (size_t)s * B, B);
+    for (int r = wave; r < 2 * B; r += 4) {
+        uint64_t x0, x1;
+        row_take_x(v, r, B, flags, x0, x1);
+        if (lane < W) sel[((size_t)s * 2 * B + r) * W + lane] = lane == 0 ? x0 : x1;
     }
 }
 
