@@ -97,7 +97,8 @@ struct WsLayout {
 
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     const size_t es = esize(d->dtype);
-    const size_t rows = (size_t)b * (2 * B > cap ? 2 * B : cap);
+    size_t rows = (size_t)b * (2 * B > cap ? 2 * B : cap);
+    if (rows < 64) rows = 64;   // fragment-major activations hold whole 16 x 64 blocks of 64 rows
     const size_t qd = (size_t)d->n_heads * d->head_dim;
     const size_t step_rows = (size_t)b * 2 * B;
     const size_t nch = conf_chunks(d->vocab);
@@ -144,21 +145,26 @@ std::vector<TraceRec> g_trace[DARD_K_COUNT];
 
 }  // namespace
 
-TraceScope::TraceScope(int kernel_class, hipStream_t s) : cls(kernel_class), st(s), ev0(nullptr) {
-    if (!(g_trace_mask & (1u << cls))) return;
-    hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return;
-    hipEventRecord(e, st);
-    ev0 = e;
+thread_local TraceScope* g_scope = nullptr;
+
+TraceScope::TraceScope(int kernel_class, hipStream_t)
+    : cls(kernel_class), on((g_trace_mask >> kernel_class) & 1u), prev(g_scope) {
+    g_scope = this;
 }
 
-TraceScope::~TraceScope() {
-    if (!ev0) return;
-    hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return;
-    hipEventRecord(e, st);
+TraceScope::~TraceScope() { g_scope = prev; }
+
+bool TraceScope::next_events(hipEvent_t* a, hipEvent_t* b) {
+    const TraceScope* t = g_scope;
+    if (!t || !t->on) return false;
+    if (hipEventCreate(a) != hipSuccess) return false;
+    if (hipEventCreate(b) != hipSuccess) {
+        hipEventDestroy(*a);
+        return false;
+    }
     std::lock_guard<std::mutex> lk(g_trace_mu);
-    g_trace[cls].push_back({(hipEvent_t)ev0, e});
+    g_trace[t->cls].push_back({*a, *b});
+    return true;
 }
 
 }  // namespace dard
@@ -392,13 +398,14 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
     void* q = f.ws + f.W.q;
     void* at = f.ws + f.W.attn;
     void* act = f.ws + f.W.act;
+    const bool fr = frag_rows(dt, rows);   // activations feeding the GEMMs fragment-major
     for (int l = 0; l < d->n_layers; ++l) {
         EpiArgs e{};
         e.kind = EPI_QKV; e.q = q; e.ldq = qd; e.kc = f.kc(l); e.vc = f.vc(l);
         e.rope = (const float*)(f.pk + f.L.rope);
         e.rows_per_seq = R; e.P = P; e.B = B; e.cap = f.cap; e.Hq = d->n_heads; e.Hkv = d->n_kv_heads; e.dh = dh;
         e.step = step;
-        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wqkv), qd + 2 * kd, e, DARD_K_GEMM_QKV, f.s));
+        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wqkv), qd + 2 * kd, e, DARD_K_GEMM_QKV, f.s, fr));
 
         AttnArgs a{};
         a.q = q; a.k = f.kc(l); a.v = f.vc(l); a.out = at; a.state = state; a.conf = conf;
@@ -406,6 +413,7 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step; a.scale = 1.f / std::sqrt((float)dh);
         a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
         a.part_slots = f.W.part_slots;
+        a.out_frag = fr;
         {
             TraceScope ts(DARD_K_ATTENTION, f.s);
             HIPOK(launch_attention(dt, a, f.s));
@@ -418,15 +426,16 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         float* gp = (float*)(f.ws + f.W.gpart);
         EpiArgs po{};
         po.kind = EPI_PARTIAL; po.y = gp; po.ldy = D;
-        HIPOK(launch_gemm(dt, at, rows, qd, qd, f.layer(l, f.L.wo), D, so > 1 ? po : r, DARD_K_GEMM_O, f.s));
-        HIPOK(launch_resid_norm(dt, h, gp, so > 1 ? so : 0, rows, D, f.layer(l, f.L.ffn_norm), d->norm_eps, xn, f.s));
+        HIPOK(launch_gemm(dt, at, rows, qd, qd, f.layer(l, f.L.wo), D, so > 1 ? po : r, DARD_K_GEMM_O, f.s, fr));
+        HIPOK(launch_resid_norm(dt, h, gp, so > 1 ? so : 0, rows, D, f.layer(l, f.L.ffn_norm), d->norm_eps, xn, fr,
+                                f.s));
         EpiArgs g{};
-        g.kind = EPI_SWIGLU; g.act = act; g.ld_act = F;
-        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wgu), 2 * F, g, DARD_K_GEMM_GU, f.s));
+        g.kind = EPI_SWIGLU; g.act = act; g.ld_act = F; g.act_frag = fr;
+        HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wgu), 2 * F, g, DARD_K_GEMM_GU, f.s, fr));
         const int sd = gemm_split(dt, rows, D, F);
-        HIPOK(launch_gemm(dt, act, rows, F, F, f.layer(l, f.L.wdown), D, sd > 1 ? po : r, DARD_K_GEMM_DOWN, f.s));
+        HIPOK(launch_gemm(dt, act, rows, F, F, f.layer(l, f.L.wdown), D, sd > 1 ? po : r, DARD_K_GEMM_DOWN, f.s, fr));
         const void* gain = l + 1 < d->n_layers ? f.layer(l + 1, f.L.attn_norm) : f.pk + f.L.final_norm;
-        HIPOK(launch_resid_norm(dt, h, gp, sd > 1 ? sd : 0, rows, D, gain, d->norm_eps, xn, f.s));
+        HIPOK(launch_resid_norm(dt, h, gp, sd > 1 ? sd : 0, rows, D, gain, d->norm_eps, xn, fr, f.s));
     }
     return DARD_OK;
 }
@@ -458,7 +467,7 @@ dard_status dard_prefill(const dard_dims* d, const void* packed, void* kv, int c
     if (rc) return rc;
     const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
     HIPOK(launch_embed_norm(d->dtype, ids, embeds, f.pk + f.L.embed, gain0, b * P, d->d_model, d->vocab, d->norm_eps, 0, 0,
-                            (float*)(f.ws + f.W.h), f.ws + f.W.xn, f.s));
+                            (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, b * P), f.s));
     return run_layers(f, P, P, 0, 0, nullptr, nullptr, 0);
 }
 
@@ -480,13 +489,13 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     float* logits = (float*)(f.ws + f.W.logits);
     const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
     HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
-                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, f.s));
+                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
     rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags);
     if (rc) return rc;
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.y = logits; e.ldy = V;
     HIPOK(launch_gemm(d->dtype, f.ws + f.W.xn, rows, d->d_model, d->d_model, f.pk + f.L.lm_head, V, e,
-                      DARD_K_GEMM_HEAD, f.s));
+                      DARD_K_GEMM_HEAD, f.s, frag_rows(d->dtype, rows)));
 
     ConfArgs c{};
     c.ls = logits; c.ld_s = V; c.ld_x = V; c.rows = b * B; c.V = V; c.state = state_in; c.step_B = B;

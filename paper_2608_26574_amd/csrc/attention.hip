@@ -290,12 +290,15 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     const size_t orow = ((size_t)s * a.R + my_row) * a.Hq + h;
     if (nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        bf16_t* out = reinterpret_cast<bf16_t*>(a.out) + orow * DH;
+        bf16_t* out = reinterpret_cast<bf16_t*>(a.out);
+        const int tok = s * a.R + my_row, KO = a.Hq * DH;
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) {
             const uint32_t w0 = (uint32_t)f2bf(o[d][0] * inv) | ((uint32_t)f2bf(o[d][1] * inv) << 16);
             const uint32_t w1 = (uint32_t)f2bf(o[d][2] * inv) | ((uint32_t)f2bf(o[d][3] * inv) << 16);
-            *reinterpret_cast<uint2*>(out + 16 * d + 4 * g) = make_uint2(w0, w1);
+            const int k = h * DH + 16 * d + 4 * g;
+            *reinterpret_cast<uint2*>(out + (a.out_frag ? frag_off(tok, k, KO) : orow * DH + 16 * d + 4 * g)) =
+                make_uint2(w0, w1);
         }
         return;
     }
@@ -315,7 +318,8 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
                                                            const float* __restrict__ part_ml, int ns,
-                                                           size_t nrow, bf16_t* __restrict__ out) {
+                                                           size_t nrow, int Hq, int frag,
+                                                           bf16_t* __restrict__ out) {
     const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
     const size_t row = t / (DH / 4);
     const int q4 = t % (DH / 4);
@@ -349,7 +353,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     const float inv = Lsum > 0.f ? 1.f / Lsum : 0.f;
     const uint32_t w0 = (uint32_t)f2bf(acc.x * inv) | ((uint32_t)f2bf(acc.y * inv) << 16);
     const uint32_t w1 = (uint32_t)f2bf(acc.z * inv) | ((uint32_t)f2bf(acc.w * inv) << 16);
-    *reinterpret_cast<uint2*>(out + row * DH + 4 * q4) = make_uint2(w0, w1);
+    const size_t o = frag ? frag_off((int)(row / Hq), (int)(row % Hq) * DH + 4 * q4, Hq * DH) : row * DH + 4 * q4;
+    *reinterpret_cast<uint2*>(out + o) = make_uint2(w0, w1);
 }
 
 // fp32 path: one thread per (sequence, row, head).
@@ -430,6 +435,7 @@ size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys) {
 }
 
 hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStream_t s) {
+    if (a.out_frag && !frag_rows(dtype, a.b * a.R)) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16) {
         const int rowtiles = (a.R + kRows - 1) / kRows;
         const int ntiles = (a.nkeys + kKeys - 1) / kKeys;
@@ -441,7 +447,7 @@ hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStre
         const int G = attention_groups(a.b, a.R, a.Hq, a.dh, tps);
         dim3 grid(a.b * a.Hq * rowtiles, ns);
 #define DARD_ATT(DHV, GV) \
-    hipLaunchKernelGGL((attn_bf16_kernel<DHV, GV, GV == 4 ? 1 : 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
+    launch((attn_bf16_kernel<DHV, GV, GV == 4 ? 1 : 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
         if (a.dh == 128) {
             if (G == 4) DARD_ATT(128, 4); else if (G == 2) DARD_ATT(128, 2); else DARD_ATT(128, 1);
         } else {
@@ -453,19 +459,19 @@ hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStre
         const size_t nrow = (size_t)a.b * a.R * a.Hq;
         const size_t threads = nrow * (a.dh / 4);
         if (a.dh == 128)
-            hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
-                               a.part_ml, ns, nrow, reinterpret_cast<bf16_t*>(a.out));
+            launch(attn_combine_kernel<128>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
+                               a.part_ml, ns, nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
         else
-            hipLaunchKernelGGL(attn_combine_kernel<64>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
-                               a.part_ml, ns, nrow, reinterpret_cast<bf16_t*>(a.out));
+            launch(attn_combine_kernel<64>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
+                               a.part_ml, ns, nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
         return hipGetLastError();
     }
     const size_t total = (size_t)a.b * a.R * a.Hq;
     dim3 grid((total + 63) / 64);
     if (a.dh == 128)
-        hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, s, a);
+        launch(attn_f32_kernel<128>, grid, dim3(64), 0, s, a);
     else
-        hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, s, a);
+        launch(attn_f32_kernel<64>, grid, dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

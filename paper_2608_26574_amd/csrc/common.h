@@ -48,6 +48,17 @@ __device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) {
     return *reinterpret_cast<const bf16x8*>(p);
 }
 
+// Element (m, k) of a fragment-major [rows][K] activation: the 16 x 64 block
+// (m/16, k/64) sits at ((m/16) * K/64 + k/64) * 1024; inside it half
+// h = (k/8) % 2 at +512h, lane l = m%16 + 16 * ((k%64)/16) at +8l, then k%8.
+// Lane l of a wave then finds the B operand of mfma16x16x32 (token m%16,
+// k = 16 * (l/16) + 8h + 0..7) at 8l of half h, as for the packed weights.
+__device__ __forceinline__ size_t frag_off(int m, int k, int K) {
+    const int kk = k & 63;
+    return ((size_t)(m >> 4) * (K >> 6) + (k >> 6)) * 1024 + ((kk >> 3) & 1) * 512 +
+           ((m & 15) + 16 * (kk >> 4)) * 8 + (kk & 7);
+}
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll

@@ -166,7 +166,7 @@ hipError_t launch_conf_partial(const ConfArgs& a, hipStream_t s) {
     b.chunk = kChunk;
     b.nchunk = conf_chunks(a.V);
     const int step_B = a.step_B;
-    hipLaunchKernelGGL(conf_partial_kernel, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
+    launch(conf_partial_kernel, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
     return hipGetLastError();
 }
 
@@ -174,7 +174,7 @@ hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const fl
                                const int32_t* cur_tok, int32_t* argmax, float* maxprob, float* pcur,
                                hipStream_t s) {
     TraceScope ts(DARD_K_CONFIDENCE, s);
-    hipLaunchKernelGGL(conf_combine_kernel, dim3((rows + 127) / 128), dim3(128), 0, s, part, rows, nchunk, ls,
+    launch(conf_combine_kernel, dim3((rows + 127) / 128), dim3(128), 0, s, part, rows, nchunk, ls,
                        ld, cur_tok, argmax, maxprob, pcur);
     return hipGetLastError();
 }

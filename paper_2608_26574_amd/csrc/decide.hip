@@ -179,7 +179,7 @@ hipError_t launch_decide(const DecideArgs& a, hipStream_t s) {
     TraceScope ts(DARD_K_DECIDE, s);
     const size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * 3 * sizeof(float) : 0;
     if (lds > 96 * 1024) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(decide_kernel, dim3(a.b), dim3(128), lds, s, a);
+    launch(decide_kernel, dim3(a.b), dim3(128), lds, s, a);
     return hipGetLastError();
 }
 

@@ -20,21 +20,27 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return t;
 }
 
-// y = h / sqrt(mean(h^2) + eps) * gain, rounded to T.
+// Offset of element (row, c) of a [rows][d] activation, row-major or fragment-major.
+__device__ __forceinline__ size_t act_off(int row, int c, int d, bool frag) {
+    return frag ? frag_off(row, c, d) : (size_t)row * d + c;
+}
+
+// xn[row] = h / sqrt(mean(h^2) + eps) * gain, rounded to T.
 template <typename T>
-__device__ void norm_row(const float* h, const T* gain, int d, float eps, T* out, float* red) {
+__device__ void norm_row(const float* h, const T* gain, int d, float eps, T* xn, int row, bool frag, float* red) {
     float ss = 0.f;
     for (int c = threadIdx.x; c < d; c += blockDim.x) ss += h[c] * h[c];
     ss = block_sum(ss, red);
     const float inv = rsqrtf(ss / (float)d + eps);
-    for (int c = threadIdx.x; c < d; c += blockDim.x) St<T>::st(out + c, h[c] * inv * St<T>::ld(gain + c));
+    for (int c = threadIdx.x; c < d; c += blockDim.x)
+        St<T>::st(xn + act_off(row, c, d, frag), h[c] * inv * St<T>::ld(gain + c));
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void embed_norm_kernel(const int32_t* __restrict__ ids, const T* __restrict__ embeds,
                                                          const T* __restrict__ table, const T* __restrict__ gain,
                                                          int d, int vocab, float eps, int step_B, int mask_id,
-                                                         float* __restrict__ h, T* __restrict__ xn) {
+                                                         float* __restrict__ h, T* __restrict__ xn, int frag) {
     __shared__ float red[8];
     const size_t row = blockIdx.x;
     int id;
@@ -50,7 +56,7 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(const int32_t* __restri
     float* hr = h + row * d;
     for (int c = threadIdx.x; c < d; c += blockDim.x) hr[c] = St<T>::ld(src + c);
     __syncthreads();
-    norm_row<T>(hr, gain, d, eps, xn + row * d, red);
+    norm_row<T>(hr, gain, d, eps, xn, (int)row, frag != 0, red);
 }
 
 // h[row] += sum_s part[s][row] (split-K partials of the preceding projection,
@@ -63,7 +69,7 @@ constexpr int kVec = 4;   // d <= 512 * 4 * kVec
 template <typename T, int NS>
 __global__ __launch_bounds__(512) void resid_norm_kernel(float* __restrict__ h, const float* __restrict__ part,
                                                          size_t split_stride, const T* __restrict__ gain,
-                                                         int d, float eps, T* __restrict__ xn) {
+                                                         int d, float eps, T* __restrict__ xn, int frag) {
     __shared__ float red[8];
     const size_t row = blockIdx.x;
     float4* hr = reinterpret_cast<float4*>(h + row * d);
@@ -97,16 +103,16 @@ __global__ __launch_bounds__(512) void resid_norm_kernel(float* __restrict__ h, 
 #pragma unroll
     for (int w = 0; w < 8; ++w) tot += red[w];
     const float inv = rsqrtf(tot / (float)d + eps);
-    T* out = xn + row * d;
 #pragma unroll
     for (int q = 0; q < kVec; ++q) {
         const int c4 = threadIdx.x + 512 * q;
         if (c4 < n4) {
-            const int c = 4 * c4;
-            St<T>::st(out + c, v[q].x * inv * St<T>::ld(gain + c));
-            St<T>::st(out + c + 1, v[q].y * inv * St<T>::ld(gain + c + 1));
-            St<T>::st(out + c + 2, v[q].z * inv * St<T>::ld(gain + c + 2));
-            St<T>::st(out + c + 3, v[q].w * inv * St<T>::ld(gain + c + 3));
+            const int c = 4 * c4;   // c..c+3 stay inside one 8-element group of the fragment layout
+            T* out = xn + act_off((int)row, c, d, frag != 0);
+            St<T>::st(out, v[q].x * inv * St<T>::ld(gain + c));
+            St<T>::st(out + 1, v[q].y * inv * St<T>::ld(gain + c + 1));
+            St<T>::st(out + 2, v[q].z * inv * St<T>::ld(gain + c + 2));
+            St<T>::st(out + 3, v[q].w * inv * St<T>::ld(gain + c + 3));
         }
     }
 }
@@ -141,33 +147,35 @@ __global__ void pack_rows_kernel(const uint8_t* __restrict__ src0, const uint8_t
 
 hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
                             int dh, hipStream_t s) {
-    hipLaunchKernelGGL(pack_rows_kernel, dim3(nrows), dim3(128), 0, s, (const uint8_t*)src0,
+    launch(pack_rows_kernel, dim3(nrows), dim3(128), 0, s, (const uint8_t*)src0,
                        (const uint8_t*)src1, (uint8_t*)dst, nrows, rowbytes, mode, dh);
     return hipGetLastError();
 }
 
 hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds, const void* table,
                              const void* gain, int rows, int d, int vocab, float eps, int step_B,
-                             int mask_id, float* h, void* xn, hipStream_t s) {
+                             int mask_id, float* h, void* xn, bool frag, hipStream_t s) {
     TraceScope ts(DARD_K_NORM, s);
+    if (frag && !frag_rows(dtype, rows)) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16)
-        hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, ids,
+        launch(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, ids,
                            (const bf16_t*)embeds, (const bf16_t*)table, (const bf16_t*)gain, d, vocab, eps, step_B,
-                           mask_id, h, (bf16_t*)xn);
+                           mask_id, h, (bf16_t*)xn, (int)frag);
     else
-        hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, ids, (const float*)embeds,
-                           (const float*)table, (const float*)gain, d, vocab, eps, step_B, mask_id, h, (float*)xn);
+        launch(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, ids, (const float*)embeds,
+                           (const float*)table, (const float*)gain, d, vocab, eps, step_B, mask_id, h, (float*)xn, 0);
     return hipGetLastError();
 }
 
 hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit, int rows, int d,
-                             const void* gain, float eps, void* xn, hipStream_t s) {
+                             const void* gain, float eps, void* xn, bool frag, hipStream_t s) {
     TraceScope ts(DARD_K_NORM, s);
+    if (frag && !frag_rows(dtype, rows)) return hipErrorInvalidValue;
     const size_t stride = (size_t)rows * d;
     if (nsplit < 0 || nsplit > 8 || d > 512 * 4 * kVec) return hipErrorInvalidValue;
 #define DARD_RN(T, NS)                                                                                 \
-    hipLaunchKernelGGL((resid_norm_kernel<T, NS>), dim3(rows), dim3(512), 0, s, h, part, stride,      \
-                       (const T*)gain, d, eps, (T*)xn)
+    launch((resid_norm_kernel<T, NS>), dim3(rows), dim3(512), 0, s, h, part, stride,      \
+                       (const T*)gain, d, eps, (T*)xn, (int)frag)
 #define DARD_RN_ALL(T)                                                                                 \
     switch (nsplit) {                                                                                  \
     case 0: DARD_RN(T, 0); break; case 1: DARD_RN(T, 1); break; case 2: DARD_RN(T, 2); break;          \
@@ -188,7 +196,7 @@ hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_
     const size_t n16 = bytes / 16;
     if (n16 == 0) return hipSuccess;
     const size_t blocks = (n16 + 255) / 256;
-    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s,
+    launch(copy_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s,
                        (const uint4*)src, (uint4*)dst, n16);
     return hipGetLastError();
 }

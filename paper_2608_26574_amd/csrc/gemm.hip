@@ -60,7 +60,7 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4
         break;
     }
     case EPI_SWIGLU: {
-        T* a = reinterpret_cast<T*>(e.act) + (size_t)m * e.ld_act + n / 2;
+        T* a = reinterpret_cast<T*>(e.act) + (e.act_frag ? frag_off(m, n / 2, e.ld_act) : (size_t)m * e.ld_act + n / 2);
         St<T>::st(a, silu(v[0]) * v[1]);
         St<T>::st(a + 1, silu(v[2]) * v[3]);
         break;
@@ -100,7 +100,7 @@ __device__ __forceinline__ bf16x8 ld_nt(const bf16_t* p) {
 }
 
 // ---------------------------------------------------------------- streaming
-template <int NW, int KSPLIT, int DEPTH>
+template <int NW, int KSPLIT, int DEPTH, bool XF>
 __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __restrict__ X, int M, int K, int ldx,
                                                                const bf16_t* __restrict__ W, int N, EpiArgs e) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -120,9 +120,15 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
     const bf16_t* wp[NW];
 #pragma unroll
     for (int j = 0; j < NW; ++j) wp[j] = W + (size_t)min(nb0 + j, N / 16 - 1) * KU * 1024 + 8 * lane;
+    // X row-major: lane (lr, g) reads token 16mb+lr at k 64u + 16g + 8h; X
+    // fragment-major: 1 KB block (mb, u), half h at +512h, lane at +8*lane.
+    // Token blocks past the last one re-read it (their results are not stored).
     const bf16_t* xp[4];
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) xp[mb] = X + (size_t)min(16 * mb + lr, M - 1) * ldx + 16 * g;
+    for (int mb = 0; mb < 4; ++mb)
+        xp[mb] = XF ? X + (size_t)min(mb, (M - 1) >> 4) * KU * 1024 + 8 * lane
+                    : X + (size_t)min(16 * mb + lr, M - 1) * ldx + 16 * g;
+    constexpr int xu = XF ? 1024 : 64, xh = XF ? 512 : 8;   // element steps per k unit / half
 
     bf16x8 wb[DEPTH][NW][2], xb[DEPTH][4][2];
     auto load = [&](int s, int u) {
@@ -133,8 +139,8 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
         }
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb) {
-            xb[s][mb][0] = ld_bf16x8(xp[mb] + 64 * u);
-            xb[s][mb][1] = ld_bf16x8(xp[mb] + 64 * u + 8);
+            xb[s][mb][0] = ld_bf16x8(xp[mb] + (size_t)xu * u);
+            xb[s][mb][1] = ld_bf16x8(xp[mb] + (size_t)xu * u + xh);
         }
     };
 #pragma unroll
@@ -334,7 +340,7 @@ __global__ void pack_frag_kernel(const bf16_t* __restrict__ src0, const bf16_t* 
 hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
                             hipStream_t s) {
     const size_t total = (size_t)N * K / 8;
-    hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+    launch(pack_frag_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
                        (const bf16_t*)src0, (const bf16_t*)src1, (bf16_t*)dst, N, K, mode, dh);
     return hipGetLastError();
 }
@@ -381,20 +387,25 @@ int gemm_split(int dtype, int M, int N, int K) {
 }
 
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
-                       const EpiArgs& e, int kernel_class, hipStream_t s) {
+                       const EpiArgs& e, int kernel_class, hipStream_t s, bool xfrag) {
     TraceScope ts(kernel_class, s);
     if (dtype == DARD_DTYPE_F32) {
         dim3 grid((N + 63) / 64, (M + 15) / 16);
-        hipLaunchKernelGGL(gemm_f32, grid, dim3(256), 0, s, reinterpret_cast<const float*>(X), M, K, ldx,
+        launch(gemm_f32, grid, dim3(256), 0, s, reinterpret_cast<const float*>(X), M, K, ldx,
                            reinterpret_cast<const float*>(W), N, e);
         return hipGetLastError();
     }
     const bf16_t* x = reinterpret_cast<const bf16_t*>(X);
     const bf16_t* w = reinterpret_cast<const bf16_t*>(W);
+    if (xfrag && !frag_rows(dtype, M)) return hipErrorInvalidValue;
     if (M <= 64) {
         const StreamCfg c = stream_cfg(N, K, e.kind == EPI_PARTIAL);
         const dim3 grid(N / (16 * c.nw), c.split), block(64 * c.ks);
-#define DARD_GS(NW, KS, D) hipLaunchKernelGGL((gemm_stream_bf16<NW, KS, D>), grid, block, 0, s, x, M, K, ldx, w, N, e)
+#define DARD_GS(NW, KS, D)                                                                               \
+    do {                                                                                                 \
+        if (xfrag) launch((gemm_stream_bf16<NW, KS, D, true>), grid, block, 0, s, x, M, K, ldx, w, N, e);  \
+        else launch((gemm_stream_bf16<NW, KS, D, false>), grid, block, 0, s, x, M, K, ldx, w, N, e);       \
+    } while (0)
         if (c.nw == 4 && c.ks == 4) DARD_GS(4, 4, 2);
         else if (c.nw == 4 && c.depth == 3) DARD_GS(4, 2, 3);
         else if (c.nw == 4) DARD_GS(4, 2, 2);
@@ -406,7 +417,7 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
         return hipGetLastError();
     }
     const int tiles_m = (M + TBM - 1) / TBM, tiles_n = (N + TBN - 1) / TBN;
-    hipLaunchKernelGGL(gemm_tiled_bf16, dim3(tiles_m * tiles_n), dim3(256), 0, s, x, M, K, ldx, w, N, e,
+    launch(gemm_tiled_bf16, dim3(tiles_m * tiles_n), dim3(256), 0, s, x, M, K, ldx, w, N, e,
                        tiles_m, tiles_n);
     return hipGetLastError();
 }

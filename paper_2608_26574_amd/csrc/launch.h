@@ -2,11 +2,21 @@
 // C ABI in api.cpp and the kernel translation units).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/dard.h"
+
 namespace dard {
+
+// Activations that feed a streaming GEMM (bf16, at most 64 token rows) are
+// stored fragment-major, in the layout of the packed weights: the 16 x 64
+// block (m/16, k/64) is contiguous, so each wave load of the GEMM reads 1 KB
+// contiguous.  Producers (norms, SwiGLU epilogue, attention output) write that
+// layout when frag_rows(dtype, rows) holds; buffers then hold 64 rows.
+inline bool frag_rows(int dtype, int rows) { return dtype == DARD_DTYPE_BF16 && rows <= 64; }
 
 // ---- mask.hip
 hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
@@ -30,6 +40,7 @@ struct AttnArgs {
     float* part;        // split partials [nsplit][b][R][Hq][dh] fp32
     float* part_ml;     // [nsplit][b][R][Hq][2]
     size_t part_slots;  // capacity of part / part_ml in (split, row, head) slots
+    int out_frag;       // 1: out is fragment-major [b*R][Hq*dh] (bf16 only)
 };
 // Key splits the launcher uses for these sizes with `slots` partial slots.
 int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots);
@@ -43,6 +54,7 @@ struct EpiArgs {
     int kind;
     float* y;  int ldy;             // STORE_F32 / RESID (fp32, RESID adds)
     void* act; int ld_act;          // SWIGLU output (dtype), columns N/2
+    int act_frag;                   // 1: act fragment-major with K = ld_act
     // QKV
     void* q; int ldq;               // [rows][Hq*dh]
     void* kc; void* vc;             // cache base of this layer: [b][Hkv][cap][dh]
@@ -51,11 +63,12 @@ struct EpiArgs {
     int P, B, cap, Hq, Hkv, dh;
     int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r
 };
-// Y = X * W^T with X [M][K] (leading dim ldx), W [N][K] packed (bf16:
-// fragment-major, fp32: row-major); epilogue per `e`.  With EPI_PARTIAL the
-// output is gemm_split(...) fp32 partials [split][M][ldy] at e.y.
+// Y = X * W^T with X [M][K] (leading dim ldx, or fragment-major when xfrag),
+// W [N][K] packed (bf16: fragment-major, fp32: row-major); epilogue per `e`.
+// With EPI_PARTIAL the output is gemm_split(...) fp32 partials [split][M][ldy]
+// at e.y.  xfrag needs frag_rows(dtype, M).
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
-                       const EpiArgs& e, int kernel_class, hipStream_t s);
+                       const EpiArgs& e, int kernel_class, hipStream_t s, bool xfrag = false);
 int gemm_split(int dtype, int M, int N, int K);
 // bf16 fragment-major packing (mode 0 plain, 1 rotary-pair rows, 2 gate/up interleave)
 hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
@@ -69,11 +82,12 @@ hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N
 hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds,
                              const void* table, const void* gain, int rows, int d, int vocab,
                              float eps, int step_B, int mask_id, float* h, void* xn,
-                             hipStream_t s);
+                             bool frag, hipStream_t s);
 // h[row] += sum of the nsplit fp32 partials part[s][row] (nsplit may be 0),
-// then xn[row] = RMSNorm(h[row]) * gain.  Needs d % 4 == 0, d <= 8192.
+// then xn[row] = RMSNorm(h[row]) * gain (fragment-major when frag).  Needs
+// d % 4 == 0, d <= 8192.
 hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit, int rows, int d,
-                             const void* gain, float eps, void* xn, hipStream_t s);
+                             const void* gain, float eps, void* xn, bool frag, hipStream_t s);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
                             int dh, hipStream_t s);
@@ -125,10 +139,27 @@ struct DecideArgs {
 hipError_t launch_decide(const DecideArgs& a, hipStream_t s);
 
 // ---- tracing (api.cpp)
+// While a TraceScope whose class is enabled (dard_trace_enable) is alive on
+// this thread, every kernel started through launch() records its own begin
+// and end timestamps, so traced times are kernel execution times without the
+// dispatch gaps between kernels.  Scopes nest; the innermost one decides.
 struct TraceScope {
     TraceScope(int kernel_class, hipStream_t s);
     ~TraceScope();
-    int cls; hipStream_t st; void* ev0;
+    // A fresh pair of timing events for the next kernel; false when the
+    // innermost scope is not traced.
+    static bool next_events(hipEvent_t* a, hipEvent_t* b);
+    int cls;
+    bool on;
+    TraceScope* prev;
 };
+
+// Kernel launch used by every entry point.
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t s, Args... args) {
+    hipEvent_t a = nullptr, b = nullptr;
+    TraceScope::next_events(&a, &b);
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, s, a, b, 0u, args...);
+}
 
 }  // namespace dard

@@ -24,7 +24,7 @@ __global__ __launch_bounds__(256) void build_state_mask_kernel(const uint8_t* __
 
 hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
                                    uint32_t flags, uint64_t* sel, hipStream_t s) {
-    hipLaunchKernelGGL(build_state_mask_kernel, dim3(b), dim3(256), 0, s, state, conf, B, flags,
+    launch(build_state_mask_kernel, dim3(b), dim3(256), 0, s, state, conf, B, flags,
                        sel);
     return hipGetLastError();
 }

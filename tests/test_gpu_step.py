@@ -179,6 +179,7 @@ def test_tiny_step_fp32_transitions(flags):
     dict(d=256, H=4, Hkv=4, dh=64, F=512, V=4096, b=2, B=16, P=40, L=2),
     dict(d=512, H=4, Hkv=2, dh=128, F=1024, V=2048, b=1, B=7, P=3, L=2),
     dict(d=512, H=4, Hkv=1, dh=128, F=512, V=1024, b=3, B=24, P=50, L=1),   # 144 rows: tiled GEMMs
+    dict(d=512, H=8, Hkv=8, dh=64, F=1024, V=2048, b=1, B=20, P=60, L=2),    # 40 and 60 rows: ragged last block
 ])
 def test_small_step_bf16(case):
     dims = synth.Dims(case["L"], case["d"], case["H"], case["Hkv"], case["dh"], case["F"], case["V"], 512, "bf16")
