@@ -122,7 +122,12 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
  *   out [b][2B][Hq][dh]     dtype
  * Query head h reads KV head h / (Hq/Hkv).  Any permutation of the head_dim
  * axis applied to both q and k gives the same result.  Needs P >= 0,
- * P + 2B <= cap, dh in {64, 128}. */
+ * P + 2B <= cap, dh in {64, 128}.
+ * Workspace (device, caller-owned, no alignment beyond 256 bytes needed):
+ * bf16 needs at least dard_attention_workspace_bytes(...) bytes, which hold
+ * the state mask the call builds and, when the key range is split across
+ * workgroups, the partial results; more room never hurts.  fp32 needs none
+ * (0 is returned and ws may be NULL). */
 size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P);
 dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v,
                                   int P, int cap, const uint8_t* state, const float* conf,

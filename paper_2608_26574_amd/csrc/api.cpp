@@ -92,7 +92,7 @@ Layout layout_of(const dard_dims* d) {
 
 // Workspace of dard_step / dard_prefill.
 struct WsLayout {
-    size_t h, xn, q, attn, act, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, total;
+    size_t h, xn, q, attn, act, sel, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, total;
 };
 
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
@@ -109,6 +109,7 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.q = o; o = align256(o + rows * qd * es);
     W.attn = o; o = align256(o + rows * qd * es);
     W.act = o; o = align256(o + rows * d->ffn_dim * es);
+    W.sel = o; o = align256(o + step_rows * ((B + 63) / 64) * 8);   // state mask of the step
     // split-key partials: room for the step's largest split (16 ways); the
     // prefill splits only as far as this room allows
     const size_t slots = (size_t)16 * b * 2 * B * d->n_heads;
@@ -188,11 +189,13 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
 
 // ---------------------------------------------------------------- attention
 size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P) {
-    if (b < 1 || B < 1 || Hq < 1 || P < 0) return 0;
-    const size_t slots = attention_partial_slots(dtype, b, 2 * B, Hq, P + 2 * B);
-    if (slots == 0) return 0;
+    if (b < 1 || B < 1 || B > 128 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16) return 0;
+    // the state mask of the block, then the partial results of a key split
+    const size_t mask = align256((size_t)b * 2 * B * ((B + 63) / 64) * 8);
+    const size_t slots = attention_partial_slots(dtype, b, 2 * B, Hq, attention_tiles(1, P, B, P + 2 * B));
+    if (slots == 0) return mask;
     // + 64 slots of slack for the alignment of the (m, l) array
-    return (slots + 64) * ((size_t)dh * 4 + 8);
+    return mask + (slots + 64) * ((size_t)dh * 4 + 8);
 }
 
 dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v, int P, int cap,
@@ -211,15 +214,21 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
     a.q = q; a.k = k; a.v = v; a.out = out; a.state = state; a.conf = conf;
     a.b = b; a.R = 2 * B; a.Hq = Hq; a.Hkv = Hkv; a.dh = dh; a.cap = cap;
     a.P = P; a.B = B; a.nkeys = P + 2 * B; a.masked = 1; a.scale = scale; a.flags = flags;
-    // as many partial slots as the given workspace holds
-    const size_t slots = ws ? ws_bytes / ((size_t)dh * 4 + 8) : 0;
-    a.part_slots = slots > 64 ? slots - 64 : 0;
-    if (a.part_slots > 0) {
-        a.part = (float*)ws;
-        a.part_ml = (float*)((char*)ws + align256(a.part_slots * dh * 4));
-    }
     hipStream_t s = (hipStream_t)stream;
     TraceScope ts(DARD_K_ATTENTION, s);
+    if (dtype == DARD_DTYPE_BF16) {
+        // the state mask first, then as many partial slots as the rest of the workspace holds
+        const size_t mask = align256((size_t)b * 2 * B * ((B + 63) / 64) * 8);
+        uint64_t* sel = (uint64_t*)ws;
+        HIPOK(launch_build_state_mask(state, conf, b, B, flags, sel, s));
+        a.sel = sel;
+        const size_t slots = (ws_bytes - mask) / ((size_t)dh * 4 + 8);
+        a.part_slots = slots > 64 ? slots - 64 : 0;
+        if (a.part_slots > 0) {
+            a.part = (float*)((char*)ws + mask);
+            a.part_ml = (float*)((char*)ws + mask + align256(a.part_slots * dh * 4));
+        }
+    }
     HIPOK(launch_attention(dtype, a, s));
     return DARD_OK;
 }
@@ -409,6 +418,7 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
 
         AttnArgs a{};
         a.q = q; a.k = f.kc(l); a.v = f.vc(l); a.out = at; a.state = state; a.conf = conf;
+        a.sel = step ? (const uint64_t*)(f.ws + f.W.sel) : nullptr;
         a.b = f.b; a.R = R; a.Hq = d->n_heads; a.Hkv = d->n_kv_heads; a.dh = dh; a.cap = f.cap;
         a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step; a.scale = 1.f / std::sqrt((float)dh);
         a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
@@ -488,6 +498,11 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     const int R = 2 * B, rows = b * R, V = d->vocab;
     float* logits = (float*)(f.ws + f.W.logits);
     const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    // the state mask (Eq. 2-3) is the same for every layer of the step: build it once
+    {
+        TraceScope ts(DARD_K_ATTENTION, f.s);
+        HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
+    }
     HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
                             params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
     rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags);

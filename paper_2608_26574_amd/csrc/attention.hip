@@ -11,9 +11,12 @@
 //   O^T += V^T P^T  (A = V^T from LDS, B = probabilities straight from the
 //                    S^T accumulators; the MFMA k index is permuted so that a
 //                    lane's 8 probabilities are its own score values)
-// The mask is built in-kernel: each wave derives its rows' "take x" bits (Eq. 2-3) with ballots;
-// prefix keys are always visible, block key P+j is x^j, P+B+j is s^j.  Tiles
-// that hold only prefix keys skip the per-key visibility test entirely.
+// Keys are tiled in two runs: the prefix [0, P) in 64-key tiles, then the
+// block [P, P + 2B) (x^j at P+j, s^j at P+B+j) in 64-key tiles of its own.  A
+// row's block visibility is the "take x" word of the state mask (Eq. 2-3,
+// built once per step) widened to 2B bits: x^j where the bit is set, s^j
+// where it is clear; so one aligned 64-bit word per block tile says which
+// keys a row sees, and full prefix tiles need no test at all.
 // Very long key ranges are additionally split across workgroups and merged
 // by a log-sum-exp combine kernel.
 //
@@ -27,7 +30,6 @@ namespace {
 
 constexpr int kRows = 64;      // query rows per workgroup
 constexpr int kKeys = 64;      // keys per tile
-// tiles in flight per group: two, or one when four groups share the registers
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -39,6 +41,35 @@ struct Lds {
     static constexpr int MERGE_BYTES = (DH / 4 + 2) * 256 * 4;   // o, m, l of every lane
     static constexpr int GROUP_BYTES = ((TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 15) / 16 * 16;
 };
+
+// The 2B-bit block visibility of a row from its take-x words (x1:x0), B <= 128:
+// bit j (j < B) = x bit j, bit B + j = NOT x bit j; returned as 4 words.
+__device__ __forceinline__ void block_vis(uint64_t x0, uint64_t x1, int B, uint64_t& v0, uint64_t& v1,
+                                          uint64_t& v2, uint64_t& v3) {
+    const uint64_t m0 = B >= 64 ? ~0ull : (1ull << B) - 1;
+    const uint64_t m1 = B >= 128 ? ~0ull : (B > 64 ? (1ull << (B - 64)) - 1 : 0ull);
+    x0 &= m0;
+    x1 &= m1;
+    const uint64_t s0 = ~x0 & m0, s1 = ~x1 & m1;
+    // word i of the 256-bit value (0 : 0 : s1 : s0) << B
+    const int q = B >> 6, r = B & 63;
+    // source word j of (s1 : s0), zero outside
+#define DARD_SRC(j) ((j) == 0 ? s0 : ((j) == 1 ? s1 : 0ull))
+#define DARD_SHL(i) (r ? (DARD_SRC((i) - q) << r) | (DARD_SRC((i) - q - 1) >> (64 - r)) : DARD_SRC((i) - q))
+    v0 = x0 | DARD_SHL(0);
+    v1 = x1 | DARD_SHL(1);
+    v2 = DARD_SHL(2);
+    v3 = DARD_SHL(3);
+#undef DARD_SHL
+#undef DARD_SRC
+}
+
+// First key and key count of tile t (npre prefix tiles over [0, pre_end),
+// then block tiles over [P, P + 2B)).
+__device__ __forceinline__ int tile_first(int t, int npre, int P) { return t < npre ? t * kKeys : P + (t - npre) * kKeys; }
+__device__ __forceinline__ int tile_count(int t, int npre, int pre_end, int B2) {
+    return t < npre ? min(kKeys, pre_end - t * kKeys) : min(kKeys, B2 - (t - npre) * kKeys);
+}
 
 template <int DH, int G, int RING>
 __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
@@ -60,11 +91,14 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     const int r0 = rt * kRows;
     const int split = blockIdx.y, nsplit = gridDim.y;
 
-    const int ntiles = (a.nkeys + kKeys - 1) / kKeys;
+    // prefix tiles [0, npre), then block tiles (masked mode)
+    const int pre_end = a.masked ? a.P : a.nkeys;
+    const int npre = (pre_end + kKeys - 1) / kKeys;
+    const int ntiles = npre + (a.masked ? (2 * a.B + kKeys - 1) / kKeys : 0);
     const int t_begin = split * tiles_per_split;
     const int t_end = min(ntiles, t_begin + tiles_per_split);
-    const int key_end = min(a.nkeys, t_end * kKeys);
     const int iters = (t_end - t_begin + G - 1) / G;   // tile steps of every group
+    const int P = a.P, B2 = 2 * a.B;
 
     const bf16_t* q = reinterpret_cast<const bf16_t*>(a.q);
     const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
@@ -75,27 +109,26 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     constexpr int VUNITS = (kKeys / 4) * (DH / 8);
     bf16x8 kreg[RING][KCH];
     bf16x8 vreg[RING][4];
-    auto load_tile = [&](int slot, int tile) {
-        const int kb0 = tile * kKeys;
+    auto load_tile = [&](int slot, int tile) __attribute__((always_inline)) {
+        const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
 #pragma unroll
         for (int it = 0; it < KCH; ++it) {
             const int qd = tid + 256 * it;
             const int key = qd / (DH / 8), c8 = qd % (DH / 8);
-            const int kabs = kb0 + key;
             bf16x8 z = {};
-            kreg[slot][it] = kabs < key_end ? ld_bf16x8(kbase + (size_t)kabs * DH + c8 * 8) : z;
+            kreg[slot][it] = key < n ? ld_bf16x8(kbase + (size_t)(k0 + key) * DH + c8 * 8) : z;
         }
         if (tid < VUNITS) {
             const int kg = tid / (DH / 8), dg = tid % (DH / 8);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int kabs = kb0 + 4 * kg + e;
+                const int key = 4 * kg + e;
                 bf16x8 z = {};
-                vreg[slot][e] = kabs < key_end ? ld_bf16x8(vbase + (size_t)kabs * DH + dg * 8) : z;
+                vreg[slot][e] = key < n ? ld_bf16x8(vbase + (size_t)(k0 + key) * DH + dg * 8) : z;
             }
         }
     };
-    auto store_tile = [&](int slot) {
+    auto store_tile = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
         for (int it = 0; it < KCH; ++it) {
             const int qd = tid + 256 * it;
@@ -129,17 +162,12 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
             qf[c] = row_ok ? ld_bf16x8(qp + 32 * c + 8 * g) : z;
         }
     }
-    // this lane's row of the state mask, built by its wave with ballots
-    uint64_t sel0 = 0, sel1 = 0;
-    if (a.masked) {
-        const BlockView bv = load_block_view(a.state + (size_t)s * a.B, a.conf + (size_t)s * a.B, a.B);
-        for (int k = 0; k < 16; ++k) {
-            const int r = r0 + wave * 16 + k;      // the same on every lane of the wave
-            if (r >= a.R) break;
-            uint64_t x0, x1;
-            row_take_x(bv, r, a.B, a.flags, x0, x1);
-            if (lr == k) { sel0 = x0; sel1 = x1; }
-        }
+    // this lane's row of the state mask, widened to the block's 2B keys
+    uint64_t bv0 = 0, bv1 = 0, bv2 = 0, bv3 = 0;
+    if (a.masked && row_ok) {
+        const int W = (a.B + 63) / 64;
+        const uint64_t* sp = a.sel + ((size_t)s * a.R + my_row) * W;
+        block_vis(sp[0], W > 1 ? sp[1] : 0ull, a.B, bv0, bv1, bv2, bv3);
     }
     const float sl2 = a.scale * kLog2e;
 
@@ -148,7 +176,7 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     for (int d = 0; d < DH / 16; ++d) o[d] = floatx4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    auto compute_tile = [&](int tile) {
+    auto compute_tile = [&](int tile) __attribute__((always_inline)) {
         // ---- S^T = K * Q^T for this wave's 16 rows: 4 blocks of 16 keys
         floatx4 sc[4];
 #pragma unroll
@@ -161,9 +189,19 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
             }
             sc[kb] = acc;
         }
-        // ---- scale; visibility only where the tile has block keys or a tail
-        const int kb0 = tile * kKeys;
-        const bool all_visible = kb0 + kKeys <= key_end && (!a.masked || kb0 + kKeys <= a.P);
+        // ---- scale; the visibility word only where the tile has block keys or a tail
+        const int n = tile_count(tile, npre, pre_end, B2);
+        const bool all_visible = tile < npre && n == kKeys;
+        uint64_t vis;
+        if (tile < npre) {
+            vis = n >= 64 ? ~0ull : (1ull << n) - 1;
+        } else {
+            // word bt of the block visibility, selected with masks (a select
+            // chain here becomes a lookup table in private memory)
+            const uint64_t bt = (uint64_t)(tile - npre);
+            vis = (bv0 & (0ull - (uint64_t)(bt == 0))) | (bv1 & (0ull - (uint64_t)(bt == 1))) |
+                  (bv2 & (0ull - (uint64_t)(bt == 2))) | (bv3 & (0ull - (uint64_t)(bt == 3)));
+        }
         float mt = -INFINITY;
         if (all_visible) {
 #pragma unroll
@@ -178,16 +216,8 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
             for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int key = kb0 + 16 * kb + 4 * g + i;
-                    bool vis = key < key_end;
-                    if (a.masked && key >= a.P) {
-                        const int j = key - a.P;
-                        const int jj = j < a.B ? j : j - a.B;
-                        const uint64_t word = jj < 64 ? sel0 : sel1;
-                        const bool bx = (word >> (jj & 63)) & 1ull;
-                        vis = vis && (j < a.B ? bx : !bx);
-                    }
-                    const float v = vis ? sc[kb][i] * sl2 : -INFINITY;
+                    const bool on = (vis >> (16 * kb + 4 * g + i)) & 1ull;
+                    const float v = on ? sc[kb][i] * sl2 : -INFINITY;
                     sc[kb][i] = v;
                     mt = fmaxf(mt, v);
                 }
@@ -399,25 +429,24 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     for (int e = 0; e < DH; ++e) out[e] = o[e] * inv;
 }
 
-// Groups per workgroup: aim at >= 1024 waves over the chip.  Four groups
-// leave 128 registers per lane, enough only for head_dim 64.
-int attention_groups(int b, int R, int Hq, int dh, int ntiles) {
+// Groups per workgroup: two when fewer than 1024 waves would cover the chip
+// (more groups would spill the register ring), never more than tiles.
+int attention_groups(int b, int R, int Hq, int ntiles) {
     const int wgs = b * Hq * ((R + kRows - 1) / kRows);
-    int G = (1024 + 4 * wgs - 1) / (4 * wgs);
-    G = G >= 4 ? 4 : (G >= 2 ? 2 : 1);
-    if (dh == 128 && G > 2) G = 2;
-    while (G > 1 && G > ntiles) G >>= 1;
-    return G;
+    return (4 * wgs < 1024 && ntiles >= 2) ? 2 : 1;
 }
 
 }  // namespace
 
-int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots) {
+int attention_tiles(int masked, int P, int B, int nkeys) {
+    return masked ? (P + kKeys - 1) / kKeys + (2 * B + kKeys - 1) / kKeys : (nkeys + kKeys - 1) / kKeys;
+}
+
+int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots) {
     if (dtype != DARD_DTYPE_BF16) return 1;
     const int rowtiles = (R + kRows - 1) / kRows;
-    const int ntiles = (nkeys + kKeys - 1) / kKeys;
     const int wgs = b * Hq * rowtiles;
-    const int G = attention_groups(b, R, Hq, 128, ntiles);   // the head_dim 128 grouping
+    const int G = attention_groups(b, R, Hq, ntiles);
     // split across workgroups only while the chip is not yet covered and
     // every group would still walk more than 3 tiles
     int ns = 1;
@@ -429,29 +458,30 @@ int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots) {
     return (ntiles + tps - 1) / tps;      // no empty split
 }
 
-size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys) {
-    const int ns = attention_splits(dtype, b, R, Hq, nkeys, (size_t)-1);
+size_t attention_partial_slots(int dtype, int b, int R, int Hq, int ntiles) {
+    const int ns = attention_splits(dtype, b, R, Hq, ntiles, (size_t)-1);
     return ns <= 1 ? 0 : (size_t)ns * b * R * Hq;
 }
 
 hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStream_t s) {
     if (a.out_frag && !frag_rows(dtype, a.b * a.R)) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16) {
+        if (a.masked && (!a.sel || a.B > 128)) return hipErrorInvalidValue;
         const int rowtiles = (a.R + kRows - 1) / kRows;
-        const int ntiles = (a.nkeys + kKeys - 1) / kKeys;
+        const int ntiles = attention_tiles(a.masked, a.P, a.B, a.nkeys);
         const bool can_split = a.part && a.part_ml;
         if (!can_split || ns < 1 || ns > kMaxSplit || (size_t)ns * a.b * a.R * a.Hq > a.part_slots) ns = 1;
         if (ns > ntiles) ns = ntiles > 0 ? ntiles : 1;
         const int tps = (ntiles + ns - 1) / ns;
         ns = ntiles > 0 ? (ntiles + tps - 1) / tps : 1;
-        const int G = attention_groups(a.b, a.R, a.Hq, a.dh, tps);
+        const int G = attention_groups(a.b, a.R, a.Hq, tps);
         dim3 grid(a.b * a.Hq * rowtiles, ns);
 #define DARD_ATT(DHV, GV) \
-    launch((attn_bf16_kernel<DHV, GV, GV == 4 ? 1 : 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
+    launch((attn_bf16_kernel<DHV, GV, 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
         if (a.dh == 128) {
-            if (G == 4) DARD_ATT(128, 4); else if (G == 2) DARD_ATT(128, 2); else DARD_ATT(128, 1);
+            if (G == 2) DARD_ATT(128, 2); else DARD_ATT(128, 1);
         } else {
-            if (G == 4) DARD_ATT(64, 4); else if (G == 2) DARD_ATT(64, 2); else DARD_ATT(64, 1);
+            if (G == 2) DARD_ATT(64, 2); else DARD_ATT(64, 1);
         }
 #undef DARD_ATT
         hipError_t e = hipGetLastError();
@@ -477,7 +507,9 @@ hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStre
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     const bool can_split = a.part && a.part_ml;
-    const int ns = can_split ? attention_splits(dtype, a.b, a.R, a.Hq, a.nkeys, a.part_slots) : 1;
+    const int ns = can_split ? attention_splits(dtype, a.b, a.R, a.Hq, attention_tiles(a.masked, a.P, a.B, a.nkeys),
+                                                a.part_slots)
+                             : 1;
     return launch_attention_splits(dtype, a, ns, s);
 }
 

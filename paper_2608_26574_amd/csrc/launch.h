@@ -28,8 +28,9 @@ struct AttnArgs {
     const void* k;      // [b][Hkv][cap][dh]
     const void* v;
     void* out;          // [b][R][Hq][dh]
-    const uint8_t* state;  // [b][B] (masked mode)
+    const uint8_t* state;  // [b][B] (masked mode, fp32 path)
     const float* conf;     // [b][B]
+    const uint64_t* sel;   // [b][R][ceil(B/64)] take-x words of the state mask (masked mode, bf16 path)
     int b, R, Hq, Hkv, dh, cap;
     int P;              // prefix keys (always visible)
     int B;              // block length (masked mode); keys = P + 2B
@@ -42,10 +43,12 @@ struct AttnArgs {
     size_t part_slots;  // capacity of part / part_ml in (split, row, head) slots
     int out_frag;       // 1: out is fragment-major [b*R][Hq*dh] (bf16 only)
 };
+// 64-key tiles of a launch: the prefix (or all keys when unmasked), then the block.
+int attention_tiles(int masked, int P, int B, int nkeys);
 // Key splits the launcher uses for these sizes with `slots` partial slots.
-int attention_splits(int dtype, int b, int R, int Hq, int nkeys, size_t slots);
+int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots);
 // Partial slots the launcher would like (0 = no split).
-size_t attention_partial_slots(int dtype, int b, int R, int Hq, int nkeys);
+size_t attention_partial_slots(int dtype, int b, int R, int Hq, int ntiles);
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---- gemm.hip
