@@ -44,21 +44,39 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
 
 __device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
 
-// Epilogue for output columns n..n+3 (n % 4 == 0) of token row m.
+// Epilogue for output columns n..n+3 (n % 4 == 0) of token row m, in two
+// halves: epi_fetch loads what the epilogue reads (the residual, or the two
+// rotary (cos, sin) pairs), epi_store combines and writes.  A kernel that
+// owns several tiles fetches for all of them before its first store, so the
+// loads overlap instead of each waiting behind the stores before it.
+__device__ __forceinline__ float4 epi_fetch(const EpiArgs& e, int m, int n) {
+    if (e.kind == EPI_RESID) return *reinterpret_cast<const float4*>(e.y + (size_t)m * e.ldy + n);
+    if (e.kind == EPI_QKV) {
+        const int qd = e.Hq * e.dh, kd = e.Hkv * e.dh;
+        if (n < qd + kd) {
+            const int r = m % e.rows_per_seq;
+            const int pos = e.step ? e.P + (r % e.B) : r;
+            const int ein = (n < qd ? n : n - qd) % e.dh;
+            const float* t = e.rope + ((size_t)pos * (e.dh / 2) + ein / 2) * 2;
+            const float2 c0 = *reinterpret_cast<const float2*>(t);
+            const float2 c1 = *reinterpret_cast<const float2*>(t + 2);
+            return make_float4(c0.x, c0.y, c1.x, c1.y);
+        }
+    }
+    return make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 template <typename T>
-__device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4 v) {
+__device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx4 v, float4 f) {
     switch (e.kind) {
     case EPI_STORE_F32:
     case EPI_PARTIAL:
         *reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n) = make_float4(v[0], v[1], v[2], v[3]);
         break;
-    case EPI_RESID: {
-        float4* p = reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n);
-        float4 h = *p;
-        h.x += v[0]; h.y += v[1]; h.z += v[2]; h.w += v[3];
-        *p = h;
+    case EPI_RESID:
+        *reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n) =
+            make_float4(f.x + v[0], f.y + v[1], f.z + v[2], f.w + v[3]);
         break;
-    }
     case EPI_SWIGLU: {
         T* a = reinterpret_cast<T*>(e.act) + (e.act_frag ? frag_off(m, n / 2, e.ld_act) : (size_t)m * e.ld_act + n / 2);
         St<T>::st(a, silu(v[0]) * v[1]);
@@ -67,16 +85,13 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4
     }
     case EPI_QKV: {
         const int s = m / e.rows_per_seq, r = m % e.rows_per_seq;
-        const int pos = e.step ? e.P + (r % e.B) : r;
         const int cidx = e.step ? e.P + r : r;
         const int qd = e.Hq * e.dh, kd = e.Hkv * e.dh;
         if (n < qd + kd) {
             // rotary pairs (v0, v1) and (v2, v3): natural dims (t, t + dh/2)
             const int ein = (n < qd ? n : n - qd) % e.dh;
-            const float2 cs0 = *reinterpret_cast<const float2*>(e.rope + ((size_t)pos * (e.dh / 2) + ein / 2) * 2);
-            const float2 cs1 = *reinterpret_cast<const float2*>(e.rope + ((size_t)pos * (e.dh / 2) + ein / 2 + 1) * 2);
-            const float a0 = v[0] * cs0.x - v[1] * cs0.y, b0 = v[1] * cs0.x + v[0] * cs0.y;
-            const float a1 = v[2] * cs1.x - v[3] * cs1.y, b1 = v[3] * cs1.x + v[2] * cs1.y;
+            const float a0 = v[0] * f.x - v[1] * f.y, b0 = v[1] * f.x + v[0] * f.y;
+            const float a1 = v[2] * f.z - v[3] * f.w, b1 = v[3] * f.z + v[2] * f.w;
             if (n < qd) {
                 store4<T>(reinterpret_cast<T*>(e.q) + (size_t)m * e.ldq + n, a0, b0, a1, b1);
             } else {
@@ -93,6 +108,11 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4
         break;
     }
     }
+}
+
+template <typename T>
+__device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4 v) {
+    epi_store<T>(e, m, n, v, epi_fetch(e, m, n));
 }
 
 __device__ __forceinline__ bf16x8 ld_nt(const bf16_t* p) {
@@ -165,34 +185,51 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
         }
     }
 
+    // Sum the KSPLIT partial tiles through LDS in wave order; wave w then
+    // finishes token blocks [NQ w, NQ (w + 1)) so the epilogue runs on every wave.
+    static_assert(4 % KSPLIT == 0, "KSPLIT divides the 4 token blocks");
+    constexpr int NQ = 4 / KSPLIT;
+    const int mb0 = wave * NQ;
+    floatx4 res[NW][NQ];
     if constexpr (KSPLIT > 1) {
-        __shared__ floatx4 red[KSPLIT - 1][NW * 4][64];
-        if (wave > 0) {
+        __shared__ floatx4 red[KSPLIT][NW * 4][64];
 #pragma unroll
-            for (int j = 0; j < NW; ++j)
+        for (int j = 0; j < NW; ++j)
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) red[wave - 1][j * 4 + mb][lane] = acc[j][mb];
-        }
+            for (int mb = 0; mb < 4; ++mb) red[wave][j * 4 + mb][lane] = acc[j][mb];
         __syncthreads();
-        if (wave != 0) return;
 #pragma unroll
-        for (int w = 0; w < KSPLIT - 1; ++w)
+        for (int j = 0; j < NW; ++j)
 #pragma unroll
-            for (int j = 0; j < NW; ++j)
+            for (int q = 0; q < NQ; ++q) {
+                floatx4 t = red[0][j * 4 + mb0 + q][lane];
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) acc[j][mb] += red[w][j * 4 + mb][lane];
+                for (int w = 1; w < KSPLIT; ++w) t += red[w][j * 4 + mb0 + q][lane];
+                res[j][q] = t;
+            }
+    } else {
+#pragma unroll
+        for (int j = 0; j < NW; ++j)
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) res[j][q] = acc[j][q];
     }
     EpiArgs ee = e;
     if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
+    float4 pre[NW][NQ];
 #pragma unroll
-    for (int j = 0; j < NW; ++j) {
-        const int n = 16 * (nb0 + j) + 4 * g;
+    for (int j = 0; j < NW; ++j)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            const int m = 16 * mb + lr;
-            if (m < M && n < N) epilogue<bf16_t>(ee, m, n, acc[j][mb]);
+        for (int q = 0; q < NQ; ++q) {
+            const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
+            pre[j][q] = (m < M && n < N) ? epi_fetch(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-    }
+#pragma unroll
+    for (int j = 0; j < NW; ++j)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
+            if (m < M && n < N) epi_store<bf16_t>(ee, m, n, res[j][q], pre[j][q]);
+        }
 }
 
 // ---------------------------------------------------------------- tiled
@@ -263,15 +300,21 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
                 for (int i = 0; i < 4; ++i) acc[j][i] = mfma16x16x32(af[j], bfr[i], acc[j][i]);
         }
     }
+    float4 pre[4][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = 16 * (nb_base + wn * 4 + j) + 4 * g;
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int m = m0 + wm * 64 + 16 * i + lr;
-            if (m < M && n < N) epilogue<bf16_t>(e, m, n, acc[j][i]);
+            const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
+            pre[j][i] = (m < M && n < N) ? epi_fetch(e, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
+            if (m < M && n < N) epi_store<bf16_t>(e, m, n, acc[j][i], pre[j][i]);
+        }
 }
 
 // ---------------------------------------------------------------- fp32
