@@ -138,7 +138,7 @@ def main():
     gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9
     roofline = {"kernel": "gemm_stream_bf16 (gate/up + SwiGLU), per launch", "bound": "hbm",
                 "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                 "algorithmic_bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_ms * 1e3, 2)}
 
     # all weight-streaming GEMMs of a step together
@@ -196,6 +196,25 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None when the GEMM
+    sources changed since the counters were taken."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    try:
+        text = open(os.path.join(root, "profiles", "gate_up_gemm_hbm_traffic.md")).read()
+        h = hashlib.sha256()
+        for f in ("gemm.hip", "common.h", "launch.h"):
+            h.update(open(os.path.join(root, "paper_2608_26574_amd", "csrc", f), "rb").read())
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if line.count(": ") == 1 and " " not in line.split(": ")[0])
+    if fields.get("source_sha256", "").strip() != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(dims, b, B, P, frac, layers_sampled=2, min_s=10.0):

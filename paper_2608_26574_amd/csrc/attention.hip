@@ -111,20 +111,31 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     bf16x8 vreg[RING][4];
     auto load_tile = [&](int slot, int tile) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
+        const bf16_t* kt = kbase + (size_t)k0 * DH;
+        const bf16_t* vt = vbase + (size_t)k0 * DH;
+        // V: thread (kg, dg) = (tid % 16, tid / 16) reads keys 4kg..4kg+3 at dims 8dg..8dg+7
+        const int kg = tid & 15, dg = tid >> 4;
+        if (n == kKeys) {   // full tile (uniform): no per-key test
 #pragma unroll
-        for (int it = 0; it < KCH; ++it) {
-            const int qd = tid + 256 * it;
-            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
-            bf16x8 z = {};
-            kreg[slot][it] = key < n ? ld_bf16x8(kbase + (size_t)(k0 + key) * DH + c8 * 8) : z;
-        }
-        if (tid < VUNITS) {
-            const int kg = tid / (DH / 8), dg = tid % (DH / 8);
+            for (int it = 0; it < KCH; ++it) kreg[slot][it] = ld_bf16x8(kt + (size_t)(tid + 256 * it) * 8);
+            if (tid < VUNITS) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int key = 4 * kg + e;
+                for (int e = 0; e < 4; ++e) vreg[slot][e] = ld_bf16x8(vt + (size_t)(4 * kg + e) * DH + dg * 8);
+            }
+        } else {
+#pragma unroll
+            for (int it = 0; it < KCH; ++it) {
+                const int qd = tid + 256 * it;
                 bf16x8 z = {};
-                vreg[slot][e] = key < n ? ld_bf16x8(vbase + (size_t)(k0 + key) * DH + dg * 8) : z;
+                kreg[slot][it] = qd / (DH / 8) < n ? ld_bf16x8(kt + (size_t)qd * 8) : z;
+            }
+            if (tid < VUNITS) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int key = 4 * kg + e;
+                    bf16x8 z = {};
+                    vreg[slot][e] = key < n ? ld_bf16x8(vt + (size_t)key * DH + dg * 8) : z;
+                }
             }
         }
     };
@@ -136,7 +147,8 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
             *reinterpret_cast<bf16x8*>(&Ks[key * KPAD + c8 * 8]) = kreg[slot][it];
         }
         if (tid < VUNITS) {
-            const int kg = tid / (DH / 8), dg = tid % (DH / 8);
+            // 16 consecutive lanes write one contiguous 128-byte run of a V^T row
+            const int kg = tid & 15, dg = tid >> 4;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 bf16x4 t4 = {vreg[slot][0][e], vreg[slot][1][e], vreg[slot][2][e], vreg[slot][3][e]};
@@ -226,14 +238,15 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
         const float m_new = fmaxf(m_run, mt);
-        const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
+        // arguments are <= 0: the hardware exp2 (v_exp_f32) needs no range handling
+        const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
         float psum = 0.f;
         bf16x8 pb[2];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = (m_new == -INFINITY) ? 0.f : exp2f(sc[kb][i] - m_new);
+                const float p = (m_new == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sc[kb][i] - m_new);
                 psum += p;
                 pb[kb >> 1][(kb & 1) * 4 + i] = (__bf16)p;
             }
