@@ -393,10 +393,12 @@ hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N
 //   ks     waves per workgroup splitting K
 //   depth  k units in flight per wave
 //   split  workgroups splitting K (fp32 partials, reduced by the consumer)
-// Chosen from measurements on MI355X at 64 tokens: the widest wave tile whose
-// grid fills the 256 CUs most evenly, more waves per workgroup when there is
-// only one workgroup per CU, and a 4-way K split for the residual projections
-// whose 4096-wide output has too few column tiles.
+// Chosen from measurements on MI355X at 64 tokens.  Every wave reads all 64
+// token rows of its k units (8 KB per unit), so a wider wave tile amortises
+// that over more weight columns: the widest of 8, 6, 4, 3 column blocks whose
+// grid still covers the 256 CUs; otherwise the tile that fills the CUs most
+// evenly, with 4 waves per workgroup.  The O and down projections, whose
+// 4096-wide output has too few column tiles, split K 4 ways instead.
 struct StreamCfg {
     int nw, ks, depth, split;
 };
@@ -408,6 +410,9 @@ StreamCfg stream_cfg(int N, int K, bool partial) {
         while (S > 1 && KU / S < 8) S /= 2;
         if (N % 64 == 0) return K > 4096 ? StreamCfg{4, 4, 2, S} : StreamCfg{4, 2, 3, S};
         return StreamCfg{1, 4, 2, S};
+    }
+    for (int c : {8, 6}) {
+        if (N % (16 * c) == 0 && N / (16 * c) >= 256) return c == 8 ? StreamCfg{8, 2, 3, 1} : StreamCfg{6, 4, 3, 1};
     }
     int nw = 0;
     double best = -1.0;
@@ -449,7 +454,9 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
         if (xfrag) launch((gemm_stream_bf16<NW, KS, D, true>), grid, block, 0, s, x, M, K, ldx, w, N, e);  \
         else launch((gemm_stream_bf16<NW, KS, D, false>), grid, block, 0, s, x, M, K, ldx, w, N, e);       \
     } while (0)
-        if (c.nw == 4 && c.ks == 4) DARD_GS(4, 4, 2);
+        if (c.nw == 8) DARD_GS(8, 2, 3);
+        else if (c.nw == 6) DARD_GS(6, 4, 3);
+        else if (c.nw == 4 && c.ks == 4) DARD_GS(4, 4, 2);
         else if (c.nw == 4 && c.depth == 3) DARD_GS(4, 2, 3);
         else if (c.nw == 4) DARD_GS(4, 2, 2);
         else if (c.nw == 3 && c.ks == 4) DARD_GS(3, 4, 3);
