@@ -32,6 +32,7 @@ constexpr int kRows = 64;      // query rows per workgroup
 constexpr int kKeys = 64;      // keys per tile
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kMinLog2 = -1e30f;   // running-max floor (log2 units): exp2 of anything below it is 0
 
 template <int DH>
 struct Lds {
@@ -78,8 +79,9 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     __shared__ __attribute__((aligned(16))) char smem[G * L::GROUP_BYTES];
 
-    const int grp = threadIdx.x >> 8, tid = threadIdx.x & 255;
-    const int lane = tid & 63, wave = tid >> 6;
+    // group and wave are wave-uniform: say so, so that tile bookkeeping stays scalar
+    const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8), tid = threadIdx.x & 255;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane & 15, g = lane >> 4;
     bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + grp * L::GROUP_BYTES);
     bf16_t* Vt = Ks + kKeys * KPAD;
@@ -186,7 +188,7 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     floatx4 o[DH / 16];
 #pragma unroll
     for (int d = 0; d < DH / 16; ++d) o[d] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_run = kMinLog2, l_run = 0.f;
 
     auto compute_tile = [&](int tile) __attribute__((always_inline)) {
         // ---- S^T = K * Q^T for this wave's 16 rows: 4 blocks of 16 keys
@@ -201,60 +203,57 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
             }
             sc[kb] = acc;
         }
-        // ---- scale; the visibility word only where the tile has block keys or a tail
+        // ---- visibility: only tiles with block keys or a ragged end test it
+        // (tile and n are wave-uniform, so this is a scalar branch)
         const int n = tile_count(tile, npre, pre_end, B2);
-        const bool all_visible = tile < npre && n == kKeys;
-        uint64_t vis;
-        if (tile < npre) {
-            vis = n >= 64 ? ~0ull : (1ull << n) - 1;
-        } else {
-            // word bt of the block visibility, selected with masks (a select
-            // chain here becomes a lookup table in private memory)
-            const uint64_t bt = (uint64_t)(tile - npre);
-            vis = (bv0 & (0ull - (uint64_t)(bt == 0))) | (bv1 & (0ull - (uint64_t)(bt == 1))) |
-                  (bv2 & (0ull - (uint64_t)(bt == 2))) | (bv3 & (0ull - (uint64_t)(bt == 3)));
-        }
-        float mt = -INFINITY;
-        if (all_visible) {
+        if (!(tile < npre && n == kKeys)) {
+            uint64_t vis;
+            if (tile < npre) {
+                vis = (1ull << n) - 1;     // n < 64 here
+            } else {
+                // word bt of the block visibility, selected with masks (a select
+                // chain here becomes a lookup table in private memory)
+                const uint64_t bt = (uint64_t)(tile - npre);
+                vis = (bv0 & (0ull - (uint64_t)(bt == 0))) | (bv1 & (0ull - (uint64_t)(bt == 1))) |
+                      (bv2 & (0ull - (uint64_t)(bt == 2))) | (bv3 & (0ull - (uint64_t)(bt == 3)));
+            }
+            // this lane's keys 16kb + 4g + i: bits 16(kb%2) + i of w[kb/2]
+            const uint32_t w0 = (uint32_t)vis >> (4 * g), w1 = (uint32_t)(vis >> 32) >> (4 * g);
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    sc[kb][i] *= sl2;
-                    mt = fmaxf(mt, sc[kb][i]);
-                }
-        } else {
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const bool on = (vis >> (16 * kb + 4 * g + i)) & 1ull;
-                    const float v = on ? sc[kb][i] * sl2 : -INFINITY;
-                    sc[kb][i] = v;
-                    mt = fmaxf(mt, v);
-                }
-            }
+                for (int i = 0; i < 4; ++i)
+                    if (!(((kb < 2 ? w0 : w1) >> (16 * (kb & 1) + i)) & 1u)) sc[kb][i] = -INFINITY;
         }
+        // ---- online softmax in the log2 domain; the running max starts at a
+        // finite floor, so rows with no visible key yet need no special case
+        float mt = sc[0][0];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sc[kb][i]);
         mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float m_new = fmaxf(m_run, mt);
+        const float m_new = fmaxf(m_run, mt * sl2);     // sl2 > 0: the max commutes with the scale
         // arguments are <= 0: the hardware exp2 (v_exp_f32) needs no range handling
-        const float alpha = (m_new == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         float psum = 0.f;
         bf16x8 pb[2];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = (m_new == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sc[kb][i] - m_new);
+                const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], sl2, -m_new));
                 psum += p;
                 pb[kb >> 1][(kb & 1) * 4 + i] = (__bf16)p;
             }
         }
         l_run = l_run * alpha + psum;
         m_run = m_new;
+        if (__ballot(alpha != 1.f)) {             // some row's max moved
 #pragma unroll
-        for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
+            for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
+        }
         // ---- O^T += V^T * P^T
 #pragma unroll
         for (int d = 0; d < DH / 16; ++d) {
@@ -460,10 +459,13 @@ int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots) 
     const int rowtiles = (R + kRows - 1) / kRows;
     const int wgs = b * Hq * rowtiles;
     const int G = attention_groups(b, R, Hq, ntiles);
-    // split across workgroups only while the chip is not yet covered and
-    // every group would still walk more than 3 tiles
+    // Measured at 64 rows x 32 heads: a tile step costs about 2 us, the
+    // combine kernel about 4.3 us plus its launch, so a split pays only when
+    // the workgroups would otherwise walk more than 5 tile steps; then about
+    // 3 tiles per split.  No split once the workgroups alone cover the chip.
+    if (wgs * G * 4 >= 1024 || (ntiles + G - 1) / G <= 5) return 1;
     int ns = 1;
-    while (ns < kMaxSplit && wgs * ns * G * 4 < 1024 && ntiles / (ns * G) > 3) ns *= 2;
+    while (ns < kMaxSplit && ntiles > 3 * ns) ns *= 2;
     const size_t per_split = (size_t)b * R * Hq;
     while (ns > 1 && (size_t)ns * per_split > slots) --ns;
     if (ns <= 1) return 1;
