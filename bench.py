@@ -193,9 +193,82 @@ def main():
         "kernel_ms_per_step": round(kern_ms, 4),
         "gaps_ms_per_step": round(ms_per_step - kern_ms, 4),
     }
+    out["ops"] = op_measurements()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
     print(json.dumps(out), flush=True)
+
+
+def op_measurements(reps=20):
+    """The two isolated operations the roofline targets name, measured cold
+    (inputs rotated through copies whose total exceeds the 256 MB MALL):
+    - state-masked attention at the 8B attention shape (32 x 128 heads, prompt
+      KV 512, block 32, candidate fraction 0.25, bf16 Q/K/V ~ N(0, 1)) for
+      batch 1, 4 and 16, against the bf16 MFMA peak (algorithmic flops
+      4 dh Hq 2B (P+B) b) and the HBM peak (K/V of P+2B keys, Q and O);
+    - the vocab-wide confidence reduction (argmax, max-prob) over fp32 logits
+      at the 8B step's row count (B + |M| = 44 rows x 126464) and at the 7B GQA
+      batch-8 step's (8 x 87 rows x 152064), against the HBM peak."""
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fn(0)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(n):
+            fn(i + 1)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    res = {"attention": [], "confidence": []}
+    P, B, H, dh, frac = 512, 32, 32, 128, 0.25
+    for bsz in (1, 4, 16):
+        cap = P + 2 * B
+        kv_bytes = bsz * H * cap * dh * 2
+        ncopy = max(4, -(-600 * 2**20 // (2 * kv_bytes)))
+        g = torch.Generator(device="cuda").manual_seed(2)
+        q = torch.randn(bsz, 2 * B, H, dh, generator=g, device="cuda").bfloat16()
+        ks = [torch.randn(bsz, H, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        vs = [torch.randn(bsz, H, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        _, state, conf = synth.workload_block(bsz, B, frac, 100, seed=3)
+        state, conf = torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()
+        out = torch.empty_like(q)
+        ws = torch.empty(max(dard.dard_attention_workspace_bytes(1, bsz, B, H, dh, P), 1), dtype=torch.uint8,
+                         device="cuda")
+
+        def att(i):
+            dard.dard_masked_attention(q, ks[i % ncopy], vs[i % ncopy], P, state, conf, dh ** -0.5, 0, out, ws)
+        ms = timed(att, reps)
+        flops = 4 * dh * H * 2 * B * (P + B) * bsz
+        nbytes = 2 * bsz * H * (P + 2 * B) * dh * 2 + 2 * q.numel() * 2
+        res["attention"].append({"batch": bsz, "us": round(ms * 1e3, 2),
+                                 "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+                                 "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                                 "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                                 "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+        del ks, vs
+    for rows, V, label in ((44, 126464, "8B step, 44 rows"), (8 * 87, 152064, "7B GQA batch-8 step, 696 rows")):
+        nbytes = rows * V * 4
+        ncopy = max(2, -(-600 * 2**20 // nbytes))
+        g = torch.Generator(device="cuda").manual_seed(4)
+        ls = [torch.randn(rows, V, generator=g, device="cuda") for _ in range(ncopy)]
+        am = torch.empty(rows, dtype=torch.int32, device="cuda")
+        mp = torch.empty(rows, device="cuda")
+        ws = torch.empty(max(dard.dard_confidence_workspace_bytes(rows, V), 1), dtype=torch.uint8, device="cuda")
+
+        def cf(i):
+            dard.dard_confidence(ls[i % ncopy], am, mp, ws=ws)
+        ms = timed(cf, reps)
+        res["confidence"].append({"shape": label, "us": round(ms * 1e3, 2),
+                                  "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                                  "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+        del ls
+    torch.cuda.empty_cache()
+    return res
 
 
 def measured_traffic():
