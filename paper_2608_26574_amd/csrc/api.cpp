@@ -98,7 +98,7 @@ struct WsLayout {
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     const size_t es = esize(d->dtype);
     size_t rows = (size_t)b * (2 * B > cap ? 2 * B : cap);
-    if (rows < 64) rows = 64;   // fragment-major activations hold whole 16 x 64 blocks of 64 rows
+    rows = (rows + 63) / 64 * 64;   // fragment-major activations hold whole 16-row blocks, 64 at least
     const size_t qd = (size_t)d->n_heads * d->head_dim;
     const size_t step_rows = (size_t)b * 2 * B;
     const size_t nch = conf_chunks(d->vocab);
@@ -120,8 +120,10 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.cpart_v = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
     W.cpart_m = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
     W.w = o; o = align256(o + (size_t)b * B * 4);
-    // split-K partials of the O and down projections (64-row tiles only)
-    W.gpart = o; o = align256(o + (size_t)8 * 64 * d->d_model * 4);
+    // split-K partials of the O and down projections: up to 8 splits of 64
+    // rows (streaming GEMM) or 4 splits of all rows (pipelined GEMM)
+    const size_t prow = rows * 4 > 8 * 64 ? rows * 4 : 8 * 64;
+    W.gpart = o; o = align256(o + prow * d->d_model * 4);
     W.total = o;
     return W;
 }

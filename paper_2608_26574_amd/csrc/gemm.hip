@@ -232,6 +232,152 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
         }
 }
 
+// ---------------------------------------------------------------- pipelined tiles
+// M > 64 (prefill, large batches) with fragment-major X.  A workgroup owns a
+// 128-token x (32 WN)-column output tile; wave (wm, wn) computes tokens
+// 64wm..64wm+63 x 16 WN columns with WN x 4 accumulator tiles.  Per 64-wide k
+// unit the workgroup copies the 2 WN weight blocks and 8 activation blocks it
+// needs (both fragment-major, so every 16-byte chunk is a plain copy) into one
+// of two LDS stages; each thread holds its chunks of the next two units in a
+// register ring, so global loads run two units ahead of the MFMAs and one
+// barrier per unit separates the stages.  An optional split of K across
+// workgroups writes fp32 partials (EPI_PARTIAL).
+constexpr int PBM = 128;
+
+template <int WN>
+struct PipeTile {
+    static constexpr int BN = 32 * WN;              // output columns per workgroup
+    static constexpr int CHW = BN / 16 * 128;       // 16-byte weight chunks per stage
+    static constexpr int CHX = PBM / 16 * 128;      // activation chunks per stage
+    static constexpr int CH = CHW + CHX;
+    static constexpr int PER = CH / 256;            // chunks per thread per unit
+};
+
+template <int WN>
+__global__ __launch_bounds__(256, 2) void gemm_pipe_bf16(const bf16_t* __restrict__ X, int M, int K,
+                                                      const bf16_t* __restrict__ W, int N, EpiArgs e,
+                                                      int tiles_m, int tiles_n) {
+    using T = PipeTile<WN>;
+    __shared__ bf16x8 lds[2][T::CH];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 15, g = lane >> 4;
+    // XCD-aware order (workgroups are dealt round-robin to the 8 XCDs): each
+    // XCD gets a contiguous run of tiles, m fastest, so tiles sharing a weight
+    // panel share that XCD's L2
+    const int total = tiles_m * tiles_n;
+    int bid = blockIdx.x;
+    if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+    const int tm = bid % tiles_m, tn = bid / tiles_m;
+    const int KU = K / 64, NB = N / 16, MB = (M + 15) / 16;
+    const int split = blockIdx.y, nsplit = gridDim.y;
+    const int u_begin = (int)((long)KU * split / nsplit), u_end = (int)((long)KU * (split + 1) / nsplit);
+    const int nu = u_end - u_begin;
+
+    // this thread's chunks: c = tid + 256 i; c < CHW: weight block c / 128 of
+    // the tile, else activation block (c - CHW) / 128; blocks past the matrix
+    // re-read its last block (their results are never stored)
+    // Loads go through buffer descriptors (base and size in scalar registers,
+    // 32-bit byte offsets per lane; the hardware returns 0 past the size).
+    static_assert(T::CHW % 256 == 0, "a thread's chunks are all weight or all activation");
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, (int)((size_t)NB * KU * 2048), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)((size_t)MB * KU * 2048), 0x00020000);
+    uint32_t off[T::PER];
+#pragma unroll
+    for (int i = 0; i < T::PER; ++i) {
+        const int c = tid + 256 * i;
+        if (i < T::CHW / 256) {
+            const int nb = min(tn * (T::BN / 16) + c / 128, NB - 1);
+            off[i] = ((uint32_t)nb * KU * 1024 + (c & 127) * 8) * 2;
+        } else {
+            const int mb = min(tm * (PBM / 16) + (c - T::CHW) / 128, MB - 1);
+            off[i] = ((uint32_t)mb * KU * 1024 + (c & 127) * 8) * 2;
+        }
+    }
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    bf16x8 ring[2][T::PER];
+    auto gload = [&](int slot, int u) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < T::PER; ++i) {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(i < T::CHW / 256 ? rw : rx,
+                                                                  off[i] + (uint32_t)u * 2048, 0, 0);
+            ring[slot][i] = __builtin_bit_cast(bf16x8, v);
+        }
+    };
+    auto sstore = [&](int stage, int slot) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < T::PER; ++i) lds[stage][tid + 256 * i] = ring[slot][i];
+    };
+
+    floatx4 acc[WN][4];
+#pragma unroll
+    for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[j][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int stage) __attribute__((always_inline)) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            bf16x8 af[WN], bfr[4];
+#pragma unroll
+            for (int j = 0; j < WN; ++j) af[j] = lds[stage][(wn * WN + j) * 128 + h * 64 + lane];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) bfr[i] = lds[stage][T::CHW + (wm * 4 + i) * 128 + h * 64 + lane];
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[j][i] = mfma16x16x32(af[j], bfr[i], acc[j][i]);
+        }
+    };
+
+    // Unit k lives in ring slot k % 2 and LDS stage k % 2.  The loop body is
+    // two straight-line steps with no data-dependent branch, so each LDS store
+    // waits only for its own slot's loads while the other slot's are in
+    // flight; prefetches past the last unit re-read the last unit and their
+    // stages are never computed.
+    const int last = u_begin + (nu > 0 ? nu - 1 : 0);
+    gload(0, u_begin);
+    gload(1, min(u_begin + 1, last));
+    sstore(0, 0);
+    gload(0, min(u_begin + 2, last));
+    for (int k = 0; k < nu; k += 2) {
+        __syncthreads();   // stage 0 holds unit k; stage 1 is no longer read
+        sstore(1, 1);      // unit k + 1
+        gload(1, min(u_begin + k + 3, last));
+        compute(0);
+        if (k + 1 >= nu) break;
+        __syncthreads();   // stage 1 holds unit k + 1; stage 0 is no longer read
+        sstore(0, 0);      // unit k + 2
+        gload(0, min(u_begin + k + 4, last));
+        compute(1);
+    }
+
+    EpiArgs ee = e;
+    if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
+    const int nb0 = tn * (T::BN / 16) + wn * WN, m0 = tm * PBM + wm * 64;
+#pragma unroll
+    for (int jh = 0; jh < WN / 2; ++jh) {   // pairs of column blocks: bounds the prefetch registers
+        float4 pre[2][4];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
+                pre[j][i] = (m < M && n < N) ? epi_fetch(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
+                if (m < M && n < N) epi_store<bf16_t>(ee, m, n, acc[2 * jh + j][i], pre[j][i]);
+            }
+    }
+}
+
 // ---------------------------------------------------------------- tiled
 constexpr int TBM = 128, TBN = 128, TBK = 64, TPAD = TBK + 8;
 
@@ -429,8 +575,20 @@ StreamCfg stream_cfg(int N, int K, bool partial) {
     return StreamCfg{nw, ks, depth, 1};
 }
 
+// K split of the pipelined kernel (O and down projections, whose residual
+// epilogue can take fp32 partials): measured on MI355X at 512-736 tokens, 4
+// ways while the tiles alone give fewer than 256 workgroups, 2 below 512; at
+// least 8 k units per split.
+int pipe_split(int M, int N, int K) {
+    const int tiles = ((M + PBM - 1) / PBM) * ((N + PipeTile<4>::BN - 1) / PipeTile<4>::BN);
+    int S = tiles < 256 ? 4 : (tiles < 512 ? 2 : 1);
+    while (S > 1 && K / 64 / S < 8) S /= 2;
+    return S;
+}
+
 int gemm_split(int dtype, int M, int N, int K) {
-    if (dtype != DARD_DTYPE_BF16 || M > 64) return 1;
+    if (dtype != DARD_DTYPE_BF16) return 1;
+    if (M > 64) return pipe_split(M, N, K);
     return stream_cfg(N, K, true).split;
 }
 
@@ -464,6 +622,12 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
         else if (c.nw == 2) DARD_GS(2, 4, 2);
         else DARD_GS(1, 4, 2);
 #undef DARD_GS
+        return hipGetLastError();
+    }
+    if (xfrag) {
+        const int tiles_m = (M + PBM - 1) / PBM, tiles_n = (N + PipeTile<4>::BN - 1) / PipeTile<4>::BN;
+        const int S = e.kind == EPI_PARTIAL ? pipe_split(M, N, K) : 1;
+        launch(gemm_pipe_bf16<4>, dim3(tiles_m * tiles_n, S), dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
         return hipGetLastError();
     }
     const int tiles_m = (M + TBM - 1) / TBM, tiles_n = (N + TBN - 1) / TBN;

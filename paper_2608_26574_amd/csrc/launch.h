@@ -11,12 +11,13 @@
 
 namespace dard {
 
-// Activations that feed a streaming GEMM (bf16, at most 64 token rows) are
-// stored fragment-major, in the layout of the packed weights: the 16 x 64
-// block (m/16, k/64) is contiguous, so each wave load of the GEMM reads 1 KB
-// contiguous.  Producers (norms, SwiGLU epilogue, attention output) write that
-// layout when frag_rows(dtype, rows) holds; buffers then hold 64 rows.
-inline bool frag_rows(int dtype, int rows) { return dtype == DARD_DTYPE_BF16 && rows <= 64; }
+// bf16 activations that feed a projection GEMM are stored fragment-major, in
+// the layout of the packed weights: the 16 x 64 block (m/16, k/64) is
+// contiguous, so every wave load (streaming GEMM) or tile copy (pipelined
+// GEMM) of them reads whole 1 KB runs.  Producers (norms, SwiGLU epilogue,
+// attention output) write that layout when frag_rows(dtype, rows) holds;
+// buffers then hold whole blocks (rows rounded up to 64).
+inline bool frag_rows(int dtype, int rows) { return dtype == DARD_DTYPE_BF16 && rows > 0; }
 
 // ---- mask.hip
 hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
