@@ -66,58 +66,64 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
 
     const int begin = ch * kChunk;
     const int end = min(a.V, begin + kChunk);
-    Acc acc{-INFINITY, 0x7fffffff, 0.f};
-    // every full float4 of this thread is loaded before any arithmetic
+    // every float4 of this thread is loaded (non-temporal: the logits are read
+    // once) before any arithmetic
     constexpr int kIt = kChunk / (4 * 256);
-    float4 sv4[kIt], xv4[kIt];
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4 sv4[kIt], xv4[kIt];
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
         const int i = begin + 4 * threadIdx.x + 4 * 256 * it;
         const bool full = i + 4 <= end;
-        sv4[it] = (use_s && full) ? *reinterpret_cast<const float4*>(ls + i) : make_float4(0.f, 0.f, 0.f, 0.f);
-        xv4[it] = (use_x && full) ? *reinterpret_cast<const float4*>(lx + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        sv4[it] = (use_s && full) ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ls + i)) : z;
+        xv4[it] = (use_x && full) ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(lx + i)) : z;
     }
+    // the (mixed) values, -inf past the end of the row
+    float v[kIt][4];
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
         const int i = begin + 4 * threadIdx.x + 4 * 256 * it;
-        if (i >= end) break;
-        float v[4];
         if (i + 4 <= end) {
-            const float4 sv = sv4[it];
+            const f32x4 sv = sv4[it];
             if (use_x) {
-                const float4 xv = xv4[it];
+                const f32x4 xv = xv4[it];
                 if (use_s) {
-                    v[0] = mixv(xv.x, sv.x, w, omw); v[1] = mixv(xv.y, sv.y, w, omw);
-                    v[2] = mixv(xv.z, sv.z, w, omw); v[3] = mixv(xv.w, sv.w, w, omw);
+                    v[it][0] = mixv(xv.x, sv.x, w, omw); v[it][1] = mixv(xv.y, sv.y, w, omw);
+                    v[it][2] = mixv(xv.z, sv.z, w, omw); v[it][3] = mixv(xv.w, sv.w, w, omw);
                 } else {
-                    v[0] = xv.x; v[1] = xv.y; v[2] = xv.z; v[3] = xv.w;
+                    v[it][0] = xv.x; v[it][1] = xv.y; v[it][2] = xv.z; v[it][3] = xv.w;
                 }
             } else {
-                v[0] = sv.x; v[1] = sv.y; v[2] = sv.z; v[3] = sv.w;
+                v[it][0] = sv.x; v[it][1] = sv.y; v[it][2] = sv.z; v[it][3] = sv.w;
             }
         } else {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 if (i + k < end) {
-                    const float sv = use_s ? ls[i + k] : 0.f;
-                    v[k] = use_x ? (use_s ? mixv(lx[i + k], sv, w, omw) : lx[i + k]) : sv;
+                    const float svk = use_s ? ls[i + k] : 0.f;
+                    v[it][k] = use_x ? (use_s ? mixv(lx[i + k], svk, w, omw) : lx[i + k]) : svk;
                 } else {
-                    v[k] = -INFINITY;
+                    v[it][k] = -INFINITY;
                 }
             }
         }
-        float lm = v[0];
-        int li = 0;
+    }
+    // pass 1: the thread's maximum and its first index (indices increase with it, then k)
+    Acc acc{-INFINITY, 0x7fffffff, 0.f};
 #pragma unroll
-        for (int k = 1; k < 4; ++k)
-            if (v[k] > lm) { lm = v[k]; li = k; }
-        if (lm > acc.m) {
-            acc.s = acc.m == -INFINITY ? 0.f : acc.s * exp2f((acc.m - lm) * kLog2e);
-            acc.m = lm;
-            acc.a = i + li;
-        }
+    for (int it = 0; it < kIt; ++it)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) acc.s += exp2f((v[k] - acc.m) * kLog2e);
+        for (int k = 0; k < 4; ++k)
+            if (v[it][k] > acc.m) { acc.m = v[it][k]; acc.a = begin + 4 * threadIdx.x + 4 * 256 * it + k; }
+    // pass 2: sum of exp(l - max); arguments are <= 0, so the hardware exp2
+    // (v_exp_f32) needs no range handling, and exp2(-inf) = 0
+    if (acc.m != -INFINITY) {
+        const float mb = acc.m * kLog2e;
+#pragma unroll
+        for (int it = 0; it < kIt; ++it)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc.s += __builtin_amdgcn_exp2f(fmaf(v[it][k], kLog2e, -mb));
     }
     // wave reduction then across the 4 waves, fixed order
 #pragma unroll

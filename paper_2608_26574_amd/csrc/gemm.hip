@@ -254,7 +254,7 @@ struct PipeTile {
 };
 
 template <int WN>
-__global__ __launch_bounds__(256, 2) void gemm_pipe_bf16(const bf16_t* __restrict__ X, int M, int K,
+__global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf16_t* __restrict__ X, int M, int K,
                                                       const bf16_t* __restrict__ W, int N, EpiArgs e,
                                                       int tiles_m, int tiles_n) {
     using T = PipeTile<WN>;
