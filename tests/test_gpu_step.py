@@ -36,7 +36,10 @@ def unpermute_k(kc, dh):
     return out
 
 
-def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", check_kv=True):
+def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", check_kv=True, n_image=0):
+    """n_image > 0: the first n_image prefix positions of every sequence are
+    embedding rows (a multimodal prefix, ids < 0) drawn N(0, 1) in the storage
+    type instead of token ids."""
     V = dims.vocab
     w = synth.make_weights(dims, seed=seed, device=wdevice)
     if lm_scale is not None:
@@ -44,11 +47,17 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
     cap = P + 2 * B + 5
     eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, cap)
     ids = synth.prompt_ids(b, P, V, seed=seed + 1)
+    embeds = None
+    if n_image:
+        ids[:, :n_image] = -1
+        g = torch.Generator().manual_seed(seed + 3)
+        td = torch.float32 if dims.dtype == "f32" else torch.bfloat16
+        embeds = torch.randn(b, P, dims.d_model, generator=g).to(td)
     if frac is None:
         tok, state, conf = synth.tiny_block(b, B, V, seed=seed + 2)
     else:
         tok, state, conf = synth.workload_block(b, B, frac, V, seed=seed + 2)
-    eng.dard_prefill(dev(ids))
+    eng.dard_prefill(dev(ids), embeds=None if embeds is None else embeds.cuda())
     cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
                           params.get("flags", 0))
     t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
@@ -60,7 +69,8 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
     torch.cuda.synchronize()
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
-    cache = O.prefill(ow, dd, ids)
+    emb_np = None if embeds is None else embeds.double().numpy()
+    cache = O.prefill(ow, dd, ids, emb_np)
     if check_kv:
         tol = 2e-2 if dims.dtype == "bf16" else 1e-4
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
@@ -71,13 +81,13 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
             assert np.max(np.abs(k_gpu - cache[layer][0])) < tol * 4, layer
             assert np.max(np.abs(v_gpu - cache[layer][1])) < tol * 4, layer
     ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
-    ref["floor"] = lambda: oracle_noise_floor(ow, dd, ids, tok, state, conf, params, ref["logits"])
+    ref["floor"] = lambda: oracle_noise_floor(ow, dd, ids, tok, state, conf, params, ref["logits"], emb_np)
     got = dict(logits=dbg["logits"].cpu().numpy(), w=dbg["w"].cpu().numpy(), state_out=s_out.cpu().numpy(),
                tok_out=t_out.cpu().numpy(), conf_out=c_out.cpu().numpy(), block_done=done.cpu().numpy())
     return tok, state, conf, got, ref
 
 
-def oracle_noise_floor(ow, dd, ids, tok, state, conf, params, logits, amp=1e-7):
+def oracle_noise_floor(ow, dd, ids, tok, state, conf, params, logits, embeds=None, amp=1e-7):
     """How far the oracle's own logits move when every value is perturbed by
     one float32 ulp (relative 1e-7) just before each bf16 storage rounding.
     Any implementation whose accumulation order differs from the oracle's
@@ -92,7 +102,7 @@ def oracle_noise_floor(ow, dd, ids, tok, state, conf, params, logits, amp=1e-7):
 
     O.storage = noisy
     try:
-        cache = O.prefill(ow, dd, ids)
+        cache = O.prefill(ow, dd, ids, embeds)
         l2, _ = O.step_logits(ow, dd, cache, tok, state, conf, params["mask_id"], params.get("flags", 0))
     finally:
         O.storage = orig
@@ -203,6 +213,19 @@ def test_llada8b_two_layers():
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = run_case(dims, 1, 32, 512, prm, seed=1, frac=0.25, wdevice="cuda")
     check_bf16_logits(got, ref, "llada8b 2 layers")
+    check_decisions(tok, state, got, ref, prm)
+
+
+def test_multimodal_prefix_two_layers():
+    """The multimodal-prefix workload at the 8B shape: 576 image-embedding
+    positions (N(0, 1), bf16) followed by 256 prompt ids, block 32, candidate
+    fraction 0.3; two layers.  The prefix KV cache and the step are checked."""
+    dims = synth.truncated(synth.LLADA8B, 2)
+    announce("multimodal prefix 2-layer step")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = run_case(dims, 1, 32, 576 + 256, prm, seed=4, frac=0.3, wdevice="cuda",
+                                          n_image=576)
+    check_bf16_logits(got, ref, "multimodal prefix 2 layers")
     check_decisions(tok, state, got, ref, prm)
 
 
