@@ -162,7 +162,7 @@ def main():
     # ---- tokens committed / s: 8 blocks of prefill + ceil(B / 6) steps each
     def generation():
         for k in range(nblocks):
-            eng.dard_prefill(ids[:, : prompt + B * k])
+            eng.dard_prefill(ids[:, : prompt + B * k].contiguous())
             for j in range(S_b):
                 step(args.warmup + (k * S_b + j) % args.steps)
     generation()
@@ -193,10 +193,56 @@ def main():
         "kernel_ms_per_step": round(kern_ms, 4),
         "gaps_ms_per_step": round(ms_per_step - kern_ms, 4),
     }
+    out["decision_driven"] = decision_driven(eng, dims, ids, b, B, prompt)
     out["ops"] = op_measurements()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
     print(json.dumps(out), flush=True)
+
+
+def decision_driven(eng, dims, ids, b, B, prompt, nblocks=2):
+    """Diagnostic: blocks decoded by the decisions themselves.  Each block
+    starts all-[Mask]; every step feeds its outputs back as the next inputs,
+    with the progress rule on (DARD_F_PROGRESS: a step that commits no token
+    commits the most confident one) and a cap of 2B steps per block.  With
+    random-init weights no confidence passes tau_u and committed tokens fall
+    back on re-verification, so blocks run to the cap: this measures the
+    decoding loop's mechanics, not the paper's tokens per step."""
+    import torch
+
+    from paper_2608_26574_amd import dard
+    F_PROGRESS = 1 << 3
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, F_PROGRESS)
+    dev = ids.device
+    bufs = [(torch.empty(b, B, dtype=torch.int32, device=dev), torch.empty(b, B, dtype=torch.uint8, device=dev),
+             torch.empty(b, B, device=dev)) for _ in range(2)]
+    done = torch.zeros(b, dtype=torch.int32, device=dev)
+    steps, capped = [], 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(nblocks):
+        P = prompt + B * k
+        eng.dard_prefill(ids[:, :P].contiguous())
+        tok, st, cf = bufs[0]
+        tok.fill_(dims.mask_id)
+        st.zero_()
+        cf.zero_()
+        n = 0
+        while True:
+            src, dst = bufs[n % 2], bufs[(n + 1) % 2]
+            eng.dard_step(P, params, src[0], src[1], src[2], dst[0], dst[1], dst[2], done)
+            n += 1
+            if int(done.min().item()) == 1:
+                break
+            if n >= 2 * B:
+                capped += 1
+                break
+        steps.append(n)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    return {"blocks": nblocks, "steps_per_block": steps, "capped_blocks": capped,
+            "tokens_per_s": round(b * B * nblocks / el, 1),
+            "note": "progress rule on, cap 2B steps; random-init weights, so blocks reach the cap"}
 
 
 def op_measurements(reps=20):

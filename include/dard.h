@@ -64,11 +64,18 @@ typedef int dard_status;
  *   MKEYS_SHADOW  the x query of an M token reads the other M positions from
  *                 s (default: from x, i.e. the x stream is vanilla decoding);
  *   VERIFY_PCUR   C/U confidence = probability of the current token instead of
- *                 the top-1 probability of Eq. 1 (default). */
+ *                 the top-1 probability of Eq. 1 (default);
+ *   PROGRESS      a decoding-loop rule, not the paper's (Alg. 1 assumes the
+ *                 confidences eventually pass tau_u): if no position of an
+ *                 unfinished block entered U in this step, the most confident
+ *                 position that is not U after the transitions (ties: lowest
+ *                 position) becomes U with its prediction, so a block of B
+ *                 positions finishes within B steps. */
 #define DARD_F_XSELF_SHADOW (1u << 0)
 #define DARD_F_MKEYS_SHADOW (1u << 1)
 #define DARD_F_VERIFY_PCUR  (1u << 2)
-#define DARD_F_ALL          (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR)
+#define DARD_F_PROGRESS     (1u << 3)
+#define DARD_F_ALL          (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS)
 
 /* Decoding hyper-parameters (Alg. 1 inputs; Sec. 4.1 uses lambda = 0.5^(1/8),
  * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0. */

@@ -49,6 +49,7 @@ STATE_M, STATE_C, STATE_U = 0, 1, 2
 F_XSELF_SHADOW = 1 << 0   # x-row of a U token does not see its own x key
 F_MKEYS_SHADOW = 1 << 1   # x-row of an M token sees M keys through s
 F_VERIFY_PCUR = 1 << 2    # C/U confidence = prob. of the current token
+F_PROGRESS = 1 << 3       # driver rule: every step of an unfinished block commits >= 1 token
 
 LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # Sec. 4.1: lambda = 0.917, i.e. 0.5^(1/8)
 P0_DEFAULT = 0.1                      # Sec. 4.1: prior constant p_0
@@ -384,11 +385,23 @@ def verify_candidates(state, c, params):
     return nxt, promoted, demoted, w
 
 
-def finalize(c, xhat, params):
+def finalize(c, xhat, params, state_in=None):
     """Transition of every position by Eq. 8 and the fill rule: next-M
-    positions hold [Mask], the others their prediction.  c, xhat: [B]."""
+    positions hold [Mask], the others their prediction.  c, xhat: [B].
+
+    With F_PROGRESS (a driver rule, not the paper's: Alg. 1 assumes that
+    confidences eventually exceed tau_u), a step of an unfinished block in
+    which no position entered U promotes the most confident position that
+    is not U after the transitions (ties: lowest position) to U with its
+    prediction, so every step commits at least one token."""
     B = len(c)
     st = np.array([transition(c[i], params["tau_c"], params["tau_u"]) for i in range(B)], dtype=np.int64)
+    if params.get("flags", 0) & F_PROGRESS and state_in is not None:
+        entered = (st == STATE_U) & (np.asarray(state_in) != STATE_U)
+        if not entered.any() and not np.all(st == STATE_U):
+            cand = [i for i in range(B) if st[i] != STATE_U]
+            best = max(cand, key=lambda i: (np.float32(c[i]), -i))
+            st[best] = STATE_U
     tok = np.where(st == STATE_M, params["mask_id"], np.asarray(xhat, dtype=np.int64))
     return st, tok, np.asarray(c, dtype=np.float64), int(np.all(st == STATE_U))
 
@@ -436,7 +449,7 @@ def decide(logits, tok, state, params):
                 xhat[i] = a
                 c[i] = np.float32(mp)
         # transitions of all tokens (C ones repeat the rule above) and fill
-        st, tk, cf, done = finalize(c, xhat, params)
+        st, tk, cf, done = finalize(c, xhat, params, state[bi])
         out["state_out"][bi] = st
         out["tok_out"][bi] = tk
         out["conf_out"][bi] = cf

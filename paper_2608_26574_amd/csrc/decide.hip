@@ -90,7 +90,9 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
     extern __shared__ float staged[];            // [2][B][nchunk][3] in step mode
     __shared__ uint8_t promoted[128], demoted[128];
     __shared__ double lam_pow[128];
-    __shared__ int all_u;
+    __shared__ int all_u, entered_u;
+    __shared__ float c_all[128];
+    __shared__ int nxt_all[128], xhat_all[128];
     const int s = blockIdx.x, i = threadIdx.x;
     const bool live = i < a.B;
     const int pos = s * a.B + i;
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
     }
 
     // ---- FINAL: confidences of every position, transition, fill
-    if (i == 0) all_u = 1;
+    if (i == 0) { all_u = 1; entered_u = 0; }
     __syncthreads();
     if (live) {
         const int tok = a.tok_in ? a.tok_in[pos] : 0;
@@ -160,6 +162,10 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         }
         const int nxt = transition(c, a.tau_c, a.tau_u);
         if (nxt != DARD_STATE_U) atomicAnd(&all_u, 0);
+        if (nxt == DARD_STATE_U && st != DARD_STATE_U) atomicOr(&entered_u, 1);
+        c_all[i] = c;
+        nxt_all[i] = nxt;
+        xhat_all[i] = xhat;
         a.state_out[pos] = (uint8_t)nxt;
         a.tok_out[pos] = nxt == DARD_STATE_M ? a.mask_id : xhat;
         a.conf_out[pos] = c;
@@ -170,6 +176,20 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         if (a.dbg_argmax_mix) a.dbg_argmax_mix[pos] = am_mix;
     }
     __syncthreads();
+    // progress rule (DARD_F_PROGRESS): no position entered U in an unfinished
+    // block -> the most confident non-U position (lowest on ties) becomes U
+    if (i == 0 && (a.flags & DARD_F_PROGRESS) && !entered_u && !all_u) {
+        int best = -1;
+        for (int j = 0; j < a.B; ++j)
+            if (nxt_all[j] != DARD_STATE_U && (best < 0 || c_all[j] > c_all[best])) best = j;
+        const int bp = s * a.B + best;
+        a.state_out[bp] = (uint8_t)DARD_STATE_U;
+        a.tok_out[bp] = xhat_all[best];
+        int done = 1;
+        for (int j = 0; j < a.B; ++j)
+            if (j != best && nxt_all[j] != DARD_STATE_U) done = 0;
+        all_u = done;
+    }
     if (i == 0 && a.block_done) a.block_done[s] = all_u;
 }
 

@@ -198,7 +198,8 @@ def _params(flags=0, tc=0.4, tu=0.9):
 
 
 @pytest.mark.parametrize("B", [1, 7, 32, 128])
-@pytest.mark.parametrize("flags,tc,tu", [(0, 0.4, 0.9), (O.F_VERIFY_PCUR, 0.3, 0.7), (0, 0.9, 0.9)])
+@pytest.mark.parametrize("flags,tc,tu", [(0, 0.4, 0.9), (O.F_VERIFY_PCUR, 0.3, 0.7), (0, 0.9, 0.9),
+                                         (O.F_PROGRESS, 0.4, 1.0), (O.F_PROGRESS | O.F_VERIFY_PCUR, 0.3, 0.7)])
 def test_commit_remask_bit_exact(B, flags, tc, tu):
     announce("commit/remask", B, flags, tc, tu)
     b = 4
@@ -229,7 +230,7 @@ def test_commit_remask_bit_exact(B, flags, tc, tu):
         assert np.array_equal(w[s].cpu().numpy().astype(np.float64), rw), s
         c = np.where(state[s] == O.STATE_M, mp_mix[s], c_sh[s])
         xh = np.where(state[s] == O.STATE_M, am_mix[s], am_s[s])
-        st, tk, cf, done = O.finalize(c, xh, p)
+        st, tk, cf, done = O.finalize(c, xh, p, state[s])
         assert np.array_equal(so[s].cpu().numpy(), st)
         assert np.array_equal(to[s].cpu().numpy(), tk)
         assert np.array_equal(co[s].cpu().numpy(), cf.astype(np.float32))

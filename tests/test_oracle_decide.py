@@ -193,3 +193,48 @@ def test_block_done_when_all_unmasked():
     out = O.decide(logits, np.array([[1, 2]]), np.array([[2, 2]], dtype=np.uint8),
                    dict(tau_c=0.4, tau_u=0.9, lam=LAM, p0=0.1, mask_id=V - 1))
     assert out["block_done"][0] == 1
+
+
+def test_progress_rule():
+    """F_PROGRESS: a step of an unfinished block in which no position entered
+    U promotes the most confident non-U position (lowest on ties) to U."""
+    p = dict(tau_c=0.4, tau_u=0.9, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=99, flags=O.F_PROGRESS)
+    c = np.array([0.1, 0.3, 0.3, 0.05, 0.95, 0.2], dtype=np.float32)
+    xhat = np.array([10, 11, 12, 13, 14, 15])
+    state_in = np.array([O.STATE_M, O.STATE_M, O.STATE_C, O.STATE_M, O.STATE_U, O.STATE_M])
+    # position 4 stays U (not a new U); nothing else passes tau_u: position 1
+    # (0.3, the lower of the tied positions 1 and 2) is promoted
+    st, tok, cf, done = O.finalize(c, xhat, p, state_in)
+    assert list(st) == [O.STATE_M, O.STATE_U, O.STATE_M, O.STATE_M, O.STATE_U, O.STATE_M]
+    assert list(tok) == [99, 11, 99, 99, 14, 99]
+    assert done == 0
+    # without the flag the same step commits nothing new
+    st0, _, _, _ = O.finalize(c, xhat, dict(p, flags=0), state_in)
+    assert list(st0) == [O.STATE_M] * 4 + [O.STATE_U, O.STATE_M]
+    # a position that enters U by Eq. 8 suppresses the rule
+    c2 = c.copy(); c2[3] = 0.91
+    st2, _, _, _ = O.finalize(c2, xhat, p, state_in)
+    assert list(st2) == [O.STATE_M, O.STATE_M, O.STATE_M, O.STATE_U, O.STATE_U, O.STATE_M]
+    # the last non-U position promoted finishes the block
+    c3 = np.array([0.95, 0.5], dtype=np.float32)
+    st3, _, _, done3 = O.finalize(c3, np.array([1, 2]), p, np.array([O.STATE_U, O.STATE_C]))
+    assert list(st3) == [O.STATE_U, O.STATE_U] and done3 == 1
+
+
+def test_progress_bounds_block_length():
+    """With F_PROGRESS, and committed tokens that stay confident (U tokens are
+    re-verified every step and may fall back, so this needs their confidence
+    above tau_u), a block finishes within B steps although no other position
+    ever passes tau_u."""
+    rng = np.random.default_rng(3)
+    B = 16
+    p = dict(tau_c=0.4, tau_u=0.9, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=99, flags=O.F_PROGRESS)
+    state = np.zeros(B, dtype=np.int64)
+    for step in range(B):
+        c = rng.uniform(0.0, 0.9, B).astype(np.float32)
+        c[state == O.STATE_U] = 0.95
+        state, _, _, done = O.finalize(c, np.arange(B), p, state)
+        assert (state == O.STATE_U).sum() == step + 1
+        if done:
+            break
+    assert done == 1 and step == B - 1
