@@ -28,18 +28,19 @@ namespace dard {
 
 namespace {
 
-constexpr int kRows = 64;      // query rows per workgroup
 constexpr int kKeys = 64;      // keys per tile
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinLog2 = -1e30f;   // running-max floor (log2 units): exp2 of anything below it is 0
 
-template <int DH>
+// LDS of one group of TPG threads: a K tile row-major and a V tile transposed
+// (or, at the end, every lane's o, m and l for the merge of the groups).
+template <int DH, int TPG>
 struct Lds {
     static constexpr int KPAD = DH + 8;       // K row stride (bf16): 16-byte bank shift per row
     static constexpr int VPAD = kKeys + 4;    // V^T row stride (bf16)
     static constexpr int TILE_BYTES = (kKeys * KPAD + DH * VPAD) * 2;
-    static constexpr int MERGE_BYTES = (DH / 4 + 2) * 256 * 4;   // o, m, l of every lane
+    static constexpr int MERGE_BYTES = (DH / 4 + 2) * TPG * 4;
     static constexpr int GROUP_BYTES = ((TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 15) / 16 * 16;
 };
 
@@ -72,15 +73,18 @@ __device__ __forceinline__ int tile_count(int t, int npre, int pre_end, int B2) 
     return t < npre ? min(kKeys, pre_end - t * kKeys) : min(kKeys, B2 - (t - npre) * kKeys);
 }
 
-template <int DH, int G, int RING>
-__global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
-    using L = Lds<DH>;
+// G groups of WPG waves; a workgroup serves 16 WPG query rows of one
+// (sequence, query head) and its groups take interleaved key tiles.
+template <int DH, int G, int RING, int WPG>
+__global__ __launch_bounds__(64 * WPG * G) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
+    constexpr int TPG = 64 * WPG, ROWS = 16 * WPG;
+    using L = Lds<DH, TPG>;
     constexpr int KPAD = L::KPAD, VPAD = L::VPAD;
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     __shared__ __attribute__((aligned(16))) char smem[G * L::GROUP_BYTES];
 
     // group and wave are wave-uniform: say so, so that tile bookkeeping stays scalar
-    const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8), tid = threadIdx.x & 255;
+    const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x / TPG), tid = threadIdx.x % TPG;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lr = lane & 15, g = lane >> 4;
     bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + grp * L::GROUP_BYTES);
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     const int h = bid % a.Hq;
     const int s = bid / a.Hq;
     const int kvh = h / (a.Hq / a.Hkv);
-    const int r0 = rt * kRows;
+    const int r0 = rt * ROWS;
     const int split = blockIdx.y, nsplit = gridDim.y;
 
     // prefix tiles [0, npre), then block tiles (masked mode)
@@ -107,36 +111,46 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
 
     // ---- issue the loads of this group's first RING tiles before anything else
-    constexpr int KCH = kKeys * DH / 8 / 256;  // 16-byte K chunks per thread
-    constexpr int VUNITS = (kKeys / 4) * (DH / 8);
+    constexpr int KCH = kKeys * DH / 8 / TPG;  // 16-byte K chunks per thread
+    constexpr int VUNITS = (kKeys / 4) * (DH / 8);           // (4 keys x 8 dims) V units per tile
+    constexpr int VQ = (VUNITS + TPG - 1) / TPG;              // V units per thread
     bf16x8 kreg[RING][KCH];
-    bf16x8 vreg[RING][4];
+    bf16x8 vreg[RING][VQ][4];
     auto load_tile = [&](int slot, int tile) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
         const bf16_t* kt = kbase + (size_t)k0 * DH;
         const bf16_t* vt = vbase + (size_t)k0 * DH;
-        // V: thread (kg, dg) = (tid % 16, tid / 16) reads keys 4kg..4kg+3 at dims 8dg..8dg+7
-        const int kg = tid & 15, dg = tid >> 4;
+        // V unit u = tid + TPG v: (kg, dg) = (u % 16, u / 16) holds keys
+        // 4kg..4kg+3 at dims 8dg..8dg+7
         if (n == kKeys) {   // full tile (uniform): no per-key test
 #pragma unroll
-            for (int it = 0; it < KCH; ++it) kreg[slot][it] = ld_bf16x8(kt + (size_t)(tid + 256 * it) * 8);
-            if (tid < VUNITS) {
+            for (int it = 0; it < KCH; ++it) kreg[slot][it] = ld_bf16x8(kt + (size_t)(tid + TPG * it) * 8);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) vreg[slot][e] = ld_bf16x8(vt + (size_t)(4 * kg + e) * DH + dg * 8);
+            for (int vq = 0; vq < VQ; ++vq) {
+                const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
+                if (u < VUNITS) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        vreg[slot][vq][e] = ld_bf16x8(vt + (size_t)(4 * kg + e) * DH + dg * 8);
+                }
             }
         } else {
 #pragma unroll
             for (int it = 0; it < KCH; ++it) {
-                const int qd = tid + 256 * it;
+                const int qd = tid + TPG * it;
                 bf16x8 z = {};
                 kreg[slot][it] = qd / (DH / 8) < n ? ld_bf16x8(kt + (size_t)qd * 8) : z;
             }
-            if (tid < VUNITS) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int key = 4 * kg + e;
-                    bf16x8 z = {};
-                    vreg[slot][e] = key < n ? ld_bf16x8(vt + (size_t)key * DH + dg * 8) : z;
+            for (int vq = 0; vq < VQ; ++vq) {
+                const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
+                if (u < VUNITS) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int key = 4 * kg + e;
+                        bf16x8 z = {};
+                        vreg[slot][vq][e] = key < n ? ld_bf16x8(vt + (size_t)key * DH + dg * 8) : z;
+                    }
                 }
             }
         }
@@ -144,17 +158,21 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
     auto store_tile = [&](int slot) __attribute__((always_inline)) {
 #pragma unroll
         for (int it = 0; it < KCH; ++it) {
-            const int qd = tid + 256 * it;
+            const int qd = tid + TPG * it;
             const int key = qd / (DH / 8), c8 = qd % (DH / 8);
             *reinterpret_cast<bf16x8*>(&Ks[key * KPAD + c8 * 8]) = kreg[slot][it];
         }
-        if (tid < VUNITS) {
-            // 16 consecutive lanes write one contiguous 128-byte run of a V^T row
-            const int kg = tid & 15, dg = tid >> 4;
+        // 16 consecutive lanes write one contiguous 128-byte run of a V^T row
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                bf16x4 t4 = {vreg[slot][0][e], vreg[slot][1][e], vreg[slot][2][e], vreg[slot][3][e]};
-                *reinterpret_cast<bf16x4*>(&Vt[(dg * 8 + e) * VPAD + 4 * kg]) = t4;
+        for (int vq = 0; vq < VQ; ++vq) {
+            const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
+            if (u < VUNITS) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    bf16x4 t4 = {vreg[slot][vq][0][e], vreg[slot][vq][1][e], vreg[slot][vq][2][e],
+                                 vreg[slot][vq][3][e]};
+                    *reinterpret_cast<bf16x4*>(&Vt[(dg * 8 + e) * VPAD + 4 * kg]) = t4;
+                }
             }
         }
     };
@@ -295,16 +313,16 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
 #pragma unroll
             for (int d = 0; d < DH / 16; ++d)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) mb[(4 * d + i) * 256 + tid] = o[d][i];
-            mb[(DH / 4) * 256 + tid] = m_run;
-            mb[(DH / 4 + 1) * 256 + tid] = l_run;
+                for (int i = 0; i < 4; ++i) mb[(4 * d + i) * TPG + tid] = o[d][i];
+            mb[(DH / 4) * TPG + tid] = m_run;
+            mb[(DH / 4 + 1) * TPG + tid] = l_run;
         }
         __syncthreads();
         if (grp > 0) return;
         float M = m_run;
 #pragma unroll
         for (int gg = 1; gg < G; ++gg)
-            M = fmaxf(M, reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES)[(DH / 4) * 256 + tid]);
+            M = fmaxf(M, reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES)[(DH / 4) * TPG + tid]);
         const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
         float lsum = l_run * f0;
 #pragma unroll
@@ -312,13 +330,13 @@ __global__ __launch_bounds__(256 * G) void attn_bf16_kernel(AttnArgs a, int rowt
 #pragma unroll
         for (int gg = 1; gg < G; ++gg) {
             const float* ob = reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES);
-            const float mg = ob[(DH / 4) * 256 + tid];
+            const float mg = ob[(DH / 4) * TPG + tid];
             const float f = mg == -INFINITY ? 0.f : exp2f(mg - M);
-            lsum += ob[(DH / 4 + 1) * 256 + tid] * f;
+            lsum += ob[(DH / 4 + 1) * TPG + tid] * f;
 #pragma unroll
             for (int d = 0; d < DH / 16; ++d)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) o[d][i] += ob[(4 * d + i) * 256 + tid] * f;
+                for (int i = 0; i < 4; ++i) o[d][i] += ob[(4 * d + i) * TPG + tid] * f;
         }
         m_run = M;
         l_run = lsum;
@@ -441,11 +459,21 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     for (int e = 0; e < DH; ++e) out[e] = o[e] * inv;
 }
 
-// Groups per workgroup: two when fewer than 1024 waves would cover the chip
-// (more groups would spill the register ring), never more than tiles.
-int attention_groups(int b, int R, int Hq, int ntiles) {
-    const int wgs = b * Hq * ((R + kRows - 1) / kRows);
-    return (4 * wgs < 1024 && ntiles >= 2) ? 2 : 1;
+// Shape of a bf16 launch: WPG waves per group (16 WPG query rows per
+// workgroup) and G groups taking interleaved key tiles.  While one-group
+// workgroups of 64 rows would leave the chip short of 1024 waves, the key
+// tiles are walked by more groups: 4 groups of 2 waves (32 rows per
+// workgroup, so a head's 64 rows take two workgroups) when there are at least
+// 4 tiles, else 2 groups of 4 waves.
+struct AttnCfg {
+    int wpg, g;
+};
+
+AttnCfg attention_cfg(int b, int R, int Hq, int ntiles) {
+    const int wgs64 = b * Hq * ((R + 63) / 64);
+    if (4 * wgs64 >= 1024 || ntiles < 2) return {4, 1};
+    if (R > 32 && ntiles >= 4) return {2, 4};
+    return {4, 2};
 }
 
 }  // namespace
@@ -456,14 +484,13 @@ int attention_tiles(int masked, int P, int B, int nkeys) {
 
 int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots) {
     if (dtype != DARD_DTYPE_BF16) return 1;
-    const int rowtiles = (R + kRows - 1) / kRows;
-    const int wgs = b * Hq * rowtiles;
-    const int G = attention_groups(b, R, Hq, ntiles);
+    const AttnCfg c = attention_cfg(b, R, Hq, ntiles);
+    const int wgs = b * Hq * ((R + 16 * c.wpg - 1) / (16 * c.wpg));
     // Measured at 64 rows x 32 heads: a tile step costs about 2 us, the
     // combine kernel about 4.3 us plus its launch, so a split pays only when
     // the workgroups would otherwise walk more than 5 tile steps; then about
     // 3 tiles per split.  No split once the workgroups alone cover the chip.
-    if (wgs * G * 4 >= 1024 || (ntiles + G - 1) / G <= 5) return 1;
+    if (wgs * c.g * c.wpg >= 1024 || (ntiles + c.g - 1) / c.g <= 5) return 1;
     int ns = 1;
     while (ns < kMaxSplit && ntiles > 3 * ns) ns *= 2;
     const size_t per_split = (size_t)b * R * Hq;
@@ -482,21 +509,21 @@ hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStre
     if (a.out_frag && !frag_rows(dtype, a.b * a.R)) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16) {
         if (a.masked && (!a.sel || a.B > 128)) return hipErrorInvalidValue;
-        const int rowtiles = (a.R + kRows - 1) / kRows;
         const int ntiles = attention_tiles(a.masked, a.P, a.B, a.nkeys);
         const bool can_split = a.part && a.part_ml;
         if (!can_split || ns < 1 || ns > kMaxSplit || (size_t)ns * a.b * a.R * a.Hq > a.part_slots) ns = 1;
         if (ns > ntiles) ns = ntiles > 0 ? ntiles : 1;
         const int tps = (ntiles + ns - 1) / ns;
         ns = ntiles > 0 ? (ntiles + tps - 1) / tps : 1;
-        const int G = attention_groups(a.b, a.R, a.Hq, tps);
+        const AttnCfg c = attention_cfg(a.b, a.R, a.Hq, tps);
+        const int rowtiles = (a.R + 16 * c.wpg - 1) / (16 * c.wpg);
         dim3 grid(a.b * a.Hq * rowtiles, ns);
-#define DARD_ATT(DHV, GV) \
-    launch((attn_bf16_kernel<DHV, GV, 2>), grid, dim3(256 * GV), 0, s, a, rowtiles, tps)
+#define DARD_ATT(DHV, GV, WV) \
+    launch((attn_bf16_kernel<DHV, GV, WV == 2 ? 1 : 2, WV>), grid, dim3(64 * WV * GV), 0, s, a, rowtiles, tps)
         if (a.dh == 128) {
-            if (G == 2) DARD_ATT(128, 2); else DARD_ATT(128, 1);
+            if (c.wpg == 2) DARD_ATT(128, 4, 2); else if (c.g == 2) DARD_ATT(128, 2, 4); else DARD_ATT(128, 1, 4);
         } else {
-            if (G == 2) DARD_ATT(64, 2); else DARD_ATT(64, 1);
+            if (c.wpg == 2) DARD_ATT(64, 4, 2); else if (c.g == 2) DARD_ATT(64, 2, 4); else DARD_ATT(64, 1, 4);
         }
 #undef DARD_ATT
         hipError_t e = hipGetLastError();
