@@ -123,7 +123,7 @@ def main():
     torch.cuda.synchronize()
     dard.dard_trace_enable(0)
     names = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "attention", "confidence",
-             "decide", "norm"]
+             "decide", "norm", "mask"]
     breakdown = {}
     for k, nm in enumerate(names):
         n, ms = dard.dard_trace_read(k)
@@ -248,10 +248,17 @@ def decision_driven(eng, dims, ids, b, B, prompt, nblocks=2):
 def op_measurements(reps=20):
     """The two isolated operations the roofline targets name, measured cold
     (inputs rotated through copies whose total exceeds the 256 MB MALL):
-    - state-masked attention at the 8B attention shape (32 x 128 heads, prompt
-      KV 512, block 32, candidate fraction 0.25, bf16 Q/K/V ~ N(0, 1)) for
-      batch 1, 4 and 16, against the bf16 MFMA peak (algorithmic flops
-      4 dh Hq 2B (P+B) b) and the HBM peak (K/V of P+2B keys, Q and O);
+    - state-masked attention, bf16 Q/K/V ~ N(0, 1), against the bf16 MFMA peak
+      (algorithmic flops 4 dh Hq 2B (P+B) b: each query row reads P + B keys)
+      and the HBM peak (K/V of P+2B keys, Q and O), at the 8B attention shape
+      (32 x 128 MHA heads, prompt KV 512, block 32, candidate fraction 0.25;
+      batch 1, 4, 16) and at the 7B GQA shape (28 query heads on 4 KV heads,
+      batch 8, block 64, candidate fraction 0.3, prefix 1024 and 1472: the
+      first and last block of a 512-token generation), the one where attention
+      is compute-bound.  `us` is the whole call (state mask + attention
+      kernels, HIP events around the calls); `kernel_us` the attention
+      kernels alone (kernel timestamps), since a step builds the mask once for
+      all its layers; mfma_frac uses kernel_us;
     - the vocab-wide confidence reduction (argmax, max-prob) over fp32 logits
       at the 8B step's row count (B + |M| = 44 rows x 126464) and at the 7B GQA
       batch-8 step's (8 x 87 rows x 152064), against the HBM peak."""
@@ -270,16 +277,29 @@ def op_measurements(reps=20):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 
+    def traced(fn, n, cls):
+        dard.dard_trace_reset()
+        dard.dard_trace_enable(1 << cls)
+        for i in range(n):
+            fn(i + 1)
+        torch.cuda.synchronize()
+        dard.dard_trace_enable(0)
+        _, ms = dard.dard_trace_read(cls)
+        dard.dard_trace_reset()
+        return ms / n
+
     res = {"attention": [], "confidence": []}
-    P, B, H, dh, frac = 512, 32, 32, 128, 0.25
-    for bsz in (1, 4, 16):
+    shapes = [("8B MHA", bsz, 32, 32, 32, 512, 0.25) for bsz in (1, 4, 16)] + \
+             [("7B GQA", 8, 28, 4, 64, P, 0.3) for P in (1024, 1472)]
+    dh = 128
+    for label, bsz, H, Hkv, B, P, frac in shapes:
         cap = P + 2 * B
-        kv_bytes = bsz * H * cap * dh * 2
+        kv_bytes = bsz * Hkv * cap * dh * 2
         ncopy = max(4, -(-600 * 2**20 // (2 * kv_bytes)))
         g = torch.Generator(device="cuda").manual_seed(2)
         q = torch.randn(bsz, 2 * B, H, dh, generator=g, device="cuda").bfloat16()
-        ks = [torch.randn(bsz, H, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
-        vs = [torch.randn(bsz, H, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        ks = [torch.randn(bsz, Hkv, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        vs = [torch.randn(bsz, Hkv, dh, cap, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
         _, state, conf = synth.workload_block(bsz, B, frac, 100, seed=3)
         state, conf = torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()
         out = torch.empty_like(q)
@@ -289,13 +309,15 @@ def op_measurements(reps=20):
         def att(i):
             dard.dard_masked_attention(q, ks[i % ncopy], vs[i % ncopy], P, state, conf, dh ** -0.5, 0, out, ws)
         ms = timed(att, reps)
+        kms = traced(att, reps, dard.K_ATTENTION)
         flops = 4 * dh * H * 2 * B * (P + B) * bsz
-        nbytes = 2 * bsz * H * (P + 2 * B) * dh * 2 + 2 * q.numel() * 2
-        res["attention"].append({"batch": bsz, "us": round(ms * 1e3, 2),
-                                 "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
-                                 "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                                 "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-                                 "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+        nbytes = 2 * bsz * Hkv * (P + 2 * B) * dh * 2 + 2 * q.numel() * 2
+        res["attention"].append({"shape": label, "batch": bsz, "heads": [H, Hkv], "block": B, "prefix": P,
+                                 "us": round(ms * 1e3, 2), "kernel_us": round(kms * 1e3, 2),
+                                 "tflops": round(flops / (kms * 1e-3) / 1e12, 2),
+                                 "mfma_frac": round(flops / (kms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                                 "gbs": round(nbytes / (kms * 1e-3) / 1e9, 1),
+                                 "hbm_frac": round(nbytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
         del ks, vs
     for rows, V, label in ((44, 126464, "8B step, 44 rows"), (8 * 87, 152064, "7B GQA batch-8 step, 696 rows")):
         nbytes = rows * V * 4

@@ -125,7 +125,9 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
  * position j either x^j (cache index P+j) or s^j (cache index P+B+j) as the
  * mask of dard_build_state_mask says.
  *   q   [b][2B][Hq][dh]     dtype
- *   k,v [b][Hkv][cap][dh]   dtype; keys P..P+2B-1 hold the block (x then s)
+ *   k   [b][Hkv][cap][dh]   dtype; keys P..P+2B-1 hold the block (x then s)
+ *   v   [b][Hkv][dh][cap]   dtype, dims-major (the transpose of k's layout),
+ *                           so a tile of V^T is contiguous per dim
  *   out [b][2B][Hq][dh]     dtype
  * Query head h reads KV head h / (Hq/Hkv).  Any permutation of the head_dim
  * axis applied to both q and k gives the same result.  Needs P >= 0,
@@ -199,9 +201,10 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
  * therefore hold each head's dims in the order (0, dh/2, 1, dh/2+1, ...),
  * which leaves every attention score unchanged.
  *
- * KV cache: [n_layers][2 (K, V)][b][Hkv][cap][dh] of the storage dtype,
- * sized by dard_kv_bytes().  Keys 0..P-1 hold the prefix (dard_prefill);
- * a step writes its block keys at P..P+2B-1. */
+ * KV cache: per layer a K block [b][Hkv][cap][dh] then a V block
+ * [b][Hkv][dh][cap] (dims-major), of the storage dtype, sized by
+ * dard_kv_bytes().  Keys 0..P-1 hold the prefix (dard_prefill); a step writes
+ * its block keys at P..P+2B-1. */
 size_t dard_packed_weight_bytes(const dard_dims* dims);
 dard_status dard_pack_weights(const dard_dims* dims, const void* const* src, int n_src,
                               void* packed, size_t packed_bytes, void* stream);
@@ -273,7 +276,8 @@ dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, 
 #define DARD_K_CONFIDENCE 6
 #define DARD_K_DECIDE     7
 #define DARD_K_NORM       8
-#define DARD_K_COUNT      9
+#define DARD_K_MASK       9
+#define DARD_K_COUNT      10
 dard_status dard_trace_enable(uint32_t class_mask);
 dard_status dard_trace_read(int kernel_class, int64_t* launches, double* total_ms);
 dard_status dard_trace_reset(void);

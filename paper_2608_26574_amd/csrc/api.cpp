@@ -110,10 +110,9 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.attn = o; o = align256(o + rows * qd * es);
     W.act = o; o = align256(o + rows * d->ffn_dim * es);
     W.sel = o; o = align256(o + step_rows * ((B + 63) / 64) * 8);   // state mask of the step
-    // split-key partials: room for the step's largest split (16 ways); the
-    // prefill splits only as far as this room allows
-    const size_t slots = (size_t)16 * b * 2 * B * d->n_heads;
-    W.part_slots = d->dtype == DARD_DTYPE_BF16 ? slots : 0;
+    // split-key attention partials: room for the step's largest split at any
+    // prefix length; a prefill splits only as far as this room allows
+    W.part_slots = attention_partial_slots(d->dtype, b, 2 * B, d->n_heads, d->n_kv_heads, 1 << 20);
     W.part = o; o = align256(o + W.part_slots * d->head_dim * 4);
     W.part_ml = o; o = align256(o + W.part_slots * 2 * 4);
     W.logits = o; o = align256(o + step_rows * d->vocab * 4);
@@ -190,14 +189,36 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
 }
 
 // ---------------------------------------------------------------- attention
+namespace {
+
+// Workspace of dard_masked_attention: the state mask of the block, then the
+// partial results of a key split (room for the largest split over every
+// KV-head count that divides Hq).
+struct AttnWs {
+    size_t mask, part, part_ml, part_slots, total;
+};
+
+AttnWs attn_ws(int dtype, int b, int B, int Hq, int dh, int P) {
+    AttnWs w{};
+    size_t slots = 0;
+    for (int hkv = 1; hkv <= Hq; ++hkv) {
+        if (Hq % hkv) continue;
+        const size_t sl = attention_partial_slots(dtype, b, 2 * B, Hq, hkv, attention_tiles(1, P, B, P + 2 * B));
+        slots = sl > slots ? sl : slots;
+    }
+    size_t o = 0;
+    w.mask = o; o = align256(o + (size_t)b * 2 * B * ((B + 63) / 64) * 8);
+    w.part = o; w.part_slots = slots; o = align256(o + slots * dh * 4);
+    w.part_ml = o; o = align256(o + slots * 8);
+    w.total = o;
+    return w;
+}
+
+}  // namespace
+
 size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P) {
-    if (b < 1 || B < 1 || B > 128 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16) return 0;
-    // the state mask of the block, then the partial results of a key split
-    const size_t mask = align256((size_t)b * 2 * B * ((B + 63) / 64) * 8);
-    const size_t slots = attention_partial_slots(dtype, b, 2 * B, Hq, attention_tiles(1, P, B, P + 2 * B));
-    if (slots == 0) return mask;
-    // + 64 slots of slack for the alignment of the (m, l) array
-    return mask + (slots + 64) * ((size_t)dh * 4 + 8);
+    if (b < 1 || B < 1 || B > 128 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16 || (dh != 64 && dh != 128)) return 0;
+    return attn_ws(dtype, b, B, Hq, dh, P).total;
 }
 
 dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v, int P, int cap,
@@ -219,17 +240,14 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
     hipStream_t s = (hipStream_t)stream;
     TraceScope ts(DARD_K_ATTENTION, s);
     if (dtype == DARD_DTYPE_BF16) {
-        // the state mask first, then as many partial slots as the rest of the workspace holds
-        const size_t mask = align256((size_t)b * 2 * B * ((B + 63) / 64) * 8);
-        uint64_t* sel = (uint64_t*)ws;
-        HIPOK(launch_build_state_mask(state, conf, b, B, flags, sel, s));
-        a.sel = sel;
-        const size_t slots = (ws_bytes - mask) / ((size_t)dh * 4 + 8);
-        a.part_slots = slots > 64 ? slots - 64 : 0;
-        if (a.part_slots > 0) {
-            a.part = (float*)((char*)ws + mask);
-            a.part_ml = (float*)((char*)ws + mask + align256(a.part_slots * dh * 4));
-        }
+        const AttnWs w = attn_ws(dtype, b, B, Hq, dh, P);
+        char* base = (char*)ws;
+        a.sel = (const uint64_t*)(base + w.mask);
+        a.part = (float*)(base + w.part);
+        a.part_ml = (float*)(base + w.part_ml);
+        a.part_slots = w.part_slots;
+        TraceScope tm(DARD_K_MASK, s);
+        HIPOK(launch_build_state_mask(state, conf, b, B, flags, (uint64_t*)(base + w.mask), s));
     }
     HIPOK(launch_attention(dtype, a, s));
     return DARD_OK;
@@ -502,7 +520,7 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
     // the state mask (Eq. 2-3) is the same for every layer of the step: build it once
     {
-        TraceScope ts(DARD_K_ATTENTION, f.s);
+        TraceScope ts(DARD_K_MASK, f.s);
         HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
     }
     HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,

@@ -1,24 +1,35 @@
 // State-masked attention over the augmented block (Sec. 2, Sec. 3.2).
 //
-// bf16 path: flash-style.  A workgroup serves 64 query rows of one (sequence,
-// query head) with G groups of 4 waves (16 rows per wave); the groups take
-// interleaved 64-key tiles of the workgroup's key range and are merged
-// through LDS at the end, so a short key range costs few serial steps
-// without any cross-workgroup synchronisation.  Per group, K tiles are staged
-// in LDS row-major and V tiles transposed (key-contiguous), so that both
-// products run on v_mfma_f32_16x16x32_bf16:
-//   S^T = K * Q^T   (A = K rows from LDS, B = this wave's Q rows in registers)
+// bf16 path: flash-style on v_mfma_f32_32x32x16_bf16.  A workgroup serves
+// 32 * WAVES query rows that read one KV head -- with grouped-query attention
+// the rows of all query heads of that KV head are one row space, so a K/V
+// tile staged once in LDS feeds every head of the group -- with G groups of
+// WAVES waves that take interleaved 64-key tiles (merged through LDS at the
+// end).  The V cache is stored dims-major (V^T, [dh][cap] per KV head), so
+// both tiles of a step are plain copies: every lane moves 16-byte chunks from
+// global memory straight into LDS (global_load_lds).  Chunks are XOR-swizzled
+// by row so the MFMA operand reads are bank-conflict free.  With two key
+// groups, the second runs half a tile step out of phase (its softmax while
+// the first group's scores run on the matrix cores, and the reverse), so the
+// two waves sharing a SIMD overlap MFMA and VALU work.
+// Each wave owns 32 query rows:
+//   S^T = K * Q^T   (A = 32 keys from LDS, B = this wave's Q rows in registers)
 //   O^T += V^T P^T  (A = V^T from LDS, B = probabilities straight from the
-//                    S^T accumulators; the MFMA k index is permuted so that a
-//                    lane's 8 probabilities are its own score values)
+//                    S^T accumulators)
+// Lane l supplies A row l%32 of S^T with key pi(l%32), pi swapping bits 2 and
+// 3, so that the 8 probabilities a lane holds for each 16-key step of O^T are
+// 8 consecutive keys and the matching V^T operand is one 16-byte read.
 // Keys are tiled in two runs: the prefix [0, P) in 64-key tiles, then the
 // block [P, P + 2B) (x^j at P+j, s^j at P+B+j) in 64-key tiles of its own.  A
 // row's block visibility is the "take x" word of the state mask (Eq. 2-3,
 // built once per step) widened to 2B bits: x^j where the bit is set, s^j
 // where it is clear; so one aligned 64-bit word per block tile says which
 // keys a row sees, and full prefix tiles need no test at all.
-// Very long key ranges are additionally split across workgroups and merged
-// by a log-sum-exp combine kernel.
+// The softmax runs in the log2 domain with a running maximum that may lag the
+// true one by up to kSlack (probabilities <= 2^kSlack), so the accumulators
+// are rescaled only when some row's maximum grows by more than that.
+// Long key ranges may also be split across workgroups (fp32 partials of
+// (o, m, l), merged in split order by a small combine kernel).
 //
 // fp32 path: one thread per (row, head), plain online softmax.
 #include "common.h"
@@ -32,17 +43,29 @@ constexpr int kKeys = 64;      // keys per tile
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinLog2 = -1e30f;   // running-max floor (log2 units): exp2 of anything below it is 0
+constexpr float kSlack = 8.f;        // a row's running max may trail its true max by this (log2 units)
 
-// LDS of one group of TPG threads: a K tile row-major and a V tile transposed
-// (or, at the end, every lane's o, m and l for the merge of the groups).
+// LDS of one group of TPG threads: three K stages [64 keys][DH] and two V^T
+// stages [DH][64 keys], unpadded and XOR-swizzled in 16-byte chunks, or, at
+// the end, every lane's o, m and l for the merge of the groups.
 template <int DH, int TPG>
 struct Lds {
-    static constexpr int KPAD = DH + 8;       // K row stride (bf16): 16-byte bank shift per row
-    static constexpr int VPAD = kKeys + 4;    // V^T row stride (bf16)
-    static constexpr int TILE_BYTES = (kKeys * KPAD + DH * VPAD) * 2;
-    static constexpr int MERGE_BYTES = (DH / 4 + 2) * TPG * 4;
-    static constexpr int GROUP_BYTES = ((TILE_BYTES > MERGE_BYTES ? TILE_BYTES : MERGE_BYTES) + 15) / 16 * 16;
+    static constexpr int TILE = kKeys * DH * 2;    // bytes of one K or V^T tile
+    static constexpr int MERGE = (DH / 2 + 2) * TPG * 4;
+    static constexpr int GROUP = ((5 * TILE > MERGE ? 5 * TILE : MERGE) + 15) / 16 * 16;
 };
+
+// s_waitcnt immediate: at most n vector-memory operations outstanding, no LDS
+// operation outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4 left at its maximum, lgkmcnt 11:8 zero).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
+// 16-byte chunk slots: K row r keeps its chunk c (dims 8c..8c+7) in slot
+// c ^ (r % (DH/8)); V^T row d (a dim) keeps its chunk c (keys 8c..8c+7) in
+// slot c ^ (d % 8).
+template <int DH>
+__device__ __forceinline__ int kslot(int r, int c) { return r * (DH / 8) + (c ^ (r & (DH / 8 - 1))); }
+__device__ __forceinline__ int vslot(int d, int c) { return d * (kKeys / 8) + (c ^ (d & 7)); }
 
 // The 2B-bit block visibility of a row from its take-x words (x1:x0), B <= 128:
 // bit j (j < B) = x bit j, bit B + j = NOT x bit j; returned as 4 words.
@@ -73,155 +96,156 @@ __device__ __forceinline__ int tile_count(int t, int npre, int pre_end, int B2) 
     return t < npre ? min(kKeys, pre_end - t * kKeys) : min(kKeys, B2 - (t - npre) * kKeys);
 }
 
-// G groups of WPG waves; a workgroup serves 16 WPG query rows of one
-// (sequence, query head) and its groups take interleaved key tiles.
-template <int DH, int G, int RING, int WPG>
-__global__ __launch_bounds__(64 * WPG * G) void attn_bf16_kernel(AttnArgs a, int rowtiles, int tiles_per_split) {
-    constexpr int TPG = 64 * WPG, ROWS = 16 * WPG;
+// Grid: x = row tile (row tile fastest, then KV head, then sequence), dealt to
+// the XCDs in contiguous runs so the workgroups reading one KV head share an
+// L2; y = key split.
+template <int DH, int WAVES, int G>
+__global__ __launch_bounds__(64 * WAVES * G) __attribute__((amdgpu_waves_per_eu(G)))
+void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
+    constexpr int TPG = 64 * WAVES, ROWS = 32 * WAVES;
+    constexpr int NCH = kKeys * DH / 8;            // 16-byte chunks per K (and per V^T) tile
+    constexpr int NI = NCH / TPG;                  // chunks per thread per tile, each
+    static_assert(NCH % TPG == 0, "whole chunks per thread");
     using L = Lds<DH, TPG>;
-    constexpr int KPAD = L::KPAD, VPAD = L::VPAD;
-    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-    __shared__ __attribute__((aligned(16))) char smem[G * L::GROUP_BYTES];
+    typedef __attribute__((address_space(3))) void* lds_ptr;
+    typedef __attribute__((address_space(1))) void* glb_ptr;
+    __shared__ __attribute__((aligned(16))) char smem[G * L::GROUP];
 
     // group and wave are wave-uniform: say so, so that tile bookkeeping stays scalar
     const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x / TPG), tid = threadIdx.x % TPG;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int lr = lane & 15, g = lane >> 4;
-    bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + grp * L::GROUP_BYTES);
-    bf16_t* Vt = Ks + kKeys * KPAD;
+    const int lr = lane & 31, eta = lane >> 5;
     int bid = blockIdx.x;
-    const int rt = bid % rowtiles; bid /= rowtiles;
-    const int h = bid % a.Hq;
-    const int s = bid / a.Hq;
-    const int kvh = h / (a.Hq / a.Hkv);
-    const int r0 = rt * ROWS;
+    const int total = gridDim.x;
+    if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
     const int split = blockIdx.y, nsplit = gridDim.y;
+    const int rt = bid % rowtiles;
+    const int kvh = (bid / rowtiles) % a.Hkv;
+    const int s = bid / rowtiles / a.Hkv;
+    const int GQ = a.Hq / a.Hkv;
+    const int nrows = GQ * a.R;
 
     // prefix tiles [0, npre), then block tiles (masked mode)
     const int pre_end = a.masked ? a.P : a.nkeys;
     const int npre = (pre_end + kKeys - 1) / kKeys;
     const int ntiles = npre + (a.masked ? (2 * a.B + kKeys - 1) / kKeys : 0);
-    const int t_begin = split * tiles_per_split;
-    const int t_end = min(ntiles, t_begin + tiles_per_split);
+    const int t_begin = split * tps;
+    const int t_end = min(ntiles, t_begin + tps);
     const int iters = (t_end - t_begin + G - 1) / G;   // tile steps of every group
-    const int P = a.P, B2 = 2 * a.B;
+    const int P = a.P, B2 = 2 * a.B, cap = a.cap;
 
-    const bf16_t* q = reinterpret_cast<const bf16_t*>(a.q);
-    const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
-    const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
+    const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * cap * DH;
+    const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * DH * cap;
+    char* gbase = smem + grp * L::GROUP;
 
-    // ---- issue the loads of this group's first RING tiles before anything else
-    constexpr int KCH = kKeys * DH / 8 / TPG;  // 16-byte K chunks per thread
-    constexpr int VUNITS = (kKeys / 4) * (DH / 8);           // (4 keys x 8 dims) V units per tile
-    constexpr int VQ = (VUNITS + TPG - 1) / TPG;              // V units per thread
-    bf16x8 kreg[RING][KCH];
-    bf16x8 vreg[RING][VQ][4];
-    auto load_tile = [&](int slot, int tile) __attribute__((always_inline)) {
+    // ---- copy the K (or V^T) tile of key tile `tile` into LDS at `dst`:
+    // chunk q = (wave * NI + j) * 64 + lane of the swizzled image.  Full tiles
+    // go straight to LDS; a ragged tile (n < 64 keys) goes through registers
+    // with its missing keys zeroed.
+    auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
-        const bf16_t* kt = kbase + (size_t)k0 * DH;
-        const bf16_t* vt = vbase + (size_t)k0 * DH;
-        // V unit u = tid + TPG v: (kg, dg) = (u % 16, u / 16) holds keys
-        // 4kg..4kg+3 at dims 8dg..8dg+7
-        if (n == kKeys) {   // full tile (uniform): no per-key test
 #pragma unroll
-            for (int it = 0; it < KCH; ++it) kreg[slot][it] = ld_bf16x8(kt + (size_t)(tid + TPG * it) * 8);
-#pragma unroll
-            for (int vq = 0; vq < VQ; ++vq) {
-                const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
-                if (u < VUNITS) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        vreg[slot][vq][e] = ld_bf16x8(vt + (size_t)(4 * kg + e) * DH + dg * 8);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int it = 0; it < KCH; ++it) {
-                const int qd = tid + TPG * it;
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            const int r = q / (DH / 8), sl = q % (DH / 8);
+            const bf16_t* src = kbase + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
+            if (n == kKeys) {
+                __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
+            } else {
                 bf16x8 z = {};
-                kreg[slot][it] = qd / (DH / 8) < n ? ld_bf16x8(kt + (size_t)qd * 8) : z;
-            }
-#pragma unroll
-            for (int vq = 0; vq < VQ; ++vq) {
-                const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
-                if (u < VUNITS) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int key = 4 * kg + e;
-                        bf16x8 z = {};
-                        vreg[slot][vq][e] = key < n ? ld_bf16x8(vt + (size_t)key * DH + dg * 8) : z;
-                    }
-                }
+                *reinterpret_cast<bf16x8*>(dst + 16 * q) = r < n ? ld_bf16x8(src) : z;
             }
         }
     };
-    auto store_tile = [&](int slot) __attribute__((always_inline)) {
+    auto issue_v = [&](int tile, char* dst) __attribute__((always_inline)) {
+        const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
 #pragma unroll
-        for (int it = 0; it < KCH; ++it) {
-            const int qd = tid + TPG * it;
-            const int key = qd / (DH / 8), c8 = qd % (DH / 8);
-            *reinterpret_cast<bf16x8*>(&Ks[key * KPAD + c8 * 8]) = kreg[slot][it];
-        }
-        // 16 consecutive lanes write one contiguous 128-byte run of a V^T row
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
+            const bf16_t* src = vbase + (size_t)d * cap + k0 + 8 * c;
+            if (n == kKeys) {
+                __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
+            } else {
+                bf16x8 vv = {};
+                if (8 * c + 8 <= n) {
+                    vv = ld_bf16x8(src);
+                } else {
 #pragma unroll
-        for (int vq = 0; vq < VQ; ++vq) {
-            const int u = tid + TPG * vq, kg = u & 15, dg = u >> 4;
-            if (u < VUNITS) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    bf16x4 t4 = {vreg[slot][vq][0][e], vreg[slot][vq][1][e], vreg[slot][vq][2][e],
-                                 vreg[slot][vq][3][e]};
-                    *reinterpret_cast<bf16x4*>(&Vt[(dg * 8 + e) * VPAD + 4 * kg]) = t4;
+                    for (int e = 0; e < 8; ++e)
+                        if (8 * c + e < n) vv[e] = __builtin_bit_cast(__bf16, src[e]);
                 }
+                *reinterpret_cast<bf16x8*>(dst + 16 * q) = vv;
             }
         }
     };
-#pragma unroll
-    for (int sl = 0; sl < RING; ++sl) {
-        const int tile = t_begin + grp + G * sl;
-        if (sl < iters && tile < t_end) load_tile(sl, tile);
+    // stage addresses by arithmetic on the LDS array (an indexed table of
+    // pointers would lose the address space and turn LDS reads into flat loads)
+    auto kst = [&](int i) __attribute__((always_inline)) { return gbase + (i % 3) * L::TILE; };
+    auto vst = [&](int i) __attribute__((always_inline)) { return gbase + (3 + (i & 1)) * L::TILE; };
+    auto tile_of = [&](int it) __attribute__((always_inline)) { return t_begin + grp + G * it; };
+    auto mine = [&](int it) __attribute__((always_inline)) { return it < iters && tile_of(it) < t_end; };
+    if (mine(0)) {
+        issue_k(tile_of(0), kst(0));
+        issue_v(tile_of(0), vst(0));
     }
 
-    // this lane's query row and its Q fragments (B operand of S^T = K Q^T)
-    const int my_row = r0 + wave * 16 + lr;
-    const bool row_ok = my_row < a.R;
-    bf16x8 qf[DH / 32];
+    // ---- this lane's query row (rows of every query head of the KV head form
+    // one row space), its Q fragments (B operand chunk c = dims 16c + 8eta ..)
+    // and its block visibility
+    const int rho = rt * ROWS + 32 * wave + lr;
+    const bool row_ok = rho < nrows;
+    const int h = kvh * GQ + (row_ok ? rho / a.R : 0);
+    const int r = row_ok ? rho % a.R : 0;
+    bf16x8 qf[DH / 16];
     {
-        const bf16_t* qp = q + (((size_t)s * a.R + (row_ok ? my_row : 0)) * a.Hq + h) * DH;
+        const bf16_t* qp = reinterpret_cast<const bf16_t*>(a.q) + (((size_t)s * a.R + r) * a.Hq + h) * DH;
 #pragma unroll
-        for (int c = 0; c < DH / 32; ++c) {
+        for (int c = 0; c < DH / 16; ++c) {
             bf16x8 z = {};
-            qf[c] = row_ok ? ld_bf16x8(qp + 32 * c + 8 * g) : z;
+            qf[c] = row_ok ? ld_bf16x8(qp + 16 * c + 8 * eta) : z;
         }
     }
-    // this lane's row of the state mask, widened to the block's 2B keys
     uint64_t bv0 = 0, bv1 = 0, bv2 = 0, bv3 = 0;
     if (a.masked && row_ok) {
         const int W = (a.B + 63) / 64;
-        const uint64_t* sp = a.sel + ((size_t)s * a.R + my_row) * W;
+        const uint64_t* sp = a.sel + ((size_t)s * a.R + r) * W;
         block_vis(sp[0], W > 1 ? sp[1] : 0ull, a.B, bv0, bv1, bv2, bv3);
     }
     const float sl2 = a.scale * kLog2e;
+    // K row this lane supplies to the S^T MFMAs: key pi(lr) of each 32-key block
+    const int krow = (lr & ~12) | ((lr & 4) << 1) | ((lr & 8) >> 1);
 
-    floatx4 o[DH / 16];
+    floatx16 o[DH / 32];
 #pragma unroll
-    for (int d = 0; d < DH / 16; ++d) o[d] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int d = 0; d < DH / 32; ++d)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
     float m_run = kMinLog2, l_run = 0.f;
 
-    auto compute_tile = [&](int tile) __attribute__((always_inline)) {
-        // ---- S^T = K * Q^T for this wave's 16 rows: 4 blocks of 16 keys
-        floatx4 sc[4];
+    // ---- S^T = K * Q^T for the K tile at ks: value v of block kb is key
+    // 32kb + 16(v/8) + 8eta + v%8 of the tile
+    // Each block's DH/16 operand reads are issued together ahead of its MFMAs
+    // (left to itself the compiler waits for each read right before its MFMA).
+    auto scores = [&](const char* ks, floatx16 (&sc)[2]) __attribute__((always_inline)) {
+        constexpr int NC = DH / 16;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < 2; ++kb) {
+            bf16x8 kf[NC];
 #pragma unroll
-            for (int c = 0; c < DH / 32; ++c) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(16 * kb + lr) * KPAD + 32 * c + 8 * g]);
-                acc = mfma16x16x32(kf, qf[c], acc);
-            }
-            sc[kb] = acc;
+            for (int c = 0; c < NC; ++c)
+                kf[c] = *reinterpret_cast<const bf16x8*>(ks + 16 * kslot<DH>(32 * kb + krow, 2 * c + eta));
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sc[kb][v] = 0.f;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) sc[kb] = mfma32x32x16(kf[c], qf[c], sc[kb]);
+            __builtin_amdgcn_sched_group_barrier(0x100, NC, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NC, 0);
         }
-        // ---- visibility: only tiles with block keys or a ragged end test it
+    };
+    // ---- mask, online softmax and O^T += V^T P^T for tile `tile`
+    auto softmax_pv = [&](floatx16 (&sc)[2], int tile, const char* vs) __attribute__((always_inline)) {
+        // visibility: only tiles with block keys or a ragged end test it
         // (tile and n are wave-uniform, so this is a scalar branch)
         const int n = tile_count(tile, npre, pre_end, B2);
         if (!(tile < npre && n == kKeys)) {
@@ -235,146 +259,170 @@ __global__ __launch_bounds__(64 * WPG * G) void attn_bf16_kernel(AttnArgs a, int
                 vis = (bv0 & (0ull - (uint64_t)(bt == 0))) | (bv1 & (0ull - (uint64_t)(bt == 1))) |
                       (bv2 & (0ull - (uint64_t)(bt == 2))) | (bv3 & (0ull - (uint64_t)(bt == 3)));
             }
-            // this lane's keys 16kb + 4g + i: bits 16(kb%2) + i of w[kb/2]
-            const uint32_t w0 = (uint32_t)vis >> (4 * g), w1 = (uint32_t)(vis >> 32) >> (4 * g);
+            const uint64_t ww = vis >> (8 * eta);
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (!(((kb < 2 ? w0 : w1) >> (16 * (kb & 1) + i)) & 1u)) sc[kb][i] = -INFINITY;
+                for (int v = 0; v < 16; ++v)
+                    if (!((ww >> (32 * kb + 16 * (v >> 3) + (v & 7))) & 1ull)) sc[kb][v] = -INFINITY;
         }
-        // ---- online softmax in the log2 domain; the running max starts at a
-        // finite floor, so rows with no visible key yet need no special case
+        // online softmax in the log2 domain
         float mt = sc[0][0];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sc[kb][i]);
-        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+            for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb][v]);
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
         const float m_new = fmaxf(m_run, mt * sl2);     // sl2 > 0: the max commutes with the scale
-        // arguments are <= 0: the hardware exp2 (v_exp_f32) needs no range handling
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        if (__ballot(m_new > m_run + kSlack)) {        // some row's max outgrew the slack
+            // arguments are <= 0: the hardware exp2 (v_exp_f32) needs no range handling
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+            for (int d = 0; d < DH / 32; ++d) o[d] *= alpha;
+            l_run *= alpha;
+            m_run = m_new;
+        }
         float psum = 0.f;
-        bf16x8 pb[2];
+        bf16x8 pb[2][2];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], sl2, -m_new));
+            for (int v = 0; v < 16; ++v) {
+                const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][v], sl2, -m_run));
                 psum += p;
-                pb[kb >> 1][(kb & 1) * 4 + i] = (__bf16)p;
+                pb[kb][v >> 3][v & 7] = (__bf16)p;
             }
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-        if (__ballot(alpha != 1.f)) {             // some row's max moved
+        l_run += psum;
+        // O^T += V^T * P^T: step st = 2kb + hh covers keys 16st + [0, 16); the
+        // lane's 8 probabilities are keys 16st + 8eta + [0, 8), V^T chunk 2st + eta
 #pragma unroll
-            for (int d = 0; d < DH / 16; ++d) o[d] *= alpha;
-        }
-        // ---- O^T += V^T * P^T
+        for (int d = 0; d < DH / 32; ++d) {
+            bf16x8 vf[4];
 #pragma unroll
-        for (int d = 0; d < DH / 16; ++d) {
+            for (int st = 0; st < 4; ++st)
+                vf[st] = *reinterpret_cast<const bf16x8*>(vs + 16 * vslot(32 * d + lr, 2 * st + eta));
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                const bf16_t* vp = &Vt[(16 * d + lr) * VPAD + 32 * c + 4 * g];
-                const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vp);
-                const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vp + 16);
-                const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                o[d] = mfma16x16x32(vf, pb[c], o[d]);
-            }
+            for (int st = 0; st < 4; ++st) o[d] = mfma32x32x16(vf[st], pb[st >> 1][st & 1], o[d]);
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
         }
     };
 
-    for (int base = 0; base < iters; base += RING) {
-#pragma unroll
-        for (int sl = 0; sl < RING; ++sl) {
-            const int it = base + sl;
-            if (it < iters) {                     // uniform across the workgroup
-                const int tile = t_begin + grp + G * it;
-                const bool mine = tile < t_end;
-                __syncthreads();                  // the previous tiles are fully consumed
-                if (mine) store_tile(sl);
-                __syncthreads();
-                if (mine) {
-                    const int next = tile + G * RING;
-                    if (next < t_end) load_tile(sl, next);
-                    compute_tile(tile);
-                }
+    // ---- main loop.  Group 0 computes step it as scores, softmax, P V; a
+    // second group runs half a step out of phase -- softmax and P V of step it,
+    // then the scores of step it + 1 -- so that on every SIMD one wave's MFMAs
+    // overlap the other's softmax.  Copies run ahead of use: V one step, K two
+    // steps (three for the second group, whose scores come a step early), so a
+    // copy's latency spans more than one step.  Each step ends by waiting for
+    // every copy except the newest K tile and publishing them with the barrier,
+    // which also retires every wave's reads of the stages the next step
+    // overwrites.  Copies complete in issue order, so V goes first.
+    const bool late = G > 1 && grp == 1;
+    if (mine(1)) issue_k(tile_of(1), kst(1));
+    if (late && mine(2)) issue_k(tile_of(2), kst(2));
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (!late) {
+        for (int it = 0; it < iters; ++it) {         // iters is uniform across the workgroup
+            if (mine(it + 1)) issue_v(tile_of(it + 1), vst(it + 1));
+            const bool ahead = mine(it + 2);
+            if (ahead) issue_k(tile_of(it + 2), kst(it + 2));
+            if (mine(it)) {
+                floatx16 sc[2];
+                scores(kst(it), sc);
+                softmax_pv(sc, tile_of(it), vst(it));
             }
+            if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+            else __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+        }
+    } else {
+        floatx16 sc[2];
+        if (mine(0)) scores(kst(0), sc);
+        for (int it = 0; it < iters; ++it) {
+            if (mine(it + 1)) issue_v(tile_of(it + 1), vst(it + 1));
+            const bool ahead = mine(it + 3);
+            if (ahead) issue_k(tile_of(it + 3), kst(it + 3));
+            if (mine(it)) softmax_pv(sc, tile_of(it), vst(it));
+            __builtin_amdgcn_sched_barrier(0);
+            if (mine(it + 1)) scores(kst(it + 1), sc);
+            if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+            else __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
         }
     }
 
     // ---- merge the groups through LDS (group 0 keeps the result)
     if constexpr (G > 1) {
-        __syncthreads();
-        float* mb = reinterpret_cast<float*>(smem + grp * L::GROUP_BYTES);
+        float* mb = reinterpret_cast<float*>(gbase);
         if (grp > 0) {
 #pragma unroll
-            for (int d = 0; d < DH / 16; ++d)
+            for (int d = 0; d < DH / 32; ++d)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) mb[(4 * d + i) * TPG + tid] = o[d][i];
-            mb[(DH / 4) * TPG + tid] = m_run;
-            mb[(DH / 4 + 1) * TPG + tid] = l_run;
+                for (int v = 0; v < 16; ++v) mb[(16 * d + v) * TPG + tid] = o[d][v];
+            mb[(DH / 2) * TPG + tid] = m_run;
+            mb[(DH / 2 + 1) * TPG + tid] = l_run;
         }
         __syncthreads();
-        if (grp > 0) return;
-        float M = m_run;
+        if (grp == 0) {
+            float M = m_run;
 #pragma unroll
-        for (int gg = 1; gg < G; ++gg)
-            M = fmaxf(M, reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES)[(DH / 4) * TPG + tid]);
-        const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
-        float lsum = l_run * f0;
+            for (int gg = 1; gg < G; ++gg)
+                M = fmaxf(M, reinterpret_cast<const float*>(smem + gg * L::GROUP)[(DH / 2) * TPG + tid]);
+            const float f0 = __builtin_amdgcn_exp2f(m_run - M);
+            float lsum = l_run * f0;
 #pragma unroll
-        for (int d = 0; d < DH / 16; ++d) o[d] *= f0;
+            for (int d = 0; d < DH / 32; ++d) o[d] *= f0;
 #pragma unroll
-        for (int gg = 1; gg < G; ++gg) {
-            const float* ob = reinterpret_cast<const float*>(smem + gg * L::GROUP_BYTES);
-            const float mg = ob[(DH / 4) * TPG + tid];
-            const float f = mg == -INFINITY ? 0.f : exp2f(mg - M);
-            lsum += ob[(DH / 4 + 1) * TPG + tid] * f;
+            for (int gg = 1; gg < G; ++gg) {
+                const float* ob = reinterpret_cast<const float*>(smem + gg * L::GROUP);
+                const float f = __builtin_amdgcn_exp2f(ob[(DH / 2) * TPG + tid] - M);
+                lsum += ob[(DH / 2 + 1) * TPG + tid] * f;
 #pragma unroll
-            for (int d = 0; d < DH / 16; ++d)
+                for (int d = 0; d < DH / 32; ++d)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) o[d][i] += ob[(4 * d + i) * TPG + tid] * f;
+                    for (int v = 0; v < 16; ++v) o[d][v] += ob[(16 * d + v) * TPG + tid] * f;
+            }
+            m_run = M;
+            l_run = lsum;
         }
-        m_run = M;
-        l_run = lsum;
     }
+    if (grp != 0) return;
 
-    // ---- epilogue: row sum over the 4 lanes sharing a row
-    float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    // ---- epilogue: the two lanes of a row hold disjoint keys; sum their l.
+    // The lane holds dims 32d + 8j + 4eta + {0..3} (O^T accumulator rows).
+    const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
     if (!row_ok) return;
-    const size_t nrow = (size_t)a.b * a.R * a.Hq;
-    const size_t orow = ((size_t)s * a.R + my_row) * a.Hq + h;
+    const size_t orow = ((size_t)s * a.R + r) * a.Hq + h;    // (sequence, row, head)
     if (nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        const int tok = s * a.R + r, KO = a.Hq * DH;
         bf16_t* out = reinterpret_cast<bf16_t*>(a.out);
-        const int tok = s * a.R + my_row, KO = a.Hq * DH;
 #pragma unroll
-        for (int d = 0; d < DH / 16; ++d) {
-            const uint32_t w0 = (uint32_t)f2bf(o[d][0] * inv) | ((uint32_t)f2bf(o[d][1] * inv) << 16);
-            const uint32_t w1 = (uint32_t)f2bf(o[d][2] * inv) | ((uint32_t)f2bf(o[d][3] * inv) << 16);
-            const int k = h * DH + 16 * d + 4 * g;
-            *reinterpret_cast<uint2*>(out + (a.out_frag ? frag_off(tok, k, KO) : orow * DH + 16 * d + 4 * g)) =
-                make_uint2(w0, w1);
-        }
+        for (int d = 0; d < DH / 32; ++d)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t w0 = (uint32_t)f2bf(o[d][4 * j] * inv) | ((uint32_t)f2bf(o[d][4 * j + 1] * inv) << 16);
+                const uint32_t w1 = (uint32_t)f2bf(o[d][4 * j + 2] * inv) | ((uint32_t)f2bf(o[d][4 * j + 3] * inv) << 16);
+                const int k = 32 * d + 8 * j + 4 * eta;
+                *reinterpret_cast<uint2*>(out + (a.out_frag ? frag_off(tok, h * DH + k, KO) : orow * DH + k)) =
+                    make_uint2(w0, w1);
+            }
         return;
     }
+    const size_t nrow = (size_t)a.b * a.R * a.Hq;
     float* po = a.part + ((size_t)split * nrow + orow) * DH;
 #pragma unroll
-    for (int d = 0; d < DH / 16; ++d)
-        *reinterpret_cast<float4*>(po + 16 * d + 4 * g) = make_float4(o[d][0], o[d][1], o[d][2], o[d][3]);
-    if (g == 0) {
-        float* pm = a.part_ml + ((size_t)split * nrow + orow) * 2;
-        pm[0] = m_run;
-        pm[1] = l_tot;
-    }
+    for (int d = 0; d < DH / 32; ++d)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(po + 32 * d + 8 * j + 4 * eta) =
+                make_float4(o[d][4 * j], o[d][4 * j + 1], o[d][4 * j + 2], o[d][4 * j + 3]);
+    if (eta == 0) *reinterpret_cast<float2*>(a.part_ml + ((size_t)split * nrow + orow) * 2) = make_float2(m_run, l_tot);
 }
 
-// Merge key splits: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M).  One
-// thread per (row, head, 4 dims); every load of a thread is issued up front.
+// Merge key splits: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), in split
+// order.  One thread per (row, head, 4 dims); every load is issued up front.
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part,
                                                            const float* __restrict__ part_ml, int ns,
@@ -389,24 +437,24 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 #pragma unroll
     for (int sp = 0; sp < kMaxSplit; ++sp) {
         if (sp < ns) {
-            m[sp] = part_ml[(sp * nrow + row) * 2];
-            l[sp] = part_ml[(sp * nrow + row) * 2 + 1];
+            const float2 ml = reinterpret_cast<const float2*>(part_ml)[sp * nrow + row];
+            m[sp] = ml.x;
+            l[sp] = ml.y;
             ov[sp] = reinterpret_cast<const float4*>(part + (sp * nrow + row) * DH)[q4];
         } else {
-            m[sp] = -INFINITY;
+            m[sp] = kMinLog2;
             l[sp] = 0.f;
             ov[sp] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
-    float M = -INFINITY;
+    float M = kMinLog2;
 #pragma unroll
     for (int sp = 0; sp < kMaxSplit; ++sp) M = fmaxf(M, m[sp]);
     float Lsum = 0.f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int sp = 0; sp < kMaxSplit; ++sp) {
-        if (m[sp] == -INFINITY) continue;
-        const float f = exp2f(m[sp] - M);
+        const float f = __builtin_amdgcn_exp2f(m[sp] - M);
         Lsum += l[sp] * f;
         acc.x += ov[sp].x * f; acc.y += ov[sp].y * f; acc.z += ov[sp].z * f; acc.w += ov[sp].w * f;
     }
@@ -451,7 +499,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
         const float alpha = expf(m - mn);
         const float p = expf(sdot - mn);
         l = l * alpha + p;
-        for (int e = 0; e < DH; ++e) o[e] = o[e] * alpha + p * vb[(size_t)key * DH + e];
+        for (int e = 0; e < DH; ++e) o[e] = o[e] * alpha + p * vb[(size_t)e * a.cap + key];
         m = mn;
     }
     float* out = reinterpret_cast<float*>(a.out) + t * DH;
@@ -459,21 +507,48 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     for (int e = 0; e < DH; ++e) out[e] = o[e] * inv;
 }
 
-// Shape of a bf16 launch: WPG waves per group (16 WPG query rows per
-// workgroup) and G groups taking interleaved key tiles.  While one-group
-// workgroups of 64 rows would leave the chip short of 1024 waves, the key
-// tiles are walked by more groups: 4 groups of 2 waves (32 rows per
-// workgroup, so a head's 64 rows take two workgroups) when there are at least
-// 4 tiles, else 2 groups of 4 waves.
+// Shape of a bf16 launch (kernel-trace sweeps at the workload shapes):
+// - more than 64 rows per KV head (grouped-query attention, prefill): 4 waves
+//   per group, and a second, phase-shifted key group while the workgroups
+//   alone leave SIMDs idle (7B GQA shape, batch 8: 35.6 -> 31.4 us);
+// - 64 rows (one MHA head's augmented block): with at least 256 workgroups,
+//   2 waves per workgroup (batch 16: 36 us); with fewer, 4 waves (the extra
+//   two only help copy tiles) and key splits of about 3 tiles each merged by
+//   the combine kernel (batch 1, prompt 736: 34 -> 20 us).
 struct AttnCfg {
-    int wpg, g;
+    int waves, g, rowtiles, ns, tps;
 };
 
-AttnCfg attention_cfg(int b, int R, int Hq, int ntiles) {
-    const int wgs64 = b * Hq * ((R + 63) / 64);
-    if (4 * wgs64 >= 1024 || ntiles < 2) return {4, 1};
-    if (R > 32 && ntiles >= 4) return {2, 4};
-    return {4, 2};
+AttnCfg attention_cfg(int b, int R, int Hq, int Hkv, int ntiles) {
+    AttnCfg c{};
+    const int nrows = (Hq / Hkv) * R;
+    c.g = 1;
+    c.ns = 1;
+    if (nrows > 64) {
+        c.waves = 4;
+        c.rowtiles = (nrows + 127) / 128;
+        const long wgs = (long)b * Hkv * c.rowtiles;
+        if (wgs * 4 < 1024 && ntiles >= 4) c.g = 2;
+    } else {
+        c.rowtiles = 1;
+        const long wgs = (long)b * Hkv;
+        c.waves = wgs >= 256 ? 2 : 4;
+        if (wgs < 256 && ntiles > 3) {
+            c.ns = (ntiles + 2) / 3;
+            c.ns = c.ns < kMaxSplit ? c.ns : kMaxSplit;
+        }
+    }
+    c.tps = ntiles > 0 ? (ntiles + c.ns - 1) / c.ns : 1;
+    c.ns = ntiles > 0 ? (ntiles + c.tps - 1) / c.tps : 1;   // no empty split
+    return c;
+}
+
+using AttnKernel = void (*)(AttnArgs, int, int);
+
+template <int DH>
+AttnKernel attention_kernel(const AttnCfg& c) {
+    if (c.g == 2) return c.waves == 2 ? attn_mfma_kernel<DH, 2, 2> : attn_mfma_kernel<DH, 4, 2>;
+    return c.waves == 2 ? attn_mfma_kernel<DH, 2, 1> : attn_mfma_kernel<DH, 4, 1>;
 }
 
 }  // namespace
@@ -482,60 +557,40 @@ int attention_tiles(int masked, int P, int B, int nkeys) {
     return masked ? (P + kKeys - 1) / kKeys + (2 * B + kKeys - 1) / kKeys : (nkeys + kKeys - 1) / kKeys;
 }
 
-int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots) {
-    if (dtype != DARD_DTYPE_BF16) return 1;
-    const AttnCfg c = attention_cfg(b, R, Hq, ntiles);
-    const int wgs = b * Hq * ((R + 16 * c.wpg - 1) / (16 * c.wpg));
-    // Measured at 64 rows x 32 heads: a tile step costs about 2 us, the
-    // combine kernel about 4.3 us plus its launch, so a split pays only when
-    // the workgroups would otherwise walk more than 5 tile steps; then about
-    // 3 tiles per split.  No split once the workgroups alone cover the chip.
-    if (wgs * c.g * c.wpg >= 1024 || (ntiles + c.g - 1) / c.g <= 5) return 1;
-    int ns = 1;
-    while (ns < kMaxSplit && ntiles > 3 * ns) ns *= 2;
-    const size_t per_split = (size_t)b * R * Hq;
-    while (ns > 1 && (size_t)ns * per_split > slots) --ns;
-    if (ns <= 1) return 1;
-    const int tps = (ntiles + ns - 1) / ns;
-    return (ntiles + tps - 1) / tps;      // no empty split
+size_t attention_partial_slots(int dtype, int b, int R, int Hq, int Hkv, int ntiles) {
+    if (dtype != DARD_DTYPE_BF16 || b < 1 || R < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv) return 0;
+    const AttnCfg c = attention_cfg(b, R, Hq, Hkv, ntiles);
+    return c.ns <= 1 ? 0 : (size_t)c.ns * b * R * Hq;
 }
 
-size_t attention_partial_slots(int dtype, int b, int R, int Hq, int ntiles) {
-    const int ns = attention_splits(dtype, b, R, Hq, ntiles, (size_t)-1);
-    return ns <= 1 ? 0 : (size_t)ns * b * R * Hq;
-}
-
-hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStream_t s) {
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     if (a.out_frag && !frag_rows(dtype, a.b * a.R)) return hipErrorInvalidValue;
+    if (a.Hkv < 1 || a.Hq % a.Hkv) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16) {
         if (a.masked && (!a.sel || a.B > 128)) return hipErrorInvalidValue;
+        if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
         const int ntiles = attention_tiles(a.masked, a.P, a.B, a.nkeys);
-        const bool can_split = a.part && a.part_ml;
-        if (!can_split || ns < 1 || ns > kMaxSplit || (size_t)ns * a.b * a.R * a.Hq > a.part_slots) ns = 1;
-        if (ns > ntiles) ns = ntiles > 0 ? ntiles : 1;
-        const int tps = (ntiles + ns - 1) / ns;
-        ns = ntiles > 0 ? (ntiles + tps - 1) / tps : 1;
-        const AttnCfg c = attention_cfg(a.b, a.R, a.Hq, tps);
-        const int rowtiles = (a.R + 16 * c.wpg - 1) / (16 * c.wpg);
-        dim3 grid(a.b * a.Hq * rowtiles, ns);
-#define DARD_ATT(DHV, GV, WV) \
-    launch((attn_bf16_kernel<DHV, GV, WV == 2 ? 1 : 2, WV>), grid, dim3(64 * WV * GV), 0, s, a, rowtiles, tps)
-        if (a.dh == 128) {
-            if (c.wpg == 2) DARD_ATT(128, 4, 2); else if (c.g == 2) DARD_ATT(128, 2, 4); else DARD_ATT(128, 1, 4);
-        } else {
-            if (c.wpg == 2) DARD_ATT(64, 4, 2); else if (c.g == 2) DARD_ATT(64, 2, 4); else DARD_ATT(64, 1, 4);
-        }
-#undef DARD_ATT
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess || ns == 1) return e;
+        AttnCfg c = attention_cfg(a.b, a.R, a.Hq, a.Hkv, ntiles);
+        // a split needs room for its partials; without it one workgroup walks every key
         const size_t nrow = (size_t)a.b * a.R * a.Hq;
+        if (c.ns > 1 && (!a.part || !a.part_ml || (size_t)c.ns * nrow > a.part_slots)) {
+            c.ns = 1;
+            c.tps = ntiles > 0 ? ntiles : 1;
+        }
+        const size_t tiles = (size_t)a.b * a.Hkv * c.rowtiles;
+        if (tiles == 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
+        dim3 grid((unsigned)tiles, c.ns);
+        const AttnKernel k = a.dh == 128 ? attention_kernel<128>(c) : attention_kernel<64>(c);
+        launch(k, grid, dim3(64 * c.waves * c.g), 0, s, a, c.rowtiles, c.tps);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess || c.ns == 1) return e;
         const size_t threads = nrow * (a.dh / 4);
         if (a.dh == 128)
-            launch(attn_combine_kernel<128>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
-                               a.part_ml, ns, nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
+            launch(attn_combine_kernel<128>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part, a.part_ml, c.ns,
+                   nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
         else
-            launch(attn_combine_kernel<64>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part,
-                               a.part_ml, ns, nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
+            launch(attn_combine_kernel<64>, dim3((threads + 255) / 256), dim3(256), 0, s, a.part, a.part_ml, c.ns,
+                   nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
         return hipGetLastError();
     }
     const size_t total = (size_t)a.b * a.R * a.Hq;
@@ -545,14 +600,6 @@ hipError_t launch_attention_splits(int dtype, const AttnArgs& a, int ns, hipStre
     else
         launch(attn_f32_kernel<64>, grid, dim3(64), 0, s, a);
     return hipGetLastError();
-}
-
-hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
-    const bool can_split = a.part && a.part_ml;
-    const int ns = can_split ? attention_splits(dtype, a.b, a.R, a.Hq, attention_tiles(a.masked, a.P, a.B, a.nkeys),
-                                                a.part_slots)
-                             : 1;
-    return launch_attention_splits(dtype, a, ns, s);
 }
 
 }  // namespace dard

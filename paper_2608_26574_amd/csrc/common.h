@@ -44,6 +44,14 @@ __device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// D(32x32) += A(32x16) * B(16x32), bf16 in, fp32 accumulate.  Lane l holds
+// A[l%32][8*(l/32) .. +7], B[8*(l/32) .. +7][l%32], and D[i][l%32] in element
+// v for i = 8*(v/4) + 4*(l/32) + v%4.
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+__device__ __forceinline__ floatx16 mfma32x32x16(bf16x8 a, bf16x8 b, floatx16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) {
     return *reinterpret_cast<const bf16x8*>(p);
 }

@@ -5,6 +5,7 @@
 //   SWIGLU     silu(gate) * up on interleaved gate/up rows, stored as dtype
 //   QKV        rotary embedding on adjacent (t, t + dh/2) pairs, Q to its
 //              buffer, K and V straight into the KV cache at the rows' keys
+//              (K [cap][dh], V dims-major [dh][cap] per KV head)
 //   PARTIAL    fp32 split-K partial [split][M][N], reduced by the consumer
 //
 // bf16 weights are packed fragment-major: the 16 x 64 block (row block nb,
@@ -100,10 +101,12 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx
                 store4<T>(kc, a0, b0, a1, b1);
             }
         } else {
+            // the V cache is dims-major ([dh][cap] per KV head): four strided stores
             const int nv = n - qd - kd;
             const int kvh = nv / e.dh, ein = nv % e.dh;
-            T* vc = reinterpret_cast<T*>(e.vc) + (((size_t)s * e.Hkv + kvh) * e.cap + cidx) * e.dh + ein;
-            store4<T>(vc, v[0], v[1], v[2], v[3]);
+            T* vc = reinterpret_cast<T*>(e.vc) + (((size_t)s * e.Hkv + kvh) * e.dh + ein) * e.cap + cidx;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) St<T>::st(vc + (size_t)i * e.cap, v[i]);
         }
         break;
     }

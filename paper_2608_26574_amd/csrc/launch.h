@@ -27,7 +27,7 @@ hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int 
 struct AttnArgs {
     const void* q;      // [b][R][Hq][dh]
     const void* k;      // [b][Hkv][cap][dh]
-    const void* v;
+    const void* v;      // [b][Hkv][dh][cap] (dims-major)
     void* out;          // [b][R][Hq][dh]
     const uint8_t* state;  // [b][B] (masked mode, fp32 path)
     const float* conf;     // [b][B]
@@ -39,17 +39,15 @@ struct AttnArgs {
     int masked;         // 1: state-specific mask on keys >= P; 0: all visible
     float scale;
     uint32_t flags;
-    float* part;        // split partials [nsplit][b][R][Hq][dh] fp32
-    float* part_ml;     // [nsplit][b][R][Hq][2]
+    float* part;        // key-split partials [nsplit][b][R][Hq][dh] fp32 (bf16 only)
+    float* part_ml;     // [nsplit][b][R][Hq][2]: running max (log2 units) and sum
     size_t part_slots;  // capacity of part / part_ml in (split, row, head) slots
     int out_frag;       // 1: out is fragment-major [b*R][Hq*dh] (bf16 only)
 };
 // 64-key tiles of a launch: the prefix (or all keys when unmasked), then the block.
 int attention_tiles(int masked, int P, int B, int nkeys);
-// Key splits the launcher uses for these sizes with `slots` partial slots.
-int attention_splits(int dtype, int b, int R, int Hq, int ntiles, size_t slots);
-// Partial slots the launcher would like (0 = no split).
-size_t attention_partial_slots(int dtype, int b, int R, int Hq, int ntiles);
+// Partial slots a launch of these sizes would use (0 = no key split).
+size_t attention_partial_slots(int dtype, int b, int R, int Hq, int Hkv, int ntiles);
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---- gemm.hip
@@ -61,7 +59,7 @@ struct EpiArgs {
     int act_frag;                   // 1: act fragment-major with K = ld_act
     // QKV
     void* q; int ldq;               // [rows][Hq*dh]
-    void* kc; void* vc;             // cache base of this layer: [b][Hkv][cap][dh]
+    void* kc; void* vc;             // cache base of this layer: K [b][Hkv][cap][dh], V [b][Hkv][dh][cap]
     const float* rope;              // [max_pos][dh/2][2] (cos, sin)
     int rows_per_seq;               // R
     int P, B, cap, Hq, Hkv, dh;

@@ -21,7 +21,7 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR = 1, 2, 4
 PHASE_VERIFY, PHASE_FINAL = 0, 1
 (K_GEMM_QKV, K_GEMM_O, K_GEMM_GU, K_GEMM_DOWN, K_GEMM_HEAD, K_ATTENTION, K_CONFIDENCE,
- K_DECIDE, K_NORM, K_COUNT) = range(10)
+ K_DECIDE, K_NORM, K_MASK, K_COUNT) = range(11)
 
 EXPORTS = [
     "dard_last_error", "dard_version", "dard_build_state_mask", "dard_attention_workspace_bytes",
@@ -154,8 +154,11 @@ def dard_attention_workspace_bytes(dtype, b, B, Hq, dh, P):
 
 
 def dard_masked_attention(q, k, v, P, state, conf, scale, flags, out, ws=None, stream=None):
+    """q [b][2B][Hq][dh], k [b][Hkv][cap][dh], v [b][Hkv][dh][cap] (dims-major)."""
     b, R, Hq, dh = q.shape
     _, Hkv, cap, _ = k.shape
+    if tuple(v.shape) != (b, Hkv, dh, cap):
+        raise ValueError(f"v must be [b][Hkv][dh][cap] = {(b, Hkv, dh, cap)}, got {tuple(v.shape)}")
     nbytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().dard_masked_attention(_dt(q), _p(q), _p(k), _p(v), P, cap, _p(state), _p(conf), b, R // 2, Hq,
                                        Hkv, dh, scale, flags, _p(out), _p(ws), nbytes, _stream(stream)))
@@ -233,10 +236,14 @@ class Engine:
         self.ws = torch.zeros(wsb, dtype=torch.uint8, device=device)
 
     def kv_view(self, dtype):
-        """KV cache as a tensor [layers][2][b][Hkv][cap][dh]."""
+        """KV cache as (K, V) tensors [layers][b][Hkv][cap][dh] (V read out of
+        its dims-major storage [layers][b][Hkv][dh][cap] as a transposed view)."""
         d = self.dims
         n = d.n_layers * 2 * self.b * d.n_kv_heads * self.cap * d.head_dim
-        return self.kv.view(dtype)[:n].view(d.n_layers, 2, self.b, d.n_kv_heads, self.cap, d.head_dim)
+        kv = self.kv.view(dtype)[:n].view(d.n_layers, 2, self.b, d.n_kv_heads, self.cap * d.head_dim)
+        k = kv[:, 0].view(d.n_layers, self.b, d.n_kv_heads, self.cap, d.head_dim)
+        v = kv[:, 1].view(d.n_layers, self.b, d.n_kv_heads, d.head_dim, self.cap).transpose(-1, -2)
+        return k, v
 
     def dard_prefill(self, ids, embeds=None, stream=None):
         b, P = ids.shape

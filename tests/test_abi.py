@@ -101,13 +101,13 @@ def test_dims_validation_and_sizes():
 
 def test_attention_workspace_sizing():
     L = dard.lib()
-    # batch 1, 32 heads, 64 rows: a short prefix is walked by one workgroup per
-    # head (room for the state mask only), a long one is split across
-    # workgroups and needs room for the partial results
-    short = L.dard_attention_workspace_bytes(1, 1, 32, 32, 128, 512)
+    # batch 1, 32 heads, 64 rows: a short prefix (3 key tiles) is walked by one
+    # workgroup per head (room for the state mask only); a longer one is split
+    # across workgroups (about 3 tiles each) and needs room for the partials
+    short = L.dard_attention_workspace_bytes(1, 1, 32, 32, 128, 96)
     assert short == 64 * 8  # 64 rows x one 8-byte mask word
-    long = L.dard_attention_workspace_bytes(1, 1, 32, 32, 128, 2048)
-    assert long > short + 64 * 32 * 128 * 4
+    long = L.dard_attention_workspace_bytes(1, 1, 32, 32, 128, 512)
+    assert long > short + 3 * 64 * 32 * 128 * 4
     # many sequences fill the chip without splitting: room for the state mask only
     # (64 sequences x 64 rows x one 8-byte word)
     assert L.dard_attention_workspace_bytes(1, 64, 32, 32, 128, 512) == 64 * 64 * 8

@@ -81,7 +81,9 @@ def _attn_case(b, B, P, Hq, Hkv, dh, dtype, cand_frac, seed, flags=0, cap_extra=
     scale = 1.0 / math.sqrt(dh)
     nws = dard.dard_attention_workspace_bytes(1 if dtype == "bf16" else 0, b, B, Hq, dh, P)
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
-    dard.dard_masked_attention(q.cuda(), k.cuda(), v.cuda(), P, dev(state), dev(conf), scale, flags, out, ws)
+    # the V operand is dims-major: [b][Hkv][dh][cap]
+    dard.dard_masked_attention(q.cuda(), k.cuda(), v.transpose(-1, -2).contiguous().cuda(), P, dev(state), dev(conf),
+                               scale, flags, out, ws)
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
     qn, kn, vn = q.double().numpy(), k.double().numpy(), v.double().numpy()
@@ -103,6 +105,16 @@ def test_attention_llada_shape(b, frac):
     assert err < 2e-2, err
 
 
+@pytest.mark.parametrize("P", [1024, 1472])
+def test_attention_dream_gqa_shape(P):
+    """The 7B GQA attention workload: 28 query heads on 4 KV heads x 128,
+    batch 8, block 64, candidate fraction 0.3, prefix of the first and last
+    block of a 512-token generation after a 1024-token prompt."""
+    announce("attention 7B-GQA-shape", P)
+    err = _attn_case(8, 64, P, 28, 4, 128, "bf16", 0.3, seed=P)
+    assert err < 2e-2, err
+
+
 @pytest.mark.parametrize("case", [
     dict(b=1, B=1, P=0, Hq=2, Hkv=2, dh=128),       # smallest block, no prefix
     dict(b=2, B=5, P=70, Hq=4, Hkv=2, dh=128),      # ragged block, ragged prefix, GQA
@@ -110,6 +122,8 @@ def test_attention_llada_shape(b, frac):
     dict(b=1, B=128, P=33, Hq=2, Hkv=2, dh=128),    # maximum block: 4 row tiles, 2 mask words
     dict(b=3, B=32, P=100, Hq=4, Hkv=4, dh=64),     # head_dim 64
     dict(b=1, B=32, P=4000, Hq=2, Hkv=1, dh=128),   # long prefix: many key splits
+    dict(b=2, B=48, P=700, Hq=6, Hkv=2, dh=64),     # head_dim 64, GQA row tiles across heads, key splits
+    dict(b=1, B=128, P=2000, Hq=4, Hkv=4, dh=128),  # maximum block with key splits
 ])
 def test_attention_edges_bf16(case):
     announce("attention edge bf16", case)

@@ -74,10 +74,11 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
     if check_kv:
         tol = 2e-2 if dims.dtype == "bf16" else 1e-4
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
-        kv = eng.kv_view(kvd).float().cpu().numpy()
+        kc, vc = eng.kv_view(kvd)
+        kc, vc = kc.float().cpu().numpy(), vc.float().cpu().numpy()
         for layer in range(dims.n_layers):
-            k_gpu = unpermute_k(kv[layer, 0, :, :, :P], dims.head_dim).transpose(0, 2, 1, 3)
-            v_gpu = kv[layer, 1, :, :, :P].transpose(0, 2, 1, 3)
+            k_gpu = unpermute_k(kc[layer, :, :, :P], dims.head_dim).transpose(0, 2, 1, 3)
+            v_gpu = vc[layer, :, :, :P].transpose(0, 2, 1, 3)
             assert np.max(np.abs(k_gpu - cache[layer][0])) < tol * 4, layer
             assert np.max(np.abs(v_gpu - cache[layer][1])) < tol * 4, layer
     ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
