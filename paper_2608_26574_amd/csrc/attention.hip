@@ -139,9 +139,12 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     char* gbase = smem + grp * L::GROUP;
 
     // ---- copy the K (or V^T) tile of key tile `tile` into LDS at `dst`:
-    // chunk q = (wave * NI + j) * 64 + lane of the swizzled image.  Full tiles
-    // go straight to LDS; a ragged tile (n < 64 keys) goes through registers
-    // with its missing keys zeroed.
+    // chunk q = (wave * NI + j) * 64 + lane of the swizzled image, straight to
+    // LDS.  In a ragged tile (n < 64 keys) nothing past the valid keys is read:
+    // K rows past n are skipped (their scores are masked, whatever the stage
+    // held), V^T chunks past n are written as zeros (their probabilities are 0
+    // and 0 * stale could be NaN), and a chunk that straddles n goes through
+    // registers element by element.
     auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
 #pragma unroll
@@ -149,12 +152,8 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             const int q = (wave * NI + j) * 64 + lane;
             const int r = q / (DH / 8), sl = q % (DH / 8);
             const bf16_t* src = kbase + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
-            if (n == kKeys) {
+            if (n == kKeys || r < n)
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
-            } else {
-                bf16x8 z = {};
-                *reinterpret_cast<bf16x8*>(dst + 16 * q) = r < n ? ld_bf16x8(src) : z;
-            }
         }
     };
     auto issue_v = [&](int tile, char* dst) __attribute__((always_inline)) {
@@ -164,13 +163,11 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             const int q = (wave * NI + j) * 64 + lane;
             const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
             const bf16_t* src = vbase + (size_t)d * cap + k0 + 8 * c;
-            if (n == kKeys) {
+            if (n == kKeys || 8 * c + 8 <= n) {
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
             } else {
                 bf16x8 vv = {};
-                if (8 * c + 8 <= n) {
-                    vv = ld_bf16x8(src);
-                } else {
+                if (8 * c < n) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
                         if (8 * c + e < n) vv[e] = __builtin_bit_cast(__bf16, src[e]);
