@@ -40,6 +40,7 @@ def main():
     ap.add_argument("--steps", type=int, default=24)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the 7B GQA and multimodal full-step lines")
     ap.add_argument("--layers", type=int, default=32, help=argparse.SUPPRESS)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -195,6 +196,8 @@ def main():
     }
     out["decision_driven"] = decision_driven(eng, dims, ids, b, B, prompt)
     out["ops"] = op_measurements()
+    if not args.no_configs and args.layers == 32:
+        out["configs"] = full_step_configs(eng)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
     print(json.dumps(out), flush=True)
@@ -243,6 +246,134 @@ def decision_driven(eng, dims, ids, b, B, prompt, nblocks=2):
     return {"blocks": nblocks, "steps_per_block": steps, "capped_blocks": capped,
             "tokens_per_s": round(b * B * nblocks / el, 1),
             "note": "progress rule on, cap 2B steps; random-init weights, so blocks reach the cap"}
+
+
+def full_step_configs(eng8b, steps=6):
+    """The two other full-step workloads, measured the same way as the headline
+    step (HIP events around `steps` dard_step calls with inputs resident;
+    prefix lengths cycling over the generation's blocks; per-step states drawn
+    at the workload's candidate fraction), plus tokens committed/s over a whole
+    generation (prefill at every block start + ceil(B / r) steps per block,
+    r = the paper's mean tokens decoded per step):
+    - 7B GQA shape: Dream-7B-like random-init model (28 layers, d 3584, 28/4
+      heads x 128, FFN 18944, vocab 152064, bf16), batch 8, prompt 1024,
+      generation 512 in blocks of 64, candidate fraction 0.3, r = 6.0;
+    - multimodal prefix at the 8B shape (the headline model's packed weights,
+      shared): batch 32, 576 image-embedding positions N(0, 1) + 256 prompt
+      ids, generation 128 in blocks of 32, candidate fraction swept 0.1 / 0.3 /
+      0.5, r = 8.8 (the paper's MMaDA figure).
+    At 1024 and 2048 rows per step every projection is a compute-bound MFMA
+    GEMM; the report gives the GEMMs' achieved TFLOP/s (2 params rows per step
+    over their traced time) and the attention's, against the bf16 MFMA peak."""
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+
+    def run(eng, dims, b, B, prompt, gen, fracs, r_tok, ids, embeds, label):
+        V = dims.vocab
+        nblocks = gen // B
+        S_b = math.ceil(B / r_tok)
+        params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, 0)
+        dev = ids.device
+        t_out = torch.empty(b, B, dtype=torch.int32, device=dev)
+        s_out = torch.empty(b, B, dtype=torch.uint8, device=dev)
+        c_out = torch.empty(b, B, device=dev)
+        done = torch.empty(b, dtype=torch.int32, device=dev)
+        P_last = prompt + gen - B
+        log(f"[bench] {label}: prefill of {b} x {P_last}")
+        eng.dard_prefill(ids[:, :P_last].contiguous(), None if embeds is None else embeds[:, :P_last].contiguous())
+        torch.cuda.synchronize()
+        res = {"per_frac": []}
+        for frac in fracs:
+            ins = []
+            for t in range(steps + 1):
+                tok, state, conf = synth.workload_block(b, B, frac, V, seed=2000 + t)
+                ins.append(tuple(torch.from_numpy(a_).cuda() for a_ in (tok, state, conf)))
+            Ps = [prompt + B * (t % nblocks) for t in range(steps + 1)]
+
+            def step(t):
+                eng.dard_step(Ps[t], params, *ins[t], t_out, s_out, c_out, done)
+            step(steps)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for t in range(steps):
+                step(t)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            res["per_frac"].append({"cand_frac": frac, "ms_per_step": round(ms, 3), "steps_per_s": round(1e3 / ms, 2)})
+            if frac == fracs[len(fracs) // 2]:
+                dard.dard_trace_reset()
+                dard.dard_trace_enable((1 << dard.K_COUNT) - 1)
+                for t in range(steps):
+                    step(t)
+                torch.cuda.synchronize()
+                dard.dard_trace_enable(0)
+                names = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head", "attention"]
+                bd = {nm: dard.dard_trace_read(k)[1] / steps for k, nm in enumerate(names)}
+                dard.dard_trace_reset()
+                rows = b * 2 * B
+                qd, kd = dims.n_heads * dims.head_dim, dims.n_kv_heads * dims.head_dim
+                params_n = dims.n_layers * ((qd + 2 * kd) * dims.d_model + dims.d_model * qd +
+                                            3 * dims.ffn_dim * dims.d_model) + V * dims.d_model
+                gemm_ms = sum(bd[n] for n in names[:5])
+                P_avg = sum(Ps[:steps]) / steps
+                att_fl = 4 * dims.head_dim * dims.n_heads * rows * (P_avg + B) * dims.n_layers
+                res["breakdown_ms_per_step"] = {k_: round(v, 3) for k_, v in bd.items()}
+                res["gemm_tflops"] = round(2 * params_n * rows / (gemm_ms * 1e-3) / 1e12, 1)
+                res["gemm_mfma_frac"] = round(2 * params_n * rows / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
+                res["attention_tflops"] = round(att_fl / (bd["attention"] * 1e-3) / 1e12, 1)
+                res["attention_mfma_frac"] = round(att_fl / (bd["attention"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
+        # tokens committed / s over one generation (the middle candidate fraction's states)
+        frac = fracs[len(fracs) // 2]
+        ins = [tuple(torch.from_numpy(a_).cuda() for a_ in synth.workload_block(b, B, frac, V, seed=3000 + j))
+               for j in range(S_b)]
+        torch.cuda.synchronize()
+        g0 = time.perf_counter()
+        for k in range(nblocks):
+            P = prompt + B * k
+            eng.dard_prefill(ids[:, :P].contiguous(), None if embeds is None else embeds[:, :P].contiguous())
+            for j in range(S_b):
+                eng.dard_step(P, params, *ins[j], t_out, s_out, c_out, done)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - g0
+        res["tokens_committed_per_s"] = round(b * gen / el, 1)
+        res["tokens_committed_note"] = f"{nblocks} blocks x (prefill + {S_b} steps), {r_tok} tokens/step as reported"
+        return res
+
+    out = {}
+    # ---- 7B GQA shape
+    d7 = synth.DREAM7B
+    b, B, prompt, gen = 8, 64, 1024, 512
+    w = synth.make_weights(d7, seed=1, device="cuda")
+    eng7 = dard.Engine(d7, w, b, B, prompt + gen + B)
+    del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    ids = torch.from_numpy(synth.prompt_ids(b, prompt + gen - B, d7.vocab, seed=2)).cuda()
+    r7 = run(eng7, d7, b, B, prompt, gen, [0.3], 6.0, ids, None, "7B GQA")
+    out["dream7b_gqa"] = {"workload": "dream7b-like full DARD step: 28 layers, d 3584, 28/4 x 128 GQA, FFN 18944, "
+                                      "vocab 152064, bf16; batch 8, prompt 1024, generation 512, block 64, "
+                                      "candidate fraction 0.3, prefix KV cache", **r7}
+    del eng7, ids
+    torch.cuda.empty_cache()
+    # ---- multimodal prefix at the 8B shape (weights shared with the headline engine)
+    d8 = synth.LLADA8B
+    b, B, n_img, n_txt, gen = 32, 32, 576, 256, 128
+    prompt = n_img + n_txt
+    engm = dard.Engine(d8, None, b, B, prompt + gen + B, packed=eng8b.packed)
+    ids = torch.from_numpy(synth.prompt_ids(b, prompt + gen - B, d8.vocab, seed=5)).cuda()
+    ids[:, :n_img] = -1
+    g = torch.Generator(device="cuda").manual_seed(6)
+    embeds = torch.randn(b, prompt + gen - B, d8.d_model, generator=g, device="cuda").bfloat16()
+    rm = run(engm, d8, b, B, prompt, gen, [0.1, 0.3, 0.5], 8.8, ids, embeds, "multimodal")
+    out["multimodal_8b"] = {"workload": "llada8b-like full DARD step with a multimodal prefix: 576 image-embedding "
+                                        "positions N(0, 1) + 256 prompt ids; batch 32, generation 128, block 32, "
+                                        "candidate fraction 0.1 / 0.3 / 0.5, prefix KV cache", **rm}
+    del engm, ids, embeds
+    torch.cuda.empty_cache()
+    return out
 
 
 def op_measurements(reps=20):

@@ -215,7 +215,9 @@ class Engine:
     """Device state of one decoding job: packed weights, KV cache and
     workspace (torch allocations), plus calls of dard_prefill / dard_step."""
 
-    def __init__(self, dims, weights, b, B, cap, stream=None, device="cuda"):
+    def __init__(self, dims, weights, b, B, cap, stream=None, device="cuda", packed=None):
+        """weights: name -> tensor (packed here), or None with `packed` = the
+        packed image of another Engine of the same dims (shared, not copied)."""
         self.dims = dims
         self.cdims = make_dims(dims)
         self.b, self.B, self.cap = b, B, cap
@@ -223,11 +225,16 @@ class Engine:
         nbytes = L.dard_packed_weight_bytes(ctypes.byref(self.cdims))
         if nbytes == 0:
             raise DardError(-2, L.dard_last_error().decode())
-        self.packed = torch.empty(nbytes, dtype=torch.uint8, device=device)
-        names = [n for n in weights]
-        srcs = (ctypes.c_void_p * len(names))(*[_p(weights[n].contiguous()) for n in names])
-        _check(L.dard_pack_weights(ctypes.byref(self.cdims), srcs, len(names), _p(self.packed), nbytes,
-                                   _stream(stream)))
+        if packed is not None:
+            if packed.numel() < nbytes:
+                raise ValueError("packed image too small for these dims")
+            self.packed = packed
+        else:
+            self.packed = torch.empty(nbytes, dtype=torch.uint8, device=device)
+            names = [n for n in weights]
+            srcs = (ctypes.c_void_p * len(names))(*[_p(weights[n].contiguous()) for n in names])
+            _check(L.dard_pack_weights(ctypes.byref(self.cdims), srcs, len(names), _p(self.packed), nbytes,
+                                       _stream(stream)))
         kvb = L.dard_kv_bytes(ctypes.byref(self.cdims), b, cap)
         self.kv = torch.zeros(max(kvb, 16), dtype=torch.uint8, device=device)
         wsb = L.dard_workspace_bytes(ctypes.byref(self.cdims), b, B, cap)
