@@ -31,6 +31,11 @@ Parity pins (see ``tests/test_oracle_*.py``):
   * guidance_weights        -- closed forms of Eq. 5-6 (lambda^8 = 1/2, a
                                hand-computed worked example, P4 of the tests).
   * transition              -- exact inequalities of Eq. 8.
+  * ordering / mixing variants of Sec. 5.1 (F_C_BIDIR, F_ORDER_*, F_FIXED_W)
+                            -- equivalences with the primary mask (all keys
+                               tied; keys = -position), closed forms of entropy
+                               and margin, scipy's entropy, exact float32
+                               identities of Eq. 7 at w in {0, 1/2, 1}.
   * step_logits / prefill   -- special cases P1 (all-M block), P2 (empty C) and
                                P3 (one-layer independence from C tokens); the
                                full multi-layer logits beyond these cases are
@@ -50,6 +55,14 @@ F_XSELF_SHADOW = 1 << 0   # x-row of a U token does not see its own x key
 F_MKEYS_SHADOW = 1 << 1   # x-row of an M token sees M keys through s
 F_VERIFY_PCUR = 1 << 2    # C/U confidence = prob. of the current token
 F_PROGRESS = 1 << 3       # driver rule: every step of an unfinished block commits >= 1 token
+# Variants of the design-choice analysis (Sec. 5.1, mask-design and mixing
+# ablations).  At most one of the four ordering flags may be set.
+F_C_BIDIR = 1 << 4        # candidates see every candidate (no ordering)
+F_ORDER_L2R = 1 << 5      # candidates ordered by position, left first
+F_ORDER_ENTROPY = 1 << 6  # ... by entropy of the prediction, lowest first
+F_ORDER_MARGIN = 1 << 7   # ... by top-1 minus top-2 probability, largest first
+F_FIXED_W = 1 << 8        # every M token mixes with the constant w_fixed
+F_ORDERS = F_C_BIDIR | F_ORDER_L2R | F_ORDER_ENTROPY | F_ORDER_MARGIN
 
 LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # Sec. 4.1: lambda = 0.917, i.e. 0.5^(1/8)
 P0_DEFAULT = 0.1                      # Sec. 4.1: prior constant p_0
@@ -106,6 +119,10 @@ def take_x(state, conf, flags=0):
       C  -- sees U in x and, by Eq. 3, the C tokens j with c_i <= c_j in x
             (itself included); the shadow query drops its own x^i (Eq. 4
             conditions the k-th candidate on the k-1 more confident ones only).
+            Variants of Sec. 5.1: F_C_BIDIR takes every C token from x;
+            F_ORDER_L2R takes the C tokens j <= i (position order replaces
+            confidence order).  Entropy and margin orderings keep this rule
+            and change the key passed as ``conf`` (see ``order_key``).
       M  -- the x query sees C and U in x; M keys are taken from x as well
             (vanilla decoding of the x stream) unless F_MKEYS_SHADOW, which
             takes them from s except its own position.  The shadow query sees
@@ -126,7 +143,13 @@ def take_x(state, conf, flags=0):
                 if j == i and (shadow or (flags & F_XSELF_SHADOW)):
                     vis = False
             elif si == STATE_C:
-                vis = sj == STATE_U or (sj == STATE_C and conf[i] <= conf[j])
+                if flags & F_C_BIDIR:
+                    before = True
+                elif flags & F_ORDER_L2R:
+                    before = j <= i
+                else:
+                    before = conf[i] <= conf[j]
+                vis = sj == STATE_U or (sj == STATE_C and before)
                 if j == i and shadow:
                     vis = False
             elif si == STATE_M:
@@ -327,6 +350,34 @@ def confidence(row, cur_tok=None):
     return a, 1.0 / z, pc
 
 
+def entropy_margin(row):
+    """Entropy and margin of the distribution softmax(row), the scores of the
+    entropy and margin orderings of Sec. 5.1 (mask-design analysis):
+    H = -sum_v p_v ln p_v (natural log, 0 ln 0 = 0) and margin = p_(1) - p_(2),
+    the two largest probabilities (p_(2) = 0 for a one-entry row).  Both in
+    float64 from the given (float32) logits."""
+    row = np.asarray(row, dtype=np.float64)
+    e = np.exp(row - np.max(row))
+    p = e / np.sum(e)
+    nz = p > 0
+    H = -float(np.sum(p[nz] * np.log(p[nz])))
+    top = np.sort(p)[::-1]
+    second = top[1] if len(top) > 1 else 0.0
+    return H, float(top[0] - second)
+
+
+def order_key(c, H, margin, flags):
+    """The per-position key that Eq. 3 compares (larger = earlier in the
+    verification chain) under the ordering the flags select: the confidence c
+    (the paper's), -H (lowest entropy first) or the margin (largest first).
+    float32 value, the type the key is stored in."""
+    if flags & F_ORDER_ENTROPY:
+        return float(np.float32(-H))
+    if flags & F_ORDER_MARGIN:
+        return float(np.float32(margin))
+    return float(np.float32(c))
+
+
 def mix_logits(lx, ls, w):
     """Eq. 7: w * logit(x) + (1 - w) * logit(s), evaluated in float32 as
     (w * lx) + ((1 - w) * ls), each operation rounded once."""
@@ -381,6 +432,9 @@ def verify_candidates(state, c, params):
             promoted[i] = nxt[i] == STATE_U
             demoted[i] = nxt[i] == STATE_M
     _, _, w = guidance_weights(promoted, demoted, params["lam"], params["p0"])
+    if params.get("flags", 0) & F_FIXED_W:
+        # mixing ablation of Sec. 5.1: one constant weight replaces Eq. 5-6
+        w = np.full(B, float(params["w_fixed"]))
     w = np.where(np.asarray(state) == STATE_M, w, 0.0).astype(np.float32).astype(np.float64)
     return nxt, promoted, demoted, w
 
@@ -410,7 +464,10 @@ def decide(logits, tok, state, params):
     """The decision part of one loop iteration of Alg. 1 for every sequence.
 
     logits: [b, 2B, V] float32 values (x rows then s rows).
-    params: dict with tau_c, tau_u, lam, p0, mask_id, flags.
+    params: dict with tau_c, tau_u, lam, p0, mask_id, flags (and w_fixed
+    with F_FIXED_W).  conf_out is the key the next step's mask orders the
+    candidates by: the confidence, or with F_ORDER_ENTROPY / F_ORDER_MARGIN
+    the negated entropy / the margin of the same row.
     Returns a dict of per-position arrays: tok_out, state_out, conf_out,
     block_done, w, and the intermediate argmax / confidences.
     """
@@ -420,13 +477,14 @@ def decide(logits, tok, state, params):
     b, B = tok.shape
     flags = params.get("flags", 0)
     out = {k: np.zeros((b, B), dtype=np.float64) for k in
-           ("w", "conf_out", "maxprob_s", "pcur_s", "maxprob_mix")}
+           ("w", "conf_out", "maxprob_s", "pcur_s", "maxprob_mix", "entropy", "margin")}
     out.update({k: np.zeros((b, B), dtype=np.int64) for k in
                 ("tok_out", "state_out", "argmax_s", "argmax_mix")})
     out["block_done"] = np.zeros(b, dtype=np.int64)
     for bi in range(b):
         xhat = np.zeros(B, dtype=np.int64)
         c = np.zeros(B)
+        key = np.zeros(B)
         # confidences of C and U tokens from the shadow stream
         for i in range(B):
             a, mp, pc = confidence(logits[bi, B + i], int(tok[bi, i]))
@@ -436,6 +494,12 @@ def decide(logits, tok, state, params):
             if state[bi, i] in (STATE_C, STATE_U):
                 xhat[i] = a
                 c[i] = np.float32(pc if flags & F_VERIFY_PCUR else mp)
+                if flags & (F_ORDER_ENTROPY | F_ORDER_MARGIN):
+                    H, mg = entropy_margin(logits[bi, B + i])
+                    out["entropy"][bi, i], out["margin"][bi, i] = np.float32(H), np.float32(mg)
+                    key[i] = order_key(c[i], H, mg, flags)
+                else:
+                    key[i] = c[i]
         # update the C tokens; promoted / demoted sets; weights of M tokens
         _, _, _, w = verify_candidates(state[bi], c, params)
         out["w"][bi] = w
@@ -448,11 +512,19 @@ def decide(logits, tok, state, params):
                 out["maxprob_mix"][bi, i] = np.float32(mp)
                 xhat[i] = a
                 c[i] = np.float32(mp)
+                if flags & (F_ORDER_ENTROPY | F_ORDER_MARGIN):
+                    H, mg = entropy_margin(mixed)
+                    out["entropy"][bi, i], out["margin"][bi, i] = np.float32(H), np.float32(mg)
+                    key[i] = order_key(c[i], H, mg, flags)
+                else:
+                    key[i] = c[i]
         # transitions of all tokens (C ones repeat the rule above) and fill
         st, tk, cf, done = finalize(c, xhat, params, state[bi])
         out["state_out"][bi] = st
         out["tok_out"][bi] = tk
-        out["conf_out"][bi] = cf
+        # the key the next step's mask orders candidates by (Eq. 3): the
+        # confidence itself unless an entropy or margin ordering is selected
+        out["conf_out"][bi] = key
         out["block_done"][bi] = done
     return out
 

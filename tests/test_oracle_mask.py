@@ -65,7 +65,14 @@ def brute_force_mask(state, conf, P, flags=0):
             elif state[i] == O.STATE_C:
                 # C queries: U keys and more confident C keys in x (Eq. 3);
                 # everything else (M and less confident C) from s.
-                higher = {j for j in C if conf[i] <= conf[j]}
+                if flags & O.F_C_BIDIR:
+                    # Sec. 5.1 bidirectional variant: every candidate in x
+                    higher = set(C)
+                elif flags & O.F_ORDER_L2R:
+                    # Sec. 5.1 left-to-right variant: candidates to the left
+                    higher = {j for j in C if j <= i}
+                else:
+                    higher = {j for j in C if conf[i] <= conf[j]}
                 xs = U | higher
                 ss = M | (C - higher)
                 if stream == "s":
@@ -100,7 +107,11 @@ def _random_block(rng, B, ties=False):
 @settings(max_examples=60, deadline=None)
 @given(B=st.integers(1, 40), P=st.integers(0, 5), seed=st.integers(0, 10**6),
        flags=st.sampled_from([0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW,
-                              O.F_XSELF_SHADOW | O.F_MKEYS_SHADOW]),
+                              O.F_XSELF_SHADOW | O.F_MKEYS_SHADOW,
+                              O.F_C_BIDIR, O.F_ORDER_L2R,
+                              O.F_C_BIDIR | O.F_MKEYS_SHADOW,
+                              O.F_ORDER_L2R | O.F_XSELF_SHADOW,
+                              O.F_ORDER_ENTROPY, O.F_ORDER_MARGIN]),
        ties=st.booleans())
 def test_rule_table_equals_brute_force(B, P, seed, flags, ties):
     rng = np.random.default_rng(seed)
