@@ -70,15 +70,36 @@ typedef int dard_status;
  *                 unfinished block entered U in this step, the most confident
  *                 position that is not U after the transitions (ties: lowest
  *                 position) becomes U with its prediction, so a block of B
- *                 positions finishes within B steps. */
-#define DARD_F_XSELF_SHADOW (1u << 0)
-#define DARD_F_MKEYS_SHADOW (1u << 1)
-#define DARD_F_VERIFY_PCUR  (1u << 2)
-#define DARD_F_PROGRESS     (1u << 3)
-#define DARD_F_ALL          (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS)
+ *                 positions finishes within B steps.
+ * Variants of the design-choice analysis (Sec. 5.1, mask-design and
+ * logit-mixing ablations); at most one of the four ordering flags is allowed:
+ *   C_BIDIR       a candidate's queries see every candidate in x (no order;
+ *                 the shadow query still never sees its own x key);
+ *   ORDER_L2R     candidates ordered by position: candidate i sees the
+ *                 candidates j <= i in x (Eq. 3 with the key -j);
+ *   ORDER_ENTROPY candidates ordered by the entropy of their prediction,
+ *                 lowest first: the key carried to the next step (conf_out
+ *                 of dard_step) is -H, H = -sum_v p_v ln p_v;
+ *   ORDER_MARGIN  ordered by the margin p_(1) - p_(2) of the two largest
+ *                 probabilities, largest first: the carried key is the margin;
+ *   FIXED_W       every masked token mixes its logits with the constant
+ *                 params.w_fixed instead of the weight of Eq. 5-6. */
+#define DARD_F_XSELF_SHADOW   (1u << 0)
+#define DARD_F_MKEYS_SHADOW   (1u << 1)
+#define DARD_F_VERIFY_PCUR    (1u << 2)
+#define DARD_F_PROGRESS       (1u << 3)
+#define DARD_F_C_BIDIR        (1u << 4)
+#define DARD_F_ORDER_L2R      (1u << 5)
+#define DARD_F_ORDER_ENTROPY  (1u << 6)
+#define DARD_F_ORDER_MARGIN   (1u << 7)
+#define DARD_F_FIXED_W        (1u << 8)
+#define DARD_F_ORDERS (DARD_F_C_BIDIR | DARD_F_ORDER_L2R | DARD_F_ORDER_ENTROPY | DARD_F_ORDER_MARGIN)
+#define DARD_F_ALL    (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS | \
+                       DARD_F_ORDERS | DARD_F_FIXED_W)
 
 /* Decoding hyper-parameters (Alg. 1 inputs; Sec. 4.1 uses lambda = 0.5^(1/8),
- * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0. */
+ * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0,
+ * and 0 <= w_fixed <= 1 when DARD_F_FIXED_W is set. */
 typedef struct {
     float tau_c;      /* c <= tau_c -> M                                   */
     float tau_u;      /* tau_c < c <= tau_u -> C, tau_u < c -> U (Eq. 8)    */
@@ -86,6 +107,7 @@ typedef struct {
     double p0;        /* prior constant of the guidance weight (Eq. 6)     */
     int32_t mask_id;  /* token id of [Mask]                                */
     uint32_t flags;   /* DARD_F_* bits                                     */
+    float w_fixed;    /* mixing weight of every M token with FIXED_W       */
 } dard_params;
 
 /* Transformer shape.  Pre-norm blocks: RMSNorm (norm_eps), rotary position
@@ -113,7 +135,9 @@ int dard_version(void);
  * Rows r < B are the x queries of position r, rows B..2B-1 the s queries of
  * position r-B.  The prefix is always visible and not encoded.
  *   state [b][B] uint8, conf [b][B] float32 (c_{t-1}, the ordering key of
- *   Eq. 3), sel [b][2B][W] uint64. */
+ *   Eq. 3; not read by C_BIDIR and ORDER_L2R), sel [b][2B][W] uint64.
+ * flags: the mask reads XSELF_SHADOW, MKEYS_SHADOW, C_BIDIR and ORDER_L2R;
+ * the other bits are accepted and ignored. */
 dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
                                   uint32_t flags, uint64_t* sel, void* stream);
 
@@ -154,12 +178,18 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
  *   maxprob[r] = 1 / sum_v exp(l_v - l_max)              (top-1 probability)
  *   pcur[r]    = exp(l_cur - l_max) * maxprob[r], l_cur = l at cur_tok[r]
  *                (only if pcur != NULL; needs cur_tok, no mixing)
+ *   entropy[r] = -sum_v p_v ln p_v of p = softmax(l)   (only if != NULL)
+ *   margin[r]  = p_(1) - p_(2), the two largest probabilities, 0 on a tie
+ *                at the top, p_(1) when V = 1          (only if != NULL)
+ *   (the scores of the entropy and margin orderings of Sec. 5.1; either
+ *   output being non-NULL selects the slightly longer pass that forms both)
  * logits_* rows have leading dimension ld >= V (elements, multiple of 4).
- * Outputs: argmax int32 [rows], maxprob float32 [rows], pcur float32 [rows]. */
+ * Outputs: argmax int32 [rows]; maxprob, pcur, entropy, margin float32 [rows]. */
 size_t dard_confidence_workspace_bytes(int rows, int V);
 dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w,
                             const int32_t* cur_tok, int rows, int V, int64_t ld,
                             int32_t* argmax, float* maxprob, float* pcur,
+                            float* entropy, float* margin,
                             void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------ a6/a8: decisions
@@ -168,13 +198,17 @@ dard_status dard_confidence(const float* logits_s, const float* logits_x, const 
  *   for C positions, the transition of Eq. 8 on c (maxprob_s, or pcur_s with
  *   VERIFY_PCUR) gives the promoted set P_t (-> U) and demoted set D_t (-> M);
  *   for every M position i:  P^i = sum_{j in P_t} lambda^|i-j|,
- *   D^i likewise (Eq. 5), w_out[i] = (P^i + p0) / (P^i + D^i + p0) (Eq. 6);
- *   w_out = 0 at C and U positions.  Reads state_in, maxprob_s / pcur_s.
+ *   D^i likewise (Eq. 5), w_out[i] = (P^i + p0) / (P^i + D^i + p0) (Eq. 6),
+ *   or params.w_fixed with FIXED_W; w_out = 0 at C and U positions.  Reads
+ *   state_in, maxprob_s / pcur_s.
  * phase DARD_PHASE_FINAL (after the mixed confidences of the M positions):
  *   c_i = maxprob_s (or pcur_s) for C/U positions, maxprob_mix for M;
  *   prediction x_i = argmax_s for C/U, argmax_mix for M;
  *   state_out by Eq. 8; tok_out = mask_id for next-M, x_i otherwise;
- *   conf_out = c_i; block_done[s] = 1 iff every position is next-U.
+ *   conf_out = the ordering key of the next step: c_i, or with ORDER_ENTROPY
+ *   / ORDER_MARGIN key_s[i] (C/U) / key_mix[i] (M), the -entropy or margin
+ *   the caller formed with dard_confidence from the same rows as c_i;
+ *   block_done[s] = 1 iff every position is next-U.
  * All per-position arrays are [b][B]; block_done is [b] int32.  Arrays not
  * read or written by a phase may be NULL. */
 #define DARD_PHASE_VERIFY 0
@@ -183,6 +217,7 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
                                const uint8_t* state_in, const float* maxprob_s,
                                const float* pcur_s, const int32_t* argmax_s,
                                const float* maxprob_mix, const int32_t* argmax_mix,
+                               const float* key_s, const float* key_mix,
                                float* w_out, uint8_t* state_out, int32_t* tok_out,
                                float* conf_out, int32_t* block_done, void* stream);
 
@@ -231,7 +266,8 @@ dard_status dard_prefill(const dard_dims* dims, const void* packed, void* kv, in
  *   candidates, mix the two logit rows of every M token with its guidance
  *   weight, apply the transitions and fill the tokens.
  *   tok_in/tok_out [b][B] int32, state_in/state_out [b][B] uint8,
- *   conf_in/conf_out [b][B] float32, block_done [b] int32.
+ *   conf_in/conf_out [b][B] float32 (the ordering key: c_i, or -entropy /
+ *   margin under ORDER_ENTROPY / ORDER_MARGIN), block_done [b] int32.
  * Outputs may alias the matching inputs.  `dbg`, when not NULL, receives
  * copies of intermediate results (any member may be NULL). */
 typedef struct {
@@ -242,6 +278,8 @@ typedef struct {
     float* pcur_s;       /* [b][B] shadow prob. of the current token (C/U)  */
     float* maxprob_mix;  /* [b][B] mixed top-1 prob. (M positions)          */
     int32_t* argmax_mix; /* [b][B]                                          */
+    float* entropy;      /* [b][B] entropy of the row that gave c_i, and    */
+    float* margin;       /* [b][B] its margin (ORDER_ENTROPY/MARGIN only)   */
 } dard_step_debug;
 
 dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int cap, int P,

@@ -116,8 +116,8 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.part = o; o = align256(o + W.part_slots * d->head_dim * 4);
     W.part_ml = o; o = align256(o + W.part_slots * 2 * 4);
     W.logits = o; o = align256(o + step_rows * d->vocab * 4);
-    W.cpart_v = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
-    W.cpart_m = o; o = align256(o + (size_t)b * B * nch * 3 * 4);
+    W.cpart_v = o; o = align256(o + (size_t)b * B * nch * kConfStatsStride * 4);
+    W.cpart_m = o; o = align256(o + (size_t)b * B * nch * kConfStatsStride * 4);
     W.w = o; o = align256(o + (size_t)b * B * 4);
     // split-K partials of the O and down projections: up to 8 splits of 64
     // rows (streaming GEMM) or 4 splits of all rows (pipelined GEMM)
@@ -127,15 +127,27 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     return W;
 }
 
+int check_flags(uint32_t flags) {
+    if (flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", flags);
+    const uint32_t o = flags & DARD_F_ORDERS;
+    if (o & (o - 1)) return fail(DARD_ERR_ARG, "more than one candidate-ordering flag (0x%x)", o);
+    return DARD_OK;
+}
+
 int check_params(const dard_params* p) {
     if (!p) return fail(DARD_ERR_ARG, "params is NULL");
     if (!(p->tau_c >= 0.f) || !(p->tau_c <= p->tau_u) || !(p->tau_u <= 1.f))
         return fail(DARD_ERR_ARG, "need 0 <= tau_c <= tau_u <= 1");
     if (!(p->lambda > 0.0) || !(p->lambda < 1.0)) return fail(DARD_ERR_ARG, "need 0 < lambda < 1");
     if (!(p->p0 > 0.0)) return fail(DARD_ERR_ARG, "need p0 > 0");
-    if (p->flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", p->flags);
+    if (int rc = check_flags(p->flags)) return rc;
+    if ((p->flags & DARD_F_FIXED_W) && !(p->w_fixed >= 0.f && p->w_fixed <= 1.f))
+        return fail(DARD_ERR_ARG, "need 0 <= w_fixed <= 1");
     return DARD_OK;
 }
+
+// Entropy or margin ordering: the confidence pass also forms their terms.
+bool needs_stats(uint32_t flags) { return (flags & (DARD_F_ORDER_ENTROPY | DARD_F_ORDER_MARGIN)) != 0; }
 
 // ---------------------------------------------------------------- tracing
 struct TraceRec {
@@ -183,7 +195,7 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
                                   uint64_t* sel, void* stream) {
     if (!state || !conf || !sel) return fail(DARD_ERR_ARG, "NULL pointer");
     if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
-    if (flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", flags);
+    if (int rc = check_flags(flags)) return rc;
     HIPOK(launch_build_state_mask(state, conf, b, B, flags, sel, (hipStream_t)stream));
     return DARD_OK;
 }
@@ -227,7 +239,7 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
                                   void* stream) {
     if (!q || !k || !v || !state || !conf || !out) return fail(DARD_ERR_ARG, "NULL pointer");
     if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
-    if (flags & ~DARD_F_ALL) return fail(DARD_ERR_ARG, "unknown flag bits 0x%x", flags);
+    if (int rc = check_flags(flags)) return rc;
     if (b < 1 || B < 1 || B > 128 || P < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || P + 2 * B > cap)
         return fail(DARD_ERR_SHAPE, "bad attention shape (b=%d B=%d P=%d cap=%d Hq=%d Hkv=%d)", b, B, P, cap, Hq, Hkv);
     if (dh != 64 && dh != 128) return fail(DARD_ERR_SHAPE, "dh must be 64 or 128");
@@ -256,12 +268,12 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
 // ---------------------------------------------------------------- confidence
 size_t dard_confidence_workspace_bytes(int rows, int V) {
     if (rows < 1 || V < 1) return 0;
-    return align256((size_t)rows * conf_chunks(V) * 3 * 4);
+    return align256((size_t)rows * conf_chunks(V) * kConfStatsStride * 4);
 }
 
 dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w, const int32_t* cur_tok,
-                            int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur, void* ws,
-                            size_t ws_bytes, void* stream) {
+                            int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur,
+                            float* entropy, float* margin, void* ws, size_t ws_bytes, void* stream) {
     if (!logits_s || !argmax || !maxprob) return fail(DARD_ERR_ARG, "NULL pointer");
     if (logits_x && !w) return fail(DARD_ERR_ARG, "mixing needs w");
     if (pcur && (!cur_tok || logits_x)) return fail(DARD_ERR_ARG, "pcur needs cur_tok and no mixing");
@@ -272,17 +284,18 @@ dard_status dard_confidence(const float* logits_s, const float* logits_x, const 
     a.ls = logits_s; a.lx = logits_x; a.w = w; a.ld_s = ld; a.ld_x = ld;
     a.rows = rows; a.V = V; a.part = (float*)ws; a.state = nullptr; a.phase = 0; a.step_B = 0;
     hipStream_t s = (hipStream_t)stream;
-    HIPOK(launch_conf_partial(a, s));
-    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), logits_s, ld, cur_tok, argmax, maxprob, pcur, s));
+    HIPOK(launch_conf_partial(a, entropy || margin, s));
+    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), logits_s, ld, cur_tok, argmax, maxprob, pcur,
+                              entropy, margin, s));
     return DARD_OK;
 }
 
 // ---------------------------------------------------------------- decisions
 dard_status dard_commit_remask(int phase, const dard_params* params, int b, int B, const uint8_t* state_in,
                                const float* maxprob_s, const float* pcur_s, const int32_t* argmax_s,
-                               const float* maxprob_mix, const int32_t* argmax_mix, float* w_out,
-                               uint8_t* state_out, int32_t* tok_out, float* conf_out, int32_t* block_done,
-                               void* stream) {
+                               const float* maxprob_mix, const int32_t* argmax_mix, const float* key_s,
+                               const float* key_mix, float* w_out, uint8_t* state_out, int32_t* tok_out,
+                               float* conf_out, int32_t* block_done, void* stream) {
     int rc = check_params(params);
     if (rc) return rc;
     if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
@@ -294,16 +307,19 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
         if (!maxprob_s || !argmax_s || !maxprob_mix || !argmax_mix || !state_out || !tok_out || !conf_out ||
             (pcur_mode && !pcur_s))
             return fail(DARD_ERR_ARG, "FINAL needs confidences, predictions and outputs");
+        if (needs_stats(params->flags) && (!key_s || !key_mix))
+            return fail(DARD_ERR_ARG, "entropy / margin ordering needs key_s and key_mix");
     } else {
         return fail(DARD_ERR_ARG, "unknown phase %d", phase);
     }
     DecideArgs a{};
     a.phase = phase; a.b = b; a.B = B;
     a.tau_c = params->tau_c; a.tau_u = params->tau_u; a.lambda = params->lambda; a.p0 = params->p0;
-    a.mask_id = params->mask_id; a.flags = params->flags;
+    a.mask_id = params->mask_id; a.flags = params->flags; a.w_fixed = params->w_fixed;
     a.state_in = state_in;
     a.maxprob_s = maxprob_s; a.pcur_s = pcur_s; a.argmax_s = argmax_s;
     a.maxprob_mix = maxprob_mix; a.argmax_mix = argmax_mix;
+    a.key_s = key_s; a.key_mix = key_mix; a.stride = kConfStride;
     a.w_out = w_out; a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out;
     a.block_done = block_done;
     HIPOK(launch_decide(a, (hipStream_t)stream));
@@ -535,12 +551,13 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     ConfArgs c{};
     c.ls = logits; c.ld_s = V; c.ld_x = V; c.rows = b * B; c.V = V; c.state = state_in; c.step_B = B;
     c.phase = 0; c.part = (float*)(f.ws + f.W.cpart_v);
-    HIPOK(launch_conf_partial(c, f.s));
+    const bool stats = needs_stats(params->flags);
+    HIPOK(launch_conf_partial(c, stats, f.s));
 
     DecideArgs a{};
     a.b = b; a.B = B; a.tau_c = params->tau_c; a.tau_u = params->tau_u; a.lambda = params->lambda;
-    a.p0 = params->p0; a.mask_id = params->mask_id; a.flags = params->flags;
-    a.state_in = state_in; a.tok_in = tok_in;
+    a.p0 = params->p0; a.mask_id = params->mask_id; a.flags = params->flags; a.w_fixed = params->w_fixed;
+    a.state_in = state_in; a.tok_in = tok_in; a.stride = stats ? kConfStatsStride : kConfStride;
     a.part_v = (const float*)(f.ws + f.W.cpart_v); a.part_m = (const float*)(f.ws + f.W.cpart_m);
     a.logits = logits; a.ld = V; a.nchunk = conf_chunks(V);
     a.w_out = (float*)(f.ws + f.W.w);
@@ -548,13 +565,14 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     HIPOK(launch_decide(a, f.s));
 
     c.phase = 1; c.w = (const float*)(f.ws + f.W.w); c.part = (float*)(f.ws + f.W.cpart_m);
-    HIPOK(launch_conf_partial(c, f.s));
+    HIPOK(launch_conf_partial(c, stats, f.s));
 
     a.phase = DARD_PHASE_FINAL;
     a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out; a.block_done = block_done;
     if (dbg) {
         a.dbg_maxprob_s = dbg->maxprob_s; a.dbg_argmax_s = dbg->argmax_s; a.dbg_pcur_s = dbg->pcur_s;
         a.dbg_maxprob_mix = dbg->maxprob_mix; a.dbg_argmax_mix = dbg->argmax_mix;
+        if (stats) { a.dbg_entropy = dbg->entropy; a.dbg_margin = dbg->margin; }
     }
     HIPOK(launch_decide(a, f.s));
     if (dbg && dbg->logits)

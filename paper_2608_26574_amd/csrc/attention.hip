@@ -486,7 +486,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
         if (a.masked && key >= a.P) {
             const int j = key - a.P;
             const int jj = j < a.B ? j : j - a.B;
-            const bool bx = take_x(st[i], st[jj], cf[i], cf[jj], shadow, i == jj, a.flags);
+            const bool bx = take_x(st[i], st[jj], cf[i], cf[jj], i, jj, shadow, a.flags);
             if (bx != (j < a.B)) continue;
         }
         float sdot = 0.f;

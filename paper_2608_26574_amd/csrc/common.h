@@ -86,15 +86,19 @@ __device__ __forceinline__ float wave_sum(float v) {
 // themselves (Eq. 3) from x; the shadow query of any position never reads its
 // own x key.  The x query of an M token reads the whole x block (or, with
 // MKEYS_SHADOW, C, U and itself from x), its shadow query only U from x.
-__device__ __forceinline__ bool take_x(int si, int sj, float ci, float cj, bool shadow,
-                                       bool self, uint32_t flags) {
+// Sec. 5.1 variants of the candidate order: C_BIDIR (every candidate),
+// ORDER_L2R (the candidates j <= i).
+__device__ __forceinline__ bool take_x(int si, int sj, float ci, float cj, int i, int j, bool shadow,
+                                       uint32_t flags) {
+    const bool self = i == j;
     if (si == DARD_STATE_U) {
         if (self && (shadow || (flags & DARD_F_XSELF_SHADOW))) return false;
         return sj == DARD_STATE_U;
     }
     if (si == DARD_STATE_C) {
         if (self && shadow) return false;
-        return sj == DARD_STATE_U || (sj == DARD_STATE_C && ci <= cj);
+        const bool before = (flags & DARD_F_C_BIDIR) ? true : (flags & DARD_F_ORDER_L2R) ? j <= i : ci <= cj;
+        return sj == DARD_STATE_U || (sj == DARD_STATE_C && before);
     }
     if (shadow) return sj == DARD_STATE_U;
     if (flags & DARD_F_MKEYS_SHADOW) return sj == DARD_STATE_C || sj == DARD_STATE_U || self;
@@ -142,8 +146,17 @@ __device__ __forceinline__ void row_take_x(const BlockView& v, int r, int B, uin
         x0 = v.U0; x1 = v.U1;
         if (shadow || (flags & DARD_F_XSELF_SHADOW)) { x0 &= ~self0; x1 &= ~self1; }
     } else if (si == DARD_STATE_C) {
-        x0 = v.U0 | __ballot(v.s0 == DARD_STATE_C && ci <= v.c0);
-        x1 = v.U1 | __ballot(v.s1 == DARD_STATE_C && ci <= v.c1);
+        if (flags & DARD_F_C_BIDIR) {
+            x0 = v.U0 | v.C0; x1 = v.U1 | v.C1;
+        } else if (flags & DARD_F_ORDER_L2R) {
+            // positions 0..i: words below i's word whole, i's word up to bit i
+            const uint64_t upto0 = i < 64 ? (i == 63 ? ~0ull : (2ull << i) - 1) : ~0ull;
+            const uint64_t upto1 = i < 64 ? 0ull : (i == 127 ? ~0ull : (2ull << (i - 64)) - 1);
+            x0 = v.U0 | (v.C0 & upto0); x1 = v.U1 | (v.C1 & upto1);
+        } else {
+            x0 = v.U0 | __ballot(v.s0 == DARD_STATE_C && ci <= v.c0);
+            x1 = v.U1 | __ballot(v.s1 == DARD_STATE_C && ci <= v.c1);
+        }
         if (shadow) { x0 &= ~self0; x1 &= ~self1; }
     } else if (shadow) {
         x0 = v.U0; x1 = v.U1;

@@ -6,6 +6,12 @@
 // rows fill the chip.  Partials are merged in chunk order, which keeps the
 // result independent of scheduling.  Mixed rows are formed on the fly,
 // (w * l_x) + ((1 - w) * l_s) with every operation rounded once in fp32.
+//
+// The statistics variant (entropy and margin orderings of Sec. 5.1) carries
+// two more terms in the same pass: t = sum exp(l - max) (l - max), so that
+// the entropy is ln(s) - t / s, and the second-largest logit m2, so that the
+// margin p_(1) - p_(2) is (1 - exp(m2 - max)) / s.  Moving a partial to a
+// larger maximum M scales s and t by e = exp(m - M) and adds (m - M) s e to t.
 #include "common.h"
 #include "launch.h"
 
@@ -20,24 +26,41 @@ struct Acc {
     float m;
     int a;
     float s;
+    float t, m2;   // statistics variant only
 };
 
 // Merge two partials; the larger maximum wins, ties go to the lower index.
+template <bool STATS>
 __device__ __forceinline__ Acc merge(Acc x, Acc y) {
     Acc r;
     const bool take_y = (y.m > x.m) || (y.m == x.m && y.a < x.a);
     r.a = take_y ? y.a : x.a;
     r.m = fmaxf(x.m, y.m);
-    const float sx = x.m == -INFINITY ? 0.f : x.s * exp2f((x.m - r.m) * kLog2e);
-    const float sy = y.m == -INFINITY ? 0.f : y.s * exp2f((y.m - r.m) * kLog2e);
-    r.s = sx + sy;
+    const float ex = x.m == -INFINITY ? 0.f : exp2f((x.m - r.m) * kLog2e);
+    const float ey = y.m == -INFINITY ? 0.f : exp2f((y.m - r.m) * kLog2e);
+    r.s = x.s * ex + y.s * ey;
+    if (STATS) {
+        const float tx = x.m == -INFINITY ? 0.f : ex * (x.t + (x.m - r.m) * x.s);
+        const float ty = y.m == -INFINITY ? 0.f : ey * (y.t + (y.m - r.m) * y.s);
+        r.t = tx + ty;
+        r.m2 = fmaxf(fminf(x.m, y.m), fmaxf(x.m2, y.m2));
+    } else {
+        r.t = 0.f;
+        r.m2 = -INFINITY;
+    }
     return r;
 }
 
+// (w * x) + (omw * s) with both products and the sum rounded separately: no
+// fused multiply-add may merge a product into the sum.
 __device__ __forceinline__ float mixv(float x, float s, float w, float omw) {
-    return __fadd_rn(__fmul_rn(w, x), __fmul_rn(omw, s));
+#pragma clang fp contract(off)
+    const float a = w * x;
+    const float b = omw * s;
+    return a + b;
 }
 
+template <bool STATS>
 __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_B) {
     const int row = blockIdx.x, ch = blockIdx.y;
     const float* ls;
@@ -110,26 +133,41 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
         }
     }
     // pass 1: the thread's maximum and its first index (indices increase with it, then k)
-    Acc acc{-INFINITY, 0x7fffffff, 0.f};
+    Acc acc{-INFINITY, 0x7fffffff, 0.f, 0.f, -INFINITY};
 #pragma unroll
     for (int it = 0; it < kIt; ++it)
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < 4; ++k) {
+            if (STATS) acc.m2 = fmaxf(acc.m2, fminf(acc.m, v[it][k]));
             if (v[it][k] > acc.m) { acc.m = v[it][k]; acc.a = begin + 4 * threadIdx.x + 4 * 256 * it + k; }
+        }
     // pass 2: sum of exp(l - max); arguments are <= 0, so the hardware exp2
-    // (v_exp_f32) needs no range handling, and exp2(-inf) = 0
+    // (v_exp_f32) needs no range handling, and exp2(-inf) = 0.  One fma per
+    // element forms l log2(e) - mb with mb = max log2(e) rounded to fp32; the
+    // rounding error r = max log2(e) - mb (exact through an fma) is common to
+    // every term, so the sums are scaled by 2^-r once at the end.  Without that
+    // step large logits (|l| ~ 100) would bias s by up to ~1e-5 relative.
     if (acc.m != -INFINITY) {
         const float mb = acc.m * kLog2e;
 #pragma unroll
         for (int it = 0; it < kIt; ++it)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) acc.s += __builtin_amdgcn_exp2f(fmaf(v[it][k], kLog2e, -mb));
+            for (int k = 0; k < 4; ++k) {
+                const float e = __builtin_amdgcn_exp2f(fmaf(v[it][k], kLog2e, -mb));
+                acc.s += e;
+                // -inf past the end of the row: e = 0 and the clamp keeps 0 * d finite
+                if (STATS) acc.t = fmaf(e, fmaxf(v[it][k] - acc.m, -3.0e38f), acc.t);
+            }
+        const float fix = exp2f(-fmaf(acc.m, kLog2e, -mb));
+        acc.s *= fix;
+        if (STATS) acc.t *= fix;
     }
     // wave reduction then across the 4 waves, fixed order
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-        Acc y{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.a, o, 64), __shfl_xor(acc.s, o, 64)};
-        acc = merge(acc, y);
+        Acc y{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.a, o, 64), __shfl_xor(acc.s, o, 64), 0.f, -INFINITY};
+        if (STATS) { y.t = __shfl_xor(acc.t, o, 64); y.m2 = __shfl_xor(acc.m2, o, 64); }
+        acc = merge<STATS>(acc, y);
     }
     __shared__ Acc red[4];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -137,28 +175,41 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
     __syncthreads();
     if (threadIdx.x == 0) {
         Acc t = red[0];
-        for (int k = 1; k < 4; ++k) t = merge(t, red[k]);
-        float* p = a.part + ((size_t)row * a.nchunk + ch) * 3;
+        for (int k = 1; k < 4; ++k) t = merge<STATS>(t, red[k]);
+        constexpr int kStride = STATS ? kConfStatsStride : kConfStride;
+        float* p = a.part + ((size_t)row * a.nchunk + ch) * kStride;
         p[0] = t.m;
         p[1] = __int_as_float(t.a);
         p[2] = t.s;
+        if (STATS) { p[3] = t.t; p[4] = t.m2; }
     }
 }
 
+template <bool STATS>
 __global__ void conf_combine_kernel(const float* __restrict__ part, int rows, int nchunk,
                                     const float* __restrict__ ls, int64_t ld, const int32_t* __restrict__ cur,
                                     int32_t* __restrict__ argmax, float* __restrict__ maxprob,
-                                    float* __restrict__ pcur) {
+                                    float* __restrict__ pcur, float* __restrict__ entropy,
+                                    float* __restrict__ margin) {
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= rows) return;
-    const float* p = part + (size_t)r * nchunk * 3;
-    Acc t{p[0], __float_as_int(p[1]), p[2]};
-    for (int c = 1; c < nchunk; ++c) t = merge(t, Acc{p[3 * c], __float_as_int(p[3 * c + 1]), p[3 * c + 2]});
+    constexpr int K = STATS ? kConfStatsStride : kConfStride;
+    const float* p = part + (size_t)r * nchunk * K;
+    auto at = [&](int c) {
+        const float* q = p + (size_t)c * K;
+        return Acc{q[0], __float_as_int(q[1]), q[2], STATS ? q[3] : 0.f, STATS ? q[4] : -INFINITY};
+    };
+    Acc t = at(0);
+    for (int c = 1; c < nchunk; ++c) t = merge<STATS>(t, at(c));
     argmax[r] = t.a;
     maxprob[r] = 1.f / t.s;
     if (pcur) {
         const float lc = ls[(size_t)r * ld + cur[r]];
         pcur[r] = exp2f((lc - t.m) * kLog2e) / t.s;
+    }
+    if (STATS) {
+        if (entropy) entropy[r] = logf(t.s) - t.t / t.s;
+        if (margin) margin[r] = (1.f - expf(t.m2 - t.m)) / t.s;
     }
 }
 
@@ -166,22 +217,30 @@ __global__ void conf_combine_kernel(const float* __restrict__ part, int rows, in
 
 int conf_chunks(int V) { return (V + kChunk - 1) / kChunk; }
 
-hipError_t launch_conf_partial(const ConfArgs& a, hipStream_t s) {
+hipError_t launch_conf_partial(const ConfArgs& a, bool stats, hipStream_t s) {
     TraceScope ts(DARD_K_CONFIDENCE, s);
     ConfArgs b = a;
     b.chunk = kChunk;
     b.nchunk = conf_chunks(a.V);
     const int step_B = a.step_B;
-    launch(conf_partial_kernel, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
+    if (stats)
+        launch(conf_partial_kernel<true>, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
+    else
+        launch(conf_partial_kernel<false>, dim3(a.rows, b.nchunk), dim3(256), 0, s, b, step_B);
     return hipGetLastError();
 }
 
 hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls, int64_t ld,
                                const int32_t* cur_tok, int32_t* argmax, float* maxprob, float* pcur,
-                               hipStream_t s) {
+                               float* entropy, float* margin, hipStream_t s) {
     TraceScope ts(DARD_K_CONFIDENCE, s);
-    launch(conf_combine_kernel, dim3((rows + 127) / 128), dim3(128), 0, s, part, rows, nchunk, ls,
-                       ld, cur_tok, argmax, maxprob, pcur);
+    const dim3 g((rows + 127) / 128), blk(128);
+    if (entropy || margin)
+        launch(conf_combine_kernel<true>, g, blk, 0, s, part, rows, nchunk, ls, ld, cur_tok, argmax, maxprob,
+               pcur, entropy, margin);
+    else
+        launch(conf_combine_kernel<false>, g, blk, 0, s, part, rows, nchunk, ls, ld, cur_tok, argmax, maxprob,
+               pcur, entropy, margin);
     return hipGetLastError();
 }
 

@@ -5,6 +5,11 @@
 // in float64 in position order from a table of lambda^k.  In step mode the
 // vocab-chunk partials of the confidence reduction are first copied to LDS
 // in one coalesced pass and merged there in chunk order.
+//
+// Sec. 5.1 variants: with a fixed weight every M position takes w_fixed
+// instead of Eq. 5-6; with the entropy or margin ordering the key carried to
+// the next step's mask (conf_out) is -entropy or the margin of the row that
+// gave the confidence, from the statistics partials (chunk stride 5).
 #include "common.h"
 #include "launch.h"
 
@@ -24,24 +29,36 @@ struct Red {
     float m;
     int a;
     float s;
+    float t, m2;   // statistics partials only: sum e (l - max), second-largest l
 };
 
-// Merge the chunk partials of one row in chunk order.
-__device__ Red combine(const float* p, int nchunk) {
-    Red t{p[0], __float_as_int(p[1]), p[2]};
+// Merge the chunk partials of one row (stride K floats each) in chunk order.
+__device__ Red combine(const float* p, int nchunk, int K) {
+    const bool stats = K == kConfStatsStride;
+    Red t{p[0], __float_as_int(p[1]), p[2], stats ? p[3] : 0.f, stats ? p[4] : -INFINITY};
     for (int c = 1; c < nchunk; ++c) {
-        const float m2 = p[3 * c], s2 = p[3 * c + 2];
-        const int a2 = __float_as_int(p[3 * c + 1]);
+        const float* q = p + (size_t)c * K;
+        const float m2 = q[0], s2 = q[2];
+        const int a2 = __float_as_int(q[1]);
         const float mm = fmaxf(t.m, m2);
         const bool take = (m2 > t.m) || (m2 == t.m && a2 < t.a);
-        const float s1 = t.m == -INFINITY ? 0.f : t.s * exp2f((t.m - mm) * kLog2e);
-        const float s2s = m2 == -INFINITY ? 0.f : s2 * exp2f((m2 - mm) * kLog2e);
+        const float e1 = t.m == -INFINITY ? 0.f : exp2f((t.m - mm) * kLog2e);
+        const float e2 = m2 == -INFINITY ? 0.f : exp2f((m2 - mm) * kLog2e);
+        if (stats) {
+            const float t1 = t.m == -INFINITY ? 0.f : e1 * (t.t + (t.m - mm) * t.s);
+            const float t2 = m2 == -INFINITY ? 0.f : e2 * (q[3] + (m2 - mm) * s2);
+            t.t = t1 + t2;
+            t.m2 = fmaxf(fminf(t.m, m2), fmaxf(t.m2, q[4]));
+        }
         t.a = take ? a2 : t.a;
+        t.s = t.s * e1 + s2 * e2;
         t.m = mm;
-        t.s = s1 + s2s;
     }
     return t;
 }
+
+__device__ __forceinline__ float red_entropy(const Red& t) { return logf(t.s) - t.t / t.s; }
+__device__ __forceinline__ float red_margin(const Red& t) { return (1.f - expf(t.m2 - t.m)) / t.s; }
 
 // Copy n floats from global to LDS with all of a thread's loads in flight.
 __device__ void stage(float* dst, const float* src, int n) {
@@ -64,26 +81,38 @@ __device__ void stage(float* dst, const float* src, int n) {
 struct PosConf {
     float maxprob, pcur;
     int argmax;
+    float entropy, margin, key;   // key: the caller's ordering key (array mode)
 };
 
 // Shadow-row confidence of position i: from staged chunk partials (step mode)
 // or from the per-position arrays.
 __device__ PosConf shadow_conf(const DecideArgs& a, const float* part, int s, int i, int tok) {
-    PosConf r;
+    PosConf r{0.f, 0.f, 0, 0.f, 0.f, 0.f};
     const int pos = s * a.B + i;
     if (part) {
-        const Red t = combine(part + (size_t)i * a.nchunk * 3, a.nchunk);
+        const Red t = combine(part + (size_t)i * a.nchunk * a.stride, a.nchunk, a.stride);
         r.maxprob = 1.f / t.s;
         r.argmax = t.a;
         tok = min(max(tok, 0), (int)a.ld - 1);   // stay inside the row whatever the id
         const float lc = a.logits[((size_t)s * 2 * a.B + a.B + i) * a.ld + tok];
         r.pcur = exp2f((lc - t.m) * kLog2e) / t.s;
+        if (a.stride == kConfStatsStride) { r.entropy = red_entropy(t); r.margin = red_margin(t); }
     } else {
         r.maxprob = a.maxprob_s[pos];
         r.argmax = a.argmax_s ? a.argmax_s[pos] : 0;
         r.pcur = a.pcur_s ? a.pcur_s[pos] : 0.f;
+        r.key = a.key_s ? a.key_s[pos] : 0.f;
     }
     return r;
+}
+
+// The key the next step's mask orders candidates by (Eq. 3 or its Sec. 5.1
+// variants): the confidence, -entropy or the margin.
+__device__ __forceinline__ float order_key(uint32_t flags, bool from_partials, float c, float entropy,
+                                           float margin, float given) {
+    if (!(flags & (DARD_F_ORDER_ENTROPY | DARD_F_ORDER_MARGIN))) return c;
+    if (!from_partials) return given;
+    return (flags & DARD_F_ORDER_ENTROPY) ? -entropy : margin;
 }
 
 __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
@@ -98,7 +127,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
     const int pos = s * a.B + i;
     const int st = live ? a.state_in[pos] : DARD_STATE_U;
     const bool pcur_mode = (a.flags & DARD_F_VERIFY_PCUR) != 0;
-    const int per_seq = a.B * a.nchunk * 3;
+    const int per_seq = a.B * a.nchunk * a.stride;
     float* sv = staged;
     float* sm = staged + per_seq;
     if (a.part_v) stage(sv, a.part_v + (size_t)s * per_seq, per_seq);
@@ -120,7 +149,9 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         __syncthreads();
         if (!live) return;
         float w = 0.f;
-        if (st == DARD_STATE_M) {
+        if (st == DARD_STATE_M && (a.flags & DARD_F_FIXED_W)) {
+            w = a.w_fixed;
+        } else if (st == DARD_STATE_M) {
             double P = 0.0, D = 0.0;
             for (int j = 0; j < a.B; ++j) {
                 const double k = lam_pow[abs(i - j)];
@@ -138,27 +169,34 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
     __syncthreads();
     if (live) {
         const int tok = a.tok_in ? a.tok_in[pos] : 0;
-        float c;
+        float c, key;
         int xhat;
-        float mp_s = 0.f, pc_s = 0.f, mp_mix = 0.f;
+        float mp_s = 0.f, pc_s = 0.f, mp_mix = 0.f, ent = 0.f, mrg = 0.f;
         int am_s = -1, am_mix = -1;
+        const bool from_part = a.part_m != nullptr;
         if (st == DARD_STATE_M) {
-            if (a.part_m) {
-                const Red t = combine(sm + (size_t)i * a.nchunk * 3, a.nchunk);
+            float given = 0.f;
+            if (from_part) {
+                const Red t = combine(sm + (size_t)i * a.nchunk * a.stride, a.nchunk, a.stride);
                 mp_mix = 1.f / t.s;
                 am_mix = t.a;
+                if (a.stride == kConfStatsStride) { ent = red_entropy(t); mrg = red_margin(t); }
             } else {
                 mp_mix = a.maxprob_mix[pos];
                 am_mix = a.argmax_mix[pos];
+                given = a.key_mix ? a.key_mix[pos] : 0.f;
             }
             c = mp_mix;
             xhat = am_mix;
+            key = order_key(a.flags, from_part, c, ent, mrg, given);
         } else {
-            const float* part = a.part_m ? (st == DARD_STATE_C ? sv : sm) : nullptr;
+            const float* part = from_part ? (st == DARD_STATE_C ? sv : sm) : nullptr;
             const PosConf pc = shadow_conf(a, part, s, i, tok);
             mp_s = pc.maxprob; pc_s = pc.pcur; am_s = pc.argmax;
+            ent = pc.entropy; mrg = pc.margin;
             c = pcur_mode ? pc.pcur : pc.maxprob;
             xhat = pc.argmax;
+            key = order_key(a.flags, from_part, c, ent, mrg, pc.key);
         }
         const int nxt = transition(c, a.tau_c, a.tau_u);
         if (nxt != DARD_STATE_U) atomicAnd(&all_u, 0);
@@ -168,12 +206,14 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
         xhat_all[i] = xhat;
         a.state_out[pos] = (uint8_t)nxt;
         a.tok_out[pos] = nxt == DARD_STATE_M ? a.mask_id : xhat;
-        a.conf_out[pos] = c;
+        a.conf_out[pos] = key;
         if (a.dbg_maxprob_s) a.dbg_maxprob_s[pos] = mp_s;
         if (a.dbg_argmax_s) a.dbg_argmax_s[pos] = am_s;
         if (a.dbg_pcur_s) a.dbg_pcur_s[pos] = pc_s;
         if (a.dbg_maxprob_mix) a.dbg_maxprob_mix[pos] = mp_mix;
         if (a.dbg_argmax_mix) a.dbg_argmax_mix[pos] = am_mix;
+        if (a.dbg_entropy) a.dbg_entropy[pos] = ent;
+        if (a.dbg_margin) a.dbg_margin[pos] = mrg;
     }
     __syncthreads();
     // progress rule (DARD_F_PROGRESS): no position entered U in an unfinished
@@ -197,7 +237,7 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
 
 hipError_t launch_decide(const DecideArgs& a, hipStream_t s) {
     TraceScope ts(DARD_K_DECIDE, s);
-    const size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * 3 * sizeof(float) : 0;
+    const size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * a.stride * sizeof(float) : 0;
     if (lds > 96 * 1024) return hipErrorInvalidValue;
     launch(decide_kernel, dim3(a.b), dim3(128), lds, s, a);
     return hipGetLastError();

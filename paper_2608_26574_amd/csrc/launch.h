@@ -101,17 +101,23 @@ struct ConfArgs {
     const float* w;        // per-row weight or NULL
     int64_t ld_s, ld_x;    // row strides (elements)
     int rows, V, nchunk, chunk;
-    float* part;           // [rows][nchunk][3]: max, argmax (as int bits), sum
+    float* part;           // [rows][nchunk][kConfStride]: max, argmax (as int bits), sum;
+                           // statistics variant [rows][nchunk][kConfStatsStride]:
+                           // also sum exp(l - max) (l - max) and the second-largest l
     // step mode: skip rows by state (phase 0: only C rows; phase 1: only M/U)
     const uint8_t* state;  // [rows] or NULL
     int phase;
     int step_B;            // >0: rows are block positions of [b][2B][V] logits
 };
+constexpr int kConfStride = 3, kConfStatsStride = 5;
 int conf_chunks(int V);
-hipError_t launch_conf_partial(const ConfArgs& a, hipStream_t s);
+// stats: also form the entropy / margin terms (partials of kConfStatsStride)
+hipError_t launch_conf_partial(const ConfArgs& a, bool stats, hipStream_t s);
+// entropy or margin != NULL reads statistics partials
 hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls,
                                int64_t ld, const int32_t* cur_tok, int32_t* argmax,
-                               float* maxprob, float* pcur, hipStream_t s);
+                               float* maxprob, float* pcur, float* entropy, float* margin,
+                               hipStream_t s);
 
 // ---- decide.hip
 struct DecideArgs {
@@ -121,22 +127,25 @@ struct DecideArgs {
     double lambda, p0;
     int32_t mask_id;
     uint32_t flags;
+    float w_fixed;
     const uint8_t* state_in;
     const int32_t* tok_in;
     // combined per-position inputs
     const float* maxprob_s; const float* pcur_s; const int32_t* argmax_s;
     const float* maxprob_mix; const int32_t* argmax_mix;
+    const float* key_s; const float* key_mix;   // ordering keys (entropy / margin orders)
     // chunk partials (step mode; used when the per-position arrays are NULL)
-    const float* part_v;     // [b*B][nchunk][3] shadow rows (phase VERIFY)
-    const float* part_m;     // [b*B][nchunk][3] mixed / shadow rows (phase FINAL)
+    const float* part_v;     // [b*B][nchunk][stride] shadow rows (phase VERIFY)
+    const float* part_m;     // [b*B][nchunk][stride] mixed / shadow rows (phase FINAL)
     const float* logits;     // [b][2B][V] (step mode, for pcur)
     int64_t ld;
-    int nchunk;
+    int nchunk, stride;      // stride kConfStatsStride: partials carry entropy / margin terms
     float* w_out;
     uint8_t* state_out; int32_t* tok_out; float* conf_out; int32_t* block_done;
     // optional debug copies
     float* dbg_maxprob_s; int32_t* dbg_argmax_s; float* dbg_pcur_s;
     float* dbg_maxprob_mix; int32_t* dbg_argmax_mix;
+    float* dbg_entropy; float* dbg_margin;
 };
 hipError_t launch_decide(const DecideArgs& a, hipStream_t s);
 

@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(HERE, "libdard.so")
 DARD_OK = 0
 STATE_M, STATE_C, STATE_U = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
-F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR = 1, 2, 4
+F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR, F_PROGRESS = 1, 2, 4, 8
+F_C_BIDIR, F_ORDER_L2R, F_ORDER_ENTROPY, F_ORDER_MARGIN, F_FIXED_W = 16, 32, 64, 128, 256
 PHASE_VERIFY, PHASE_FINAL = 0, 1
 (K_GEMM_QKV, K_GEMM_O, K_GEMM_GU, K_GEMM_DOWN, K_GEMM_HEAD, K_ATTENTION, K_CONFIDENCE,
  K_DECIDE, K_NORM, K_MASK, K_COUNT) = range(11)
@@ -40,7 +41,8 @@ class DardError(RuntimeError):
 
 class dard_params(ctypes.Structure):
     _fields_ = [("tau_c", ctypes.c_float), ("tau_u", ctypes.c_float), ("lambda_", ctypes.c_double),
-                ("p0", ctypes.c_double), ("mask_id", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("p0", ctypes.c_double), ("mask_id", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("w_fixed", ctypes.c_float)]
 
 
 class dard_dims(ctypes.Structure):
@@ -51,7 +53,7 @@ class dard_dims(ctypes.Structure):
 
 class dard_step_debug(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("logits", "w", "maxprob_s", "argmax_s", "pcur_s",
-                                               "maxprob_mix", "argmax_mix")]
+                                               "maxprob_mix", "argmax_mix", "entropy", "margin")]
 
 
 _lib = None
@@ -74,8 +76,8 @@ def lib():
             "dard_masked_attention": (i32, [i32, vp, vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, f32,
                                             u32, vp, vp, sz, vp]),
             "dard_confidence_workspace_bytes": (sz, [i32, i32]),
-            "dard_confidence": (i32, [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, sz, vp]),
-            "dard_commit_remask": (i32, [i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "dard_confidence": (i32, [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "dard_commit_remask": (i32, [i32, vp, i32, i32] + [vp] * 14),
             "dard_packed_weight_bytes": (sz, [vp]),
             "dard_pack_weights": (i32, [vp, vp, i32, vp, sz, vp]),
             "dard_kv_bytes": (sz, [vp, i32, i32]),
@@ -129,8 +131,8 @@ def _ref(x):
     return ctypes.byref(x) if x is not None else None
 
 
-def make_params(tau_c=0.4, tau_u=0.9, lam=0.5 ** (1 / 8), p0=0.1, mask_id=0, flags=0):
-    return dard_params(tau_c, tau_u, lam, p0, mask_id, flags)
+def make_params(tau_c=0.4, tau_u=0.9, lam=0.5 ** (1 / 8), p0=0.1, mask_id=0, flags=0, w_fixed=0.0):
+    return dard_params(tau_c, tau_u, lam, p0, mask_id, flags, w_fixed)
 
 
 def make_dims(d):
@@ -169,20 +171,22 @@ def dard_confidence_workspace_bytes(rows, V):
 
 
 def dard_confidence(logits_s, argmax, maxprob, logits_x=None, w=None, cur_tok=None, pcur=None, ws=None,
-                    stream=None):
+                    stream=None, entropy=None, margin=None):
     rows, V = logits_s.shape
     nbytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().dard_confidence(_p(logits_s), _p(logits_x), _p(w), _p(cur_tok), rows, V, logits_s.stride(0),
-                                 _p(argmax), _p(maxprob), _p(pcur), _p(ws), nbytes, _stream(stream)))
+                                 _p(argmax), _p(maxprob), _p(pcur), _p(entropy), _p(margin), _p(ws), nbytes,
+                                 _stream(stream)))
 
 
 def dard_commit_remask(phase, params, state_in, maxprob_s=None, pcur_s=None, argmax_s=None, maxprob_mix=None,
                        argmax_mix=None, w_out=None, state_out=None, tok_out=None, conf_out=None,
-                       block_done=None, stream=None):
+                       block_done=None, stream=None, key_s=None, key_mix=None):
     b, B = state_in.shape
     _check(lib().dard_commit_remask(phase, ctypes.byref(params), b, B, _p(state_in), _p(maxprob_s), _p(pcur_s),
-                                    _p(argmax_s), _p(maxprob_mix), _p(argmax_mix), _p(w_out), _p(state_out),
-                                    _p(tok_out), _p(conf_out), _p(block_done), _stream(stream)))
+                                    _p(argmax_s), _p(maxprob_mix), _p(argmax_mix), _p(key_s), _p(key_mix),
+                                    _p(w_out), _p(state_out), _p(tok_out), _p(conf_out), _p(block_done),
+                                    _stream(stream)))
 
 
 def dard_pack_matrix(W, Wp, stream=None):
@@ -263,7 +267,8 @@ class Engine:
         dbg = None
         if debug is not None:
             dbg = dard_step_debug(*[_p(debug.get(k)) for k in ("logits", "w", "maxprob_s", "argmax_s", "pcur_s",
-                                                               "maxprob_mix", "argmax_mix")])
+                                                               "maxprob_mix", "argmax_mix", "entropy",
+                                                               "margin")])
         _check(lib().dard_step(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap, P,
                                ctypes.byref(params), b, B, _p(tok_in), _p(state_in), _p(conf_in), _p(tok_out),
                                _p(state_out), _p(conf_out), _p(block_done), _ref(dbg), _p(self.ws),

@@ -51,29 +51,40 @@ def test_host_validation_errors():
     # B outside [1, 128]
     assert L.dard_build_state_mask(fake, fake, 1, 0, 0, fake, None) == -2
     assert L.dard_build_state_mask(fake, fake, 1, 129, 0, fake, None) == -2
-    # unknown flag bits
-    assert L.dard_build_state_mask(fake, fake, 1, 4, 1 << 7, fake, None) == -1
+    # unknown flag bits; two candidate orderings at once
+    assert L.dard_build_state_mask(fake, fake, 1, 4, 1 << 12, fake, None) == -1
     assert b"flag" in L.dard_last_error()
+    assert L.dard_build_state_mask(fake, fake, 1, 4, dard.F_C_BIDIR | dard.F_ORDER_L2R, fake, None) == -1
+    assert b"ordering" in L.dard_last_error()
     # attention: P + 2B > cap, bad dh, GQA ratio
     args = [1, fake, fake, fake]
     assert L.dard_masked_attention(*args, 10, 11, fake, fake, 1, 1, 4, 4, 128, 0.1, 0, fake, None, 0, None) == -2
     assert L.dard_masked_attention(*args, 0, 64, fake, fake, 1, 8, 4, 4, 96, 0.1, 0, fake, None, 0, None) == -2
     assert L.dard_masked_attention(*args, 0, 64, fake, fake, 1, 8, 6, 4, 128, 0.1, 0, fake, None, 0, None) == -2
     # confidence: mixing without w, ld not a multiple of 4
-    assert L.dard_confidence(fake, fake, None, None, 2, 10, 12, fake, fake, None, fake, 1 << 20, None) == -1
-    assert L.dard_confidence(fake, None, None, None, 2, 10, 10, fake, fake, None, fake, 1 << 20, None) == -2
+    assert L.dard_confidence(fake, fake, None, None, 2, 10, 12, fake, fake, None, None, None, fake, 1 << 20,
+                             None) == -1
+    assert L.dard_confidence(fake, None, None, None, 2, 10, 10, fake, fake, None, None, None, fake, 1 << 20,
+                             None) == -2
     # confidence: workspace too small
-    assert L.dard_confidence(fake, None, None, None, 2, 16, 16, fake, fake, None, fake, 4, None) == -5
+    assert L.dard_confidence(fake, None, None, None, 2, 16, 16, fake, fake, None, None, None, fake, 4, None) == -5
     # commit/remask: thresholds out of order, lambda outside (0, 1), unknown phase
-    bad = _params(tau_c=0.95, tau_u=0.9)
-    assert L.dard_commit_remask(0, ctypes.byref(bad), 1, 4, fake, fake, None, None, None, None, fake,
-                                None, None, None, None, None) == -1
-    bad = _params(lam=1.0)
-    assert L.dard_commit_remask(0, ctypes.byref(bad), 1, 4, fake, fake, None, None, None, None, fake,
-                                None, None, None, None, None) == -1
-    good = _params()
-    assert L.dard_commit_remask(7, ctypes.byref(good), 1, 4, fake, fake, None, None, None, None, fake,
-                                None, None, None, None, None) == -1
+    def remask(phase, p, *outs):
+        rest = list(outs) + [None] * (4 - len(outs))
+        return L.dard_commit_remask(phase, ctypes.byref(p), 1, 4, fake, fake, None, None, None, None, None, None,
+                                    fake, *rest, None)
+    assert remask(0, _params(tau_c=0.95, tau_u=0.9)) == -1
+    assert remask(0, _params(lam=1.0)) == -1
+    assert remask(7, _params()) == -1
+    # fixed mixing weight outside [0, 1]; two orderings at once
+    assert remask(0, _params(flags=dard.F_FIXED_W, w_fixed=1.5)) == -1
+    assert b"w_fixed" in L.dard_last_error()
+    assert remask(0, _params(flags=dard.F_ORDER_ENTROPY | dard.F_ORDER_MARGIN)) == -1
+    # FINAL under the entropy ordering needs the caller's keys
+    p = _params(flags=dard.F_ORDER_ENTROPY)
+    assert L.dard_commit_remask(1, ctypes.byref(p), 1, 4, fake, fake, None, fake, fake, fake, None, None,
+                                None, fake, fake, fake, None, None) == -1
+    assert b"key" in L.dard_last_error()
 
 
 def test_dims_validation_and_sizes():

@@ -46,7 +46,9 @@ def test_linear(dtype, M, N, K):
 
 # ---------------------------------------------------------------- mask
 @pytest.mark.parametrize("B", [1, 5, 32, 63, 64, 65, 128])
-@pytest.mark.parametrize("flags", [0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW])
+@pytest.mark.parametrize("flags", [0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW, O.F_C_BIDIR, O.F_ORDER_L2R,
+                                   O.F_ORDER_L2R | O.F_XSELF_SHADOW, O.F_C_BIDIR | O.F_MKEYS_SHADOW,
+                                   O.F_ORDER_ENTROPY, O.F_ORDER_MARGIN | O.F_FIXED_W])
 def test_state_mask_bit_exact(B, flags):
     announce("mask", B, flags)
     b = 3
@@ -131,11 +133,28 @@ def test_attention_edges_bf16(case):
     assert err < 2e-2, err
 
 
-@pytest.mark.parametrize("flags", [O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW])
+@pytest.mark.parametrize("flags", [O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW, O.F_C_BIDIR, O.F_ORDER_L2R])
 def test_attention_flags_bf16(flags):
     announce("attention flags", flags)
     err = _attn_case(2, 16, 40, 4, 4, 128, "bf16", None, seed=9, flags=flags)
     assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("flags", [O.F_C_BIDIR, O.F_ORDER_L2R, O.F_ORDER_L2R | O.F_XSELF_SHADOW])
+def test_attention_orderings_8b_shape(flags):
+    """Candidate-ordering variants (Sec. 5.1) at the 8B shape, batch 4,
+    half the block candidates: the mask differs from the primary one in most
+    candidate rows."""
+    announce("attention ordering 8B-shape", flags)
+    err = _attn_case(4, 32, 512, 32, 32, 128, "bf16", 0.5, seed=21 + flags, flags=flags)
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("flags", [O.F_C_BIDIR, O.F_ORDER_L2R])
+def test_attention_orderings_f32(flags):
+    announce("attention ordering f32", flags)
+    err = _attn_case(2, 7, 9, 4, 2, 128, "f32", None, seed=5, flags=flags)
+    assert err < 1e-4, err
 
 
 @pytest.mark.parametrize("case", [dict(b=1, B=32, P=64, Hq=4, Hkv=4, dh=64),
@@ -177,7 +196,8 @@ def test_confidence_plain(rows, V):
     ls_d = ls.cuda()
     L = dard.lib()
     dard._check(L.dard_confidence(ls_d.data_ptr(), None, None, cur.cuda().data_ptr(), rows, V, ld,
-                                  am.data_ptr(), mp.data_ptr(), pc.data_ptr(), ws.data_ptr(), ws.numel(),
+                                  am.data_ptr(), mp.data_ptr(), pc.data_ptr(), None, None, ws.data_ptr(),
+                                  ws.numel(),
                                   torch.cuda.current_stream().cuda_stream))
     torch.cuda.synchronize()
     ram, rmp, rpc = _conf_ref(ls[:, :V].numpy(), cur=cur.numpy())
@@ -204,6 +224,96 @@ def test_confidence_mixed(wvals):
     ram, rmp, _ = _conf_ref(ls.numpy(), lx.numpy(), w.numpy())
     assert np.array_equal(am.cpu().numpy(), ram)
     assert np.max(np.abs(mp.cpu().numpy() - rmp) / rmp) < 1e-5
+
+
+def _mix_tie_pair(w, seed=0):
+    """Two (x, s) logit pairs whose mixtures (w x) + ((1 - w) s), each product
+    and the sum rounded separately in float32 (Eq. 7 as the library states
+    it), are equal, while a fused multiply-add w x + round((1 - w) s) makes
+    the second one larger.  Found by search on the CPU."""
+    rng = np.random.default_rng(seed)
+    w = np.float32(w)
+    omw = np.float32(1) - w
+    x = (rng.standard_normal(200000) * 4).astype(np.float32)
+    s = (rng.standard_normal(200000) * 4).astype(np.float32)
+    sep = (w * x) + (omw * s)
+    fused = (np.float64(w) * x + (omw * s).astype(np.float64)).astype(np.float32)
+    order = np.argsort(sep, kind="stable")
+    for a in range(len(order) - 1):
+        i, j = order[a], order[a + 1]
+        if sep[i] == sep[j] and fused[i] != fused[j]:
+            lo, hi = (i, j) if fused[i] < fused[j] else (j, i)
+            return (x[lo], s[lo]), (x[hi], s[hi])
+    raise AssertionError("no pair found")
+
+
+def test_confidence_mixing_rounds_each_product():
+    """Eq. 7 evaluated with every operation rounded once: on a planted tie of
+    the separately rounded mixtures the lower index wins; a kernel that fused
+    a product into the sum would pick the higher one."""
+    announce("confidence mixing rounding")
+    V, w = 4096, 0.3
+    (x0, s0), (x1, s1) = _mix_tie_pair(w)
+    ls = np.full((1, V), -30.0, dtype=np.float32)
+    lx = np.full((1, V), -30.0, dtype=np.float32)
+    lx[0, 1000], ls[0, 1000] = x0, s0
+    lx[0, 3000], ls[0, 3000] = x1, s1
+    am = torch.empty(1, dtype=torch.int32, device="cuda")
+    mp = torch.empty(1, device="cuda")
+    ws = torch.empty(dard.dard_confidence_workspace_bytes(1, V), dtype=torch.uint8, device="cuda")
+    dard.dard_confidence(dev(ls), am, mp, logits_x=dev(lx), w=dev(np.array([w], dtype=np.float32)), ws=ws)
+    torch.cuda.synchronize()
+    assert O.confidence(O.mix_logits(lx[0], ls[0], w))[0] == 1000
+    assert am.item() == 1000
+
+
+@pytest.mark.parametrize("rows,V,mixed", [(5, 126464, False), (3, 152064, False), (4, 2048, False),
+                                          (3, 10, False), (2, 8195, False), (1, 1, False), (5, 126464, True),
+                                          (3, 9000, True)])
+def test_confidence_entropy_margin(rows, V, mixed):
+    """Entropy and margin of each (mixed) row, the scores of the entropy and
+    margin orderings (Sec. 5.1), against the oracle's float64 definitions,
+    with the top-1 statistics of the same launch unchanged."""
+    announce("confidence entropy/margin", rows, V, mixed)
+    g = torch.Generator().manual_seed(V * 3 + rows)
+    ld = (V + 3) // 4 * 4
+    ls = (torch.randn(rows, ld, generator=g) * 3).float()
+    lx = (torch.randn(rows, ld, generator=g) * 3).float() if mixed else None
+    # sharp rows, flat rows and a tie at the top
+    ls[0, :V] *= 0.01
+    if rows > 1:
+        ls[1, V // 2] = 40.0
+    if rows > 2 and V > 4:
+        ls[2, 1] = ls[2, V - 1] = 30.0
+        if mixed:
+            lx[2, 1] = lx[2, V - 1] = 30.0
+    w = torch.linspace(0.0, 1.0, rows) if mixed else None
+    am = torch.empty(rows, dtype=torch.int32, device="cuda")
+    mp = torch.empty(rows, device="cuda")
+    ent = torch.empty(rows, device="cuda")
+    mrg = torch.empty(rows, device="cuda")
+    ws = torch.empty(dard.dard_confidence_workspace_bytes(rows, V), dtype=torch.uint8, device="cuda")
+    # V columns in rows of ld elements: the padding is never read
+    ls_d = ls.cuda()
+    lx_d = None if lx is None else lx.cuda()
+    w_d = None if w is None else w.cuda()
+    ptr = lambda t: None if t is None else t.data_ptr()
+    dard._check(dard.lib().dard_confidence(ls_d.data_ptr(), ptr(lx_d), ptr(w_d), None, rows, V, ld,
+                                           am.data_ptr(), mp.data_ptr(), None, ent.data_ptr(), mrg.data_ptr(),
+                                           ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    lsn = ls[:, :V].numpy()
+    lxn = None if lx is None else lx[:, :V].numpy()
+    ram, rmp, _ = _conf_ref(lsn, lxn, None if w is None else w.numpy())
+    assert np.array_equal(am.cpu().numpy(), ram)
+    assert np.max(np.abs(mp.cpu().numpy() - rmp) / rmp) < 1e-5
+    for r in range(rows):
+        row = lsn[r] if lxn is None else O.mix_logits(lxn[r], lsn[r], w[r].item())
+        H, m = O.entropy_margin(row)
+        assert abs(ent[r].item() - H) <= 1e-4 + 1e-5 * H, (r, ent[r].item(), H)
+        assert abs(mrg[r].item() - m) <= 1e-6 + 1e-5 * m, (r, mrg[r].item(), m)
+    if rows > 2 and V > 4:
+        assert mrg[2].item() == 0.0
 
 
 # ---------------------------------------------------------------- decisions
@@ -249,3 +359,45 @@ def test_commit_remask_bit_exact(B, flags, tc, tu):
         assert np.array_equal(to[s].cpu().numpy(), tk)
         assert np.array_equal(co[s].cpu().numpy(), cf.astype(np.float32))
         assert bd[s].item() == done
+
+
+@pytest.mark.parametrize("B", [7, 32, 128])
+@pytest.mark.parametrize("flags,wf", [(O.F_FIXED_W, 0.0), (O.F_FIXED_W, 0.5), (O.F_FIXED_W, 1.0),
+                                      (O.F_ORDER_ENTROPY, 0.0), (O.F_ORDER_MARGIN | O.F_FIXED_W, 0.25)])
+def test_commit_remask_variants_bit_exact(B, flags, wf):
+    """Fixed guidance weight and the carried key of the entropy / margin
+    orderings (Sec. 5.1) through the per-position entry point."""
+    announce("commit/remask variants", B, flags, wf)
+    b, tc, tu = 3, 0.4, 0.9
+    rng = np.random.default_rng(B * 5 + flags)
+    p = dict(_params(flags, tc, tu), w_fixed=wf)
+    state = rng.integers(0, 3, (b, B)).astype(np.uint8)
+    pool = np.array([0.0, tc, 0.5, tu, 0.99, 1.0], dtype=np.float32)
+    mp_s = rng.choice(pool, (b, B)).astype(np.float32)
+    mp_mix = rng.choice(pool, (b, B)).astype(np.float32)
+    am_s = rng.integers(0, 998, (b, B)).astype(np.int32)
+    am_mix = rng.integers(0, 998, (b, B)).astype(np.int32)
+    key_s = rng.standard_normal((b, B)).astype(np.float32)
+    key_mix = rng.standard_normal((b, B)).astype(np.float32)
+    cp = dard.make_params(tc, tu, O.LAMBDA_DEFAULT, 0.1, 999, flags, wf)
+    w = torch.empty(b, B, device="cuda")
+    dard.dard_commit_remask(dard.PHASE_VERIFY, cp, dev(state), maxprob_s=dev(mp_s), w_out=w)
+    so = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    to = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    co = torch.empty(b, B, device="cuda")
+    dard.dard_commit_remask(dard.PHASE_FINAL, cp, dev(state), dev(mp_s), None, dev(am_s), dev(mp_mix),
+                            dev(am_mix), None, so, to, co, None, key_s=dev(key_s), key_mix=dev(key_mix))
+    torch.cuda.synchronize()
+    for s in range(b):
+        _, _, _, rw = O.verify_candidates(state[s], mp_s[s], p)
+        assert np.array_equal(w[s].cpu().numpy().astype(np.float64), rw), s
+        c = np.where(state[s] == O.STATE_M, mp_mix[s], mp_s[s])
+        xh = np.where(state[s] == O.STATE_M, am_mix[s], am_s[s])
+        st, tk, cf, _ = O.finalize(c, xh, p, state[s])
+        assert np.array_equal(so[s].cpu().numpy(), st)
+        assert np.array_equal(to[s].cpu().numpy(), tk)
+        if flags & (O.F_ORDER_ENTROPY | O.F_ORDER_MARGIN):
+            key = np.where(state[s] == O.STATE_M, key_mix[s], key_s[s])
+        else:
+            key = cf.astype(np.float32)
+        assert np.array_equal(co[s].cpu().numpy(), key)

@@ -59,7 +59,7 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
         tok, state, conf = synth.workload_block(b, B, frac, V, seed=seed + 2)
     eng.dard_prefill(dev(ids), embeds=None if embeds is None else embeds.cuda())
     cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
-                          params.get("flags", 0))
+                          params.get("flags", 0), params.get("w_fixed", 0.0))
     t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
     s_out = torch.zeros(b, B, dtype=torch.uint8, device="cuda")
     c_out = torch.zeros(b, B, device="cuda")
@@ -121,20 +121,34 @@ def check_bf16_logits(got, ref, label):
     assert err < max(2e-2, 2.0 * floor), (err, floor)
 
 
+def confidences(dec, state, flags):
+    """c_i of Eq. 8 from the oracle's decision record (conf_out carries the
+    ordering key, which is c_i only under the primary ordering)."""
+    shadow = dec["pcur_s"] if flags & O.F_VERIFY_PCUR else dec["maxprob_s"]
+    return np.where(state == O.STATE_M, dec["maxprob_mix"], shadow)
+
+
 def check_decisions(tok, state, got, ref, params):
+    flags = params.get("flags", 0)
     # op level: the oracle's decisions on the GPU's logits are exactly the GPU's
     dec = O.decide(got["logits"], tok, state, params)
     assert np.array_equal(dec["w"].astype(np.float32), got["w"])
     assert np.array_equal(dec["tok_out"], got["tok_out"])
+    c_dec = confidences(dec, state, flags)
     near = np.zeros_like(state, dtype=bool)
     for t in (params["tau_c"], params["tau_u"]):
-        near |= np.abs(dec["conf_out"] - t) < 1e-5
+        near |= np.abs(c_dec - t) < 1e-5
     assert np.array_equal(dec["state_out"][~near], got["state_out"][~near])
-    assert np.allclose(dec["conf_out"], got["conf_out"], rtol=1e-5, atol=1e-7)
+    if flags & O.F_ORDER_ENTROPY:
+        # key -H: float32 sums over the vocabulary, |H| up to ln V
+        assert np.allclose(dec["conf_out"], got["conf_out"], rtol=1e-5, atol=1e-4)
+    else:
+        assert np.allclose(dec["conf_out"], got["conf_out"], rtol=1e-5, atol=1e-7)
     assert np.array_equal(dec["block_done"], got["block_done"])
     # step level against the independent oracle, with measured margins
     eps = float(np.max(np.abs(got["logits"] - ref["logits"])))
-    eps_c = float(np.max(np.abs(got["conf_out"] - ref["conf_out"])))
+    c_ref = confidences(ref, state, flags)
+    eps_c = float(np.max(np.abs(confidences(dec, state, flags) - c_ref)))
     b, B = state.shape
     excluded = 0
     for s in range(b):
@@ -144,7 +158,7 @@ def check_decisions(tok, state, got, ref, params):
             for r in rows:
                 top2 = np.sort(ref["logits"][s, r])[-2:]
                 gaps.append(top2[1] - top2[0])
-            c = ref["conf_out"][s, i]
+            c = c_ref[s, i]
             if min(gaps) <= 2 * eps or min(abs(c - params["tau_c"]), abs(c - params["tau_u"])) <= 2 * eps_c:
                 excluded += 1
                 continue
@@ -153,8 +167,8 @@ def check_decisions(tok, state, got, ref, params):
     return eps, excluded
 
 
-def P(mask_id, flags=0, tc=0.4, tu=0.9):
-    return dict(tau_c=tc, tau_u=tu, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=mask_id, flags=flags)
+def P(mask_id, flags=0, tc=0.4, tu=0.9, w_fixed=0.0):
+    return dict(tau_c=tc, tau_u=tu, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=mask_id, flags=flags, w_fixed=w_fixed)
 
 
 def test_tiny_step_fp32():
@@ -169,13 +183,17 @@ def test_tiny_step_fp32():
     assert excl == 0
 
 
-@pytest.mark.parametrize("flags", [0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW, O.F_VERIFY_PCUR])
-def test_tiny_step_fp32_transitions(flags):
+@pytest.mark.parametrize("flags,wf", [(0, 0.0), (O.F_XSELF_SHADOW, 0.0), (O.F_MKEYS_SHADOW, 0.0),
+                                      (O.F_VERIFY_PCUR, 0.0), (O.F_C_BIDIR, 0.0), (O.F_ORDER_L2R, 0.0),
+                                      (O.F_ORDER_ENTROPY, 0.0), (O.F_ORDER_MARGIN, 0.0), (O.F_FIXED_W, 0.0),
+                                      (O.F_FIXED_W, 0.5), (O.F_FIXED_W | O.F_ORDER_L2R, 1.0)])
+def test_tiny_step_fp32_transitions(flags, wf):
     """A sharpened LM head spreads the confidences over (0, 1) so that real
-    promotions, demotions and mixing weights occur."""
+    promotions, demotions and mixing weights occur.  Also the ordering and
+    mixing variants of Sec. 5.1."""
     dims = synth.TINY
-    announce("tiny fp32 step, sharp head", flags)
-    prm = P(dims.mask_id, flags)
+    announce("tiny fp32 step, sharp head", flags, wf)
+    prm = P(dims.mask_id, flags, w_fixed=wf)
     tok, state, conf, got, ref = run_case(dims, 2, 32, 64, prm, seed=5, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     # the sharpened head multiplies every upstream rounding difference by 20
@@ -214,6 +232,20 @@ def test_llada8b_two_layers():
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = run_case(dims, 1, 32, 512, prm, seed=1, frac=0.25, wdevice="cuda")
     check_bf16_logits(got, ref, "llada8b 2 layers")
+    check_decisions(tok, state, got, ref, prm)
+
+
+@pytest.mark.parametrize("flags,wf", [(O.F_C_BIDIR, 0.0), (O.F_ORDER_L2R | O.F_FIXED_W, 1.0),
+                                      (O.F_ORDER_MARGIN, 0.0), (O.F_ORDER_ENTROPY | O.F_FIXED_W, 0.5)])
+def test_llada8b_two_layers_variants(flags, wf):
+    """Ordering and mixing variants of Sec. 5.1 at the 8B shape (two layers,
+    prompt 512, block 32, half the block candidates)."""
+    dims = synth.truncated(synth.LLADA8B, 2)
+    announce("llada8b 2-layer step variant", flags, wf)
+    prm = P(dims.mask_id, flags, w_fixed=wf)
+    tok, state, conf, got, ref = run_case(dims, 1, 32, 512, prm, seed=6, frac=0.5, wdevice="cuda",
+                                          check_kv=False)
+    check_bf16_logits(got, ref, f"llada8b 2 layers, flags {flags}")
     check_decisions(tok, state, got, ref, prm)
 
 
