@@ -459,12 +459,22 @@ def op_measurements(reps=20):
         mp = torch.empty(rows, device="cuda")
         ws = torch.empty(max(dard.dard_confidence_workspace_bytes(rows, V), 1), dtype=torch.uint8, device="cuda")
 
+        ent = torch.empty(rows, device="cuda")
+        mrg = torch.empty(rows, device="cuda")
+
         def cf(i):
             dard.dard_confidence(ls[i % ncopy], am, mp, ws=ws)
+
+        def cf_stats(i):   # with the entropy / margin scores of the ordering variants
+            dard.dard_confidence(ls[i % ncopy], am, mp, ws=ws, entropy=ent, margin=mrg)
         ms = timed(cf, reps)
+        ms_st = timed(cf_stats, reps)
         res["confidence"].append({"shape": label, "us": round(ms * 1e3, 2),
                                   "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-                                  "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
+                                  "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                  "entropy_margin_us": round(ms_st * 1e3, 2),
+                                  "entropy_margin_hbm_frac": round(nbytes / (ms_st * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                                                   4)})
         del ls
     torch.cuda.empty_cache()
     return res
