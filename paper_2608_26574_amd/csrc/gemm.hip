@@ -43,22 +43,67 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
     *reinterpret_cast<uint2*>(p) = make_uint2(w0, w1);
 }
 
-__device__ __forceinline__ float silu(float x) { return x / (1.f + expf(-x)); }
+// Two adjacent values (p 2-element aligned): one 4- or 8-byte store.
+template <typename T>
+__device__ __forceinline__ void store2(T* p, float a, float b);
+template <>
+__device__ __forceinline__ void store2<float>(float* p, float a, float b) {
+    *reinterpret_cast<float2*>(p) = make_float2(a, b);
+}
+template <>
+__device__ __forceinline__ void store2<bf16_t>(bf16_t* p, float a, float b) {
+    *reinterpret_cast<uint32_t*>(p) = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+// x * sigmoid(x) with the hardware exp2 and reciprocal (about 1 ulp each):
+// exp2 of a large argument is +inf and its reciprocal 0, so the limits hold.
+__device__ __forceinline__ float silu(float x) {
+    return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x * -1.4426950408889634f));
+}
+
+// The epilogue kind is uniform over a launch; kernels branch on it once and
+// run a loop specialised for it (Kind<k>), so a tile's epilogue carries no
+// per-tile dispatch and no code of the other kinds.
+template <int K>
+struct Kind {
+    static constexpr int value = K;
+};
+
+template <typename F>
+__device__ __forceinline__ void with_kind(int kind, F&& f) {
+    switch (kind) {
+    case EPI_STORE_F32: f(Kind<EPI_STORE_F32>{}); break;
+    case EPI_PARTIAL: f(Kind<EPI_PARTIAL>{}); break;
+    case EPI_RESID: f(Kind<EPI_RESID>{}); break;
+    case EPI_SWIGLU: f(Kind<EPI_SWIGLU>{}); break;
+    case EPI_QKV: f(Kind<EPI_QKV>{}); break;
+    default: break;
+    }
+}
+
+// Row m of the QKV output: sequence s, rotary position and cache index.
+struct QkvRow {
+    int s, pos, cidx;
+};
+__device__ __forceinline__ QkvRow qkv_row(const EpiArgs& e, int m) {
+    const int s = m / e.rows_per_seq, r = m - s * e.rows_per_seq;
+    return QkvRow{s, e.step ? e.P + (r % e.B) : r, e.step ? e.P + r : r};
+}
 
 // Epilogue for output columns n..n+3 (n % 4 == 0) of token row m, in two
 // halves: epi_fetch loads what the epilogue reads (the residual, or the two
 // rotary (cos, sin) pairs), epi_store combines and writes.  A kernel that
 // owns several tiles fetches for all of them before its first store, so the
-// loads overlap instead of each waiting behind the stores before it.
+// loads overlap instead of each waiting behind the stores before it.  head_dim
+// is 64 or 128, so dims and heads come from shifts.
+template <int EK>
 __device__ __forceinline__ float4 epi_fetch(const EpiArgs& e, int m, int n) {
-    if (e.kind == EPI_RESID) return *reinterpret_cast<const float4*>(e.y + (size_t)m * e.ldy + n);
-    if (e.kind == EPI_QKV) {
+    if constexpr (EK == EPI_RESID) return *reinterpret_cast<const float4*>(e.y + (size_t)m * e.ldy + n);
+    if constexpr (EK == EPI_QKV) {
         const int qd = e.Hq * e.dh, kd = e.Hkv * e.dh;
         if (n < qd + kd) {
-            const int r = m % e.rows_per_seq;
-            const int pos = e.step ? e.P + (r % e.B) : r;
-            const int ein = (n < qd ? n : n - qd) % e.dh;
-            const float* t = e.rope + ((size_t)pos * (e.dh / 2) + ein / 2) * 2;
+            const int ein = (n < qd ? n : n - qd) & (e.dh - 1);
+            const float* t = e.rope + ((size_t)qkv_row(e, m).pos * (e.dh / 2) + ein / 2) * 2;
             const float2 c0 = *reinterpret_cast<const float2*>(t);
             const float2 c1 = *reinterpret_cast<const float2*>(t + 2);
             return make_float4(c0.x, c0.y, c1.x, c1.y);
@@ -67,55 +112,40 @@ __device__ __forceinline__ float4 epi_fetch(const EpiArgs& e, int m, int n) {
     return make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-template <typename T>
+template <typename T, int EK>
 __device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx4 v, float4 f) {
-    switch (e.kind) {
-    case EPI_STORE_F32:
-    case EPI_PARTIAL:
+    if constexpr (EK == EPI_STORE_F32 || EK == EPI_PARTIAL) {
         *reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n) = make_float4(v[0], v[1], v[2], v[3]);
-        break;
-    case EPI_RESID:
+    } else if constexpr (EK == EPI_RESID) {
         *reinterpret_cast<float4*>(e.y + (size_t)m * e.ldy + n) =
             make_float4(f.x + v[0], f.y + v[1], f.z + v[2], f.w + v[3]);
-        break;
-    case EPI_SWIGLU: {
+    } else if constexpr (EK == EPI_SWIGLU) {
+        // interleaved rows: (gate, up) pairs at (n, n+1) and (n+2, n+3)
         T* a = reinterpret_cast<T*>(e.act) + (e.act_frag ? frag_off(m, n / 2, e.ld_act) : (size_t)m * e.ld_act + n / 2);
-        St<T>::st(a, silu(v[0]) * v[1]);
-        St<T>::st(a + 1, silu(v[2]) * v[3]);
-        break;
-    }
-    case EPI_QKV: {
-        const int s = m / e.rows_per_seq, r = m % e.rows_per_seq;
-        const int cidx = e.step ? e.P + r : r;
+        store2<T>(a, silu(v[0]) * v[1], silu(v[2]) * v[3]);
+    } else if constexpr (EK == EPI_QKV) {
+        const QkvRow row = qkv_row(e, m);
         const int qd = e.Hq * e.dh, kd = e.Hkv * e.dh;
+        const int sh = e.dh == 128 ? 7 : 6;
         if (n < qd + kd) {
             // rotary pairs (v0, v1) and (v2, v3): natural dims (t, t + dh/2)
-            const int ein = (n < qd ? n : n - qd) % e.dh;
             const float a0 = v[0] * f.x - v[1] * f.y, b0 = v[1] * f.x + v[0] * f.y;
             const float a1 = v[2] * f.z - v[3] * f.w, b1 = v[3] * f.z + v[2] * f.w;
             if (n < qd) {
                 store4<T>(reinterpret_cast<T*>(e.q) + (size_t)m * e.ldq + n, a0, b0, a1, b1);
             } else {
-                const int kvh = (n - qd) / e.dh;
-                T* kc = reinterpret_cast<T*>(e.kc) + (((size_t)s * e.Hkv + kvh) * e.cap + cidx) * e.dh + ein;
+                const int nk = n - qd, kvh = nk >> sh, ein = nk & (e.dh - 1);
+                T* kc = reinterpret_cast<T*>(e.kc) + (((size_t)row.s * e.Hkv + kvh) * e.cap + row.cidx) * e.dh + ein;
                 store4<T>(kc, a0, b0, a1, b1);
             }
         } else {
             // the V cache is dims-major ([dh][cap] per KV head): four strided stores
-            const int nv = n - qd - kd;
-            const int kvh = nv / e.dh, ein = nv % e.dh;
-            T* vc = reinterpret_cast<T*>(e.vc) + (((size_t)s * e.Hkv + kvh) * e.dh + ein) * e.cap + cidx;
+            const int nv = n - qd - kd, kvh = nv >> sh, ein = nv & (e.dh - 1);
+            T* vc = reinterpret_cast<T*>(e.vc) + (((size_t)row.s * e.Hkv + kvh) * e.dh + ein) * e.cap + row.cidx;
 #pragma unroll
             for (int i = 0; i < 4; ++i) St<T>::st(vc + (size_t)i * e.cap, v[i]);
         }
-        break;
     }
-    }
-}
-
-template <typename T>
-__device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, floatx4 v) {
-    epi_store<T>(e, m, n, v, epi_fetch(e, m, n));
 }
 
 __device__ __forceinline__ bf16x8 ld_nt(const bf16_t* p) {
@@ -218,21 +248,24 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
     }
     EpiArgs ee = e;
     if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
-    float4 pre[NW][NQ];
+    with_kind(e.kind, [&](auto kind) {
+        constexpr int EK = decltype(kind)::value;
+        float4 pre[NW][NQ];
 #pragma unroll
-    for (int j = 0; j < NW; ++j)
+        for (int j = 0; j < NW; ++j)
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
-            pre[j][q] = (m < M && n < N) ? epi_fetch(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+            for (int q = 0; q < NQ; ++q) {
+                const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
+                pre[j][q] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
 #pragma unroll
-    for (int j = 0; j < NW; ++j)
+        for (int j = 0; j < NW; ++j)
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
-            if (m < M && n < N) epi_store<bf16_t>(ee, m, n, res[j][q], pre[j][q]);
-        }
+            for (int q = 0; q < NQ; ++q) {
+                const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
+                if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, res[j][q], pre[j][q]);
+            }
+    });
 }
 
 // ---------------------------------------------------------------- pipelined tiles
@@ -361,24 +394,27 @@ __global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf1
     EpiArgs ee = e;
     if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
     const int nb0 = tn * (T::BN / 16) + wn * WN, m0 = tm * PBM + wm * 64;
+    with_kind(e.kind, [&](auto kind) {
+        constexpr int EK = decltype(kind)::value;
 #pragma unroll
-    for (int jh = 0; jh < WN / 2; ++jh) {   // pairs of column blocks: bounds the prefetch registers
-        float4 pre[2][4];
+        for (int jh = 0; jh < WN / 2; ++jh) {   // pairs of column blocks: bounds the prefetch registers
+            float4 pre[2][4];
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
-                pre[j][i] = (m < M && n < N) ? epi_fetch(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
-            }
+                for (int i = 0; i < 4; ++i) {
+                    const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
+                    pre[j][i] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
-                if (m < M && n < N) epi_store<bf16_t>(ee, m, n, acc[2 * jh + j][i], pre[j][i]);
-            }
-    }
+                for (int i = 0; i < 4; ++i) {
+                    const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
+                    if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, acc[2 * jh + j][i], pre[j][i]);
+                }
+        }
+    });
 }
 
 // ---------------------------------------------------------------- tiled
@@ -449,21 +485,24 @@ __global__ __launch_bounds__(256) void gemm_tiled_bf16(const bf16_t* __restrict_
                 for (int i = 0; i < 4; ++i) acc[j][i] = mfma16x16x32(af[j], bfr[i], acc[j][i]);
         }
     }
-    float4 pre[4][4];
+    with_kind(e.kind, [&](auto kind) {
+        constexpr int EK = decltype(kind)::value;
+        float4 pre[4][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
-            pre[j][i] = (m < M && n < N) ? epi_fetch(e, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
+                pre[j][i] = (m < M && n < N) ? epi_fetch<EK>(e, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
-            if (m < M && n < N) epi_store<bf16_t>(e, m, n, acc[j][i], pre[j][i]);
-        }
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nb_base + wn * 4 + j) + 4 * g, m = m0 + wm * 64 + 16 * i + lr;
+                if (m < M && n < N) epi_store<bf16_t, EK>(e, m, n, acc[j][i], pre[j][i]);
+            }
+    });
 }
 
 // ---------------------------------------------------------------- fp32
@@ -496,7 +535,11 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
         }
         __syncthreads();
     }
-    if (m < M && n < N) epilogue<float>(e, m, n, floatx4{acc[0], acc[1], acc[2], acc[3]});
+    if (m < M && n < N)
+        with_kind(e.kind, [&](auto kind) {
+            constexpr int EK = decltype(kind)::value;
+            epi_store<float, EK>(e, m, n, floatx4{acc[0], acc[1], acc[2], acc[3]}, epi_fetch<EK>(e, m, n));
+        });
 }
 
 // Fragment-major packing of a bf16 weight matrix (see the file comment), with
