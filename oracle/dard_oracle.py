@@ -36,6 +36,12 @@ Parity pins (see ``tests/test_oracle_*.py``):
                                tied; keys = -position), closed forms of entropy
                                and margin, scipy's entropy, exact float32
                                identities of Eq. 7 at w in {0, 1/2, 1}.
+  * full-sequence mode (no prefix cache; full_step_logits)
+                            -- one-layer equality with the prefix-cache step,
+                               a plain forward without the shadow block (rows
+                               outside the block at one layer, every original
+                               row without candidates, P1), and a brute-force
+                               mask from the rules.
   * step_logits / prefill   -- special cases P1 (all-M block), P2 (empty C) and
                                P3 (one-layer independence from C tokens); the
                                full multi-layer logits beyond these cases are
@@ -332,6 +338,78 @@ def step_logits(weights, dims, cache, tok, state, conf, mask_id, flags=0):
     xn = storage(rmsnorm(h, weights["final_norm"], dims["norm_eps"]), dims["dtype"])
     logits = to_f32(xn @ weights["lm_head"].T)
     return logits, block_kv
+
+
+def full_sequence_visible(state, conf, N, blk, flags=0):
+    """Dense mask of the full-sequence mode (no prefix cache): rows and keys
+    are the N positions of the whole sequence (prompt, committed blocks, the
+    current block x at blk..blk+B-1, future all-[Mask] blocks) followed by the
+    B shadow positions s.  Returns bool [N + B, N + B].
+
+    The paper gives the per-state rules of Sec. 3.2 for the current block and
+    its shadow only; this mode reads the rest as plain bidirectional decoding
+    of the original sequence (the appendix on the attention overhead counts
+    the shadow block as B extra queries and keys on top of it):
+      * a query outside the current block sees the N original positions and
+        no shadow key (the shadow exists for verifying the current block);
+      * a query of the current block (x^i or s^i) sees every position outside
+        the current block, and for each block position j exactly one of x^j
+        and s^j, chosen by the state rules (``take_x``).
+    """
+    X = take_x(state, conf, flags)
+    B = X.shape[1]
+    vis = np.zeros((N + B, N + B), dtype=bool)
+    ctx = np.ones(N, dtype=bool)
+    ctx[blk:blk + B] = False
+    for r in range(N):
+        if ctx[r]:
+            vis[r, :N] = True
+    for i in range(B):
+        for row, xrow in ((blk + i, i), (N + i, B + i)):
+            vis[row, :N] = ctx
+            vis[row, blk:blk + B] = X[xrow]
+            vis[row, N:] = ~X[xrow]
+    return vis
+
+
+def full_step_logits(weights, dims, seq, blk, B, state, conf, mask_id, flags=0, all_rows=False):
+    """One DARD step in full-sequence mode: the model runs over the whole
+    sequence plus the shadow block, every step, without a prefix cache (the
+    setting of the paper's single-step latency table).
+
+    seq: [b, N] token ids of the whole sequence, the current block's tokens
+    at blk..blk+B-1 and [Mask] in future blocks.  The shadow block embeds
+    [Mask] at the positions of the current block.  Returns float32-valued
+    logits [b, 2B, V] (x rows of the current block, then its s rows), or with
+    all_rows the logits of all N + B rows.
+    """
+    seq = np.asarray(seq)
+    state = np.asarray(state)
+    conf = np.asarray(conf, dtype=np.float32)
+    b, N = seq.shape
+    ids = np.concatenate([seq, np.full((b, B), mask_id, dtype=seq.dtype)], axis=1)
+    h = to_f32(embed_rows(weights, dims, ids))
+    pos = np.concatenate([np.arange(N), blk + np.arange(B)])
+    scale = 1.0 / math.sqrt(dims["head_dim"])
+    masks = [full_sequence_visible(state[bi], conf[bi], N, blk, flags) for bi in range(b)]
+    for layer in range(dims["n_layers"]):
+        h, _ = _layer(weights["layers"][layer], dims, h, pos, None, lambda bi: masks[bi], scale)
+    xn = storage(rmsnorm(h, weights["final_norm"], dims["norm_eps"]), dims["dtype"])
+    logits = to_f32(xn @ weights["lm_head"].T)
+    if all_rows:
+        return logits
+    rows = np.concatenate([blk + np.arange(B), N + np.arange(B)])
+    return logits[:, rows]
+
+
+def dard_step_full(weights, dims, seq, blk, B, state, conf, params):
+    """A DARD step in full-sequence mode: the forward above, then the same
+    decisions (Alg. 1) on the current block's 2B logit rows."""
+    tok = np.asarray(seq)[:, blk:blk + B]
+    logits = full_step_logits(weights, dims, seq, blk, B, state, conf, params["mask_id"], params.get("flags", 0))
+    out = decide(logits, tok, state, params)
+    out["logits"] = logits
+    return out
 
 
 # --------------------------------------------------------------------------
