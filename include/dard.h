@@ -288,6 +288,30 @@ dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int c
                       uint8_t* state_out, float* conf_out, int32_t* block_done,
                       const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------ a1-a8: full-sequence step
+ * The same step without a prefix cache, in the setting of the paper's
+ * single-step latency table (appendix on latency and memory; the attention
+ * overhead paragraph counts the shadow block as B extra queries and keys):
+ * every step runs the model over the whole sequence of N positions -- prompt,
+ * committed blocks, the current block at positions blk..blk+B-1 and the
+ * future blocks, which hold [Mask] -- plus the current block's shadow.
+ * Mask reading (the paper states the per-state rules for the current block
+ * only): a query outside the current block sees the N original positions and
+ * no shadow key; a query of the current block (x or s) sees every position
+ * outside the block and, for each block position, x^j or s^j by the rules
+ * of dard_build_state_mask.  Decisions as in dard_step.
+ *   seq [b][N] int32 (the current block's tokens at blk..blk+B-1),
+ *   state_in, conf_in, tok_out, state_out, conf_out, block_done as in
+ *   dard_step.  Needs 1 <= B <= 128, 0 <= blk <= N - B, N + B <= cap,
+ *   N <= max_pos; kv sized by dard_kv_bytes(dims, b, cap) (all N + B keys of
+ *   every layer are rewritten by each call) and ws by
+ *   dard_workspace_bytes(dims, b, B, cap). */
+dard_status dard_step_full(const dard_dims* dims, const void* packed, void* kv, int cap, int N, int blk,
+                           const dard_params* params, int b, int B, const int32_t* seq,
+                           const uint8_t* state_in, const float* conf_in, int32_t* tok_out,
+                           uint8_t* state_out, float* conf_out, int32_t* block_done,
+                           const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------ plain linear layer
  * Y[m][n] = sum_k X[m][k] * W[n][k] in float32 (the projection GEMM of every
  * layer and the LM head, exposed for testing and measurement).

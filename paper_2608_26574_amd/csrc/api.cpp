@@ -92,7 +92,7 @@ Layout layout_of(const dard_dims* d) {
 
 // Workspace of dard_step / dard_prefill.
 struct WsLayout {
-    size_t h, xn, q, attn, act, sel, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, total;
+    size_t h, xn, q, attn, act, sel, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, ids, tok, total;
 };
 
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
@@ -119,6 +119,8 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.cpart_v = o; o = align256(o + (size_t)b * B * nch * kConfStatsStride * 4);
     W.cpart_m = o; o = align256(o + (size_t)b * B * nch * kConfStatsStride * 4);
     W.w = o; o = align256(o + (size_t)b * B * 4);
+    W.ids = o; o = align256(o + rows * 4);          // full-sequence mode: row token ids
+    W.tok = o; o = align256(o + (size_t)b * B * 4);   // and the current block's tokens
     // split-K partials of the O and down projections: up to 8 splits of 64
     // rows (streaming GEMM) or 4 splits of all rows (pipelined GEMM)
     const size_t prow = rows * 4 > 8 * 64 ? rows * 4 : 8 * 64;
@@ -427,12 +429,14 @@ struct Fwd {
     }
 };
 
-// The transformer layers over `rows` token rows (R per sequence).  step != 0:
+// The transformer layers over `rows` token rows (R per sequence).  step 1:
 // the rows are the augmented block (x then s) of block length B after P
-// cached keys, attention under the state mask; step == 0: the rows are the P
-// prefix tokens, attention bidirectional among them.
+// cached keys, attention under the state mask; step 0: the rows are the P
+// prefix tokens, attention bidirectional among them; step 2 (full sequence):
+// the P = N - B positions outside the current block (which starts at blk),
+// then its x and s rows, with the keys in the same order.
 int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state, const float* conf,
-               uint32_t flags) {
+               uint32_t flags, int blk = 0) {
     const dard_dims* d = f.d;
     const int dt = d->dtype;
     const int rows = f.b * R;
@@ -449,14 +453,15 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         e.kind = EPI_QKV; e.q = q; e.ldq = qd; e.kc = f.kc(l); e.vc = f.vc(l);
         e.rope = (const float*)(f.pk + f.L.rope);
         e.rows_per_seq = R; e.P = P; e.B = B; e.cap = f.cap; e.Hq = d->n_heads; e.Hkv = d->n_kv_heads; e.dh = dh;
-        e.step = step;
+        e.step = step; e.blk = blk;
         HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wqkv), qd + 2 * kd, e, DARD_K_GEMM_QKV, f.s, fr));
 
         AttnArgs a{};
         a.q = q; a.k = f.kc(l); a.v = f.vc(l); a.out = at; a.state = state; a.conf = conf;
         a.sel = step ? (const uint64_t*)(f.ws + f.W.sel) : nullptr;
         a.b = f.b; a.R = R; a.Hq = d->n_heads; a.Hkv = d->n_kv_heads; a.dh = dh; a.cap = f.cap;
-        a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step; a.scale = 1.f / std::sqrt((float)dh);
+        a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step != 0; a.scale = 1.f / std::sqrt((float)dh);
+        a.ctx_rows = step == 2 ? P : 0;
         a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
         a.part_slots = f.W.part_slots;
         a.out_frag = fr;
@@ -517,35 +522,21 @@ dard_status dard_prefill(const dard_dims* d, const void* packed, void* kv, int c
     return run_layers(f, P, P, 0, 0, nullptr, nullptr, 0);
 }
 
-dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap, int P, const dard_params* params,
-                      int b, int B, const int32_t* tok_in, const uint8_t* state_in, const float* conf_in,
-                      int32_t* tok_out, uint8_t* state_out, float* conf_out, int32_t* block_done,
-                      const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream) {
-    Fwd f;
-    int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
-    if (rc) return rc;
-    rc = check_params(params);
-    if (rc) return rc;
-    if (!tok_in || !state_in || !conf_in || !tok_out || !state_out || !conf_out)
-        return fail(DARD_ERR_ARG, "NULL pointer");
-    if (P < 0 || P + 2 * B > cap || P + B > d->max_pos)
-        return fail(DARD_ERR_SHAPE, "need P >= 0, P + 2B <= cap, P + B <= max_pos");
-    if (params->mask_id < 0 || params->mask_id >= d->vocab) return fail(DARD_ERR_ARG, "mask_id outside the vocab");
-    const int R = 2 * B, rows = b * R, V = d->vocab;
+namespace {
+
+// The end of a step, shared by both modes: LM head over the final-normalised
+// rows xrows (x then s rows of each sequence, b * 2B rows), the shadow
+// confidences of the candidates, verification and guidance weights, the
+// mixed confidences and the transitions (a4-a8).
+int step_tail(const Fwd& f, const dard_params* params, int b, int B, const void* xrows, const int32_t* tok_in,
+              const uint8_t* state_in, int32_t* tok_out, uint8_t* state_out, float* conf_out, int32_t* block_done,
+              const dard_step_debug* dbg) {
+    const dard_dims* d = f.d;
+    const int rows = b * 2 * B, V = d->vocab;
     float* logits = (float*)(f.ws + f.W.logits);
-    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
-    // the state mask (Eq. 2-3) is the same for every layer of the step: build it once
-    {
-        TraceScope ts(DARD_K_MASK, f.s);
-        HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
-    }
-    HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
-                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
-    rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags);
-    if (rc) return rc;
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.y = logits; e.ldy = V;
-    HIPOK(launch_gemm(d->dtype, f.ws + f.W.xn, rows, d->d_model, d->d_model, f.pk + f.L.lm_head, V, e,
+    HIPOK(launch_gemm(d->dtype, xrows, rows, d->d_model, d->d_model, f.pk + f.L.lm_head, V, e,
                       DARD_K_GEMM_HEAD, f.s, frag_rows(d->dtype, rows)));
 
     ConfArgs c{};
@@ -580,6 +571,74 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     if (dbg && dbg->w)
         HIPOK(hipMemcpyAsync(dbg->w, f.ws + f.W.w, (size_t)b * B * 4, hipMemcpyDeviceToDevice, f.s));
     return DARD_OK;
+}
+
+int check_step_args(const dard_dims* d, const dard_params* params, const void* tok, const uint8_t* state_in,
+                    const float* conf_in, const int32_t* tok_out, const uint8_t* state_out, const float* conf_out) {
+    if (int rc = check_params(params)) return rc;
+    if (!tok || !state_in || !conf_in || !tok_out || !state_out || !conf_out) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (params->mask_id < 0 || params->mask_id >= d->vocab) return fail(DARD_ERR_ARG, "mask_id outside the vocab");
+    return DARD_OK;
+}
+
+}  // namespace
+
+dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap, int P, const dard_params* params,
+                      int b, int B, const int32_t* tok_in, const uint8_t* state_in, const float* conf_in,
+                      int32_t* tok_out, uint8_t* state_out, float* conf_out, int32_t* block_done,
+                      const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
+    if (rc) return rc;
+    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out);
+    if (rc) return rc;
+    if (P < 0 || P + 2 * B > cap || P + B > d->max_pos)
+        return fail(DARD_ERR_SHAPE, "need P >= 0, P + 2B <= cap, P + B <= max_pos");
+    const int R = 2 * B, rows = b * R;
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    // the state mask (Eq. 2-3) is the same for every layer of the step: build it once
+    {
+        TraceScope ts(DARD_K_MASK, f.s);
+        HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
+    }
+    HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
+                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
+    rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags);
+    if (rc) return rc;
+    return step_tail(f, params, b, B, f.ws + f.W.xn, tok_in, state_in, tok_out, state_out, conf_out, block_done, dbg);
+}
+
+dard_status dard_step_full(const dard_dims* d, const void* packed, void* kv, int cap, int N, int blk,
+                           const dard_params* params, int b, int B, const int32_t* seq, const uint8_t* state_in,
+                           const float* conf_in, int32_t* tok_out, uint8_t* state_out, float* conf_out,
+                           int32_t* block_done, const dard_step_debug* dbg, void* ws, size_t ws_bytes,
+                           void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
+    if (rc) return rc;
+    rc = check_step_args(d, params, seq, state_in, conf_in, tok_out, state_out, conf_out);
+    if (rc) return rc;
+    if (N < B || blk < 0 || blk + B > N || N + B > cap || N > d->max_pos)
+        return fail(DARD_ERR_SHAPE, "need B <= N, 0 <= blk <= N - B, N + B <= cap, N <= max_pos");
+    const int R = N + B, Nc = N - B, rows = b * R;
+    int32_t* row_ids = (int32_t*)(f.ws + f.W.ids);
+    int32_t* tok = (int32_t*)(f.ws + f.W.tok);
+    HIPOK(launch_full_rows(seq, b, N, blk, B, params->mask_id, row_ids, tok, f.s));
+    {
+        TraceScope ts(DARD_K_MASK, f.s);
+        HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
+    }
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    HIPOK(launch_embed_norm(d->dtype, row_ids, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab,
+                            d->norm_eps, 0, 0, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
+    rc = run_layers(f, R, Nc, B, 2, state_in, conf_in, params->flags, blk);
+    if (rc) return rc;
+    // the current block's x and s rows (the last 2B of each sequence) feed the
+    // LM head; the Q buffer (rows x d_model) is free once the last layer ran
+    void* xrows = f.ws + f.W.q;
+    HIPOK(launch_gather_rows(d->dtype, f.ws + f.W.xn, b, R, Nc, 2 * B, d->d_model, frag_rows(d->dtype, rows), xrows,
+                             f.s));
+    return step_tail(f, params, b, B, xrows, tok, state_in, tok_out, state_out, conf_out, block_done, dbg);
 }
 
 // ---------------------------------------------------------------- linear

@@ -205,9 +205,13 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     }
     uint64_t bv0 = 0, bv1 = 0, bv2 = 0, bv3 = 0;
     if (a.masked && row_ok) {
-        const int W = (a.B + 63) / 64;
-        const uint64_t* sp = a.sel + ((size_t)s * a.R + r) * W;
-        block_vis(sp[0], W > 1 ? sp[1] : 0ull, a.B, bv0, bv1, bv2, bv3);
+        if (r < a.ctx_rows) {   // outside the block: every x key, no shadow key
+            block_vis(~0ull, ~0ull, a.B, bv0, bv1, bv2, bv3);
+        } else {
+            const int W = (a.B + 63) / 64;
+            const uint64_t* sp = a.sel + ((size_t)s * (a.R - a.ctx_rows) + (r - a.ctx_rows)) * W;
+            block_vis(sp[0], W > 1 ? sp[1] : 0ull, a.B, bv0, bv1, bv2, bv3);
+        }
     }
     const float sl2 = a.scale * kLog2e;
     // K row this lane supplies to the S^T MFMAs: key pi(lr) of each 32-key block
@@ -478,15 +482,18 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     float qr[DH], o[DH];
     for (int e = 0; e < DH; ++e) { qr[e] = q[e]; o[e] = 0.f; }
     float m = -INFINITY, l = 0.f;
-    const int i = a.masked ? r % a.B : 0;
-    const bool shadow = a.masked && r >= a.B;
+    // rows before ctx_rows lie outside the block: x keys only
+    const bool ctx = a.masked && r < a.ctx_rows;
+    const int rb = r - a.ctx_rows;
+    const int i = a.masked && !ctx ? rb % a.B : 0;
+    const bool shadow = a.masked && !ctx && rb >= a.B;
     const uint8_t* st = a.masked ? a.state + (size_t)s * a.B : nullptr;
     const float* cf = a.masked ? a.conf + (size_t)s * a.B : nullptr;
     for (int key = 0; key < a.nkeys; ++key) {
         if (a.masked && key >= a.P) {
             const int j = key - a.P;
             const int jj = j < a.B ? j : j - a.B;
-            const bool bx = take_x(st[i], st[jj], cf[i], cf[jj], i, jj, shadow, a.flags);
+            const bool bx = ctx || take_x(st[i], st[jj], cf[i], cf[jj], i, jj, shadow, a.flags);
             if (bx != (j < a.B)) continue;
         }
         float sdot = 0.f;

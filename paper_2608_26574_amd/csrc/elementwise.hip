@@ -201,4 +201,59 @@ hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- full-sequence rows
+__global__ void full_rows_kernel(const int32_t* __restrict__ seq, int N, int blk, int B, int mask_id,
+                                 int32_t* __restrict__ row_ids, int32_t* __restrict__ tok) {
+    const int s = blockIdx.y, R = N + B, Nc = N - B;
+    const int32_t* sq = seq + (size_t)s * N;
+    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < R; r += gridDim.x * blockDim.x) {
+        int id;
+        if (r < Nc) id = sq[r < blk ? r : r + B];
+        else if (r < N) id = sq[blk + (r - Nc)];
+        else id = mask_id;
+        row_ids[(size_t)s * R + r] = id;
+        if (r >= Nc && r < N) tok[(size_t)s * B + (r - Nc)] = id;
+    }
+}
+
+hipError_t launch_full_rows(const int32_t* seq, int b, int N, int blk, int B, int mask_id, int32_t* row_ids,
+                            int32_t* tok, hipStream_t s) {
+    if (b < 1 || B < 1 || N < B || blk < 0 || blk + B > N) return hipErrorInvalidValue;
+    launch(full_rows_kernel, dim3((N + B + 255) / 256, b), dim3(256), 0, s, seq, N, blk, B, mask_id, row_ids, tok);
+    return hipGetLastError();
+}
+
+// One thread per 16 bytes of a destination row.  In the fragment-major layout
+// the 8 bf16 values k..k+7 (k % 8 == 0) of a row are contiguous.
+template <typename T>
+__global__ void gather_rows_kernel(const T* __restrict__ src, int R, int first, int count, int d, int frag,
+                                   T* __restrict__ dst, size_t n16) {
+    constexpr int E = 16 / sizeof(T);
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n16) return;
+    const int per_row = d / E;
+    const int mo = (int)(t / per_row), k = (int)(t % per_row) * E;
+    const int s = mo / count, mi = s * R + first + mo % count;
+    const size_t so = frag ? frag_off(mi, k, d) : (size_t)mi * d + k;
+    const size_t dO = frag ? frag_off(mo, k, d) : (size_t)mo * d + k;
+    *reinterpret_cast<uint4*>(dst + dO) = *reinterpret_cast<const uint4*>(src + so);
+}
+
+hipError_t launch_gather_rows(int dtype, const void* src, int b, int R, int first, int count, int d, bool frag,
+                              void* dst, hipStream_t s) {
+    if (b < 1 || count < 1 || first < 0 || first + count > R || d % (dtype == DARD_DTYPE_BF16 ? 64 : 4))
+        return hipErrorInvalidValue;
+    if (frag && !frag_rows(dtype, b * R)) return hipErrorInvalidValue;
+    const size_t es = dtype == DARD_DTYPE_BF16 ? 2 : 4;
+    const size_t n16 = (size_t)b * count * d * es / 16;
+    const unsigned blocks = (unsigned)((n16 + 255) / 256);
+    if (dtype == DARD_DTYPE_BF16)
+        launch(gather_rows_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t*)src, R, first, count, d,
+               (int)frag, (bf16_t*)dst, n16);
+    else
+        launch(gather_rows_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float*)src, R, first, count, d, 0,
+               (float*)dst, n16);
+    return hipGetLastError();
+}
+
 }  // namespace dard

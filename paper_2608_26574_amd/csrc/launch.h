@@ -31,12 +31,14 @@ struct AttnArgs {
     void* out;          // [b][R][Hq][dh]
     const uint8_t* state;  // [b][B] (masked mode, fp32 path)
     const float* conf;     // [b][B]
-    const uint64_t* sel;   // [b][R][ceil(B/64)] take-x words of the state mask (masked mode, bf16 path)
+    const uint64_t* sel;   // [b][R - ctx_rows][ceil(B/64)] take-x words of the block rows (masked mode, bf16)
     int b, R, Hq, Hkv, dh, cap;
     int P;              // prefix keys (always visible)
     int B;              // block length (masked mode); keys = P + 2B
     int nkeys;          // total keys per sequence
     int masked;         // 1: state-specific mask on keys >= P; 0: all visible
+    int ctx_rows;       // masked mode: leading rows of a sequence outside the block (full-sequence
+                        // mode); they see the P keys and the B x keys, no shadow key
     float scale;
     uint32_t flags;
     float* part;        // key-split partials [nsplit][b][R][Hq][dh] fp32 (bf16 only)
@@ -63,7 +65,10 @@ struct EpiArgs {
     const float* rope;              // [max_pos][dh/2][2] (cos, sin)
     int rows_per_seq;               // R
     int P, B, cap, Hq, Hkv, dh;
-    int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r
+    int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r;
+                                    // 2 (full sequence): cache r, pos r (r < blk), r + B (blk <= r < P),
+                                    //   blk + (r - P) % B (block rows r >= P)
+    int blk;                        // step 2: position of the current block
 };
 // Y = X * W^T with X [M][K] (leading dim ldx, or fragment-major when xfrag),
 // W [N][K] packed (bf16: fragment-major, fp32: row-major); epilogue per `e`.
@@ -91,6 +96,15 @@ hipError_t launch_embed_norm(int dtype, const int32_t* ids, const void* embeds,
 hipError_t launch_resid_norm(int dtype, float* h, const float* part, int nsplit, int rows, int d,
                              const void* gain, float eps, void* xn, bool frag, hipStream_t s);
 hipError_t launch_copy_rows(const void* src, void* dst, size_t bytes, hipStream_t s);
+// Full-sequence mode rows: row_ids [b][N + B] = the sequence seq [b][N] with the
+// current block (positions blk..blk+B-1) moved behind the other N - B
+// positions, then B shadow rows of mask_id; tok [b][B] = the block's tokens.
+hipError_t launch_full_rows(const int32_t* seq, int b, int N, int blk, int B, int mask_id, int32_t* row_ids,
+                            int32_t* tok, hipStream_t s);
+// Copy rows first..first+count-1 of every sequence of R rows ([b*R][d], dtype,
+// fragment-major when frag) to a compact [b*count][d] of the same layout.
+hipError_t launch_gather_rows(int dtype, const void* src, int b, int R, int first, int count, int d, bool frag,
+                              void* dst, hipStream_t s);
 hipError_t launch_pack_rows(const void* src0, const void* src1, void* dst, int nrows, int rowbytes, int mode,
                             int dh, hipStream_t s);
 

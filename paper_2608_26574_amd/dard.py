@@ -28,7 +28,8 @@ EXPORTS = [
     "dard_last_error", "dard_version", "dard_build_state_mask", "dard_attention_workspace_bytes",
     "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
-    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_pack_matrix", "dard_linear", "dard_trace_enable",
+    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_pack_matrix", "dard_linear",
+    "dard_trace_enable",
     "dard_trace_read", "dard_trace_reset",
 ]
 
@@ -84,6 +85,8 @@ def lib():
             "dard_workspace_bytes": (sz, [vp, i32, i32, i32]),
             "dard_prefill": (i32, [vp, vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]),
             "dard_step": (i32, [vp, vp, vp, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "dard_step_full": (i32, [vp, vp, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                     vp]),
             "dard_pack_matrix": (i32, [i32, vp, i32, i32, vp, vp]),
             "dard_linear": (i32, [i32, vp, i32, i32, vp, i32, vp, vp]),
             "dard_trace_enable": (i32, [u32]),
@@ -215,6 +218,13 @@ def dard_trace_reset():
     _check(lib().dard_trace_reset())
 
 
+def _debug(debug):
+    if debug is None:
+        return None
+    return dard_step_debug(*[_p(debug.get(k)) for k in ("logits", "w", "maxprob_s", "argmax_s", "pcur_s",
+                                                        "maxprob_mix", "argmax_mix", "entropy", "margin")])
+
+
 class Engine:
     """Device state of one decoding job: packed weights, KV cache and
     workspace (torch allocations), plus calls of dard_prefill / dard_step."""
@@ -265,11 +275,19 @@ class Engine:
                   debug=None, stream=None):
         b, B = tok_in.shape
         dbg = None
-        if debug is not None:
-            dbg = dard_step_debug(*[_p(debug.get(k)) for k in ("logits", "w", "maxprob_s", "argmax_s", "pcur_s",
-                                                               "maxprob_mix", "argmax_mix", "entropy",
-                                                               "margin")])
+        dbg = _debug(debug)
         _check(lib().dard_step(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap, P,
                                ctypes.byref(params), b, B, _p(tok_in), _p(state_in), _p(conf_in), _p(tok_out),
                                _p(state_out), _p(conf_out), _p(block_done), _ref(dbg), _p(self.ws),
                                self.ws.numel(), _stream(stream)))
+
+    def dard_step_full(self, blk, params, seq, state_in, conf_in, tok_out, state_out, conf_out, block_done=None,
+                       debug=None, stream=None):
+        """Full-sequence step: seq [b][N] (current block at blk..blk+B-1)."""
+        b, N = seq.shape
+        B = state_in.shape[1]
+        dbg = _debug(debug)
+        _check(lib().dard_step_full(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap, N, blk,
+                                    ctypes.byref(params), b, B, _p(seq), _p(state_in), _p(conf_in), _p(tok_out),
+                                    _p(state_out), _p(conf_out), _p(block_done), _ref(dbg), _p(self.ws),
+                                    self.ws.numel(), _stream(stream)))
