@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "DARD decode steps/sec and tokens committed/sec at 8B shape; attention % MFMA peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+TRACE_PERIOD = 33             # timing events on one gate/up launch in 33 inside the timed region
 TOKENS_PER_STEP = 6.0          # mean tokens decoded per DARD step on LLaDA (paper, Sec. on ordering)
 
 
@@ -97,9 +98,12 @@ def main():
         step(t)
     torch.cuda.synchronize()
 
-    # ---- timed region: K steps; the dominant kernel's launches carry HIP timing events
-    # (begin and end timestamps of the kernel itself)
+    # ---- timed region: K steps; one gate/up launch in 33 (about one per step,
+    # a different layer each step) carries HIP timing events, the begin and
+    # end timestamps of the kernel itself (events on every launch would cost
+    # a few microseconds each)
     dard.dard_trace_reset()
+    dard.dard_trace_sample(TRACE_PERIOD)
     dard.dard_trace_enable(1 << dard.K_GEMM_GU)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -113,6 +117,7 @@ def main():
     ms_total = ev0.elapsed_time(ev1)
     dard.dard_trace_enable(0)
     n_gu, ms_gu = dard.dard_trace_read(dard.K_GEMM_GU)
+    dard.dard_trace_sample(1)
     ms_per_step = ms_total / args.steps
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})")
 
@@ -160,6 +165,25 @@ def main():
                  "hbm_frac": round(att_bytes / (att_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                  "ms_per_step": round(att_ms, 4)}
 
+    # ---- the ordering / mixing variants cost: the same steps under each flag
+    variants = {}
+    for vname, vflags in (("entropy_order", dard.F_ORDER_ENTROPY), ("margin_order", dard.F_ORDER_MARGIN),
+                          ("bidirectional", dard.F_C_BIDIR), ("left_to_right", dard.F_ORDER_L2R),
+                          ("fixed_w_0.5", dard.F_FIXED_W)):
+        vp = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, vflags, 0.5)
+
+        def vstep(t):
+            tok, state, conf = inputs[t]
+            eng.dard_step(Ps[t], vp, tok, state, conf, t_out, s_out, c_out, done)
+        vstep(args.warmup)
+        torch.cuda.synchronize()
+        ev0.record()
+        for t in range(args.warmup, total):
+            vstep(t)
+        ev1.record()
+        torch.cuda.synchronize()
+        variants[vname + "_ms_per_step"] = round(ev0.elapsed_time(ev1) / args.steps, 4)
+
     # ---- tokens committed / s: 8 blocks of prefill + ceil(B / 6) steps each
     def generation():
         for k in range(nblocks):
@@ -193,6 +217,7 @@ def main():
         "breakdown_ms_per_step": {k: round(v["ms_per_step"], 4) for k, v in breakdown.items()},
         "kernel_ms_per_step": round(kern_ms, 4),
         "gaps_ms_per_step": round(ms_per_step - kern_ms, 4),
+        "variants": variants,
     }
     out["decision_driven"] = decision_driven(eng, dims, ids, b, B, prompt)
     out["ops"] = op_measurements()
@@ -373,7 +398,74 @@ def full_step_configs(eng8b, steps=6):
                                         "candidate fraction 0.1 / 0.3 / 0.5, prefix KV cache", **rm}
     del engm, ids, embeds
     torch.cuda.empty_cache()
+    out["paper_latency_8b"] = paper_latency_workload(eng8b, steps)
     return out
+
+
+def paper_latency_workload(eng8b, steps=6):
+    """The setting of the paper's single-step latency table, at the 8B shape
+    (the headline model's packed weights, shared): full-sequence steps
+    (dard_step_full: prompt + the whole generation with future [Mask] blocks +
+    the shadow block, no prefix cache), batch 1, a 256-token prompt standing in
+    for a MATH-500 prompt, generation 256 in blocks of 128, candidate fraction
+    0.25; the current block first (one future block) and last.  Block 256
+    needs more than 128 block positions, which the mask words do not hold.
+    The paper's figures (186.8 ms per step at block 128 and 232.0 ms at block
+    256 on an RTX A6000) are context from other hardware, not a target."""
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+
+    d8 = synth.LLADA8B
+    b, B, prompt, gen, frac = 1, 128, 256, 256, 0.25
+    N = prompt + gen
+    eng = dard.Engine(d8, None, b, B, N + B, packed=eng8b.packed)
+    seq = torch.from_numpy(synth.prompt_ids(b, N, d8.vocab, seed=7)).cuda()
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, d8.mask_id, 0)
+    t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    c_out = torch.empty(b, B, device="cuda")
+    done = torch.empty(b, dtype=torch.int32, device="cuda")
+    res = {"workload": "llada8b-like full-sequence DARD step (no prefix cache): batch 1, prompt 256, generation 256, "
+                       "block 128, candidate fraction 0.25",
+           "paper_context": "186.8 ms/step at block 128, 232.0 ms at block 256 (RTX A6000, LLaDA-8B, MATH-500)"}
+    ms_blocks = []
+    for k in range(gen // B):
+        blk = prompt + k * B
+        sq = seq.clone()
+        sq[:, blk + B:] = d8.mask_id
+        ins = []
+        for t in range(steps + 1):
+            tok, state, conf = synth.workload_block(b, B, frac, d8.vocab, seed=4000 + t)
+            sq_t = sq.clone()
+            sq_t[:, blk:blk + B] = torch.from_numpy(tok).cuda()
+            ins.append((sq_t, torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()))
+
+        def step(t):
+            eng.dard_step_full(blk, params, ins[t][0], ins[t][1], ins[t][2], t_out, s_out, c_out, done)
+        step(steps)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(steps):
+            step(t)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        ms_blocks.append(ms)
+        res[f"block{k}_ms_per_step"] = round(ms, 3)
+    # tokens committed / s over the generation at the paper's 6.0 tokens per step
+    S_b = math.ceil(B / TOKENS_PER_STEP)
+    res["tokens_committed_per_s"] = round(b * gen / (S_b * sum(ms_blocks) * 1e-3), 1)
+    res["tokens_committed_note"] = f"{gen // B} blocks x {S_b} steps at the measured per-step times"
+    rows = N + B
+    qd = d8.n_heads * d8.head_dim
+    params_layers = d8.n_layers * (3 * qd * d8.d_model + d8.d_model * qd + 3 * d8.ffn_dim * d8.d_model)
+    flops = 2 * params_layers * rows + 2 * d8.vocab * d8.d_model * 2 * B
+    res["model_tflops"] = round(flops / (min(ms_blocks) * 1e-3) / 1e12, 1)
+    del eng
+    torch.cuda.empty_cache()
+    return res
 
 
 def op_measurements(reps=20):

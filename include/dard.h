@@ -328,7 +328,10 @@ dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, 
  * When enabled, the library brackets each launch of the kernel classes in
  * `class_mask` with HIP events on the launch stream.  dard_trace_read()
  * synchronises with those events and returns, for one class, the number of
- * launches seen and their summed duration since the last reset. */
+ * launches timed and their summed duration since the last reset.  Timing
+ * events cost a few microseconds per launch; dard_trace_sample(n) times only
+ * every n-th launch of each traced class (counted from the last reset;
+ * 1 = every launch, the default). */
 #define DARD_K_GEMM_QKV   0
 #define DARD_K_GEMM_O     1
 #define DARD_K_GEMM_GU    2
@@ -343,6 +346,7 @@ dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, 
 dard_status dard_trace_enable(uint32_t class_mask);
 dard_status dard_trace_read(int kernel_class, int64_t* launches, double* total_ms);
 dard_status dard_trace_reset(void);
+dard_status dard_trace_sample(int period);
 
 #ifdef __cplusplus
 }

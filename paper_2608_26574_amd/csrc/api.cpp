@@ -158,6 +158,8 @@ struct TraceRec {
 std::mutex g_trace_mu;
 uint32_t g_trace_mask = 0;
 std::vector<TraceRec> g_trace[DARD_K_COUNT];
+int g_trace_period = 1;               // every period-th launch of a traced class is timed
+long long g_trace_seen[DARD_K_COUNT];
 
 }  // namespace
 
@@ -173,6 +175,10 @@ TraceScope::~TraceScope() { g_scope = prev; }
 bool TraceScope::next_events(hipEvent_t* a, hipEvent_t* b) {
     const TraceScope* t = g_scope;
     if (!t || !t->on) return false;
+    {
+        std::lock_guard<std::mutex> lk(g_trace_mu);
+        if (g_trace_seen[t->cls]++ % g_trace_period != 0) return false;
+    }
     if (hipEventCreate(a) != hipSuccess) return false;
     if (hipEventCreate(b) != hipSuccess) {
         hipEventDestroy(*a);
@@ -689,8 +695,16 @@ dard_status dard_trace_read(int cls, int64_t* launches, double* total_ms) {
     return DARD_OK;
 }
 
+dard_status dard_trace_sample(int period) {
+    if (period < 1) return fail(DARD_ERR_ARG, "period must be >= 1");
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    g_trace_period = period;
+    return DARD_OK;
+}
+
 dard_status dard_trace_reset(void) {
     std::lock_guard<std::mutex> lk(g_trace_mu);
+    for (auto& n : g_trace_seen) n = 0;
     for (auto& v : g_trace) {
         for (auto& r : v) {
             hipEventSynchronize(r.b);

@@ -30,7 +30,7 @@ EXPORTS = [
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
     "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_pack_matrix", "dard_linear",
     "dard_trace_enable",
-    "dard_trace_read", "dard_trace_reset",
+    "dard_trace_read", "dard_trace_reset", "dard_trace_sample",
 ]
 
 
@@ -92,6 +92,7 @@ def lib():
             "dard_trace_enable": (i32, [u32]),
             "dard_trace_read": (i32, [i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]),
             "dard_trace_reset": (i32, []),
+            "dard_trace_sample": (i32, [i32]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -216,6 +217,10 @@ def dard_trace_read(cls):
 
 def dard_trace_reset():
     _check(lib().dard_trace_reset())
+
+
+def dard_trace_sample(period):
+    _check(lib().dard_trace_sample(period))
 
 
 def _debug(debug):
