@@ -36,6 +36,12 @@ Parity pins (see ``tests/test_oracle_*.py``):
                                tied; keys = -position), closed forms of entropy
                                and margin, scipy's entropy, exact float32
                                identities of Eq. 7 at w in {0, 1/2, 1}.
+  * shared prompt cache (prefill_suffix, join_shared)
+                            -- a dense block-causal forward of prompt +
+                               committed positions, one-layer equality with
+                               the per-sequence prefill, and the batch-shared
+                               cache equal to per-sequence caches of equal
+                               prompts.
   * full-sequence mode (no prefix cache; full_step_logits)
                             -- one-layer equality with the prefix-cache step,
                                a plain forward without the shadow block (rows
@@ -308,6 +314,47 @@ def prefill(weights, dims, ids, embeds=None):
                        lambda bi: allvis, scale)
         cache.append(kv)
     return cache
+
+
+def prefill_suffix(weights, dims, shared, ids, embeds=None):
+    """Per-sequence part of a prefix cache whose first Ps positions are shared
+    by the whole batch (the same image and prompt for every sequence).
+
+    The paper caches the system, visual and text-prompt tokens (appendix on the
+    attention overhead); with one prompt for the batch that cache is computed
+    once, over the prompt alone (``prefill`` with b = 1), and shared.  Reading
+    for the positions after it (each sequence's committed blocks, recomputed at
+    a block start): their rows see the shared prompt and their own positions,
+    bidirectionally among those.
+
+    shared: per layer (K, V) of the prompt, each [1, Ps, Hkv, dh].
+    ids: [b, Pc] ids of the positions Ps..Ps+Pc-1.  Returns per layer (K, V),
+    each [b, Pc, Hkv, dh].
+    """
+    ids = np.asarray(ids)
+    b, Pc = ids.shape
+    Ps = shared[0][0].shape[1] if dims["n_layers"] > 0 else 0
+    h = to_f32(embed_rows(weights, dims, ids, embeds))
+    pos = Ps + np.arange(Pc)
+    scale = 1.0 / math.sqrt(dims["head_dim"])
+    allvis = np.ones((Pc, Ps + Pc), dtype=bool)
+    cache = []
+    for layer in range(dims["n_layers"]):
+        kv_sh = tuple(np.broadcast_to(t, (b,) + t.shape[1:]) for t in shared[layer])
+        h, kv = _layer(weights["layers"][layer], dims, h, pos, kv_sh, lambda bi: allvis, scale)
+        cache.append(kv)
+    return cache
+
+
+def join_shared(shared, suffix):
+    """Per-sequence prefix cache [b, Ps + Pc] from the shared prompt's cache
+    (broadcast over the batch) followed by each sequence's suffix."""
+    out = []
+    for (ks, vs), (kc, vc) in zip(shared, suffix):
+        b = kc.shape[0]
+        out.append((np.concatenate([np.broadcast_to(ks, (b,) + ks.shape[1:]), kc], axis=1),
+                    np.concatenate([np.broadcast_to(vs, (b,) + vs.shape[1:]), vc], axis=1)))
+    return out
 
 
 def step_logits(weights, dims, cache, tok, state, conf, mask_id, flags=0):
