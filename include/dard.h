@@ -288,6 +288,33 @@ dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int c
                       uint8_t* state_out, float* conf_out, int32_t* block_done,
                       const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------ shared prompt cache
+ * Batching many sequences that share one prompt (the same image and text,
+ * appendix on the attention overhead: the system, visual and text-prompt
+ * tokens are prefix-cached): the prompt's cache is computed once, by
+ * dard_prefill with b = 1 over the Ps prompt positions into kv_shared (a KV
+ * cache of the same layout for one sequence and cap_shared keys), and every
+ * sequence reads it in place of its own first Ps keys.  Reading for the
+ * positions after it (each sequence's committed blocks, recomputed at a
+ * block start): their rows see the shared prompt and their own positions,
+ * bidirectionally among those; the prompt is not re-encoded with them.
+ *   dard_prefill_suffix: positions Ps..Ps+Pc-1 of each sequence, ids
+ *     [b][Pc]; writes keys Ps..Ps+Pc-1 of every layer into kv (keys below Ps
+ *     of kv are never read or written).
+ *   dard_step_shared: dard_step with a prefix of P >= Ps keys whose first Ps
+ *     come from kv_shared.
+ * Needs Ps a multiple of 64 (whole key tiles), 64 <= Ps <= cap_shared, and
+ * the sizes of dard_prefill / dard_step for the per-sequence part. */
+dard_status dard_prefill_suffix(const dard_dims* dims, const void* packed, void* kv, int cap,
+                                const void* kv_shared, int cap_shared, int Ps, int b, int Pc,
+                                const int32_t* ids, void* ws, size_t ws_bytes, void* stream);
+dard_status dard_step_shared(const dard_dims* dims, const void* packed, void* kv, int cap,
+                             const void* kv_shared, int cap_shared, int Ps, int P,
+                             const dard_params* params, int b, int B, const int32_t* tok_in,
+                             const uint8_t* state_in, const float* conf_in, int32_t* tok_out,
+                             uint8_t* state_out, float* conf_out, int32_t* block_done,
+                             const dard_step_debug* dbg, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------ a1-a8: full-sequence step
  * The same step without a prefix cache, in the setting of the paper's
  * single-step latency table (appendix on latency and memory; the attention

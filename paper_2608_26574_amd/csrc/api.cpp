@@ -425,6 +425,8 @@ struct Fwd {
     char* ws;
     int b, cap;
     hipStream_t s;
+    const char* kv_sh = nullptr;   // a prompt cache the batch shares (b = 1, cap_sh keys)
+    int cap_sh = 0;
 
     const void* layer(int l, size_t off) const { return pk + L.layer0 + L.layer_stride * l + off; }
     void* kc(int l) const {
@@ -433,6 +435,12 @@ struct Fwd {
     void* vc(int l) const {
         return kv + (size_t)(2 * l + 1) * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
     }
+    const void* kc_sh(int l) const {
+        return kv_sh + (size_t)(2 * l) * d->n_kv_heads * cap_sh * d->head_dim * esize(d->dtype);
+    }
+    const void* vc_sh(int l) const {
+        return kv_sh + (size_t)(2 * l + 1) * d->n_kv_heads * cap_sh * d->head_dim * esize(d->dtype);
+    }
 };
 
 // The transformer layers over `rows` token rows (R per sequence).  step 1:
@@ -440,9 +448,12 @@ struct Fwd {
 // cached keys, attention under the state mask; step 0: the rows are the P
 // prefix tokens, attention bidirectional among them; step 2 (full sequence):
 // the P = N - B positions outside the current block (which starts at blk),
-// then its x and s rows, with the keys in the same order.
+// then its x and s rows, with the keys in the same order; step 3: the rows
+// are the positions P..P+R-1 after a shared prompt of P keys, attention
+// bidirectional over the prompt and themselves.  P_sh > 0: keys [0, P_sh)
+// come from the shared prompt cache f.kv_sh.
 int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state, const float* conf,
-               uint32_t flags, int blk = 0) {
+               uint32_t flags, int blk = 0, int P_sh = 0) {
     const dard_dims* d = f.d;
     const int dt = d->dtype;
     const int rows = f.b * R;
@@ -464,10 +475,15 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
 
         AttnArgs a{};
         a.q = q; a.k = f.kc(l); a.v = f.vc(l); a.out = at; a.state = state; a.conf = conf;
-        a.sel = step ? (const uint64_t*)(f.ws + f.W.sel) : nullptr;
+        a.sel = (step == 1 || step == 2) ? (const uint64_t*)(f.ws + f.W.sel) : nullptr;
         a.b = f.b; a.R = R; a.Hq = d->n_heads; a.Hkv = d->n_kv_heads; a.dh = dh; a.cap = f.cap;
-        a.P = P; a.B = B; a.nkeys = step ? P + 2 * B : P; a.masked = step != 0; a.scale = 1.f / std::sqrt((float)dh);
+        const bool masked = step == 1 || step == 2;
+        a.P = P; a.B = B; a.nkeys = masked ? P + 2 * B : (step == 3 ? P + R : P); a.masked = masked;
+        a.scale = 1.f / std::sqrt((float)dh);
         a.ctx_rows = step == 2 ? P : 0;
+        if (P_sh > 0) {
+            a.k_sh = f.kc_sh(l); a.v_sh = f.vc_sh(l); a.cap_sh = f.cap_sh; a.P_sh = P_sh;
+        }
         a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
         a.part_slots = f.W.part_slots;
         a.out_frag = fr;
@@ -645,6 +661,61 @@ dard_status dard_step_full(const dard_dims* d, const void* packed, void* kv, int
     HIPOK(launch_gather_rows(d->dtype, f.ws + f.W.xn, b, R, Nc, 2 * B, d->d_model, frag_rows(d->dtype, rows), xrows,
                              f.s));
     return step_tail(f, params, b, B, xrows, tok, state_in, tok_out, state_out, conf_out, block_done, dbg);
+}
+
+namespace {
+
+int attach_shared(Fwd& f, const void* kv_shared, int cap_shared, int Ps, int P) {
+    if (!kv_shared) return fail(DARD_ERR_ARG, "NULL shared cache");
+    if (Ps < 64 || Ps % 64 || Ps > cap_shared || Ps > P)
+        return fail(DARD_ERR_SHAPE, "need a shared prompt of 64k keys, 64 <= Ps <= min(cap_shared, P)");
+    f.kv_sh = (const char*)kv_shared;
+    f.cap_sh = cap_shared;
+    return DARD_OK;
+}
+
+}  // namespace
+
+dard_status dard_prefill_suffix(const dard_dims* d, const void* packed, void* kv, int cap, const void* kv_shared,
+                                int cap_shared, int Ps, int b, int Pc, const int32_t* ids, void* ws, size_t ws_bytes,
+                                void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, 1, ws, ws_bytes, stream);
+    if (rc) return rc;
+    if (!ids) return fail(DARD_ERR_ARG, "NULL ids");
+    if (Pc < 1 || Ps + Pc > cap || Ps + Pc > d->max_pos) return fail(DARD_ERR_SHAPE, "need Pc >= 1, Ps + Pc <= min(cap, max_pos)");
+    rc = attach_shared(f, kv_shared, cap_shared, Ps, Ps + Pc);
+    if (rc) return rc;
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    HIPOK(launch_embed_norm(d->dtype, ids, nullptr, f.pk + f.L.embed, gain0, b * Pc, d->d_model, d->vocab, d->norm_eps,
+                            0, 0, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, b * Pc), f.s));
+    return run_layers(f, Pc, Ps, 0, 3, nullptr, nullptr, 0, 0, Ps);
+}
+
+dard_status dard_step_shared(const dard_dims* d, const void* packed, void* kv, int cap, const void* kv_shared,
+                             int cap_shared, int Ps, int P, const dard_params* params, int b, int B,
+                             const int32_t* tok_in, const uint8_t* state_in, const float* conf_in, int32_t* tok_out,
+                             uint8_t* state_out, float* conf_out, int32_t* block_done, const dard_step_debug* dbg,
+                             void* ws, size_t ws_bytes, void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
+    if (rc) return rc;
+    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out);
+    if (rc) return rc;
+    if (P + 2 * B > cap || P + B > d->max_pos) return fail(DARD_ERR_SHAPE, "need P + 2B <= cap, P + B <= max_pos");
+    rc = attach_shared(f, kv_shared, cap_shared, Ps, P);
+    if (rc) return rc;
+    const int R = 2 * B, rows = b * R;
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    {
+        TraceScope ts(DARD_K_MASK, f.s);
+        HIPOK(launch_build_state_mask(state_in, conf_in, b, B, params->flags, (uint64_t*)(f.ws + f.W.sel), f.s));
+    }
+    HIPOK(launch_embed_norm(d->dtype, tok_in, nullptr, f.pk + f.L.embed, gain0, rows, d->d_model, d->vocab, d->norm_eps, B,
+                            params->mask_id, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, rows), f.s));
+    rc = run_layers(f, R, P, B, 1, state_in, conf_in, params->flags, 0, Ps);
+    if (rc) return rc;
+    return step_tail(f, params, b, B, f.ws + f.W.xn, tok_in, state_in, tok_out, state_out, conf_out, block_done, dbg);
 }
 
 // ---------------------------------------------------------------- linear

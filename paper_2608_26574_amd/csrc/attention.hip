@@ -136,6 +136,9 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
 
     const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * cap * DH;
     const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * DH * cap;
+    // keys below P_sh (whole tiles) come from the cache the batch shares
+    const bf16_t* kbase_sh = a.P_sh ? reinterpret_cast<const bf16_t*>(a.k_sh) + (size_t)kvh * a.cap_sh * DH : kbase;
+    const bf16_t* vbase_sh = a.P_sh ? reinterpret_cast<const bf16_t*>(a.v_sh) + (size_t)kvh * DH * a.cap_sh : vbase;
     char* gbase = smem + grp * L::GROUP;
 
     // ---- copy the K (or V^T) tile of key tile `tile` into LDS at `dst`:
@@ -147,22 +150,26 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     // registers element by element.
     auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
+        const bf16_t* kb = k0 < a.P_sh ? kbase_sh : kbase;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
             const int r = q / (DH / 8), sl = q % (DH / 8);
-            const bf16_t* src = kbase + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
+            const bf16_t* src = kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
             if (n == kKeys || r < n)
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
         }
     };
     auto issue_v = [&](int tile, char* dst) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
+        const bool sh = k0 < a.P_sh;
+        const bf16_t* vb = sh ? vbase_sh : vbase;
+        const int vcap = sh ? a.cap_sh : cap;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
             const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
-            const bf16_t* src = vbase + (size_t)d * cap + k0 + 8 * c;
+            const bf16_t* src = vb + (size_t)d * vcap + k0 + 8 * c;
             if (n == kKeys || 8 * c + 8 <= n) {
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
             } else {
@@ -479,6 +486,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
     const float* q = reinterpret_cast<const float*>(a.q) + t * DH;
     const float* kb = reinterpret_cast<const float*>(a.k) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
     const float* vb = reinterpret_cast<const float*>(a.v) + ((size_t)s * a.Hkv + kvh) * a.cap * DH;
+    const float* kb_sh = a.P_sh ? reinterpret_cast<const float*>(a.k_sh) + (size_t)kvh * a.cap_sh * DH : kb;
+    const float* vb_sh = a.P_sh ? reinterpret_cast<const float*>(a.v_sh) + (size_t)kvh * a.cap_sh * DH : vb;
     float qr[DH], o[DH];
     for (int e = 0; e < DH; ++e) { qr[e] = q[e]; o[e] = 0.f; }
     float m = -INFINITY, l = 0.f;
@@ -496,14 +505,18 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
             const bool bx = ctx || take_x(st[i], st[jj], cf[i], cf[jj], i, jj, shadow, a.flags);
             if (bx != (j < a.B)) continue;
         }
+        const bool sh = key < a.P_sh;
+        const float* kk = sh ? kb_sh : kb;
+        const float* vv = sh ? vb_sh : vb;
+        const int vcap = sh ? a.cap_sh : a.cap;
         float sdot = 0.f;
-        for (int e = 0; e < DH; ++e) sdot += qr[e] * kb[(size_t)key * DH + e];
+        for (int e = 0; e < DH; ++e) sdot += qr[e] * kk[(size_t)key * DH + e];
         sdot *= a.scale;
         const float mn = fmaxf(m, sdot);
         const float alpha = expf(m - mn);
         const float p = expf(sdot - mn);
         l = l * alpha + p;
-        for (int e = 0; e < DH; ++e) o[e] = o[e] * alpha + p * vb[(size_t)e * a.cap + key];
+        for (int e = 0; e < DH; ++e) o[e] = o[e] * alpha + p * vv[(size_t)e * vcap + key];
         m = mn;
     }
     float* out = reinterpret_cast<float*>(a.out) + t * DH;

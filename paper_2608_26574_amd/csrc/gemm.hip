@@ -89,6 +89,8 @@ __device__ __forceinline__ QkvRow qkv_row(const EpiArgs& e, int m) {
     const int s = m / e.rows_per_seq, r = m - s * e.rows_per_seq;
     if (e.step == 2)   // full sequence: the other positions, then the block's x and s rows
         return QkvRow{s, r < e.P ? (r < e.blk ? r : r + e.B) : e.blk + (r - e.P) % e.B, r};
+    if (e.step == 3)   // positions after a shared prompt of P
+        return QkvRow{s, e.P + r, e.P + r};
     return QkvRow{s, e.step ? e.P + (r % e.B) : r, e.step ? e.P + r : r};
 }
 

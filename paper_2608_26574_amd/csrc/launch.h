@@ -39,6 +39,9 @@ struct AttnArgs {
     int masked;         // 1: state-specific mask on keys >= P; 0: all visible
     int ctx_rows;       // masked mode: leading rows of a sequence outside the block (full-sequence
                         // mode); they see the P keys and the B x keys, no shadow key
+    const void* k_sh;   // keys [0, P_sh) of every sequence come from one cache shared by the
+    const void* v_sh;   // batch (K [Hkv][cap_sh][dh], V [Hkv][dh][cap_sh]); P_sh % 64 == 0
+    int cap_sh, P_sh;
     float scale;
     uint32_t flags;
     float* part;        // key-split partials [nsplit][b][R][Hq][dh] fp32 (bf16 only)
@@ -67,7 +70,8 @@ struct EpiArgs {
     int P, B, cap, Hq, Hkv, dh;
     int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r;
                                     // 2 (full sequence): cache r, pos r (r < blk), r + B (blk <= r < P),
-                                    //   blk + (r - P) % B (block rows r >= P)
+                                    //   blk + (r - P) % B (block rows r >= P);
+                                    // 3 (positions after a shared prompt of P): pos = cache = P + r
     int blk;                        // step 2: position of the current block
 };
 // Y = X * W^T with X [M][K] (leading dim ldx, or fragment-major when xfrag),

@@ -28,7 +28,8 @@ EXPORTS = [
     "dard_last_error", "dard_version", "dard_build_state_mask", "dard_attention_workspace_bytes",
     "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
-    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_pack_matrix", "dard_linear",
+    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_prefill_suffix",
+    "dard_step_shared", "dard_pack_matrix", "dard_linear",
     "dard_trace_enable",
     "dard_trace_read", "dard_trace_reset", "dard_trace_sample",
 ]
@@ -87,6 +88,9 @@ def lib():
             "dard_step": (i32, [vp, vp, vp, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
             "dard_step_full": (i32, [vp, vp, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                      vp]),
+            "dard_prefill_suffix": (i32, [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp, sz, vp]),
+            "dard_step_shared": (i32, [vp, vp, vp, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                       vp, vp, sz, vp]),
             "dard_pack_matrix": (i32, [i32, vp, i32, i32, vp, vp]),
             "dard_linear": (i32, [i32, vp, i32, i32, vp, i32, vp, vp]),
             "dard_trace_enable": (i32, [u32]),
@@ -285,6 +289,24 @@ class Engine:
                                ctypes.byref(params), b, B, _p(tok_in), _p(state_in), _p(conf_in), _p(tok_out),
                                _p(state_out), _p(conf_out), _p(block_done), _ref(dbg), _p(self.ws),
                                self.ws.numel(), _stream(stream)))
+
+    def dard_prefill_suffix(self, shared, Ps, ids, stream=None):
+        """Positions Ps.. of each sequence after the prompt cached in `shared`
+        (an Engine of the same dims with b = 1 whose dard_prefill ran over Ps
+        prompt positions); ids [b][Pc]."""
+        b, Pc = ids.shape
+        _check(lib().dard_prefill_suffix(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap,
+                                         _p(shared.kv), shared.cap, Ps, b, Pc, _p(ids), _p(self.ws), self.ws.numel(),
+                                         _stream(stream)))
+
+    def dard_step_shared(self, shared, Ps, P, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out,
+                         block_done=None, debug=None, stream=None):
+        b, B = tok_in.shape
+        dbg = _debug(debug)
+        _check(lib().dard_step_shared(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap,
+                                      _p(shared.kv), shared.cap, Ps, P, ctypes.byref(params), b, B, _p(tok_in),
+                                      _p(state_in), _p(conf_in), _p(tok_out), _p(state_out), _p(conf_out),
+                                      _p(block_done), _ref(dbg), _p(self.ws), self.ws.numel(), _stream(stream)))
 
     def dard_step_full(self, blk, params, seq, state_in, conf_in, tok_out, state_out, conf_out, block_done=None,
                        debug=None, stream=None):

@@ -1,0 +1,126 @@
+"""GPU parity of the batch-shared prompt cache: dard_prefill (b = 1) over the
+prompt, dard_prefill_suffix for each sequence's committed positions, and
+dard_step_shared, against the oracle's prefill / prefill_suffix / join_shared
+and its step, with the decision-parity protocol of the step tests."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dard_oracle as O
+from paper_2608_26574_amd import dard, synth
+
+from test_gpu_step import P, check_bf16_logits, check_decisions
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(*a):
+    print("[case]", *a, file=sys.stderr, flush=True)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", n_image=0):
+    V = dims.vocab
+    w = synth.make_weights(dims, seed=seed, device=wdevice)
+    if lm_scale is not None:
+        w["lm_head"] = (w["lm_head"].float() * lm_scale).to(w["lm_head"].dtype)
+    sh = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, 1, B, Ps)
+    eng = dard.Engine(dims, None, b, B, Ps + Pc + 2 * B + 3, packed=sh.packed)
+    prompt = synth.prompt_ids(1, Ps, V, seed=seed + 1)
+    embeds = None
+    if n_image:
+        prompt[:, :n_image] = -1
+        g = torch.Generator().manual_seed(seed + 3)
+        td = torch.float32 if dims.dtype == "f32" else torch.bfloat16
+        embeds = torch.randn(1, Ps, dims.d_model, generator=g).to(td)
+    committed = synth.prompt_ids(b, Pc, V, seed=seed + 4)
+    if frac is None:
+        tok, state, conf = synth.tiny_block(b, B, V, seed=seed + 2)
+    else:
+        tok, state, conf = synth.workload_block(b, B, frac, V, seed=seed + 2)
+    sh.dard_prefill(dev(prompt), embeds=None if embeds is None else embeds.cuda())
+    if Pc:
+        eng.dard_prefill_suffix(sh, Ps, dev(committed))
+    cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
+                          params.get("flags", 0), params.get("w_fixed", 0.0))
+    t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
+    s_out = torch.zeros(b, B, dtype=torch.uint8, device="cuda")
+    c_out = torch.zeros(b, B, device="cuda")
+    done = torch.zeros(b, dtype=torch.int32, device="cuda")
+    dbg = {"logits": torch.zeros(b, 2 * B, V, device="cuda"), "w": torch.zeros(b, B, device="cuda")}
+    eng.dard_step_shared(sh, Ps, Ps + Pc, cp, dev(tok), dev(state), dev(conf), t_out, s_out, c_out, done, debug=dbg)
+    torch.cuda.synchronize()
+    ow = synth.OracleWeights(dims, w)
+    dd = dims.as_dict()
+    shared = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
+    suffix = O.prefill_suffix(ow, dd, shared, committed)
+    cache = O.join_shared(shared, suffix)
+    ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
+
+    def floor(amp=1e-7):
+        rng = np.random.default_rng(0)
+        orig = O.storage
+        O.storage = lambda x, dt: orig(np.asarray(x, dtype=np.float64) * (1.0 + amp * rng.standard_normal(np.shape(x))), dt)
+        try:
+            shp = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
+            c2 = O.join_shared(shp, O.prefill_suffix(ow, dd, shp, committed))
+            l2, _ = O.step_logits(ow, dd, c2, tok, state, conf, params["mask_id"], params.get("flags", 0))
+        finally:
+            O.storage = orig
+        return float(np.max(np.abs(l2 - ref["logits"])))
+
+    ref["floor"] = floor
+    got = dict(logits=dbg["logits"].cpu().numpy(), w=dbg["w"].cpu().numpy(), state_out=s_out.cpu().numpy(),
+               tok_out=t_out.cpu().numpy(), conf_out=c_out.cpu().numpy(), block_done=done.cpu().numpy())
+    # the suffix keys written by dard_prefill_suffix (V of every layer; K is stored with
+    # each head's rotary pairs interleaved)
+    if Pc:
+        kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
+        _, vc = eng.kv_view(kvd)
+        vc = vc.float().cpu().numpy()
+        tol = 1e-4 if dims.dtype == "f32" else 8e-2
+        for layer in range(dims.n_layers):
+            v_gpu = vc[layer, :, :, Ps:Ps + Pc].transpose(0, 2, 1, 3)
+            assert np.max(np.abs(v_gpu - suffix[layer][1])) < tol, layer
+    return tok, state, conf, got, ref
+
+
+@pytest.mark.parametrize("b,Ps,Pc", [(2, 64, 32), (3, 128, 0), (1, 64, 96)])
+def test_tiny_shared_step_fp32(b, Ps, Pc):
+    dims = synth.TINY
+    announce("tiny fp32 shared step", b, Ps, Pc)
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = shared_case(dims, b, Ps, Pc, 32, prm, seed=3, lm_scale=20.0)
+    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    assert err < 1e-4 * 20, err
+    eps, excl = check_decisions(tok, state, got, ref, prm)
+    assert excl <= 1
+
+
+def test_small_shared_step_bf16_gqa():
+    dims = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16")
+    announce("small bf16 shared step")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = shared_case(dims, 4, 128, 64, 32, prm, seed=5, lm_scale=8.0)
+    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    assert err < 2e-2 * 8, err
+    eps, excl = check_decisions(tok, state, got, ref, prm)
+    assert excl <= state.size // 2
+
+
+def test_multimodal_shared_prompt_two_layers():
+    """8B shape, two layers: one 576-embedding image + 256-id prompt shared by
+    a batch of 4, one committed block of 32 per sequence, block 32, candidate
+    fraction 0.3."""
+    dims = synth.truncated(synth.LLADA8B, 2)
+    announce("8B shared multimodal prompt, 2 layers")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = shared_case(dims, 4, 832, 32, 32, prm, seed=4, frac=0.3, wdevice="cuda",
+                                             n_image=576)
+    check_bf16_logits(got, ref, "8B shared prompt 2 layers")
+    check_decisions(tok, state, got, ref, prm)
