@@ -28,7 +28,7 @@ METRIC = "DARD decode steps/sec and tokens committed/sec at 8B shape; attention 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 TRACE_PERIOD = 33             # timing events on one gate/up launch in 33 inside the timed region
-TOKENS_PER_STEP = 6.0          # mean tokens decoded per DARD step on LLaDA (paper, Sec. on ordering)
+TOKENS_PER_STEP = 6.0          # mean tokens decoded per DARD step on LLaDA (App. C.2)
 
 
 def log(*a):

@@ -97,7 +97,7 @@ typedef int dard_status;
 #define DARD_F_ALL    (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS | \
                        DARD_F_ORDERS | DARD_F_FIXED_W)
 
-/* Decoding hyper-parameters (Alg. 1 inputs; Sec. 4.1 uses lambda = 0.5^(1/8),
+/* Decoding hyper-parameters (Alg. 1 inputs; App. A.2 fixes lambda = 0.5^(1/8),
  * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0,
  * and 0 <= w_fixed <= 1 when DARD_F_FIXED_W is set. */
 typedef struct {
@@ -142,7 +142,7 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
                                   uint32_t flags, uint64_t* sel, void* stream);
 
 /* ------------------------------------------------------------ a3: attention
- * State-masked attention over the augmented block (Sec. 2 "parallelized
+ * State-masked attention over the augmented block (Sec. 3.1 "parallelized
  * inference over distinct decoding contexts", Sec. 3.2 masks):
  *   out[s][r][h] = sum_k softmax_k(scale * q[s][r][h] . k_k) v_k
  * over the visible keys of row r: the prefix keys 0..P-1, and for every block
@@ -246,7 +246,7 @@ dard_status dard_pack_weights(const dard_dims* dims, const void* const* src, int
 size_t dard_kv_bytes(const dard_dims* dims, int b, int cap);
 
 /* ------------------------------------------------------------ a9: prefill
- * Prefix KV cache of block decoding (appendix on attention overhead: prefix
+ * Prefix KV cache of block decoding (App. C.5, attention overhead: prefix
  * caching of system, visual and text-prompt tokens).  Runs the model over the
  * P prefix positions of each sequence with bidirectional attention among them
  * and writes K/V[0..P-1] of every layer.
@@ -290,7 +290,7 @@ dard_status dard_step(const dard_dims* dims, const void* packed, void* kv, int c
 
 /* ------------------------------------------------------------ shared prompt cache
  * Batching many sequences that share one prompt (the same image and text,
- * appendix on the attention overhead: the system, visual and text-prompt
+ * App. C.5, attention overhead: the system, visual and text-prompt
  * tokens are prefix-cached): the prompt's cache is computed once, by
  * dard_prefill with b = 1 over the Ps prompt positions into kv_shared (a KV
  * cache of the same layout for one sequence and cap_shared keys), and every
@@ -317,7 +317,7 @@ dard_status dard_step_shared(const dard_dims* dims, const void* packed, void* kv
 
 /* ------------------------------------------------------------ a1-a8: full-sequence step
  * The same step without a prefix cache, in the setting of the paper's
- * single-step latency table (appendix on latency and memory; the attention
+ * single-step latency table (App. C.5, latency and memory table; the attention
  * overhead paragraph counts the shadow block as B extra queries and keys):
  * every step runs the model over the whole sequence of N positions -- prompt,
  * committed blocks, the current block at positions blk..blk+B-1 and the

@@ -76,8 +76,8 @@ F_ORDER_MARGIN = 1 << 7   # ... by top-1 minus top-2 probability, largest first
 F_FIXED_W = 1 << 8        # every M token mixes with the constant w_fixed
 F_ORDERS = F_C_BIDIR | F_ORDER_L2R | F_ORDER_ENTROPY | F_ORDER_MARGIN
 
-LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # Sec. 4.1: lambda = 0.917, i.e. 0.5^(1/8)
-P0_DEFAULT = 0.1                      # Sec. 4.1: prior constant p_0
+LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # App. A.2: lambda = 0.917, i.e. 0.5^(1/8)
+P0_DEFAULT = 0.1                      # App. A.2: prior constant p_0
 
 
 # --------------------------------------------------------------------------
@@ -112,7 +112,7 @@ def storage(x, dtype):
 
 
 # --------------------------------------------------------------------------
-# state-specific attention mask (Sec. 2 "parallelized inference", Eq. 2-3,
+# state-specific attention mask (Sec. 3.1 "parallelized inference", Eq. 2-3,
 # Sec. 3.2 paragraphs on U, C and M tokens)
 # --------------------------------------------------------------------------
 def take_x(state, conf, flags=0):
@@ -296,8 +296,9 @@ def embed_rows(weights, dims, ids, embeds=None):
 
 
 def prefill(weights, dims, ids, embeds=None):
-    """Prefix cache of block decoding (App. "attention overhead": prefix
-    caching).  The prefix tokens attend bidirectionally to each other only.
+    """Prefix cache of block decoding (App. C.5, attention overhead of the
+    shadow sequence: prefix caching).  The prefix tokens attend
+    bidirectionally to each other only.
 
     ids: [b, P] (negative = take ``embeds[b, p]``).  Returns a list over layers
     of (K, V), each [b, P, Hkv, dh], rounded to the storage type.
@@ -320,7 +321,7 @@ def prefill_suffix(weights, dims, shared, ids, embeds=None):
     """Per-sequence part of a prefix cache whose first Ps positions are shared
     by the whole batch (the same image and prompt for every sequence).
 
-    The paper caches the system, visual and text-prompt tokens (appendix on the
+    The paper caches the system, visual and text-prompt tokens (App. C.5, on the
     attention overhead); with one prompt for the batch that cache is computed
     once, over the prompt alone (``prefill`` with b = 1), and shared.  Reading
     for the positions after it (each sequence's committed blocks, recomputed at
@@ -363,7 +364,7 @@ def step_logits(weights, dims, cache, tok, state, conf, mask_id, flags=0):
 
     cache: per layer (K, V) of the prefix, each [b, P, Hkv, dh].
     tok, state, conf: [b, B].  x^i embeds tok[i]; every s^i embeds [Mask].
-    x^i and s^i share the position P + i (Sec. 2).  Returns float32-valued
+    x^i and s^i share the position P + i (Sec. 3.1).  Returns float32-valued
     logits [b, 2B, V] (rows 0..B-1 from x, B..2B-1 from s) and the block's
     per-layer (K, V).
     """
@@ -395,7 +396,7 @@ def full_sequence_visible(state, conf, N, blk, flags=0):
 
     The paper gives the per-state rules of Sec. 3.2 for the current block and
     its shadow only; this mode reads the rest as plain bidirectional decoding
-    of the original sequence (the appendix on the attention overhead counts
+    of the original sequence (App. C.5, on the attention overhead, counts
     the shadow block as B extra queries and keys on top of it):
       * a query outside the current block sees the N original positions and
         no shadow key (the shadow exists for verifying the current block);

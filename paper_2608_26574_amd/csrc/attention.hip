@@ -1,4 +1,4 @@
-// State-masked attention over the augmented block (Sec. 2, Sec. 3.2).
+// State-masked attention over the augmented block (Sec. 3.1, Sec. 3.2).
 //
 // bf16 path: flash-style on v_mfma_f32_32x32x16_bf16.  A workgroup serves
 // 32 * WAVES query rows that read one KV head -- with grouped-query attention

@@ -1,7 +1,7 @@
 """Pins of the oracle's full-sequence mode (no prefix cache): the whole
 sequence, future all-[Mask] blocks included, plus the shadow block run through
 the model at every step (the setting of the paper's single-step latency
-table and of its attention-overhead appendix).
+table and of its attention-overhead paragraph, App. C.5).
 
 The mode is pinned by what its reading fixes exactly: the mask against a
 brute-force construction from the rules; a plain forward of the original
