@@ -128,7 +128,7 @@ int dard_version(void);
 
 /* ------------------------------------------------------------ a1: mask
  * State-specific attention mask of Sec. 3.2 (Eq. 2-4) for b sequences of
- * block length B (1 <= B <= 128).  By Eq. 2 every query row sees exactly one
+ * block length B (1 <= B <= 256).  By Eq. 2 every query row sees exactly one
  * of x^j and s^j, so the block part of the mask is one bit per (row, j):
  *   sel[s][r][w] (uint64, W = ceil(B/64) words per row), bit j%64 of word j/64
  *   = 1 if row r reads x^j, 0 if it reads s^j.
@@ -329,7 +329,7 @@ dard_status dard_step_shared(const dard_dims* dims, const void* packed, void* kv
  * of dard_build_state_mask.  Decisions as in dard_step.
  *   seq [b][N] int32 (the current block's tokens at blk..blk+B-1),
  *   state_in, conf_in, tok_out, state_out, conf_out, block_done as in
- *   dard_step.  Needs 1 <= B <= 128, 0 <= blk <= N - B, N + B <= cap,
+ *   dard_step.  Needs 1 <= B <= 256, 0 <= blk <= N - B, N + B <= cap,
  *   N <= max_pos; kv sized by dard_kv_bytes(dims, b, cap) (all N + B keys of
  *   every layer are rewritten by each call) and ws by
  *   dard_workspace_bytes(dims, b, B, cap). */

@@ -202,7 +202,7 @@ int dard_version(void) { return 1; }
 dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b, int B, uint32_t flags,
                                   uint64_t* sel, void* stream) {
     if (!state || !conf || !sel) return fail(DARD_ERR_ARG, "NULL pointer");
-    if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
+    if (b < 1 || B < 1 || B > 256) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 256");
     if (int rc = check_flags(flags)) return rc;
     HIPOK(launch_build_state_mask(state, conf, b, B, flags, sel, (hipStream_t)stream));
     return DARD_OK;
@@ -237,7 +237,7 @@ AttnWs attn_ws(int dtype, int b, int B, int Hq, int dh, int P) {
 }  // namespace
 
 size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P) {
-    if (b < 1 || B < 1 || B > 128 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16 || (dh != 64 && dh != 128)) return 0;
+    if (b < 1 || B < 1 || B > 256 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16 || (dh != 64 && dh != 128)) return 0;
     return attn_ws(dtype, b, B, Hq, dh, P).total;
 }
 
@@ -248,7 +248,7 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
     if (!q || !k || !v || !state || !conf || !out) return fail(DARD_ERR_ARG, "NULL pointer");
     if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
     if (int rc = check_flags(flags)) return rc;
-    if (b < 1 || B < 1 || B > 128 || P < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || P + 2 * B > cap)
+    if (b < 1 || B < 1 || B > 256 || P < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || P + 2 * B > cap)
         return fail(DARD_ERR_SHAPE, "bad attention shape (b=%d B=%d P=%d cap=%d Hq=%d Hkv=%d)", b, B, P, cap, Hq, Hkv);
     if (dh != 64 && dh != 128) return fail(DARD_ERR_SHAPE, "dh must be 64 or 128");
     const size_t need = dard_attention_workspace_bytes(dtype, b, B, Hq, dh, P);
@@ -306,7 +306,7 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
                                float* conf_out, int32_t* block_done, void* stream) {
     int rc = check_params(params);
     if (rc) return rc;
-    if (b < 1 || B < 1 || B > 128) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 128");
+    if (b < 1 || B < 1 || B > 256) return fail(DARD_ERR_SHAPE, "need b >= 1 and 1 <= B <= 256");
     const bool pcur_mode = params->flags & DARD_F_VERIFY_PCUR;
     if (!state_in) return fail(DARD_ERR_ARG, "NULL state_in");
     if (phase == DARD_PHASE_VERIFY) {
@@ -410,7 +410,7 @@ dard_status dard_pack_weights(const dard_dims* d, const void* const* src, int n_
 
 // ---------------------------------------------------------------- forward
 size_t dard_workspace_bytes(const dard_dims* d, int b, int B, int cap) {
-    if (check_dims(d) || b < 1 || B < 1 || B > 128 || cap < 2 * B) return 0;
+    if (check_dims(d) || b < 1 || B < 1 || B > 256 || cap < 2 * B) return 0;
     return ws_layout(d, b, B, cap).total;
 }
 
@@ -518,7 +518,7 @@ int fwd_setup(Fwd& f, const dard_dims* d, const void* packed, void* kv, int cap,
     int rc = check_dims(d);
     if (rc) return rc;
     if (!packed || !kv || !ws) return fail(DARD_ERR_ARG, "NULL pointer");
-    if (b < 1 || B < 1 || B > 128 || cap < 2 * B) return fail(DARD_ERR_SHAPE, "need b >= 1, 1 <= B <= 128, cap >= 2B");
+    if (b < 1 || B < 1 || B > 256 || cap < 2 * B) return fail(DARD_ERR_SHAPE, "need b >= 1, 1 <= B <= 256, cap >= 2B");
     f.d = d; f.L = layout_of(d); f.W = ws_layout(d, b, B, cap);
     if (ws_bytes < f.W.total) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", f.W.total);
     f.pk = (const char*)packed; f.kv = (char*)kv; f.ws = (char*)ws; f.b = b; f.cap = cap;

@@ -67,26 +67,42 @@ template <int DH>
 __device__ __forceinline__ int kslot(int r, int c) { return r * (DH / 8) + (c ^ (r & (DH / 8 - 1))); }
 __device__ __forceinline__ int vslot(int d, int c) { return d * (kKeys / 8) + (c ^ (d & 7)); }
 
-// The 2B-bit block visibility of a row from its take-x words (x1:x0), B <= 128:
-// bit j (j < B) = x bit j, bit B + j = NOT x bit j; returned as 4 words.
-__device__ __forceinline__ void block_vis(uint64_t x0, uint64_t x1, int B, uint64_t& v0, uint64_t& v1,
-                                          uint64_t& v2, uint64_t& v3) {
-    const uint64_t m0 = B >= 64 ? ~0ull : (1ull << B) - 1;
-    const uint64_t m1 = B >= 128 ? ~0ull : (B > 64 ? (1ull << (B - 64)) - 1 : 0ull);
-    x0 &= m0;
-    x1 &= m1;
-    const uint64_t s0 = ~x0 & m0, s1 = ~x1 & m1;
-    // word i of the 256-bit value (0 : 0 : s1 : s0) << B
-    const int q = B >> 6, r = B & 63;
-    // source word j of (s1 : s0), zero outside
-#define DARD_SRC(j) ((j) == 0 ? s0 : ((j) == 1 ? s1 : 0ull))
-#define DARD_SHL(i) (r ? (DARD_SRC((i) - q) << r) | (DARD_SRC((i) - q - 1) >> (64 - r)) : DARD_SRC((i) - q))
-    v0 = x0 | DARD_SHL(0);
-    v1 = x1 | DARD_SHL(1);
-    v2 = DARD_SHL(2);
-    v3 = DARD_SHL(3);
-#undef DARD_SHL
-#undef DARD_SRC
+// The 2B-bit block visibility of a row, x^j for the set bits j of its take-x
+// value X (B <= 256 bits, zero above B), s^j for the clear ones: bits [0, B)
+// are X, bits [B, 2B) are NOT X.  block_word gives bits [64 bt, 64 bt + 64),
+// the word of block tile bt.
+__device__ __forceinline__ uint64_t word_at(const uint64_t (&x)[kBlockWords], int q) {
+    uint64_t w = 0ull;
+#pragma unroll
+    for (int k = 0; k < kBlockWords; ++k) w = q == k ? x[k] : w;
+    return w;
+}
+// Bits [start, start + 64) of X (start may be negative), zero outside [0, B).
+__device__ __forceinline__ uint64_t bits64(const uint64_t (&x)[kBlockWords], int B, int start) {
+    if (start >= B || start <= -64) return 0ull;
+    uint64_t v;
+    if (start < 0) {
+        v = word_at(x, 0) << (-start);
+    } else {
+        const int q = start >> 6, sh = start & 63;
+        v = word_at(x, q) >> sh;
+        if (sh) v |= word_at(x, q + 1) << (64 - sh);
+    }
+    const int n = B - start;
+    return n < 64 ? v & ((1ull << n) - 1) : v;
+}
+// Bits j of a word with 0 <= start + j < B.
+__device__ __forceinline__ uint64_t range_mask(int start, int B) {
+    const int lo = start < 0 ? -start : 0;
+    const int hi = B - start < 64 ? B - start : 64;
+    if (hi <= lo) return 0ull;
+    const uint64_t up = hi >= 64 ? ~0ull : (1ull << hi) - 1;
+    const uint64_t low = lo >= 64 ? ~0ull : (1ull << lo) - 1;
+    return up & ~low;
+}
+__device__ __forceinline__ uint64_t block_word(const uint64_t (&x)[kBlockWords], int B, int bt) {
+    const int s0 = 64 * bt;
+    return bits64(x, B, s0) | (~bits64(x, B, s0 - B) & range_mask(s0 - B, B));
 }
 
 // First key and key count of tile t (npre prefix tiles over [0, pre_end),
@@ -210,14 +226,19 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             qf[c] = row_ok ? ld_bf16x8(qp + 16 * c + 8 * eta) : z;
         }
     }
-    uint64_t bv0 = 0, bv1 = 0, bv2 = 0, bv3 = 0;
+    uint64_t xw[kBlockWords];     // the row's take-x words
+#pragma unroll
+    for (int q = 0; q < kBlockWords; ++q) xw[q] = 0ull;
     if (a.masked && row_ok) {
+        const int W = (a.B + 63) / 64;
         if (r < a.ctx_rows) {   // outside the block: every x key, no shadow key
-            block_vis(~0ull, ~0ull, a.B, bv0, bv1, bv2, bv3);
+#pragma unroll
+            for (int q = 0; q < kBlockWords; ++q) xw[q] = block_word_mask(a.B, q);
         } else {
-            const int W = (a.B + 63) / 64;
             const uint64_t* sp = a.sel + ((size_t)s * (a.R - a.ctx_rows) + (r - a.ctx_rows)) * W;
-            block_vis(sp[0], W > 1 ? sp[1] : 0ull, a.B, bv0, bv1, bv2, bv3);
+#pragma unroll
+            for (int q = 0; q < kBlockWords; ++q)
+                if (q < W) xw[q] = sp[q];
         }
     }
     const float sl2 = a.scale * kLog2e;
@@ -261,11 +282,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             if (tile < npre) {
                 vis = (1ull << n) - 1;     // n < 64 here
             } else {
-                // word bt of the block visibility, selected with masks (a select
-                // chain here becomes a lookup table in private memory)
-                const uint64_t bt = (uint64_t)(tile - npre);
-                vis = (bv0 & (0ull - (uint64_t)(bt == 0))) | (bv1 & (0ull - (uint64_t)(bt == 1))) |
-                      (bv2 & (0ull - (uint64_t)(bt == 2))) | (bv3 & (0ull - (uint64_t)(bt == 3)));
+                vis = block_word(xw, a.B, tile - npre);
             }
             const uint64_t ww = vis >> (8 * eta);
 #pragma unroll
@@ -584,7 +601,7 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     if (a.out_frag && !frag_rows(dtype, a.b * a.R)) return hipErrorInvalidValue;
     if (a.Hkv < 1 || a.Hq % a.Hkv) return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_BF16) {
-        if (a.masked && (!a.sel || a.B > 128)) return hipErrorInvalidValue;
+        if (a.masked && (!a.sel || a.B > kMaxBlock)) return hipErrorInvalidValue;
         if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
         const int ntiles = attention_tiles(a.masked, a.P, a.B, a.nkeys);
         AttnCfg c = attention_cfg(a.b, a.R, a.Hq, a.Hkv, ntiles);

@@ -105,65 +105,83 @@ __device__ __forceinline__ bool take_x(int si, int sj, float ci, float cj, int i
     return true;
 }
 
-// The same rule for whole rows, one wave at a time: lane l holds positions l
-// and l + 64 of the block (B <= 128), ballots give the U and C sets as bit
-// masks, and a candidate row's set {j in C : c_i <= c_j} (Eq. 3) is one more
-// ballot.  Every lane of the wave must call these with the same arguments.
+// The same rule for whole rows, one wave at a time: lane l holds positions
+// l, l + 64, l + 128 and l + 192 of the block (B <= 256), ballots give the U
+// and C sets as bit masks, and a candidate row's set {j in C : c_i <= c_j}
+// (Eq. 3) is one more ballot per word.  Every lane of the wave must call
+// these with the same arguments.
+constexpr int kMaxBlock = 256;
+constexpr int kBlockWords = kMaxBlock / 64;
+
 struct BlockView {
-    int s0, s1;        // states of positions lane, lane + 64 (-1 beyond B)
-    float c0, c1;      // their confidences
-    uint64_t U0, U1, C0, C1;
+    int st[kBlockWords];       // states of positions lane + 64 q (-1 beyond B)
+    float c[kBlockWords];      // their confidences
+    uint64_t U[kBlockWords], C[kBlockWords];
 };
 
 __device__ __forceinline__ BlockView load_block_view(const uint8_t* state, const float* conf, int B) {
     const int lane = threadIdx.x & 63;
     BlockView v;
-    v.s0 = lane < B ? (int)state[lane] : -1;
-    v.s1 = lane + 64 < B ? (int)state[lane + 64] : -1;
-    v.c0 = lane < B ? conf[lane] : 0.f;
-    v.c1 = lane + 64 < B ? conf[lane + 64] : 0.f;
-    v.U0 = __ballot(v.s0 == DARD_STATE_U);
-    v.U1 = __ballot(v.s1 == DARD_STATE_U);
-    v.C0 = __ballot(v.s0 == DARD_STATE_C);
-    v.C1 = __ballot(v.s1 == DARD_STATE_C);
+#pragma unroll
+    for (int q = 0; q < kBlockWords; ++q) {
+        const int j = lane + 64 * q;
+        v.st[q] = j < B ? (int)state[j] : -1;
+        v.c[q] = j < B ? conf[j] : 0.f;
+        v.U[q] = __ballot(v.st[q] == DARD_STATE_U);
+        v.C[q] = __ballot(v.st[q] == DARD_STATE_C);
+    }
     return v;
 }
 
-// "Take x" words (positions 0..63, 64..127) of query row r (x rows r < B,
-// shadow rows r >= B); r must be the same on every lane.
-__device__ __forceinline__ void row_take_x(const BlockView& v, int r, int B, uint32_t flags, uint64_t& x0,
-                                           uint64_t& x1) {
+// Positions [0, B) as words: bit j of word q set for 64 q + j < B.
+__device__ __forceinline__ uint64_t block_word_mask(int B, int q) {
+    const int n = B - 64 * q;
+    return n >= 64 ? ~0ull : (n > 0 ? (1ull << n) - 1 : 0ull);
+}
+
+// "Take x" words x[q] (positions 64 q .. 64 q + 63) of query row r (x rows
+// r < B, shadow rows r >= B); r must be the same on every lane.
+__device__ __forceinline__ void row_take_x(const BlockView& v, int r, int B, uint32_t flags,
+                                           uint64_t (&x)[kBlockWords]) {
     const int i = r % B;
     const bool shadow = r >= B;
-    const int sa = __shfl(v.s0, i & 63, 64), sb = __shfl(v.s1, i & 63, 64);
-    const float ca = __shfl(v.c0, i & 63, 64), cb = __shfl(v.c1, i & 63, 64);
-    const int si = i < 64 ? sa : sb;
-    const float ci = i < 64 ? ca : cb;
-    const uint64_t self0 = i < 64 ? 1ull << i : 0ull, self1 = i < 64 ? 0ull : 1ull << (i - 64);
-    const uint64_t all0 = B >= 64 ? ~0ull : (1ull << B) - 1;
-    const uint64_t all1 = B >= 128 ? ~0ull : (B > 64 ? (1ull << (B - 64)) - 1 : 0ull);
-    if (si == DARD_STATE_U) {
-        x0 = v.U0; x1 = v.U1;
-        if (shadow || (flags & DARD_F_XSELF_SHADOW)) { x0 &= ~self0; x1 &= ~self1; }
-    } else if (si == DARD_STATE_C) {
-        if (flags & DARD_F_C_BIDIR) {
-            x0 = v.U0 | v.C0; x1 = v.U1 | v.C1;
-        } else if (flags & DARD_F_ORDER_L2R) {
-            // positions 0..i: words below i's word whole, i's word up to bit i
-            const uint64_t upto0 = i < 64 ? (i == 63 ? ~0ull : (2ull << i) - 1) : ~0ull;
-            const uint64_t upto1 = i < 64 ? 0ull : (i == 127 ? ~0ull : (2ull << (i - 64)) - 1);
-            x0 = v.U0 | (v.C0 & upto0); x1 = v.U1 | (v.C1 & upto1);
+    const int qi = i >> 6, li = i & 63;
+    int si = -1;
+    float ci = 0.f;
+#pragma unroll
+    for (int q = 0; q < kBlockWords; ++q) {
+        const int sq = __shfl(v.st[q], li, 64);
+        const float cq = __shfl(v.c[q], li, 64);
+        if (q == qi) { si = sq; ci = cq; }
+    }
+#pragma unroll
+    for (int q = 0; q < kBlockWords; ++q) {
+        const uint64_t self = q == qi ? 1ull << li : 0ull;
+        uint64_t w;
+        if (si == DARD_STATE_U) {
+            w = v.U[q];
+            if (shadow || (flags & DARD_F_XSELF_SHADOW)) w &= ~self;
+        } else if (si == DARD_STATE_C) {
+            uint64_t cw;
+            if (flags & DARD_F_C_BIDIR) {
+                cw = v.C[q];
+            } else if (flags & DARD_F_ORDER_L2R) {
+                // candidates at positions 0..i
+                const uint64_t upto = q < qi ? ~0ull : (q == qi ? (li == 63 ? ~0ull : (2ull << li) - 1) : 0ull);
+                cw = v.C[q] & upto;
+            } else {
+                cw = __ballot(v.st[q] == DARD_STATE_C && ci <= v.c[q]);
+            }
+            w = v.U[q] | cw;
+            if (shadow) w &= ~self;
+        } else if (shadow) {
+            w = v.U[q];
+        } else if (flags & DARD_F_MKEYS_SHADOW) {
+            w = v.U[q] | v.C[q] | self;
         } else {
-            x0 = v.U0 | __ballot(v.s0 == DARD_STATE_C && ci <= v.c0);
-            x1 = v.U1 | __ballot(v.s1 == DARD_STATE_C && ci <= v.c1);
+            w = block_word_mask(B, q);
         }
-        if (shadow) { x0 &= ~self0; x1 &= ~self1; }
-    } else if (shadow) {
-        x0 = v.U0; x1 = v.U1;
-    } else if (flags & DARD_F_MKEYS_SHADOW) {
-        x0 = v.U0 | v.C0 | self0; x1 = v.U1 | v.C1 | self1;
-    } else {
-        x0 = all0; x1 = all1;
+        x[q] = w;
     }
 }
 

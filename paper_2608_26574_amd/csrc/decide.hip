@@ -60,19 +60,22 @@ __device__ Red combine(const float* p, int nchunk, int K) {
 __device__ __forceinline__ float red_entropy(const Red& t) { return logf(t.s) - t.t / t.s; }
 __device__ __forceinline__ float red_margin(const Red& t) { return (1.f - expf(t.m2 - t.m)) / t.s; }
 
+constexpr int kThreads = kMaxBlock;   // one thread per block position
+constexpr size_t kStageBytes = 64 * 1024;   // chunk partials larger than this are read in place
+
 // Copy n floats from global to LDS with all of a thread's loads in flight.
 __device__ void stage(float* dst, const float* src, int n) {
     constexpr int U = 8;
-    for (int base = 0; base < n; base += U * 128) {
+    for (int base = 0; base < n; base += U * kThreads) {
         float v[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const int t = base + k * 128 + threadIdx.x;
+            const int t = base + k * kThreads + threadIdx.x;
             v[k] = t < n ? src[t] : 0.f;
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-            const int t = base + k * 128 + threadIdx.x;
+            const int t = base + k * kThreads + threadIdx.x;
             if (t < n) dst[t] = v[k];
         }
     }
@@ -115,23 +118,29 @@ __device__ __forceinline__ float order_key(uint32_t flags, bool from_partials, f
     return (flags & DARD_F_ORDER_ENTROPY) ? -entropy : margin;
 }
 
-__global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
-    extern __shared__ float staged[];            // [2][B][nchunk][3] in step mode
-    __shared__ uint8_t promoted[128], demoted[128];
-    __shared__ double lam_pow[128];
+__global__ __launch_bounds__(kThreads) void decide_kernel(DecideArgs a, int in_lds) {
+    extern __shared__ float staged[];            // [2][B][nchunk][stride] in step mode (in_lds)
+    __shared__ uint8_t promoted[kThreads], demoted[kThreads];
+    __shared__ double lam_pow[kThreads];
     __shared__ int all_u, entered_u;
-    __shared__ float c_all[128];
-    __shared__ int nxt_all[128], xhat_all[128];
+    __shared__ float c_all[kThreads];
+    __shared__ int nxt_all[kThreads], xhat_all[kThreads];
     const int s = blockIdx.x, i = threadIdx.x;
     const bool live = i < a.B;
     const int pos = s * a.B + i;
     const int st = live ? a.state_in[pos] : DARD_STATE_U;
     const bool pcur_mode = (a.flags & DARD_F_VERIFY_PCUR) != 0;
     const int per_seq = a.B * a.nchunk * a.stride;
-    float* sv = staged;
-    float* sm = staged + per_seq;
-    if (a.part_v) stage(sv, a.part_v + (size_t)s * per_seq, per_seq);
-    if (a.part_m && a.phase == DARD_PHASE_FINAL) stage(sm, a.part_m + (size_t)s * per_seq, per_seq);
+    // the sequence's chunk partials: copied to LDS in one coalesced pass, or
+    // (large blocks) read where they are
+    const float* sv = a.part_v ? a.part_v + (size_t)s * per_seq : nullptr;
+    const float* sm = a.part_m ? a.part_m + (size_t)s * per_seq : nullptr;
+    if (in_lds) {
+        if (a.part_v) stage(staged, sv, per_seq);
+        if (a.part_m && a.phase == DARD_PHASE_FINAL) stage(staged + per_seq, sm, per_seq);
+        sv = a.part_v ? staged : nullptr;
+        sm = a.part_m ? staged + per_seq : nullptr;
+    }
 
     if (a.phase == DARD_PHASE_VERIFY) {
         promoted[i] = 0;
@@ -237,9 +246,11 @@ __global__ __launch_bounds__(128) void decide_kernel(DecideArgs a) {
 
 hipError_t launch_decide(const DecideArgs& a, hipStream_t s) {
     TraceScope ts(DARD_K_DECIDE, s);
-    const size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * a.stride * sizeof(float) : 0;
-    if (lds > 96 * 1024) return hipErrorInvalidValue;
-    launch(decide_kernel, dim3(a.b), dim3(128), lds, s, a);
+    if (a.B < 1 || a.B > kThreads) return hipErrorInvalidValue;
+    size_t lds = (a.part_v || a.part_m) ? (size_t)2 * a.B * a.nchunk * a.stride * sizeof(float) : 0;
+    const int in_lds = lds > 0 && lds <= kStageBytes;
+    if (!in_lds) lds = 0;
+    launch(decide_kernel, dim3(a.b), dim3(kThreads), lds, s, a, in_lds);
     return hipGetLastError();
 }
 

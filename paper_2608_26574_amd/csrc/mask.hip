@@ -16,9 +16,12 @@ __global__ __launch_bounds__(256) void build_state_mask_kernel(const uint8_t* __
     const int W = (B + 63) / 64;
     const BlockView v = load_block_view(state + (size_t)s * B, conf + (size_t)s * B, B);
     for (int r = wave; r < 2 * B; r += 4) {
-        uint64_t x0, x1;
-        row_take_x(v, r, B, flags, x0, x1);
-        if (lane < W) sel[((size_t)s * 2 * B + r) * W + lane] = lane == 0 ? x0 : x1;
+        uint64_t x[kBlockWords];
+        row_take_x(v, r, B, flags, x);
+        uint64_t mine = x[0];
+#pragma unroll
+        for (int q = 1; q < kBlockWords; ++q) mine = lane == q ? x[q] : mine;
+        if (lane < W) sel[((size_t)s * 2 * B + r) * W + lane] = mine;
     }
 }
 

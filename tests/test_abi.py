@@ -48,9 +48,9 @@ def test_host_validation_errors():
     fake = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
     # NULL pointers
     assert L.dard_build_state_mask(None, fake, 1, 4, 0, fake, None) == -1
-    # B outside [1, 128]
+    # B outside [1, 256]
     assert L.dard_build_state_mask(fake, fake, 1, 0, 0, fake, None) == -2
-    assert L.dard_build_state_mask(fake, fake, 1, 129, 0, fake, None) == -2
+    assert L.dard_build_state_mask(fake, fake, 1, 257, 0, fake, None) == -2
     # unknown flag bits; two candidate orderings at once
     assert L.dard_build_state_mask(fake, fake, 1, 4, 1 << 12, fake, None) == -1
     assert b"flag" in L.dard_last_error()

@@ -117,6 +117,34 @@ def test_block128_full_step_fp32():
     assert excl <= state.size // 2
 
 
+def test_block256_full_step_fp32():
+    """Block 256, the longest of the paper's latency table: the whole 256-token
+    generation is one block after a 64-token prompt; fp32."""
+    dims = synth.Dims(2, 256, 4, 4, 64, 512, 2048, 1024, "f32")
+    announce("block-256 fp32 full step")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = full_case(dims, 1, 64, 256, 256, 0, prm, seed=6, lm_scale=8.0)
+    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    assert err < 1e-4 * 8, err
+
+
+def test_llada8b_block256_full_step_two_layers():
+    """The paper's block-256 latency setting at the 8B shape (two layers):
+    prompt 128, one generation block of 256 (its partials exceed the decision
+    kernel's LDS staging, so they are read in place)."""
+    dims = synth.truncated(synth.LLADA8B, 2)
+    announce("llada8b 2-layer full step, block 256")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = full_case(dims, 1, 128, 256, 256, 0, prm, seed=2, frac=0.25, wdevice="cuda")
+    d = got["logits"] - ref["logits"]
+    err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
+    floor = ref["floor"]() if err >= 2e-2 else 0.0
+    print(f"llada8b block-256 full step: max {err:.3e} rms {rms:.3e} floor {floor:.3e}", file=sys.stderr)
+    assert rms < 2e-2
+    assert err < max(2e-2, 2.0 * floor), (err, floor)
+    check_decisions(tok, state, got, ref, prm)
+
+
 def test_llada8b_full_step_two_layers():
     """The paper's latency setting at the 8B shape (two layers): prompt 128,
     generation 256 in blocks of 128, the first block current (one future

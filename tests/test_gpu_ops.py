@@ -45,7 +45,7 @@ def test_linear(dtype, M, N, K):
 
 
 # ---------------------------------------------------------------- mask
-@pytest.mark.parametrize("B", [1, 5, 32, 63, 64, 65, 128])
+@pytest.mark.parametrize("B", [1, 5, 32, 63, 64, 65, 128, 129, 200, 256])
 @pytest.mark.parametrize("flags", [0, O.F_XSELF_SHADOW, O.F_MKEYS_SHADOW, O.F_C_BIDIR, O.F_ORDER_L2R,
                                    O.F_ORDER_L2R | O.F_XSELF_SHADOW, O.F_C_BIDIR | O.F_MKEYS_SHADOW,
                                    O.F_ORDER_ENTROPY, O.F_ORDER_MARGIN | O.F_FIXED_W])
@@ -125,7 +125,9 @@ def test_attention_dream_gqa_shape(P):
     dict(b=3, B=32, P=100, Hq=4, Hkv=4, dh=64),     # head_dim 64
     dict(b=1, B=32, P=4000, Hq=2, Hkv=1, dh=128),   # long prefix: many key splits
     dict(b=2, B=48, P=700, Hq=6, Hkv=2, dh=64),     # head_dim 64, GQA row tiles across heads, key splits
-    dict(b=1, B=128, P=2000, Hq=4, Hkv=4, dh=128),  # maximum block with key splits
+    dict(b=1, B=128, P=2000, Hq=4, Hkv=4, dh=128),  # block 128 with key splits
+    dict(b=1, B=256, P=100, Hq=2, Hkv=1, dh=128),   # maximum block: 8 block tiles, 4 mask words
+    dict(b=2, B=200, P=64, Hq=4, Hkv=2, dh=64),     # ragged block straddling mask words
 ])
 def test_attention_edges_bf16(case):
     announce("attention edge bf16", case)
@@ -321,7 +323,7 @@ def _params(flags=0, tc=0.4, tu=0.9):
     return dict(tau_c=tc, tau_u=tu, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=999, flags=flags)
 
 
-@pytest.mark.parametrize("B", [1, 7, 32, 128])
+@pytest.mark.parametrize("B", [1, 7, 32, 128, 256])
 @pytest.mark.parametrize("flags,tc,tu", [(0, 0.4, 0.9), (O.F_VERIFY_PCUR, 0.3, 0.7), (0, 0.9, 0.9),
                                          (O.F_PROGRESS, 0.4, 1.0), (O.F_PROGRESS | O.F_VERIFY_PCUR, 0.3, 0.7)])
 def test_commit_remask_bit_exact(B, flags, tc, tu):

@@ -183,6 +183,19 @@ def test_tiny_step_fp32():
     assert excl == 0
 
 
+@pytest.mark.parametrize("B", [200, 256])
+def test_tiny_step_fp32_long_block(B):
+    """Blocks longer than 128 positions (up to 4 mask words per row), prompt 64."""
+    dims = synth.TINY
+    announce("tiny fp32 step, block", B)
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = run_case(dims, 1, B, 64, prm, seed=7, lm_scale=20.0)
+    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    assert err < 1e-4 * 20, err
+    eps, excl = check_decisions(tok, state, got, ref, prm)
+    assert excl <= 2
+
+
 @pytest.mark.parametrize("flags,wf", [(0, 0.0), (O.F_XSELF_SHADOW, 0.0), (O.F_MKEYS_SHADOW, 0.0),
                                       (O.F_VERIFY_PCUR, 0.0), (O.F_C_BIDIR, 0.0), (O.F_ORDER_L2R, 0.0),
                                       (O.F_ORDER_ENTROPY, 0.0), (O.F_ORDER_MARGIN, 0.0), (O.F_FIXED_W, 0.0),
