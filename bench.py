@@ -481,68 +481,63 @@ def shared_prompt_workload(eng8b, steps=6):
 
 
 def paper_latency_workload(eng8b, steps=6):
-    """The setting of the paper's single-step latency table, at the 8B shape
-    (the headline model's packed weights, shared): full-sequence steps
+    """The setting of the paper's single-step latency table (App. C.5), at the
+    8B shape (the headline model's packed weights, shared): full-sequence steps
     (dard_step_full: prompt + the whole generation with future [Mask] blocks +
     the shadow block, no prefix cache), batch 1, a 256-token prompt standing in
-    for a MATH-500 prompt, generation 256 in blocks of 128, candidate fraction
-    0.25; the current block first (one future block) and last.  Block 256
-    needs more than 128 block positions, which the mask words do not hold.
-    The paper's figures (186.8 ms per step at block 128 and 232.0 ms at block
-    256 on an RTX A6000) are context from other hardware, not a target."""
+    for a MATH-500 prompt, generation 256, candidate fraction 0.25; block 128
+    (the current block first, with one future block, and last) and block 256
+    (the whole generation one block).  The paper's figures (186.8 ms per step
+    at block 128 and 232.0 ms at block 256 on an RTX A6000) are context from
+    other hardware, not a target."""
     import torch
 
     from paper_2608_26574_amd import dard, synth
 
     d8 = synth.LLADA8B
-    b, B, prompt, gen, frac = 1, 128, 256, 256, 0.25
+    b, prompt, gen, frac = 1, 256, 256, 0.25
     N = prompt + gen
-    eng = dard.Engine(d8, None, b, B, N + B, packed=eng8b.packed)
-    seq = torch.from_numpy(synth.prompt_ids(b, N, d8.vocab, seed=7)).cuda()
+    seq0 = torch.from_numpy(synth.prompt_ids(b, N, d8.vocab, seed=7)).cuda()
     params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, d8.mask_id, 0)
-    t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
-    s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
-    c_out = torch.empty(b, B, device="cuda")
-    done = torch.empty(b, dtype=torch.int32, device="cuda")
     res = {"workload": "llada8b-like full-sequence DARD step (no prefix cache): batch 1, prompt 256, generation 256, "
-                       "block 128, candidate fraction 0.25",
+                       "blocks of 128 and of 256, candidate fraction 0.25",
            "paper_context": "186.8 ms/step at block 128, 232.0 ms at block 256 (RTX A6000, LLaDA-8B, MATH-500)"}
-    ms_blocks = []
-    for k in range(gen // B):
-        blk = prompt + k * B
-        sq = seq.clone()
-        sq[:, blk + B:] = d8.mask_id
-        ins = []
-        for t in range(steps + 1):
-            tok, state, conf = synth.workload_block(b, B, frac, d8.vocab, seed=4000 + t)
-            sq_t = sq.clone()
-            sq_t[:, blk:blk + B] = torch.from_numpy(tok).cuda()
-            ins.append((sq_t, torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()))
+    for B in (128, 256):
+        eng = dard.Engine(d8, None, b, B, N + B, packed=eng8b.packed)
+        t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
+        s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+        c_out = torch.empty(b, B, device="cuda")
+        done = torch.empty(b, dtype=torch.int32, device="cuda")
+        ms_blocks = []
+        for k in range(gen // B):
+            blk = prompt + k * B
+            ins = []
+            for t in range(steps + 1):
+                tok, state, conf = synth.workload_block(b, B, frac, d8.vocab, seed=4000 + t)
+                sq = seq0.clone()
+                sq[:, blk + B:] = d8.mask_id
+                sq[:, blk:blk + B] = torch.from_numpy(tok).cuda()
+                ins.append((sq, torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()))
 
-        def step(t):
-            eng.dard_step_full(blk, params, ins[t][0], ins[t][1], ins[t][2], t_out, s_out, c_out, done)
-        step(steps)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for t in range(steps):
-            step(t)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
-        ms_blocks.append(ms)
-        res[f"block{k}_ms_per_step"] = round(ms, 3)
-    # tokens committed / s over the generation at the paper's 6.0 tokens per step
-    S_b = math.ceil(B / TOKENS_PER_STEP)
-    res["tokens_committed_per_s"] = round(b * gen / (S_b * sum(ms_blocks) * 1e-3), 1)
-    res["tokens_committed_note"] = f"{gen // B} blocks x {S_b} steps at the measured per-step times"
-    rows = N + B
-    qd = d8.n_heads * d8.head_dim
-    params_layers = d8.n_layers * (3 * qd * d8.d_model + d8.d_model * qd + 3 * d8.ffn_dim * d8.d_model)
-    flops = 2 * params_layers * rows + 2 * d8.vocab * d8.d_model * 2 * B
-    res["model_tflops"] = round(flops / (min(ms_blocks) * 1e-3) / 1e12, 1)
-    del eng
-    torch.cuda.empty_cache()
+            def step(t):
+                eng.dard_step_full(blk, params, ins[t][0], ins[t][1], ins[t][2], t_out, s_out, c_out, done)
+            step(steps)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for t in range(steps):
+                step(t)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            ms_blocks.append(ms)
+            res[f"block{B}_{'first' if k == 0 else 'last'}_ms_per_step"] = round(ms, 3)
+        # tokens committed / s over the generation at the paper's 6.0 tokens per step
+        S_b = math.ceil(B / TOKENS_PER_STEP)
+        res[f"block{B}_tokens_committed_per_s"] = round(b * gen / (S_b * sum(ms_blocks) * 1e-3), 1)
+        del eng
+        torch.cuda.empty_cache()
+    res["tokens_committed_note"] = "gen / (ceil(B / 6.0) steps per block x the measured per-step times)"
     return res
 
 
