@@ -9,7 +9,11 @@ Runs, in this order and with inputs rotated through copies larger than the
      prefix 512, block 32, candidate fraction 0.25), 10 calls;
   3. the vocab-wide confidence reduction over 696 rows x 152064 fp32 logits
      (the 7B GQA batch-8 step's rows), 10 calls;
-  4. one 1 GiB device-to-device copy (the calibration of the byte counters).
+  4. 3 DARD steps of the 7B GQA model truncated to 2 layers (28/4 heads x
+     128, d 3584, FFN 18944, vocab 152064, bf16) at batch 8, block 64,
+     prefix 1024: 1024 token rows, so every projection and the LM head run
+     the MFMA-bound tiled GEMM;
+  5. one 1 GiB device-to-device copy (the calibration of the byte counters).
 A profiler pass (rocprofv3 --kernel-trace, or --pmc with MFMA or byte
 counters) attributes each kernel to its operation by name and grid.
 """
@@ -53,6 +57,24 @@ def confidence(rows, V, calls):
     torch.cuda.synchronize()
 
 
+def gqa_steps(steps):
+    dims = synth.truncated(synth.DREAM7B, 2)
+    b, B, P = 8, 64, 1024
+    w = synth.make_weights(dims, seed=1, device="cuda")
+    eng = dard.Engine(dims, w, b, B, P + 2 * B)
+    del w
+    ids = torch.from_numpy(synth.prompt_ids(b, P, dims.vocab, seed=2)).cuda()
+    eng.dard_prefill(ids)
+    tok, state, conf = (torch.from_numpy(a).cuda() for a in synth.workload_block(b, B, 0.3, dims.vocab, seed=3))
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, 0)
+    t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    c_out = torch.empty(b, B, device="cuda")
+    for _ in range(steps):
+        eng.dard_step(P, params, tok, state, conf, t_out, s_out, c_out)
+    torch.cuda.synchronize()
+
+
 def main():
     attention(8, 28, 4, 64, 1024, 0.3, 10, seed=1)
     print("[ops] GQA attention done", flush=True)
@@ -60,6 +82,8 @@ def main():
     print("[ops] MHA attention done", flush=True)
     confidence(8 * 87, 152064, 10)
     print("[ops] confidence done", flush=True)
+    gqa_steps(3)
+    print("[ops] 7B GQA steps done", flush=True)
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
     dst.copy_(src)
