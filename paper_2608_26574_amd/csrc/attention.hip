@@ -546,9 +546,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 //   per group, and a second, phase-shifted key group while the workgroups
 //   alone leave SIMDs idle (7B GQA shape, batch 8: 35.6 -> 31.4 us);
 // - 64 rows (one MHA head's augmented block): with at least 256 workgroups,
-//   2 waves per workgroup (batch 16: 36 us); with fewer, 4 waves (the extra
-//   two only help copy tiles) and key splits of about 3 tiles each merged by
-//   the combine kernel (batch 1, prompt 736: 34 -> 20 us).
+//   2 waves per workgroup (batch 16: 36 us); with few heads (batch 1-2), 4
+//   waves and key splits of about 3 tiles merged by the combine kernel
+//   (batch 1, prompt 736: 34 -> 20 us); in between (batch 4), no split and a
+//   second key group of 2 waves taking alternate tiles (43 -> 35 us).
 struct AttnCfg {
     int waves, g, rowtiles, ns, tps;
 };
@@ -565,11 +566,21 @@ AttnCfg attention_cfg(int b, int R, int Hq, int Hkv, int ntiles) {
         if (wgs * 4 < 1024 && ntiles >= 4) c.g = 2;
     } else {
         c.rowtiles = 1;
+        c.waves = 2;
         const long wgs = (long)b * Hkv;
-        c.waves = wgs >= 256 ? 2 : 4;
-        if (wgs < 256 && ntiles > 3) {
-            c.ns = (ntiles + 2) / 3;
-            c.ns = c.ns < kMaxSplit ? c.ns : kMaxSplit;
+        const long by_tiles = (ntiles + 2) / 3;
+        if (wgs < 256 && wgs * by_tiles <= 256) {
+            // few heads: key splits of about three tiles merged by the combine
+            // kernel, 4 waves per workgroup (the extra two only copy tiles)
+            c.waves = 4;
+            c.ns = (int)(by_tiles < kMaxSplit ? by_tiles : kMaxSplit);
+        } else if (wgs < 256) {
+            // more heads, still short of the chip: splits toward ~128
+            // workgroups, and two key groups of two waves taking alternate tiles
+            long ns = (128 + wgs / 2) / wgs;
+            ns = ns < 1 ? 1 : (ns > kMaxSplit ? kMaxSplit : ns);
+            c.ns = (int)ns;
+            if ((ntiles + c.ns - 1) / c.ns >= 2) c.g = 2;
         }
     }
     c.tps = ntiles > 0 ? (ntiles + c.ns - 1) / c.ns : 1;
