@@ -71,13 +71,14 @@ def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None,
     return tok, state, conf, got, ref
 
 
-@pytest.mark.parametrize("blk_index,flags", [(0, 0), (1, 0), (2, 0), (1, O.F_MKEYS_SHADOW), (1, O.F_ORDER_L2R)])
+@pytest.mark.parametrize("blk_index,flags", [(0, 0), (1, 0), (2, 0), (1, O.F_MKEYS_SHADOW), (1, O.F_ORDER_L2R),
+                                             (0, O.F_ORDER_ENTROPY | O.F_FIXED_W), (2, O.F_C_BIDIR | O.F_PROGRESS)])
 def test_tiny_full_step_fp32(blk_index, flags):
     """Tiny fp32 model, prompt 40, generation 96 in blocks of 32: the current
     block first (two future blocks), in the middle, and last."""
     dims = synth.TINY
     announce("tiny fp32 full step", blk_index, flags)
-    prm = P(dims.mask_id, flags)
+    prm = P(dims.mask_id, flags, w_fixed=0.5)
     tok, state, conf, got, ref = full_case(dims, 1, 40, 96, 32, blk_index, prm, seed=3, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 20, err

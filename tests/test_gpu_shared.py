@@ -90,11 +90,12 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
     return tok, state, conf, got, ref
 
 
-@pytest.mark.parametrize("b,Ps,Pc", [(2, 64, 32), (3, 128, 0), (1, 64, 96)])
-def test_tiny_shared_step_fp32(b, Ps, Pc):
+@pytest.mark.parametrize("b,Ps,Pc,flags", [(2, 64, 32, 0), (3, 128, 0, 0), (1, 64, 96, 0),
+                                          (2, 64, 32, O.F_ORDER_MARGIN | O.F_MKEYS_SHADOW)])
+def test_tiny_shared_step_fp32(b, Ps, Pc, flags):
     dims = synth.TINY
-    announce("tiny fp32 shared step", b, Ps, Pc)
-    prm = P(dims.mask_id)
+    announce("tiny fp32 shared step", b, Ps, Pc, flags)
+    prm = P(dims.mask_id, flags)
     tok, state, conf, got, ref = shared_case(dims, b, Ps, Pc, 32, prm, seed=3, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 20, err
