@@ -55,11 +55,6 @@ struct Lds {
     static constexpr int GROUP = ((5 * TILE > MERGE ? 5 * TILE : MERGE) + 15) / 16 * 16;
 };
 
-// s_waitcnt immediate: at most n vector-memory operations outstanding, no LDS
-// operation outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
-// 6:4 left at its maximum, lgkmcnt 11:8 zero).
-constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
-
 // 16-byte chunk slots: K row r keeps its chunk c (dims 8c..8c+7) in slot
 // c ^ (r % (DH/8)); V^T row d (a dim) keeps its chunk c (keys 8c..8c+7) in
 // slot c ^ (d % 8).
@@ -359,7 +354,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             }
             if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
             else __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
+            wg_barrier();
         }
     } else {
         floatx16 sc[2];
@@ -373,7 +368,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             if (mine(it + 1)) scores(kst(it + 1), sc);
             if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
             else __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
+            wg_barrier();
         }
     }
 

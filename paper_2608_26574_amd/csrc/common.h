@@ -52,6 +52,22 @@ __device__ __forceinline__ floatx16 mfma32x32x16(bf16x8 a, bf16x8 b, floatx16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// s_waitcnt immediate: at most n vector-memory operations outstanding, no LDS
+// operation outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4 left at its maximum, lgkmcnt 11:8 zero).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
+// Workgroup barrier that waits for nothing itself.  __syncthreads() also
+// drains every outstanding vector-memory operation (its fence does), which
+// would cancel copies issued ahead for later steps; callers of wg_barrier
+// first wait (s_waitcnt) for exactly the operations it has to cover.  The
+// empty asm statements keep the compiler from moving memory accesses across.
+__device__ __forceinline__ void wg_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ bf16x8 ld_bf16x8(const bf16_t* p) {
     return *reinterpret_cast<const bf16x8*>(p);
 }

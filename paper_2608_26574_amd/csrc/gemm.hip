@@ -421,6 +421,164 @@ __global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf1
     });
 }
 
+// ---------------------------------------------------------------- large tiles
+// M >= 256 (prefill of long prefixes, large batches) with fragment-major X.
+// A workgroup of 4 waves (2 x 2) owns a (32 TI)-token x (32 TJ)-column output
+// tile; wave (wm, wn) computes 16 TI tokens x 16 TJ columns with TI x TJ
+// accumulator tiles, so every operand read from LDS feeds 8 or 4 MFMAs.  The
+// K loop runs over 32-wide slices (one half of a 64-wide fragment-major unit,
+// 1 KB per 16-row block): a slice stage is the 2 TI activation halves and the
+// 2 TJ weight halves the tile needs, copied with global_load_lds straight into
+// LDS in the layout the MFMA operand reads use (a wave's read is 1 KB
+// contiguous, so conflict-free).  NST stages keep the copies NST - 1 slices
+// ahead of the MFMAs with one barrier per slice; the barrier is the plain
+// s_barrier, since __syncthreads() would also wait for the newer copies.
+// OCC workgroups share a CU (the launches use 2, so one workgroup's copy
+// waits and barriers overlap the other's MFMAs).
+template <int LPW>
+__device__ __forceinline__ void wait_copies(int newer) {   // all but the newest `newer` slices' copies
+    switch (newer) {
+    case 0: __builtin_amdgcn_s_waitcnt(waitcnt_vm(0)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(waitcnt_vm(LPW)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * LPW)); break;
+    default: __builtin_amdgcn_s_waitcnt(waitcnt_vm(3 * LPW)); break;
+    }
+}
+
+template <int TI, int TJ, int NST, int OCC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void gemm_big_bf16(const bf16_t* __restrict__ X, int M, int K, const bf16_t* __restrict__ W, int N, EpiArgs e,
+                   int tiles_m, int tiles_n) {
+    constexpr int XB = 2 * TI, WB = 2 * TJ;        // 16-row blocks per tile side
+    constexpr int STAGE = (XB + WB) * 1024;        // bytes per slice stage
+    constexpr int LPW = (XB + WB) / 4;             // 1 KB copies per wave per slice
+    static_assert((XB + WB) % 4 == 0, "whole copies per wave");
+    static_assert(NST >= 2 && NST <= 5 && 3 * LPW <= 63, "stage count and vmcnt range");
+    static_assert(NST * STAGE >= 4 * (TJ / 2) * TI * 1024, "the epilogue's parking space fits the stages");
+    typedef __attribute__((address_space(3))) void* lds_ptr;
+    typedef __attribute__((address_space(1))) void* glb_ptr;
+    __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 15, g = lane >> 4;
+    // XCD-aware order (workgroups are dealt round-robin to the 8 XCDs): each
+    // XCD gets a contiguous run of tiles, m fastest, so the tiles that share a
+    // weight panel share that XCD's L2
+    const int total = tiles_m * tiles_n;
+    int bid = blockIdx.x;
+    if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+    const int tm = bid % tiles_m, tn = bid / tiles_m;
+    const int KU = K / 64, NB = N / 16, MB = (M + 15) / 16;
+    const int split = blockIdx.y, nsplit = gridDim.y;
+    const int u_begin = (int)((long)KU * split / nsplit), u_end = (int)((long)KU * (split + 1) / nsplit);
+    const int s_begin = 2 * u_begin, nsl = 2 * (u_end - u_begin);
+
+    // this wave's copies: block q = wave * LPW + j of the stage, activation
+    // blocks first; blocks past the matrix re-read its last block (their
+    // results are never stored)
+    const bf16_t* src[LPW];
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+        const int q = wave * LPW + j;
+        if (q < XB) {
+            const int mb = min(tm * XB + q, MB - 1);
+            src[j] = X + (size_t)mb * KU * 1024 + 8 * lane;
+        } else {
+            const int nb = min(tn * WB + (q - XB), NB - 1);
+            src[j] = W + (size_t)nb * KU * 1024 + 8 * lane;
+        }
+    }
+    // slice sl of a block: unit sl / 2, half sl % 2
+    auto issue = [&](int sl, int stage) __attribute__((always_inline)) {
+        const size_t off = (size_t)(sl >> 1) * 1024 + (sl & 1) * 512;
+        char* dst = smem + stage * STAGE + wave * LPW * 1024;
+#pragma unroll
+        for (int j = 0; j < LPW; ++j)
+            __builtin_amdgcn_global_load_lds((glb_ptr)(src[j] + off), (lds_ptr)(dst + j * 1024), 16, 0, 0);
+    };
+
+    floatx4 acc[TJ][TI];
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+        for (int i = 0; i < TI; ++i) acc[j][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int stage) __attribute__((always_inline)) {
+        const char* st = smem + stage * STAGE;
+        bf16x8 xf[TI], wf[TJ];
+#pragma unroll
+        for (int i = 0; i < TI; ++i) xf[i] = *reinterpret_cast<const bf16x8*>(st + (wm * TI + i) * 1024 + 16 * lane);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            wf[j] = *reinterpret_cast<const bf16x8*>(st + (XB + wn * TJ + j) * 1024 + 16 * lane);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int i = 0; i < TI; ++i) acc[j][i] = mfma16x16x32(wf[j], xf[i], acc[j][i]);
+    };
+
+    // Slice t lives in stage t % NST.  Step t waits for its own copies (the
+    // newer ones stay in flight), and the barrier both publishes them and
+    // retires every wave's reads of slice t - 1, whose stage the copy of slice
+    // t + NST - 1 then overwrites.
+#pragma unroll
+    for (int p = 0; p < NST - 1; ++p)
+        if (p < nsl) issue(s_begin + p, p);
+    for (int t = 0; t < nsl; ++t) {
+        wait_copies<LPW>(min(nsl - 1 - t, NST - 2));
+        // (no compiler barrier around it: one keeps the accumulators out of
+        // registers; the LDS reads of the step follow its copy issue, and the
+        // barrier has side effects, so nothing moves across it)
+        __builtin_amdgcn_s_barrier();
+        if (t + NST - 1 < nsl) issue(s_begin + t + NST - 1, (t + NST - 1) % NST);
+        compute(t % NST);
+    }
+
+    // Epilogue through LDS, half the column blocks at a time: each wave parks
+    // its accumulators in its own LDS region (written straight from the
+    // accumulator registers) and reads them back one tile at a time, which
+    // keeps the epilogue's registers small.  Every wave has finished reading
+    // the slice stages once it passes the barrier.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __builtin_amdgcn_s_barrier();
+    EpiArgs ee = e;
+    if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
+    const int nb0 = tn * WB + wn * TJ, m0 = tm * 32 * TI + wm * 16 * TI;
+    floatx4* park = reinterpret_cast<floatx4*>(smem) + wave * (TJ / 2) * TI * 64 + lane;
+    with_kind(e.kind, [&](auto kind) {
+        constexpr int EK = decltype(kind)::value;
+        // the halves are separate instances (compile-time indices into acc,
+        // which must stay in registers)
+        auto half = [&](auto hjc) __attribute__((always_inline)) {
+            constexpr int hj = decltype(hjc)::value;
+#pragma unroll
+            for (int j = 0; j < TJ / 2; ++j)
+#pragma unroll
+                for (int i = 0; i < TI; ++i) park[(j * TI + i) * 64] = acc[hj * (TJ / 2) + j][i];
+            asm volatile("" ::: "memory");   // the tiles are read back from LDS, not forwarded
+#pragma unroll
+            for (int j = 0; j < TJ / 2; ++j) {
+                const int n = 16 * (nb0 + hj * (TJ / 2) + j) + 4 * g;
+                float4 pre[TI];
+#pragma unroll
+                for (int i = 0; i < TI; ++i) {
+                    const int m = m0 + 16 * i + lr;
+                    pre[i] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int i = 0; i < TI; ++i) {
+                    const int m = m0 + 16 * i + lr;
+                    if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, park[(j * TI + i) * 64], pre[i]);
+                }
+            }
+        };
+        half(Kind<0>{});
+        half(Kind<1>{});
+    });
+}
+
 // ---------------------------------------------------------------- tiled
 constexpr int TBM = 128, TBN = 128, TBK = 64, TPAD = TBK + 8;
 
@@ -636,9 +794,45 @@ int pipe_split(int M, int N, int K) {
     return S;
 }
 
+// Large-tile kernel choice for M >= 256: two workgroups per CU, tiles of
+// 256 x 128 (A), 128 x 256 (B) or 128 x 128 (C) tokens x columns.  The time
+// model is rounds of 512 workgroups times the work of one tile over its
+// relative throughput, fitted to kernel-trace sweeps on MI355X over the 7B
+// batch-8 and 8B batch-32 steps (1024 / 2048 rows) and prefills of 640 to
+// 26624 rows: A 1.0, B 0.97 (1.2 from 4096 rows, where each XCD's run of
+// tiles shares a wider weight panel), C 0.72.  Partial (split-K) epilogues
+// split K while there are fewer than two workgroups per CU, keeping at least
+// 8 k units per split.
+struct BigCfg {
+    int ti, tj, split;   // ti == 0: use the pipelined kernel
+};
+BigCfg big_cfg(int M, int N, int K, bool partial) {
+    if (M < 256) return BigCfg{0, 0, 1};
+    const int cand[3][2] = {{8, 4}, {4, 8}, {4, 4}};
+    const double eff[3] = {1.0, M >= 4096 ? 1.2 : 0.97, 0.72};
+    BigCfg best{0, 0, 1};
+    double best_t = 0.0;
+    for (int v = 0; v < 3; ++v) {
+        const int ti = cand[v][0], tj = cand[v][1];
+        const long tiles = (long)((M + 32 * ti - 1) / (32 * ti)) * ((N + 32 * tj - 1) / (32 * tj));
+        int S = 1;
+        if (partial)
+            while (S < 4 && tiles * S < 512 && K / 64 / (2 * S) >= 8) S *= 2;
+        const double t = (double)((tiles * S + 511) / 512) * (32.0 * ti) * (32.0 * tj) * ((double)K / S) / eff[v];
+        if (best.ti == 0 || t < best_t) {
+            best = BigCfg{ti, tj, S};
+            best_t = t;
+        }
+    }
+    return best;
+}
+
 int gemm_split(int dtype, int M, int N, int K) {
     if (dtype != DARD_DTYPE_BF16) return 1;
-    if (M > 64) return pipe_split(M, N, K);
+    if (M > 64) {
+        const BigCfg c = big_cfg(M, N, K, true);
+        return c.ti ? c.split : pipe_split(M, N, K);
+    }
     return stream_cfg(N, K, true).split;
 }
 
@@ -675,6 +869,18 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
         return hipGetLastError();
     }
     if (xfrag) {
+        const BigCfg c = big_cfg(M, N, K, e.kind == EPI_PARTIAL);
+        if (c.ti) {
+            const int tiles_m = (M + 32 * c.ti - 1) / (32 * c.ti), tiles_n = (N + 32 * c.tj - 1) / (32 * c.tj);
+            const dim3 grid(tiles_m * tiles_n, c.split);
+            if (c.ti == 8)
+                launch(gemm_big_bf16<8, 4, 3, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
+            else if (c.tj == 8)
+                launch(gemm_big_bf16<4, 8, 3, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
+            else
+                launch(gemm_big_bf16<4, 4, 5, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
+            return hipGetLastError();
+        }
         const int tiles_m = (M + PBM - 1) / PBM, tiles_n = (N + PipeTile<4>::BN - 1) / PipeTile<4>::BN;
         const int S = e.kind == EPI_PARTIAL ? pipe_split(M, N, K) : 1;
         launch(gemm_pipe_bf16<4>, dim3(tiles_m * tiles_n, S), dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);

@@ -222,9 +222,12 @@ def test_tiny_step_fp32_transitions(flags, wf):
     dict(d=512, H=4, Hkv=2, dh=128, F=1024, V=2048, b=1, B=7, P=3, L=2),
     dict(d=512, H=4, Hkv=1, dh=128, F=512, V=1024, b=3, B=24, P=50, L=1),   # 144 rows: tiled GEMMs
     dict(d=512, H=8, Hkv=8, dh=64, F=1024, V=2048, b=1, B=20, P=60, L=2),    # 40 and 60 rows: ragged last block
+    dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=1, B=16, P=300, L=2),    # 300 prefill rows: 128 x 128 large tiles
+    dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=4, B=16, P=1030, L=1),   # 4120 prefill rows: 128 x 256 large tiles
 ])
 def test_small_step_bf16(case):
-    dims = synth.Dims(case["L"], case["d"], case["H"], case["Hkv"], case["dh"], case["F"], case["V"], 512, "bf16")
+    dims = synth.Dims(case["L"], case["d"], case["H"], case["Hkv"], case["dh"], case["F"], case["V"],
+                      max(512, case["P"] + case["B"] + 8), "bf16")
     announce("small bf16 step", case)
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = run_case(dims, case["b"], case["B"], case["P"], prm, seed=3, lm_scale=8.0)
