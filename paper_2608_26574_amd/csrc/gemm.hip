@@ -22,7 +22,11 @@
 //     summed in LDS in a fixed order; DEPTH units per wave are in flight in a
 //     register ring.  Weights are read with non-temporal loads (streamed once).
 //     Optional split of K across SPLIT workgroups writes fp32 partials.
-//   gemm_tiled: 128 x 128 tiles through LDS for large M (prefill, big batches).
+//   gemm_pipe: 64 < M < 256 with fragment-major X, 128 x 128 tiles through a
+//     register ring and an LDS double buffer.
+//   gemm_big: M >= 256 with fragment-major X (prefill, large batches), tiles of
+//     up to 256 x 128 / 128 x 256 fed by global_load_lds slice stages.
+//   gemm_tiled: row-major X (dard_linear), 128 x 128 tiles through LDS.
 #include "common.h"
 #include "launch.h"
 

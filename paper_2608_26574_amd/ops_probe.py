@@ -12,7 +12,7 @@ Runs, in this order and with inputs rotated through copies larger than the
   4. 3 DARD steps of the 7B GQA model truncated to 2 layers (28/4 heads x
      128, d 3584, FFN 18944, vocab 152064, bf16) at batch 8, block 64,
      prefix 1024: 1024 token rows, so every projection and the LM head run
-     the MFMA-bound tiled GEMM;
+     the MFMA-bound large-tile GEMM;
   5. one 1 GiB device-to-device copy (the calibration of the byte counters).
 A profiler pass (rocprofv3 --kernel-trace, or --pmc with MFMA or byte
 counters) attributes each kernel to its operation by name and grid.

@@ -220,7 +220,7 @@ def test_tiny_step_fp32_transitions(flags, wf):
 @pytest.mark.parametrize("case", [
     dict(d=256, H=4, Hkv=4, dh=64, F=512, V=4096, b=2, B=16, P=40, L=2),
     dict(d=512, H=4, Hkv=2, dh=128, F=1024, V=2048, b=1, B=7, P=3, L=2),
-    dict(d=512, H=4, Hkv=1, dh=128, F=512, V=1024, b=3, B=24, P=50, L=1),   # 144 rows: tiled GEMMs
+    dict(d=512, H=4, Hkv=1, dh=128, F=512, V=1024, b=3, B=24, P=50, L=1),   # 144 rows: pipelined GEMMs
     dict(d=512, H=8, Hkv=8, dh=64, F=1024, V=2048, b=1, B=20, P=60, L=2),    # 40 and 60 rows: ragged last block
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=1, B=16, P=300, L=2),    # 300 prefill rows: 128 x 128 large tiles
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=4, B=16, P=1030, L=1),   # 4120 prefill rows: 128 x 256 large tiles
@@ -280,7 +280,7 @@ def test_multimodal_prefix_two_layers():
 
 def test_dream7b_gqa_two_layers():
     """GQA shape (28 query / 4 KV heads, d 3584, FFN 18944, vocab 152064),
-    block 64: 256 step rows go through the tiled GEMMs; two layers, batch 2."""
+    block 64: 256 step rows go through the large-tile GEMMs; two layers, batch 2."""
     dims = synth.truncated(synth.DREAM7B, 2)
     announce("dream7b gqa 2-layer step")
     prm = P(dims.mask_id)
