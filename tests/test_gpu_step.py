@@ -224,6 +224,7 @@ def test_tiny_step_fp32_transitions(flags, wf):
     dict(d=512, H=8, Hkv=8, dh=64, F=1024, V=2048, b=1, B=20, P=60, L=2),    # 40 and 60 rows: ragged last block
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=1, B=16, P=300, L=2),    # 300 prefill rows: 128 x 128 large tiles
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=4, B=16, P=1030, L=1),   # 4120 prefill rows: 128 x 256 large tiles
+    dict(d=320, H=5, Hkv=5, dh=64, F=576, V=1040, b=1, B=12, P=300, L=1),    # ragged last column tile in every GEMM
 ])
 def test_small_step_bf16(case):
     dims = synth.Dims(case["L"], case["d"], case["H"], case["Hkv"], case["dh"], case["F"], case["V"],
