@@ -122,7 +122,7 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.ids = o; o = align256(o + rows * 4);          // full-sequence mode: row token ids
     W.tok = o; o = align256(o + (size_t)b * B * 4);   // and the current block's tokens
     // split-K partials of the O and down projections: up to 8 splits of 64
-    // rows (streaming GEMM) or 4 splits of all rows (pipelined GEMM)
+    // rows (streaming GEMM) or 4 splits of all rows (pipelined and large-tile GEMMs)
     const size_t prow = rows * 4 > 8 * 64 ? rows * 4 : 8 * 64;
     W.gpart = o; o = align256(o + prow * d->d_model * 4);
     W.total = o;
