@@ -799,12 +799,16 @@ int pipe_split(int M, int N, int K) {
 }
 
 // Large-tile kernel choice for M >= 256: two workgroups per CU, tiles of
-// 256 x 128 (A), 128 x 256 (B) or 128 x 128 (C) tokens x columns.  The time
-// model is rounds of 512 workgroups times the work of one tile over its
-// relative throughput, fitted to kernel-trace sweeps on MI355X over the 7B
-// batch-8 and 8B batch-32 steps (1024 / 2048 rows) and prefills of 640 to
-// 26624 rows: A 1.0, B 0.97 (1.2 from 4096 rows, where each XCD's run of
-// tiles shares a wider weight panel), C 0.72.  Partial (split-K) epilogues
+// 256 x 128 (A), 128 x 256 (B), 128 x 128 (C) or 128 x 192 (D) tokens x
+// columns.  The time model is rounds of 512 workgroups times the work of one
+// tile over its relative throughput (a round costs about the same however
+// full it is), fitted to kernel-trace sweeps on MI355X over the 7B batch-8
+// and 8B batch-32 steps (1024 / 2048 rows) and prefills of 640 to 26624
+// rows: A 1.0, B 0.97 (1.2 from 4096 rows, where each XCD's run of tiles
+// shares a wider weight panel), C 0.72, D 0.9 (D only without a K split: as
+// split-K partials it measured 12-24 % slower than A at 640 rows; with full
+// sums it takes 9-17 % off the QKV and gate/up projections of 700-800-row
+// prefills and 4 % off the 8B batch-32 QKV).  Partial (split-K) epilogues
 // split K while there are fewer than two workgroups per CU, keeping at least
 // 8 k units per split.
 struct BigCfg {
@@ -812,11 +816,12 @@ struct BigCfg {
 };
 BigCfg big_cfg(int M, int N, int K, bool partial) {
     if (M < 256) return BigCfg{0, 0, 1};
-    const int cand[3][2] = {{8, 4}, {4, 8}, {4, 4}};
-    const double eff[3] = {1.0, M >= 4096 ? 1.2 : 0.97, 0.72};
+    const int cand[4][2] = {{8, 4}, {4, 8}, {4, 4}, {4, 6}};
+    const double eff[4] = {1.0, M >= 4096 ? 1.2 : 0.97, 0.72, 0.9};
     BigCfg best{0, 0, 1};
     double best_t = 0.0;
-    for (int v = 0; v < 3; ++v) {
+    for (int v = 0; v < 4; ++v) {
+        if (v == 3 && partial) continue;
         const int ti = cand[v][0], tj = cand[v][1];
         const long tiles = (long)((M + 32 * ti - 1) / (32 * ti)) * ((N + 32 * tj - 1) / (32 * tj));
         int S = 1;
@@ -881,6 +886,8 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
                 launch(gemm_big_bf16<8, 4, 3, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
             else if (c.tj == 8)
                 launch(gemm_big_bf16<4, 8, 3, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
+            else if (c.tj == 6)
+                launch(gemm_big_bf16<4, 6, 4, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
             else
                 launch(gemm_big_bf16<4, 4, 5, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
             return hipGetLastError();
