@@ -24,8 +24,12 @@
  *     first; on any violation nothing is enqueued and the call returns
  *     DARD_ERR_ARG / DARD_ERR_SHAPE / DARD_ERR_UNSUPPORTED.  A failing HIP call
  *     returns DARD_ERR_HIP.  dard_last_error() gives a thread-local message.
- *   - Token state codes outside {0,1,2} in device arrays are not checked and
- *     give unspecified (but memory-safe) results.
+ *   - Token state codes outside {0,1,2} in device arrays give unspecified
+ *     (but memory-safe) results.  They are found by dard_check_states(), or,
+ *     inside a step, with the DARD_F_CHECK_STATES flag (see block_done).
+ *   - Token ids in device arrays are clamped into [0, vocab) wherever a
+ *     kernel indexes a table or a logit row with them (memory-safe; an id
+ *     outside the vocabulary reads the nearest valid entry).
  */
 #ifndef DARD_H
 #define DARD_H
@@ -83,7 +87,14 @@ typedef int dard_status;
  *   ORDER_MARGIN  ordered by the margin p_(1) - p_(2) of the two largest
  *                 probabilities, largest first: the carried key is the margin;
  *   FIXED_W       every masked token mixes its logits with the constant
- *                 params.w_fixed instead of the weight of Eq. 5-6. */
+ *                 params.w_fixed instead of the weight of Eq. 5-6.
+ * Validation:
+ *   CHECK_STATES  the steps (dard_step, dard_step_full, dard_step_shared) and
+ *                 the FINAL phase of dard_commit_remask check every state
+ *                 code of state_in: a sequence holding a code outside {0,1,2}
+ *                 gets block_done[s] = DARD_BAD_STATE instead of 0 / 1
+ *                 (block_done must then be given).  The codes themselves are
+ *                 the caller's: there is no other effect on the results. */
 #define DARD_F_XSELF_SHADOW   (1u << 0)
 #define DARD_F_MKEYS_SHADOW   (1u << 1)
 #define DARD_F_VERIFY_PCUR    (1u << 2)
@@ -93,9 +104,14 @@ typedef int dard_status;
 #define DARD_F_ORDER_ENTROPY  (1u << 6)
 #define DARD_F_ORDER_MARGIN   (1u << 7)
 #define DARD_F_FIXED_W        (1u << 8)
+#define DARD_F_CHECK_STATES   (1u << 9)
 #define DARD_F_ORDERS (DARD_F_C_BIDIR | DARD_F_ORDER_L2R | DARD_F_ORDER_ENTROPY | DARD_F_ORDER_MARGIN)
 #define DARD_F_ALL    (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS | \
-                       DARD_F_ORDERS | DARD_F_FIXED_W)
+                       DARD_F_ORDERS | DARD_F_FIXED_W | DARD_F_CHECK_STATES)
+
+/* block_done value of a sequence whose state_in held a code outside {0,1,2}
+ * (only with DARD_F_CHECK_STATES). */
+#define DARD_BAD_STATE (-1)
 
 /* Decoding hyper-parameters (Alg. 1 inputs; App. A.2 fixes lambda = 0.5^(1/8),
  * p0 = 0.1).  Requires 0 <= tau_c <= tau_u <= 1, 0 < lambda < 1, p0 > 0,
@@ -125,6 +141,15 @@ typedef struct {
 /* ------------------------------------------------------------ library */
 const char* dard_last_error(void);
 int dard_version(void);
+
+/* ------------------------------------------------------------ state codes
+ * Validation of n token state codes (Sec. 3.2 and Eq. 8 define exactly the
+ * three states M = 0, C = 1, U = 2):
+ *   status[0] = number of codes outside {0, 1, 2},
+ *   status[1] = index of the first of them, or -1 if there is none.
+ * state: device uint8 [n] (n >= 1); status: device int32 [2], written by one
+ * kernel on `stream` (no initialisation needed). */
+dard_status dard_check_states(const uint8_t* state, int n, int32_t* status, void* stream);
 
 /* ------------------------------------------------------------ a1: mask
  * State-specific attention mask of Sec. 3.2 (Eq. 2-4) for b sequences of
@@ -177,7 +202,8 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
  *   argmax[r]  = first index of the largest l_v
  *   maxprob[r] = 1 / sum_v exp(l_v - l_max)              (top-1 probability)
  *   pcur[r]    = exp(l_cur - l_max) * maxprob[r], l_cur = l at cur_tok[r]
- *                (only if pcur != NULL; needs cur_tok, no mixing)
+ *                (only if pcur != NULL; needs cur_tok [rows] int32, no
+ *                mixing; an id outside [0, V) is clamped into it)
  *   entropy[r] = -sum_v p_v ln p_v of p = softmax(l)   (only if != NULL)
  *   margin[r]  = p_(1) - p_(2), the two largest probabilities, 0 on a tie
  *                at the top, p_(1) when V = 1          (only if != NULL)
@@ -350,6 +376,21 @@ dard_status dard_step_full(const dard_dims* dims, const void* packed, void* kv, 
 dard_status dard_pack_matrix(int dtype, const void* W, int N, int K, void* Wp, void* stream);
 dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, int N,
                         float* Y, void* stream);
+
+/* The kernel and tiling the library runs for a projection of M token rows,
+ * N output columns and K inputs (a host-side query; nothing is launched):
+ *   plan[0] = DARD_GEMM_* kernel, plan[1] x plan[2] = the workgroup tile in
+ *   units of 32 rows x 32 columns (the streaming kernel: 16-column blocks
+ *   per wave in plan[2]), plan[3] = workgroups splitting K.
+ * partial != 0 asks for the plan of a split-K (residual) projection; step
+ * and prefill activations are fragment-major (frag_x != 0), dard_linear's
+ * row-major (frag_x = 0).  plan: host int32 [4]. */
+#define DARD_GEMM_STREAM 0
+#define DARD_GEMM_PIPE   1
+#define DARD_GEMM_BIG    2
+#define DARD_GEMM_TILED  3
+#define DARD_GEMM_F32    4
+dard_status dard_gemm_plan(int dtype, int M, int N, int K, int partial, int frag_x, int32_t* plan);
 
 /* ------------------------------------------------------------ tracing
  * When enabled, the library brackets each launch of the kernel classes in

@@ -110,9 +110,15 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     W.attn = o; o = align256(o + rows * qd * es);
     W.act = o; o = align256(o + rows * d->ffn_dim * es);
     W.sel = o; o = align256(o + step_rows * ((B + 63) / 64) * 8);   // state mask of the step
-    // split-key attention partials: room for the step's largest split at any
-    // prefix length; a prefill splits only as far as this room allows
-    W.part_slots = attention_partial_slots(d->dtype, b, 2 * B, d->n_heads, d->n_kv_heads, 1 << 20);
+    // split-key attention partials: room for the largest split a step picks at
+    // any prefix length the cache holds (0 .. cap - 2B keys); a prefill splits
+    // only as far as this room allows
+    W.part_slots = 0;
+    const int max_tiles = attention_tiles(1, cap - 2 * B > 0 ? cap - 2 * B : 0, B, cap);
+    for (int t = 1; t <= max_tiles; ++t) {
+        const size_t sl = attention_partial_slots(d->dtype, b, 2 * B, d->n_heads, d->n_kv_heads, t);
+        W.part_slots = sl > W.part_slots ? sl : W.part_slots;
+    }
     W.part = o; o = align256(o + W.part_slots * d->head_dim * 4);
     W.part_ml = o; o = align256(o + W.part_slots * 2 * 4);
     W.logits = o; o = align256(o + step_rows * d->vocab * 4);
@@ -197,6 +203,14 @@ extern "C" {
 
 const char* dard_last_error(void) { return g_err.c_str(); }
 int dard_version(void) { return 1; }
+
+// ---------------------------------------------------------------- state codes
+dard_status dard_check_states(const uint8_t* state, int n, int32_t* status, void* stream) {
+    if (!state || !status) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (n < 1) return fail(DARD_ERR_SHAPE, "need n >= 1");
+    HIPOK(launch_check_states(state, n, status, (hipStream_t)stream));
+    return DARD_OK;
+}
 
 // ---------------------------------------------------------------- mask
 dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b, int B, uint32_t flags,
@@ -293,7 +307,7 @@ dard_status dard_confidence(const float* logits_s, const float* logits_x, const 
     a.rows = rows; a.V = V; a.part = (float*)ws; a.state = nullptr; a.phase = 0; a.step_B = 0;
     hipStream_t s = (hipStream_t)stream;
     HIPOK(launch_conf_partial(a, entropy || margin, s));
-    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), logits_s, ld, cur_tok, argmax, maxprob, pcur,
+    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), V, logits_s, ld, cur_tok, argmax, maxprob, pcur,
                               entropy, margin, s));
     return DARD_OK;
 }
@@ -315,6 +329,8 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
         if (!maxprob_s || !argmax_s || !maxprob_mix || !argmax_mix || !state_out || !tok_out || !conf_out ||
             (pcur_mode && !pcur_s))
             return fail(DARD_ERR_ARG, "FINAL needs confidences, predictions and outputs");
+        if ((params->flags & DARD_F_CHECK_STATES) && !block_done)
+            return fail(DARD_ERR_ARG, "DARD_F_CHECK_STATES reports through block_done");
         if (needs_stats(params->flags) && (!key_s || !key_mix))
             return fail(DARD_ERR_ARG, "entropy / margin ordering needs key_s and key_mix");
     } else {
@@ -596,9 +612,12 @@ int step_tail(const Fwd& f, const dard_params* params, int b, int B, const void*
 }
 
 int check_step_args(const dard_dims* d, const dard_params* params, const void* tok, const uint8_t* state_in,
-                    const float* conf_in, const int32_t* tok_out, const uint8_t* state_out, const float* conf_out) {
+                    const float* conf_in, const int32_t* tok_out, const uint8_t* state_out, const float* conf_out,
+                    const int32_t* block_done) {
     if (int rc = check_params(params)) return rc;
     if (!tok || !state_in || !conf_in || !tok_out || !state_out || !conf_out) return fail(DARD_ERR_ARG, "NULL pointer");
+    if ((params->flags & DARD_F_CHECK_STATES) && !block_done)
+        return fail(DARD_ERR_ARG, "DARD_F_CHECK_STATES reports through block_done");
     if (params->mask_id < 0 || params->mask_id >= d->vocab) return fail(DARD_ERR_ARG, "mask_id outside the vocab");
     return DARD_OK;
 }
@@ -612,7 +631,7 @@ dard_status dard_step(const dard_dims* d, const void* packed, void* kv, int cap,
     Fwd f;
     int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
     if (rc) return rc;
-    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out);
+    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out, block_done);
     if (rc) return rc;
     if (P < 0 || P + 2 * B > cap || P + B > d->max_pos)
         return fail(DARD_ERR_SHAPE, "need P >= 0, P + 2B <= cap, P + B <= max_pos");
@@ -638,7 +657,7 @@ dard_status dard_step_full(const dard_dims* d, const void* packed, void* kv, int
     Fwd f;
     int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
     if (rc) return rc;
-    rc = check_step_args(d, params, seq, state_in, conf_in, tok_out, state_out, conf_out);
+    rc = check_step_args(d, params, seq, state_in, conf_in, tok_out, state_out, conf_out, block_done);
     if (rc) return rc;
     if (N < B || blk < 0 || blk + B > N || N + B > cap || N > d->max_pos)
         return fail(DARD_ERR_SHAPE, "need B <= N, 0 <= blk <= N - B, N + B <= cap, N <= max_pos");
@@ -700,7 +719,7 @@ dard_status dard_step_shared(const dard_dims* d, const void* packed, void* kv, i
     Fwd f;
     int rc = fwd_setup(f, d, packed, kv, cap, b, B, ws, ws_bytes, stream);
     if (rc) return rc;
-    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out);
+    rc = check_step_args(d, params, tok_in, state_in, conf_in, tok_out, state_out, conf_out, block_done);
     if (rc) return rc;
     if (P + 2 * B > cap || P + B > d->max_pos) return fail(DARD_ERR_SHAPE, "need P + 2B <= cap, P + B <= max_pos");
     rc = attach_shared(f, kv_shared, cap_shared, Ps, P);
@@ -742,6 +761,15 @@ dard_status dard_linear(int dtype, const void* X, int M, int K, const void* Wp, 
     EpiArgs e{};
     e.kind = EPI_STORE_F32; e.y = Y; e.ldy = N;
     HIPOK(launch_gemm(dtype, X, M, K, K, Wp, N, e, DARD_K_GEMM_HEAD, (hipStream_t)stream));
+    return DARD_OK;
+}
+
+dard_status dard_gemm_plan(int dtype, int M, int N, int K, int partial, int frag_x, int32_t* plan) {
+    if (!plan) return fail(DARD_ERR_ARG, "NULL pointer");
+    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
+    if (M < 1 || N < 1 || K < 1) return fail(DARD_ERR_SHAPE, "need M, N, K >= 1");
+    if (dtype == DARD_DTYPE_BF16 && (K % 64 || N % 16)) return fail(DARD_ERR_SHAPE, "bf16 needs K %% 64 == 0, N %% 16 == 0");
+    gemm_plan(dtype, M, N, K, partial != 0, frag_x != 0, plan);
     return DARD_OK;
 }
 

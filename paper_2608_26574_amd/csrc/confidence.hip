@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
 }
 
 template <bool STATS>
-__global__ void conf_combine_kernel(const float* __restrict__ part, int rows, int nchunk,
+__global__ void conf_combine_kernel(const float* __restrict__ part, int rows, int nchunk, int V,
                                     const float* __restrict__ ls, int64_t ld, const int32_t* __restrict__ cur,
                                     int32_t* __restrict__ argmax, float* __restrict__ maxprob,
                                     float* __restrict__ pcur, float* __restrict__ entropy,
@@ -204,7 +204,10 @@ __global__ void conf_combine_kernel(const float* __restrict__ part, int rows, in
     argmax[r] = t.a;
     maxprob[r] = 1.f / t.s;
     if (pcur) {
-        const float lc = ls[(size_t)r * ld + cur[r]];
+        // token ids are device data: an id outside [0, V) reads the nearest
+        // entry of the row instead of memory past it
+        const int ct = min(max(cur[r], 0), V - 1);
+        const float lc = ls[(size_t)r * ld + ct];
         pcur[r] = exp2f((lc - t.m) * kLog2e) / t.s;
     }
     if (STATS) {
@@ -230,16 +233,16 @@ hipError_t launch_conf_partial(const ConfArgs& a, bool stats, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls, int64_t ld,
+hipError_t launch_conf_combine(const float* part, int rows, int nchunk, int V, const float* ls, int64_t ld,
                                const int32_t* cur_tok, int32_t* argmax, float* maxprob, float* pcur,
                                float* entropy, float* margin, hipStream_t s) {
     TraceScope ts(DARD_K_CONFIDENCE, s);
     const dim3 g((rows + 127) / 128), blk(128);
     if (entropy || margin)
-        launch(conf_combine_kernel<true>, g, blk, 0, s, part, rows, nchunk, ls, ld, cur_tok, argmax, maxprob,
+        launch(conf_combine_kernel<true>, g, blk, 0, s, part, rows, nchunk, V, ls, ld, cur_tok, argmax, maxprob,
                pcur, entropy, margin);
     else
-        launch(conf_combine_kernel<false>, g, blk, 0, s, part, rows, nchunk, ls, ld, cur_tok, argmax, maxprob,
+        launch(conf_combine_kernel<false>, g, blk, 0, s, part, rows, nchunk, V, ls, ld, cur_tok, argmax, maxprob,
                pcur, entropy, margin);
     return hipGetLastError();
 }

@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(DecideArgs a, int in_l
     extern __shared__ float staged[];            // [2][B][nchunk][stride] in step mode (in_lds)
     __shared__ uint8_t promoted[kThreads], demoted[kThreads];
     __shared__ double lam_pow[kThreads];
-    __shared__ int all_u, entered_u;
+    __shared__ int all_u, entered_u, bad_code;
     __shared__ float c_all[kThreads];
     __shared__ int nxt_all[kThreads], xhat_all[kThreads];
     const int s = blockIdx.x, i = threadIdx.x;
@@ -174,8 +174,9 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(DecideArgs a, int in_l
     }
 
     // ---- FINAL: confidences of every position, transition, fill
-    if (i == 0) { all_u = 1; entered_u = 0; }
+    if (i == 0) { all_u = 1; entered_u = 0; bad_code = 0; }
     __syncthreads();
+    if (live && st > DARD_STATE_U) atomicOr(&bad_code, 1);
     if (live) {
         const int tok = a.tok_in ? a.tok_in[pos] : 0;
         float c, key;
@@ -239,7 +240,8 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(DecideArgs a, int in_l
             if (j != best && nxt_all[j] != DARD_STATE_U) done = 0;
         all_u = done;
     }
-    if (i == 0 && a.block_done) a.block_done[s] = all_u;
+    if (i == 0 && a.block_done)
+        a.block_done[s] = ((a.flags & DARD_F_CHECK_STATES) && bad_code) ? DARD_BAD_STATE : all_u;
 }
 
 }  // namespace

@@ -836,6 +836,41 @@ BigCfg big_cfg(int M, int N, int K, bool partial) {
     return best;
 }
 
+void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan) {
+    plan[1] = plan[2] = 0;
+    plan[3] = 1;
+    if (dtype == DARD_DTYPE_F32) {
+        plan[0] = DARD_GEMM_F32;
+        return;
+    }
+    if (M <= 64) {
+        const StreamCfg c = stream_cfg(N, K, partial);
+        plan[0] = DARD_GEMM_STREAM;
+        plan[1] = 4;
+        plan[2] = c.nw;
+        plan[3] = c.split;
+        return;
+    }
+    if (!xfrag) {
+        plan[0] = DARD_GEMM_TILED;
+        plan[1] = TBM / 32;
+        plan[2] = TBN / 32;
+        return;
+    }
+    const BigCfg c = big_cfg(M, N, K, partial);
+    if (c.ti) {
+        plan[0] = DARD_GEMM_BIG;
+        plan[1] = c.ti;
+        plan[2] = c.tj;
+        plan[3] = c.split;
+        return;
+    }
+    plan[0] = DARD_GEMM_PIPE;
+    plan[1] = PBM / 32;
+    plan[2] = PipeTile<4>::BN / 32;
+    plan[3] = partial ? pipe_split(M, N, K) : 1;
+}
+
 int gemm_split(int dtype, int M, int N, int K) {
     if (dtype != DARD_DTYPE_BF16) return 1;
     if (M > 64) {

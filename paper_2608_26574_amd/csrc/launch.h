@@ -22,6 +22,8 @@ inline bool frag_rows(int dtype, int rows) { return dtype == DARD_DTYPE_BF16 && 
 // ---- mask.hip
 hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
                                    uint32_t flags, uint64_t* sel, hipStream_t s);
+// status[0] = number of codes outside {0, 1, 2} among state[0..n), status[1] = first index or -1
+hipError_t launch_check_states(const uint8_t* state, int n, int32_t* status, hipStream_t s);
 
 // ---- attention.hip
 struct AttnArgs {
@@ -81,6 +83,8 @@ struct EpiArgs {
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
                        const EpiArgs& e, int kernel_class, hipStream_t s, bool xfrag = false);
 int gemm_split(int dtype, int M, int N, int K);
+// The kernel and tiling launch_gemm picks for these sizes (dard_gemm_plan).
+void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan);
 // bf16 fragment-major packing (mode 0 plain, 1 rotary-pair rows, 2 gate/up interleave)
 hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
                             hipStream_t s);
@@ -132,7 +136,7 @@ int conf_chunks(int V);
 // stats: also form the entropy / margin terms (partials of kConfStatsStride)
 hipError_t launch_conf_partial(const ConfArgs& a, bool stats, hipStream_t s);
 // entropy or margin != NULL reads statistics partials
-hipError_t launch_conf_combine(const float* part, int rows, int nchunk, const float* ls,
+hipError_t launch_conf_combine(const float* part, int rows, int nchunk, int V, const float* ls,
                                int64_t ld, const int32_t* cur_tok, int32_t* argmax,
                                float* maxprob, float* pcur, float* entropy, float* margin,
                                hipStream_t s);

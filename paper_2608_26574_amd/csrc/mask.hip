@@ -25,6 +25,29 @@ __global__ __launch_bounds__(256) void build_state_mask_kernel(const uint8_t* __
     }
 }
 
+// Codes outside {0, 1, 2}: their number and the first index.  One workgroup
+// walks all n codes, so nothing has to be initialised beforehand.
+__global__ __launch_bounds__(256) void check_states_kernel(const uint8_t* __restrict__ state, int n,
+                                                           int32_t* __restrict__ status) {
+    __shared__ int cnt, first;
+    if (threadIdx.x == 0) { cnt = 0; first = 0x7fffffff; }
+    __syncthreads();
+    int c = 0, f = 0x7fffffff;
+    for (int i = threadIdx.x; i < n; i += 256)
+        if (state[i] > DARD_STATE_U) { ++c; f = min(f, i); }
+    if (c) { atomicAdd(&cnt, c); atomicMin(&first, f); }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        status[0] = cnt;
+        status[1] = cnt ? first : -1;
+    }
+}
+
+hipError_t launch_check_states(const uint8_t* state, int n, int32_t* status, hipStream_t s) {
+    launch(check_states_kernel, dim3(1), dim3(256), 0, s, state, n, status);
+    return hipGetLastError();
+}
+
 hipError_t launch_build_state_mask(const uint8_t* state, const float* conf, int b, int B,
                                    uint32_t flags, uint64_t* sel, hipStream_t s) {
     launch(build_state_mask_kernel, dim3(b), dim3(256), 0, s, state, conf, B, flags,

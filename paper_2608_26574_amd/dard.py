@@ -20,16 +20,19 @@ STATE_M, STATE_C, STATE_U = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR, F_PROGRESS = 1, 2, 4, 8
 F_C_BIDIR, F_ORDER_L2R, F_ORDER_ENTROPY, F_ORDER_MARGIN, F_FIXED_W = 16, 32, 64, 128, 256
+F_CHECK_STATES = 512
+BAD_STATE = -1
+GEMM_STREAM, GEMM_PIPE, GEMM_BIG, GEMM_TILED, GEMM_F32 = range(5)
 PHASE_VERIFY, PHASE_FINAL = 0, 1
 (K_GEMM_QKV, K_GEMM_O, K_GEMM_GU, K_GEMM_DOWN, K_GEMM_HEAD, K_ATTENTION, K_CONFIDENCE,
  K_DECIDE, K_NORM, K_MASK, K_COUNT) = range(11)
 
 EXPORTS = [
-    "dard_last_error", "dard_version", "dard_build_state_mask", "dard_attention_workspace_bytes",
+    "dard_last_error", "dard_version", "dard_check_states", "dard_build_state_mask", "dard_attention_workspace_bytes",
     "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
     "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_prefill_suffix",
-    "dard_step_shared", "dard_pack_matrix", "dard_linear",
+    "dard_step_shared", "dard_pack_matrix", "dard_linear", "dard_gemm_plan",
     "dard_trace_enable",
     "dard_trace_read", "dard_trace_reset", "dard_trace_sample",
 ]
@@ -73,6 +76,7 @@ def lib():
         sig = {
             "dard_last_error": (ctypes.c_char_p, []),
             "dard_version": (i32, []),
+            "dard_check_states": (i32, [vp, i32, vp, vp]),
             "dard_build_state_mask": (i32, [vp, vp, i32, i32, u32, vp, vp]),
             "dard_attention_workspace_bytes": (sz, [i32, i32, i32, i32, i32, i32]),
             "dard_masked_attention": (i32, [i32, vp, vp, vp, i32, i32, vp, vp, i32, i32, i32, i32, i32, f32,
@@ -93,6 +97,7 @@ def lib():
                                        vp, vp, sz, vp]),
             "dard_pack_matrix": (i32, [i32, vp, i32, i32, vp, vp]),
             "dard_linear": (i32, [i32, vp, i32, i32, vp, i32, vp, vp]),
+            "dard_gemm_plan": (i32, [i32, i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32)]),
             "dard_trace_enable": (i32, [u32]),
             "dard_trace_read": (i32, [i32, ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]),
             "dard_trace_reset": (i32, []),
@@ -152,6 +157,19 @@ def make_dims(d):
 # ------------------------------------------------------------------ entry points
 def dard_version():
     return lib().dard_version()
+
+
+def dard_check_states(state, status, stream=None):
+    """status (int32 [2] on the device) = (codes outside {0,1,2}, first index or -1)."""
+    _check(lib().dard_check_states(_p(state), state.numel(), _p(status), _stream(stream)))
+
+
+def dard_gemm_plan(M, N, K, partial=False, frag_x=True, dtype=DTYPE_BF16):
+    """(kernel, tile rows / 32, tile columns / 32, K split) the library runs for
+    a projection of these sizes."""
+    plan = (ctypes.c_int32 * 4)()
+    _check(lib().dard_gemm_plan(dtype, M, N, K, int(partial), int(frag_x), plan))
+    return tuple(plan)
 
 
 def dard_build_state_mask(state, conf, flags, sel, stream=None):

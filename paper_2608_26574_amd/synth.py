@@ -95,15 +95,22 @@ def make_weights(dims: Dims, seed: int = 1, device="cpu", std: float = 0.02):
 class OracleWeights:
     """float64 numpy view of the weights in the nesting the oracle reads
     (``w['embed']``, ``w['layers'][l]['wq']``, ...).  Layers are converted on
-    access so that a 32-layer model never sits in host memory as float64."""
+    access so that a 32-layer model never sits in host memory as float64.
+    With ``host_copy`` every tensor is first copied once into host memory as
+    float32 (exact for bf16 and fp32 values), so that repeated passes over a
+    deep model convert from there instead of fetching it again."""
 
-    def __init__(self, dims: Dims, tensors):
+    def __init__(self, dims: Dims, tensors, host_copy: bool = False):
         self.dims = dims
         self.t = tensors
+        if host_copy:
+            self.t = {k: v.detach().to("cpu", torch.float32).numpy() for k, v in tensors.items()}
         self.layers = _LayerView(self)
 
     @staticmethod
     def _np(t):
+        if isinstance(t, np.ndarray):
+            return t.astype(np.float64)
         return t.detach().to("cpu", torch.float32).numpy().astype(np.float64)
 
     def __getitem__(self, key):

@@ -124,3 +124,37 @@ def test_attention_workspace_sizing():
     assert L.dard_attention_workspace_bytes(1, 64, 32, 32, 128, 512) == 64 * 64 * 8
     # the fp32 path never splits
     assert L.dard_attention_workspace_bytes(0, 1, 32, 4, 64, 64) == 0
+
+
+def test_gemm_plan_query():
+    """The host-side plan query reports the kernel and tiling launch_gemm runs
+    (no GPU needed)."""
+    # decoding step rows: the weight-streaming kernel; O / down split K
+    assert dard.dard_gemm_plan(64, 24576, 4096)[0] == dard.GEMM_STREAM
+    assert dard.dard_gemm_plan(64, 4096, 12288, partial=True)[3] > 1
+    # 64 < M < 256: the pipelined kernel; M >= 256: the large tiles
+    assert dard.dard_gemm_plan(144, 1024, 512)[0] == dard.GEMM_PIPE
+    assert dard.dard_gemm_plan(1024, 37888, 3584)[0] == dard.GEMM_BIG
+    # a 700-row prefill of a wide FFN fills whole rounds with 128 x 192 tiles
+    assert dard.dard_gemm_plan(700, 16256, 320)[:3] == (dard.GEMM_BIG, 4, 6)
+    # split-K partial epilogues never take the 128 x 192 tile
+    assert dard.dard_gemm_plan(700, 16256, 320, partial=True)[1:3] != (4, 6)
+    # row-major activations (dard_linear) and fp32
+    assert dard.dard_gemm_plan(300, 256, 128, frag_x=False)[0] == dard.GEMM_TILED
+    assert dard.dard_gemm_plan(300, 256, 128, dtype=dard.DTYPE_F32)[0] == dard.GEMM_F32
+    L = dard.lib()
+    plan = (ctypes.c_int32 * 4)()
+    assert L.dard_gemm_plan(1, 64, 100, 64, 0, 1, plan) == -2      # N % 16 != 0
+    assert L.dard_gemm_plan(1, 64, 128, 64, 0, 1, None) == -1
+
+
+def test_state_check_validation():
+    L = dard.lib()
+    fake = ctypes.c_void_p(0x1000)
+    assert L.dard_check_states(None, 4, fake, None) == -1
+    assert L.dard_check_states(fake, 0, fake, None) == -2
+    # a step under DARD_F_CHECK_STATES reports through block_done, which must be given
+    p = _params(flags=dard.F_CHECK_STATES)
+    assert L.dard_commit_remask(1, ctypes.byref(p), 1, 4, fake, fake, None, fake, fake, fake, None, None,
+                                None, fake, fake, fake, None, None) == -1
+    assert b"block_done" in L.dard_last_error()

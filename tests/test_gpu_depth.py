@@ -1,0 +1,106 @@
+"""Full-depth checks at the 8B shape: all 32 layers, as the benchmark runs
+them (the other step tests truncate the model to one or two layers).
+
+  P1  (Sec. 3.2 mask rules; the first step of a block) with every position
+      masked, the x row and the shadow row of a position read the same keys
+      (x^j and s^j both embed [Mask] at the same position) through the same
+      arithmetic, so their logits agree exactly at any depth; w = 1.
+  P2  with no candidates, the x and shadow rows of every M position read
+      equal keys (by induction over the layers), so their logits agree up
+      to the rounding-order noise of the computation; w = 1.
+  Oracle comparison at 32 layers: the logits within the bf16 tolerance rule
+      (rms <= 2e-2, max <= max(2e-2, twice the oracle's own noise floor, the
+      maximum over three perturbation seeds)), the decisions by the op-level
+      protocol (exact), and P2's difference within the same bound."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dard_oracle as O
+from paper_2608_26574_amd import dard, synth
+from parity import (P, announce, check_bf16_logits, check_op_level, check_step_level, collect, cparams, dev,
+                    noise_floor, step_buffers)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def llada8b():
+    dims = synth.LLADA8B
+    announce("llada8b 32-layer model: weights and prefill")
+    b, B, Pp = 1, 32, 96
+    w = synth.make_weights(dims, seed=1, device="cuda")
+    eng = dard.Engine(dims, w, b, B, Pp + 2 * B)
+    ids = synth.prompt_ids(b, Pp, dims.vocab, seed=2)
+    eng.dard_prefill(dev(ids))
+    torch.cuda.synchronize()
+    ow = synth.OracleWeights(dims, w, host_copy=True)
+    del w
+    torch.cuda.empty_cache()
+    return dict(dims=dims, eng=eng, ids=ids, ow=ow, b=b, B=B, P=Pp)
+
+
+def gpu_step(m, tok, state, conf, params):
+    out, dbg = step_buffers(m["b"], m["B"], m["dims"].vocab)
+    m["eng"].dard_step(m["P"], cparams(dard, params), dev(tok), dev(state), dev(conf), out["tok_out"],
+                       out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+    return collect(out, dbg)
+
+
+@pytest.mark.timeout(600)
+def test_p1_all_masked_block_32_layers(llada8b):
+    m = llada8b
+    dims, B = m["dims"], m["B"]
+    announce("P1 at 32 layers")
+    tok = np.full((1, B), dims.mask_id, dtype=np.int32)
+    state = np.zeros((1, B), dtype=np.uint8)
+    conf = np.zeros((1, B), dtype=np.float32)
+    prm = P(dims.mask_id)
+    got = gpu_step(m, tok, state, conf, prm)
+    lx, ls = got["logits"][0, :B], got["logits"][0, B:]
+    diff = float(np.max(np.abs(lx - ls)))
+    print(f"P1 32 layers: max |x - s| logits {diff:.3e}", file=sys.stderr, flush=True)
+    assert diff <= 1e-6, diff
+    assert np.all(got["w"] == 1.0)
+    check_op_level(tok, state, got, prm)
+
+
+@pytest.mark.timeout(1200)
+def test_oracle_and_p2_32_layers(llada8b):
+    m = llada8b
+    dims, B, ow, ids = m["dims"], m["B"], m["ow"], m["ids"]
+    dd = dims.as_dict()
+    prm = P(dims.mask_id)
+    # candidate fraction 0.25 (the workload's states)
+    tok, state, conf = synth.workload_block(1, B, 0.25, dims.vocab, seed=1000)
+    announce("32-layer GPU step")
+    got = gpu_step(m, tok, state, conf, prm)
+    announce("32-layer oracle prefill and step")
+    cache = O.prefill(ow, dd, ids)
+    ref = O.dard_step(ow, dd, cache, tok, state, conf, prm)
+
+    def perturbed():
+        announce("32-layer oracle, perturbed")
+        c2 = O.prefill(ow, dd, ids)
+        return O.step_logits(ow, dd, c2, tok, state, conf, prm["mask_id"])[0]
+
+    floor = noise_floor(perturbed, ref["logits"])
+    ref["floor"] = lambda: floor
+    err, rms, _ = check_bf16_logits(got, ref, "llada8b 32 layers")
+    check_op_level(tok, state, got, prm)
+    check_step_level(tok, state, got, ref, prm, "llada8b 32 layers")
+    # P2: no candidates (the C positions of the same block become U)
+    state2 = np.where(state == O.STATE_C, O.STATE_U, state).astype(np.uint8)
+    announce("P2 at 32 layers")
+    got2 = gpu_step(m, tok, state2, conf, prm)
+    M = state2[0] == O.STATE_M
+    d = got2["logits"][0, :B][M] - got2["logits"][0, B:][M]
+    p2max, p2rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
+    print(f"32 layers: GPU vs oracle max {err:.3e} rms {rms:.3e}, oracle noise floor (3 seeds) {floor:.3e}; "
+          f"P2 max |x - s| {p2max:.3e} rms {p2rms:.3e}", file=sys.stderr, flush=True)
+    assert p2rms < 2e-2, p2rms
+    assert p2max < max(2e-2, 2.0 * floor), (p2max, floor)
+    assert np.all(got2["w"] == 1.0)
+    check_op_level(tok, state2, got2, prm)

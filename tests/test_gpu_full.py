@@ -2,8 +2,6 @@
 sequence with its future masked blocks plus the shadow block) against the
 oracle's full-sequence mode, with the decision-parity protocol of the
 prefix-cache step tests."""
-import sys
-
 import numpy as np
 import pytest
 import torch
@@ -11,17 +9,12 @@ import torch
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
-from test_gpu_step import P, check_decisions
+from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
+                    dev, noise_floor, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
-
-def announce(*a):
-    print("[case]", *a, file=sys.stderr, flush=True)
-
-
-def dev(a):
-    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+WORKLOAD_LM_SCALE = 6.0
 
 
 def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None, frac=None, wdevice="cpu"):
@@ -30,9 +23,7 @@ def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None,
     V = dims.vocab
     N = prompt + gen
     blk = prompt + blk_index * B
-    w = synth.make_weights(dims, seed=seed, device=wdevice)
-    if lm_scale is not None:
-        w["lm_head"] = (w["lm_head"].float() * lm_scale).to(w["lm_head"].dtype)
+    w = sharpen(synth.make_weights(dims, seed=seed, device=wdevice), lm_scale)
     eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, N + B)
     seq = synth.prompt_ids(b, N, V, seed=seed + 1)
     if frac is None:
@@ -41,33 +32,16 @@ def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None,
         tok, state, conf = synth.workload_block(b, B, frac, V, seed=seed + 2)
     seq[:, blk:blk + B] = tok
     seq[:, blk + B:] = dims.mask_id
-    cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
-                          params.get("flags", 0), params.get("w_fixed", 0.0))
-    t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
-    s_out = torch.zeros(b, B, dtype=torch.uint8, device="cuda")
-    c_out = torch.zeros(b, B, device="cuda")
-    done = torch.zeros(b, dtype=torch.int32, device="cuda")
-    dbg = {"logits": torch.zeros(b, 2 * B, V, device="cuda"), "w": torch.zeros(b, B, device="cuda")}
-    eng.dard_step_full(blk, cp, dev(seq), dev(state), dev(conf), t_out, s_out, c_out, done, debug=dbg)
-    torch.cuda.synchronize()
+    out, dbg = step_buffers(b, B, V)
+    eng.dard_step_full(blk, cparams(dard, params), dev(seq), dev(state), dev(conf), out["tok_out"], out["state_out"],
+                       out["conf_out"], out["block_done"], debug=dbg)
+    got = collect(out, dbg)
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     ref = O.dard_step_full(ow, dd, seq, blk, B, state, conf, params)
-
-    def floor(amp=1e-7):
-        # the oracle's own logits under one-ulp perturbations before every bf16 rounding
-        rng = np.random.default_rng(0)
-        orig = O.storage
-        O.storage = lambda x, dt: orig(np.asarray(x, dtype=np.float64) * (1.0 + amp * rng.standard_normal(np.shape(x))), dt)
-        try:
-            l2 = O.full_step_logits(ow, dd, seq, blk, B, state, conf, params["mask_id"], params.get("flags", 0))
-        finally:
-            O.storage = orig
-        return float(np.max(np.abs(l2 - ref["logits"])))
-
-    ref["floor"] = floor
-    got = dict(logits=dbg["logits"].cpu().numpy(), w=dbg["w"].cpu().numpy(), state_out=s_out.cpu().numpy(),
-               tok_out=t_out.cpu().numpy(), conf_out=c_out.cpu().numpy(), block_done=done.cpu().numpy())
+    ref["floor"] = lambda: noise_floor(
+        lambda: O.full_step_logits(ow, dd, seq, blk, B, state, conf, params["mask_id"], params.get("flags", 0)),
+        ref["logits"])
     return tok, state, conf, got, ref
 
 
@@ -82,7 +56,7 @@ def test_tiny_full_step_fp32(blk_index, flags):
     tok, state, conf, got, ref = full_case(dims, 1, 40, 96, 32, blk_index, prm, seed=3, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 20, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"tiny full step {blk_index} {flags}")
     assert excl <= 1
 
 
@@ -98,9 +72,8 @@ def test_small_full_step_bf16(case):
                                            seed=4, lm_scale=8.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 2e-2 * 8, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
-    print(f"max |dlogit| {eps:.3e}, rows excluded {excl} of {state.size}", file=sys.stderr)
-    assert excl <= state.size // 2
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step")
+    assert excl <= state.size // 4
 
 
 def test_block128_full_step_fp32():
@@ -113,9 +86,8 @@ def test_block128_full_step_fp32():
     tok, state, conf, got, ref = full_case(dims, 1, 64, 256, 128, 0, prm, seed=4, lm_scale=8.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 8, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
-    print(f"max |dlogit| {eps:.3e}, rows excluded {excl} of {state.size}", file=sys.stderr)
-    assert excl <= state.size // 2
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step")
+    assert excl <= state.size // 4
 
 
 def test_block256_full_step_fp32():
@@ -136,14 +108,10 @@ def test_llada8b_block256_full_step_two_layers():
     dims = synth.truncated(synth.LLADA8B, 2)
     announce("llada8b 2-layer full step, block 256")
     prm = P(dims.mask_id)
-    tok, state, conf, got, ref = full_case(dims, 1, 128, 256, 256, 0, prm, seed=2, frac=0.25, wdevice="cuda")
-    d = got["logits"] - ref["logits"]
-    err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
-    floor = ref["floor"]() if err >= 2e-2 else 0.0
-    print(f"llada8b block-256 full step: max {err:.3e} rms {rms:.3e} floor {floor:.3e}", file=sys.stderr)
-    assert rms < 2e-2
-    assert err < max(2e-2, 2.0 * floor), (err, floor)
-    check_decisions(tok, state, got, ref, prm)
+    tok, state, conf, got, ref = full_case(dims, 1, 128, 256, 256, 0, prm, seed=2, frac=0.25, wdevice="cuda",
+                                           lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "llada8b block-256 full step", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "llada8b block-256 full step")
 
 
 def test_llada8b_full_step_two_layers():
@@ -153,11 +121,7 @@ def test_llada8b_full_step_two_layers():
     dims = synth.truncated(synth.LLADA8B, 2)
     announce("llada8b 2-layer full step")
     prm = P(dims.mask_id)
-    tok, state, conf, got, ref = full_case(dims, 1, 128, 256, 128, 0, prm, seed=1, frac=0.25, wdevice="cuda")
-    d = got["logits"] - ref["logits"]
-    err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
-    floor = ref["floor"]() if err >= 2e-2 else 0.0
-    print(f"llada8b full step: max {err:.3e} rms {rms:.3e} floor {floor:.3e}", file=sys.stderr)
-    assert rms < 2e-2
-    assert err < max(2e-2, 2.0 * floor), (err, floor)
-    check_decisions(tok, state, got, ref, prm)
+    tok, state, conf, got, ref = full_case(dims, 1, 128, 256, 128, 0, prm, seed=1, frac=0.25, wdevice="cuda",
+                                           lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "llada8b full step", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "llada8b full step")

@@ -403,3 +403,19 @@ def test_commit_remask_variants_bit_exact(B, flags, wf):
         else:
             key = cf.astype(np.float32)
         assert np.array_equal(co[s].cpu().numpy(), key)
+
+
+def test_check_states():
+    """dard_check_states counts the codes outside {0, 1, 2} and finds the first."""
+    announce("state-code check")
+    st = torch.tensor([0, 1, 2, 2, 1, 0, 3, 0, 7, 2], dtype=torch.uint8, device="cuda")
+    status = torch.full((2,), 99, dtype=torch.int32, device="cuda")
+    dard.dard_check_states(st, status)
+    assert status.cpu().tolist() == [2, 6]
+    st = torch.randint(0, 3, (5000,), dtype=torch.uint8, device="cuda")
+    dard.dard_check_states(st, status)
+    assert status.cpu().tolist() == [0, -1]
+    st[4097] = 255
+    st[4999] = 3
+    dard.dard_check_states(st, status)
+    assert status.cpu().tolist() == [2, 4097]

@@ -2,8 +2,6 @@
 prompt, dard_prefill_suffix for each sequence's committed positions, and
 dard_step_shared, against the oracle's prefill / prefill_suffix / join_shared
 and its step, with the decision-parity protocol of the step tests."""
-import sys
-
 import numpy as np
 import pytest
 import torch
@@ -11,24 +9,17 @@ import torch
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
-from test_gpu_step import P, check_bf16_logits, check_decisions
+from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
+                    dev, noise_floor, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
-
-def announce(*a):
-    print("[case]", *a, file=sys.stderr, flush=True)
-
-
-def dev(a):
-    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+WORKLOAD_LM_SCALE = 6.0
 
 
 def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", n_image=0):
     V = dims.vocab
-    w = synth.make_weights(dims, seed=seed, device=wdevice)
-    if lm_scale is not None:
-        w["lm_head"] = (w["lm_head"].float() * lm_scale).to(w["lm_head"].dtype)
+    w = sharpen(synth.make_weights(dims, seed=seed, device=wdevice), lm_scale)
     sh = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, 1, B, Ps)
     eng = dard.Engine(dims, None, b, B, Ps + Pc + 2 * B + 3, packed=sh.packed)
     prompt = synth.prompt_ids(1, Ps, V, seed=seed + 1)
@@ -46,15 +37,10 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
     sh.dard_prefill(dev(prompt), embeds=None if embeds is None else embeds.cuda())
     if Pc:
         eng.dard_prefill_suffix(sh, Ps, dev(committed))
-    cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
-                          params.get("flags", 0), params.get("w_fixed", 0.0))
-    t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
-    s_out = torch.zeros(b, B, dtype=torch.uint8, device="cuda")
-    c_out = torch.zeros(b, B, device="cuda")
-    done = torch.zeros(b, dtype=torch.int32, device="cuda")
-    dbg = {"logits": torch.zeros(b, 2 * B, V, device="cuda"), "w": torch.zeros(b, B, device="cuda")}
-    eng.dard_step_shared(sh, Ps, Ps + Pc, cp, dev(tok), dev(state), dev(conf), t_out, s_out, c_out, done, debug=dbg)
-    torch.cuda.synchronize()
+    out, dbg = step_buffers(b, B, V)
+    eng.dard_step_shared(sh, Ps, Ps + Pc, cparams(dard, params), dev(tok), dev(state), dev(conf), out["tok_out"],
+                         out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+    got = collect(out, dbg)
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     shared = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
@@ -62,21 +48,12 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
     cache = O.join_shared(shared, suffix)
     ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
 
-    def floor(amp=1e-7):
-        rng = np.random.default_rng(0)
-        orig = O.storage
-        O.storage = lambda x, dt: orig(np.asarray(x, dtype=np.float64) * (1.0 + amp * rng.standard_normal(np.shape(x))), dt)
-        try:
-            shp = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
-            c2 = O.join_shared(shp, O.prefill_suffix(ow, dd, shp, committed))
-            l2, _ = O.step_logits(ow, dd, c2, tok, state, conf, params["mask_id"], params.get("flags", 0))
-        finally:
-            O.storage = orig
-        return float(np.max(np.abs(l2 - ref["logits"])))
+    def perturbed():
+        shp = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
+        c2 = O.join_shared(shp, O.prefill_suffix(ow, dd, shp, committed))
+        return O.step_logits(ow, dd, c2, tok, state, conf, params["mask_id"], params.get("flags", 0))[0]
 
-    ref["floor"] = floor
-    got = dict(logits=dbg["logits"].cpu().numpy(), w=dbg["w"].cpu().numpy(), state_out=s_out.cpu().numpy(),
-               tok_out=t_out.cpu().numpy(), conf_out=c_out.cpu().numpy(), block_done=done.cpu().numpy())
+    ref["floor"] = lambda: noise_floor(perturbed, ref["logits"])
     # the suffix keys written by dard_prefill_suffix (V of every layer; K is stored with
     # each head's rotary pairs interleaved)
     if Pc:
@@ -99,7 +76,7 @@ def test_tiny_shared_step_fp32(b, Ps, Pc, flags):
     tok, state, conf, got, ref = shared_case(dims, b, Ps, Pc, 32, prm, seed=3, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 20, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "tiny shared step")
     assert excl <= 1
 
 
@@ -110,8 +87,8 @@ def test_small_shared_step_bf16_gqa():
     tok, state, conf, got, ref = shared_case(dims, 4, 128, 64, 32, prm, seed=5, lm_scale=8.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 2e-2 * 8, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
-    assert excl <= state.size // 2
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small shared step")
+    assert excl <= state.size // 4
 
 
 def test_multimodal_shared_prompt_two_layers():
@@ -122,6 +99,6 @@ def test_multimodal_shared_prompt_two_layers():
     announce("8B shared multimodal prompt, 2 layers")
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = shared_case(dims, 4, 832, 32, 32, prm, seed=4, frac=0.3, wdevice="cuda",
-                                             n_image=576)
-    check_bf16_logits(got, ref, "8B shared prompt 2 layers")
-    check_decisions(tok, state, got, ref, prm)
+                                             n_image=576, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "8B shared prompt 2 layers", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "8B shared prompt 2 layers")

@@ -1,31 +1,26 @@
 """GPU parity of dard_prefill and dard_step (the whole hot path) against the
-oracle.
+oracle, with the decision-parity protocol of tests/parity.py: the oracle's
+decision functions applied to the GPU's own confidences and weights must give
+the GPU's states, tokens and keys exactly (op level); against the independent
+oracle step the decisions must agree wherever the measured margins make them
+unambiguous, with the excluded positions counted (step level).
 
-Decision parity protocol: the oracle's decision functions applied to the
-GPU's own logits must reproduce the GPU's states, tokens and confidences
-exactly (op level); against the independent oracle step, argmax is compared on
-rows whose top-1 / top-2 logit gap exceeds twice the measured logit error and
-states where the confidence is further than twice the confidence error from a
-threshold, and the excluded rows are counted."""
-import math
-import sys
-
+At the workload shapes the LM head is sharpened (x6) so that the shadow
+top-1 probabilities spread over (0, 1): with the random-init head every
+position would fall to M and the comparison would say nothing about the
+vocab-wide argmax, the promotions or the demotions."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
+from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
+                    dev, noise_floor, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
-
-def announce(*a):
-    print("[case]", *a, file=sys.stderr, flush=True)
-
-
-def dev(a):
-    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+WORKLOAD_LM_SCALE = 6.0
 
 
 def unpermute_k(kc, dh):
@@ -36,37 +31,33 @@ def unpermute_k(kc, dh):
     return out
 
 
-def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", check_kv=True, n_image=0):
+def run_case(dims, b, B, P_, params, seed=1, lm_scale=None, frac=None, wdevice="cpu", check_kv=True, n_image=0,
+             state_override=None):
     """n_image > 0: the first n_image prefix positions of every sequence are
     embedding rows (a multimodal prefix, ids < 0) drawn N(0, 1) in the storage
     type instead of token ids."""
     V = dims.vocab
-    w = synth.make_weights(dims, seed=seed, device=wdevice)
-    if lm_scale is not None:
-        w["lm_head"] = (w["lm_head"].float() * lm_scale).to(w["lm_head"].dtype)
-    cap = P + 2 * B + 5
+    w = sharpen(synth.make_weights(dims, seed=seed, device=wdevice), lm_scale)
+    cap = P_ + 2 * B + 5
     eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, cap)
-    ids = synth.prompt_ids(b, P, V, seed=seed + 1)
+    ids = synth.prompt_ids(b, P_, V, seed=seed + 1)
     embeds = None
     if n_image:
         ids[:, :n_image] = -1
         g = torch.Generator().manual_seed(seed + 3)
         td = torch.float32 if dims.dtype == "f32" else torch.bfloat16
-        embeds = torch.randn(b, P, dims.d_model, generator=g).to(td)
+        embeds = torch.randn(b, P_, dims.d_model, generator=g).to(td)
     if frac is None:
         tok, state, conf = synth.tiny_block(b, B, V, seed=seed + 2)
     else:
         tok, state, conf = synth.workload_block(b, B, frac, V, seed=seed + 2)
+    if state_override is not None:
+        tok, state, conf = state_override(tok, state, conf)
     eng.dard_prefill(dev(ids), embeds=None if embeds is None else embeds.cuda())
-    cp = dard.make_params(params["tau_c"], params["tau_u"], params["lam"], params["p0"], params["mask_id"],
-                          params.get("flags", 0), params.get("w_fixed", 0.0))
-    t_out = torch.zeros(b, B, dtype=torch.int32, device="cuda")
-    s_out = torch.zeros(b, B, dtype=torch.uint8, device="cuda")
-    c_out = torch.zeros(b, B, device="cuda")
-    done = torch.zeros(b, dtype=torch.int32, device="cuda")
-    dbg = {"logits": torch.zeros(b, 2 * B, V, device="cuda"), "w": torch.zeros(b, B, device="cuda")}
-    eng.dard_step(P, cp, dev(tok), dev(state), dev(conf), t_out, s_out, c_out, done, debug=dbg)
-    torch.cuda.synchronize()
+    out, dbg = step_buffers(b, B, V)
+    eng.dard_step(P_, cparams(dard, params), dev(tok), dev(state), dev(conf), out["tok_out"], out["state_out"],
+                  out["conf_out"], out["block_done"], debug=dbg)
+    got = collect(out, dbg)
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     emb_np = None if embeds is None else embeds.double().numpy()
@@ -77,98 +68,18 @@ def run_case(dims, b, B, P, params, seed=1, lm_scale=None, frac=None, wdevice="c
         kc, vc = eng.kv_view(kvd)
         kc, vc = kc.float().cpu().numpy(), vc.float().cpu().numpy()
         for layer in range(dims.n_layers):
-            k_gpu = unpermute_k(kc[layer, :, :, :P], dims.head_dim).transpose(0, 2, 1, 3)
-            v_gpu = vc[layer, :, :, :P].transpose(0, 2, 1, 3)
+            k_gpu = unpermute_k(kc[layer, :, :, :P_], dims.head_dim).transpose(0, 2, 1, 3)
+            v_gpu = vc[layer, :, :, :P_].transpose(0, 2, 1, 3)
             assert np.max(np.abs(k_gpu - cache[layer][0])) < tol * 4, layer
             assert np.max(np.abs(v_gpu - cache[layer][1])) < tol * 4, layer
     ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
-    ref["floor"] = lambda: oracle_noise_floor(ow, dd, ids, tok, state, conf, params, ref["logits"], emb_np)
-    got = dict(logits=dbg["logits"].cpu().numpy(), w=dbg["w"].cpu().numpy(), state_out=s_out.cpu().numpy(),
-               tok_out=t_out.cpu().numpy(), conf_out=c_out.cpu().numpy(), block_done=done.cpu().numpy())
+
+    def perturbed():
+        c2 = O.prefill(ow, dd, ids, emb_np)
+        return O.step_logits(ow, dd, c2, tok, state, conf, params["mask_id"], params.get("flags", 0))[0]
+
+    ref["floor"] = lambda: noise_floor(perturbed, ref["logits"])
     return tok, state, conf, got, ref
-
-
-def oracle_noise_floor(ow, dd, ids, tok, state, conf, params, logits, embeds=None, amp=1e-7):
-    """How far the oracle's own logits move when every value is perturbed by
-    one float32 ulp (relative 1e-7) just before each bf16 storage rounding.
-    Any implementation whose accumulation order differs from the oracle's
-    flips some of those roundings, so this is the noise floor of the
-    comparison."""
-    rng = np.random.default_rng(0)
-    orig = O.storage
-
-    def noisy(x, dt):
-        x = np.asarray(x, dtype=np.float64)
-        return orig(x * (1.0 + amp * rng.standard_normal(x.shape)), dt)
-
-    O.storage = noisy
-    try:
-        cache = O.prefill(ow, dd, ids, embeds)
-        l2, _ = O.step_logits(ow, dd, cache, tok, state, conf, params["mask_id"], params.get("flags", 0))
-    finally:
-        O.storage = orig
-    return float(np.max(np.abs(l2 - logits)))
-
-
-def check_bf16_logits(got, ref, label):
-    """bf16 multi-layer logits: the root-mean-square error within 2e-2 and the
-    maximum error within 2e-2 or twice the oracle's own noise floor."""
-    d = got["logits"] - ref["logits"]
-    err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
-    floor = ref["floor"]() if err >= 2e-2 else 0.0
-    print(f"{label}: max |dlogit| {err:.3e} rms {rms:.3e} oracle noise floor {floor:.3e}", file=sys.stderr)
-    assert rms < 2e-2, rms
-    assert err < max(2e-2, 2.0 * floor), (err, floor)
-
-
-def confidences(dec, state, flags):
-    """c_i of Eq. 8 from the oracle's decision record (conf_out carries the
-    ordering key, which is c_i only under the primary ordering)."""
-    shadow = dec["pcur_s"] if flags & O.F_VERIFY_PCUR else dec["maxprob_s"]
-    return np.where(state == O.STATE_M, dec["maxprob_mix"], shadow)
-
-
-def check_decisions(tok, state, got, ref, params):
-    flags = params.get("flags", 0)
-    # op level: the oracle's decisions on the GPU's logits are exactly the GPU's
-    dec = O.decide(got["logits"], tok, state, params)
-    assert np.array_equal(dec["w"].astype(np.float32), got["w"])
-    assert np.array_equal(dec["tok_out"], got["tok_out"])
-    c_dec = confidences(dec, state, flags)
-    near = np.zeros_like(state, dtype=bool)
-    for t in (params["tau_c"], params["tau_u"]):
-        near |= np.abs(c_dec - t) < 1e-5
-    assert np.array_equal(dec["state_out"][~near], got["state_out"][~near])
-    if flags & O.F_ORDER_ENTROPY:
-        # key -H: float32 sums over the vocabulary, |H| up to ln V
-        assert np.allclose(dec["conf_out"], got["conf_out"], rtol=1e-5, atol=1e-4)
-    else:
-        assert np.allclose(dec["conf_out"], got["conf_out"], rtol=1e-5, atol=1e-7)
-    assert np.array_equal(dec["block_done"], got["block_done"])
-    # step level against the independent oracle, with measured margins
-    eps = float(np.max(np.abs(got["logits"] - ref["logits"])))
-    c_ref = confidences(ref, state, flags)
-    eps_c = float(np.max(np.abs(confidences(dec, state, flags) - c_ref)))
-    b, B = state.shape
-    excluded = 0
-    for s in range(b):
-        for i in range(B):
-            rows = [B + i] if state[s, i] != O.STATE_M else [i, B + i]
-            gaps = []
-            for r in rows:
-                top2 = np.sort(ref["logits"][s, r])[-2:]
-                gaps.append(top2[1] - top2[0])
-            c = c_ref[s, i]
-            if min(gaps) <= 2 * eps or min(abs(c - params["tau_c"]), abs(c - params["tau_u"])) <= 2 * eps_c:
-                excluded += 1
-                continue
-            assert got["state_out"][s, i] == ref["state_out"][s, i], (s, i)
-            assert got["tok_out"][s, i] == ref["tok_out"][s, i], (s, i)
-    return eps, excluded
-
-
-def P(mask_id, flags=0, tc=0.4, tu=0.9, w_fixed=0.0):
-    return dict(tau_c=tc, tau_u=tu, lam=O.LAMBDA_DEFAULT, p0=0.1, mask_id=mask_id, flags=flags, w_fixed=w_fixed)
 
 
 def test_tiny_step_fp32():
@@ -179,7 +90,7 @@ def test_tiny_step_fp32():
     tok, state, conf, got, ref = run_case(dims, 1, 32, 64, P(dims.mask_id))
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4, err
-    eps, excl = check_decisions(tok, state, got, ref, P(dims.mask_id))
+    eps, excl, _ = check_decisions(tok, state, got, ref, P(dims.mask_id), "tiny fp32")
     assert excl == 0
 
 
@@ -192,7 +103,7 @@ def test_tiny_step_fp32_long_block(B):
     tok, state, conf, got, ref = run_case(dims, 1, B, 64, prm, seed=7, lm_scale=20.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     assert err < 1e-4 * 20, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"tiny fp32 block {B}")
     assert excl <= 2
 
 
@@ -211,7 +122,7 @@ def test_tiny_step_fp32_transitions(flags, wf):
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     # the sharpened head multiplies every upstream rounding difference by 20
     assert err < 1e-4 * 20, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"tiny fp32 flags {flags}")
     assert excl <= 1
     # the sharpened head really exercises the decisions
     assert len(np.unique(got["state_out"])) >= 2
@@ -225,31 +136,40 @@ def test_tiny_step_fp32_transitions(flags, wf):
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=1, B=16, P=300, L=2),    # 300 prefill rows: 128 x 128 large tiles
     dict(d=256, H=4, Hkv=2, dh=64, F=512, V=1024, b=4, B=16, P=1030, L=1),   # 4120 prefill rows: 128 x 256 large tiles
     dict(d=320, H=5, Hkv=5, dh=64, F=576, V=1040, b=1, B=12, P=300, L=1),    # ragged last column tile in every GEMM
+    # 700 prefill rows (not a multiple of 128) and 2F = 16256 (not a multiple of
+    # 192): the gate/up projection of the prefill takes the 128 x 192 tile, with a
+    # ragged last tile in both directions
+    dict(d=320, H=5, Hkv=5, dh=64, F=8128, V=1040, b=1, B=12, P=700, L=1, big_tile=(4, 6)),
 ])
 def test_small_step_bf16(case):
     dims = synth.Dims(case["L"], case["d"], case["H"], case["Hkv"], case["dh"], case["F"], case["V"],
                       max(512, case["P"] + case["B"] + 8), "bf16")
     announce("small bf16 step", case)
+    if "big_tile" in case:
+        # the tile choice the library makes for these shapes (so that retuning its
+        # cost model cannot silently drop the coverage of that tile)
+        plan = dard.dard_gemm_plan(case["b"] * case["P"], 2 * case["F"], case["d"])
+        assert plan[0] == dard.GEMM_BIG and plan[1:3] == case["big_tile"], plan
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = run_case(dims, case["b"], case["B"], case["P"], prm, seed=3, lm_scale=8.0)
     err = np.max(np.abs(got["logits"] - ref["logits"]))
     # the bf16 tolerance is stated for the unsharpened model; a head sharpened
     # 8x multiplies the effect of every upstream bf16 rounding flip by 8
     assert err < 2e-2 * 8, err
-    eps, excl = check_decisions(tok, state, got, ref, prm)
-    print(f"max |dlogit| {eps:.3e}, rows excluded by the margin rule {excl} of {state.size}", file=sys.stderr)
-    assert excl <= state.size // 2
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small bf16")
+    assert excl <= state.size // 4
 
 
 def test_llada8b_two_layers():
     """The 8B-shape step (d 4096, 32 x 128, FFN 12288, vocab 126464, prompt 512,
-    block 32, candidate fraction 0.25) truncated to two layers."""
+    block 32, candidate fraction 0.25) truncated to two layers, batch 2."""
     dims = synth.truncated(synth.LLADA8B, 2)
     announce("llada8b 2-layer step")
     prm = P(dims.mask_id)
-    tok, state, conf, got, ref = run_case(dims, 1, 32, 512, prm, seed=1, frac=0.25, wdevice="cuda")
-    check_bf16_logits(got, ref, "llada8b 2 layers")
-    check_decisions(tok, state, got, ref, prm)
+    tok, state, conf, got, ref = run_case(dims, 2, 32, 512, prm, seed=1, frac=0.25, wdevice="cuda",
+                                          lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "llada8b 2 layers", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "llada8b 2 layers")
 
 
 @pytest.mark.parametrize("flags,wf", [(O.F_C_BIDIR, 0.0), (O.F_ORDER_L2R | O.F_FIXED_W, 1.0),
@@ -261,9 +181,10 @@ def test_llada8b_two_layers_variants(flags, wf):
     announce("llada8b 2-layer step variant", flags, wf)
     prm = P(dims.mask_id, flags, w_fixed=wf)
     tok, state, conf, got, ref = run_case(dims, 1, 32, 512, prm, seed=6, frac=0.5, wdevice="cuda",
-                                          check_kv=False)
-    check_bf16_logits(got, ref, f"llada8b 2 layers, flags {flags}")
-    check_decisions(tok, state, got, ref, prm)
+                                          check_kv=False, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, f"llada8b 2 layers, flags {flags}", scale=WORKLOAD_LM_SCALE)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"llada8b variant {flags}")
+    assert excl <= state.size // 10
 
 
 def test_multimodal_prefix_two_layers():
@@ -273,10 +194,10 @@ def test_multimodal_prefix_two_layers():
     dims = synth.truncated(synth.LLADA8B, 2)
     announce("multimodal prefix 2-layer step")
     prm = P(dims.mask_id)
-    tok, state, conf, got, ref = run_case(dims, 1, 32, 576 + 256, prm, seed=4, frac=0.3, wdevice="cuda",
-                                          n_image=576)
-    check_bf16_logits(got, ref, "multimodal prefix 2 layers")
-    check_decisions(tok, state, got, ref, prm)
+    tok, state, conf, got, ref = run_case(dims, 2, 32, 576 + 256, prm, seed=4, frac=0.3, wdevice="cuda",
+                                          n_image=576, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "multimodal prefix 2 layers", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "multimodal prefix 2 layers")
 
 
 def test_dream7b_gqa_two_layers():
@@ -286,6 +207,58 @@ def test_dream7b_gqa_two_layers():
     announce("dream7b gqa 2-layer step")
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = run_case(dims, 2, 64, 300, prm, seed=2, frac=0.3, wdevice="cuda",
-                                          check_kv=False)
-    check_bf16_logits(got, ref, "dream7b 2 layers")
-    check_decisions(tok, state, got, ref, prm)
+                                          check_kv=False, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "dream7b 2 layers", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "dream7b 2 layers")
+
+
+def test_dream7b_gqa_batch8_one_layer():
+    """The 7B GQA step at its benchmark batch: 8 sequences of block 64, i.e.
+    1024 step rows through the large-tile GEMMs and the batched GQA attention
+    the benchmark times; one layer, prefix 160 (ragged key tile)."""
+    dims = synth.truncated(synth.DREAM7B, 1)
+    announce("dream7b gqa batch-8 1-layer step")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = run_case(dims, 8, 64, 160, prm, seed=8, frac=0.3, wdevice="cuda",
+                                          check_kv=False, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "dream7b batch 8, 1 layer", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "dream7b batch 8, 1 layer")
+
+
+def test_multimodal_batch32_one_layer():
+    """The multimodal workload at its benchmark batch: 32 sequences of block 32
+    (2048 step rows), each prefix 64 image-embedding positions + 32 ids; one
+    layer."""
+    dims = synth.truncated(synth.LLADA8B, 1)
+    announce("multimodal batch-32 1-layer step")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = run_case(dims, 32, 32, 96, prm, seed=9, frac=0.3, wdevice="cuda",
+                                          check_kv=False, n_image=64, lm_scale=WORKLOAD_LM_SCALE)
+    check_bf16_logits(got, ref, "multimodal batch 32, 1 layer", scale=WORKLOAD_LM_SCALE)
+    check_workload_decisions(tok, state, got, ref, prm, "multimodal batch 32, 1 layer")
+
+
+def test_step_reports_bad_state_codes():
+    """With DARD_F_CHECK_STATES a sequence whose state_in holds a code outside
+    {0, 1, 2} reports DARD_BAD_STATE in block_done; the other sequences'
+    results are those of the unchecked step."""
+    dims = synth.TINY
+    announce("step with a bad state code")
+    b, B, P_ = 3, 16, 20
+    w = synth.make_weights(dims, seed=1)
+    eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, P_ + 2 * B)
+    eng.dard_prefill(dev(synth.prompt_ids(b, P_, dims.vocab, seed=2)))
+    tok, state, conf = synth.tiny_block(b, B, dims.vocab, seed=3)
+    state[1, 5] = 3
+    res = []
+    for flags in (0, dard.F_CHECK_STATES):
+        out, dbg = step_buffers(b, B, dims.vocab)
+        eng.dard_step(P_, cparams(dard, P(dims.mask_id, flags)), dev(tok), dev(state), dev(conf), out["tok_out"],
+                      out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+        res.append(collect(out, dbg))
+    assert res[1]["block_done"][1] == dard.BAD_STATE
+    assert res[0]["block_done"][1] in (0, 1)
+    for s in (0, 2):
+        assert res[1]["block_done"][s] == res[0]["block_done"][s]
+        for k in ("tok_out", "state_out", "conf_out"):
+            assert np.array_equal(res[1][k][s], res[0][k][s]), k

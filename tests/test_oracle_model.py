@@ -236,3 +236,122 @@ def test_uniform_attention_closed_form():
     expect_logits = O.to_f32(O.rmsnorm(O.to_f32(expect_h1), np.ones(d), 1e-5) @ w["lm_head"].T)
     logits, _ = O.step_logits(w, dims, cache, tok, state, conf, 49)
     assert np.allclose(logits[0], expect_logits, rtol=0, atol=1e-5)
+
+
+def _ffn_pin_model(rng, d, perm_g, perm_u, perm_d):
+    """One layer whose attention contributes nothing (W_o = 0) and whose FFN
+    reads single coordinates: gate row k = e_{perm_g[k]}, up row k =
+    e_{perm_u[k]}, down row j = e_{perm_d[j]}; unit norm gains, no eps."""
+    F = d
+    eye = np.eye(d)
+    lay = dict(attn_norm=np.ones(d), wq=rng.standard_normal((d, d)) * 0.1, wk=rng.standard_normal((d, d)) * 0.1,
+               wv=rng.standard_normal((d, d)) * 0.1, wo=np.zeros((d, d)), ffn_norm=np.ones(d),
+               w_gate=eye[perm_g], w_up=eye[perm_u], w_down=np.eye(F)[perm_d])
+    return lay
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ffn_closed_form(dtype):
+    """Closed form of the feed-forward half of a layer (SwiGLU, the bf16
+    rounding of its output, the down projection and the residual add).  With
+    W_o = 0 the attention half adds nothing; embeddings of entries +-1 have
+    unit RMS, so with unit gains and eps = 0 the normalised row is the row
+    itself.  Gate and up rows pick single coordinates (two different
+    permutations) and the down projection a third, so the update of
+    coordinate j is silu(x_g) * x_u with g = perm_g[perm_d[j]], u =
+    perm_u[perm_d[j]], rounded to the storage type, where
+    silu(1) = 1 / (1 + e^-1) and silu(-1) = -1 / (1 + e)."""
+    d = 16
+    rng = np.random.default_rng(21)
+    perm_g, perm_u, perm_d = rng.permutation(d), rng.permutation(d), rng.permutation(d)
+    assert not np.array_equal(perm_g, perm_u)
+    lay = _ffn_pin_model(rng, d, perm_g, perm_u, perm_d)
+    V = 12
+    embed = rng.choice([-1.0, 1.0], size=(V, d))
+    w = dict(embed=embed, layers=[lay], final_norm=np.ones(d), lm_head=np.eye(V, d))
+    dims = dict(n_layers=1, d_model=d, n_heads=2, n_kv_heads=2, head_dim=8, ffn_dim=d, vocab=V, max_pos=64,
+                dtype=dtype, norm_eps=0.0, rope_theta=10000.0)
+    silu_pos, silu_neg = 1.0 / (1.0 + math.exp(-1.0)), -1.0 / (1.0 + math.e)
+    ids = np.array([[3, 7, 1, 10, 4]])
+    cache = O.prefill(w, dims, ids)
+    # the prefill's residual after the layer is not returned; run the step
+    # instead and read it back through an identity LM head with unit RMS rows
+    kinds = [2, 0, 1, 2]
+    B = len(kinds)
+    tok, state, conf = _block(B, V, kinds)
+    tok[0] = [2, V - 1, 5, 9]
+    h1_rows = []
+    for r in range(2 * B):
+        x = embed[tok[0, r]] if r < B else embed[V - 1]
+        act = np.empty(d)
+        for k in range(d):
+            g, u = x[perm_g[k]], x[perm_u[k]]
+            act[k] = (silu_pos if g > 0 else silu_neg) * u
+        act = O.storage(act, dtype)
+        h1_rows.append(O.to_f32(x + act[perm_d]))
+    h1 = np.stack(h1_rows)
+    rms = np.sqrt(np.mean(h1 * h1, axis=1, keepdims=True))
+    expect = O.to_f32(O.storage(h1 / rms, dtype) @ w["lm_head"].T)
+    logits, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    assert np.allclose(logits[0], expect, rtol=0, atol=1e-6)
+
+
+def test_ffn_closed_form_catches_a_gate_up_swap():
+    """The pin above fails for an oracle whose FFN swaps gate and up (planted
+    here by swapping the two weight matrices, which is the same arithmetic)."""
+    d = 16
+    rng = np.random.default_rng(21)
+    perm_g, perm_u, perm_d = rng.permutation(d), rng.permutation(d), rng.permutation(d)
+    lay = _ffn_pin_model(rng, d, perm_g, perm_u, perm_d)
+    lay["w_gate"], lay["w_up"] = lay["w_up"], lay["w_gate"]
+    V = 12
+    embed = rng.choice([-1.0, 1.0], size=(V, d))
+    w = dict(embed=embed, layers=[lay], final_norm=np.ones(d), lm_head=np.eye(V, d))
+    dims = dict(n_layers=1, d_model=d, n_heads=2, n_kv_heads=2, head_dim=8, ffn_dim=d, vocab=V, max_pos=64,
+                dtype="bf16", norm_eps=0.0, rope_theta=10000.0)
+    silu_pos, silu_neg = 1.0 / (1.0 + math.exp(-1.0)), -1.0 / (1.0 + math.e)
+    cache = O.prefill(w, dims, np.array([[3, 7, 1]]))
+    tok, state, conf = _block(2, V, [2, 0])
+    tok[0] = [2, V - 1]
+    x = embed[2]
+    act = O.storage(np.array([(silu_pos if x[perm_g[k]] > 0 else silu_neg) * x[perm_u[k]] for k in range(d)]),
+                    "bf16")
+    h1 = O.to_f32(x + act[perm_d])
+    expect = O.to_f32(O.storage(h1 / np.sqrt(np.mean(h1 * h1)), "bf16") @ w["lm_head"].T)
+    logits, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    assert not np.allclose(logits[0, 0], expect, rtol=0, atol=1e-6)
+
+
+def test_ffn_closed_form_catches_a_missing_rounding():
+    """... and an oracle that keeps the SwiGLU output unrounded (planted by
+    making the storage rounding the identity for that one call)."""
+    d = 16
+    rng = np.random.default_rng(21)
+    perm_g, perm_u, perm_d = rng.permutation(d), rng.permutation(d), rng.permutation(d)
+    lay = _ffn_pin_model(rng, d, perm_g, perm_u, perm_d)
+    V = 12
+    embed = rng.choice([-1.0, 1.0], size=(V, d))
+    w = dict(embed=embed, layers=[lay], final_norm=np.ones(d), lm_head=np.eye(V, d))
+    dims = dict(n_layers=1, d_model=d, n_heads=2, n_kv_heads=2, head_dim=8, ffn_dim=d, vocab=V, max_pos=64,
+                dtype="bf16", norm_eps=0.0, rope_theta=10000.0)
+    orig = O.storage
+    calls = []
+
+    def skip_swiglu_rounding(x, dt):
+        calls.append(np.shape(x))
+        # storage calls of a one-layer step: embedding, then the layer's norm, q,
+        # k, v, attention output, norm and SwiGLU output (the 8th), then the final norm
+        return np.asarray(x, dtype=np.float64) if len(calls) == 8 else orig(x, dt)
+
+    cache = O.prefill(w, dims, np.array([[3, 7, 1]]))
+    tok, state, conf = _block(2, V, [2, 0])
+    tok[0] = [2, V - 1]
+    O.storage = skip_swiglu_rounding
+    try:
+        calls.clear()
+        logits, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    finally:
+        O.storage = orig
+    assert len(calls) == 9
+    ref, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
+    assert not np.allclose(logits, ref, rtol=0, atol=1e-6)
