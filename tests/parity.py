@@ -25,6 +25,7 @@ step level (against the independent oracle, measured margins)
 """
 from __future__ import annotations
 
+import math
 import sys
 
 import numpy as np
@@ -74,13 +75,15 @@ def collect(out, dbg):
     return got
 
 
-def noise_floor(run_perturbed, ref_logits, seeds=(0, 1, 2), amp=1e-7):
-    """How far the oracle's own logits move when every value is perturbed by
-    one float32 ulp (relative `amp`) just before each storage rounding; the
-    maximum over several perturbation seeds.  run_perturbed() recomputes the
-    logits with O.storage replaced."""
+def perturbed_logits(run_perturbed, seeds=(0, 1, 2), amp=1e-7):
+    """The oracle's logits with every value perturbed by one float32 ulp
+    (relative `amp`) just before each storage rounding, once per seed:
+    run_perturbed() recomputes the logits while O.storage is replaced.  Any
+    implementation whose accumulation order differs from the oracle's flips
+    some of those roundings, so these runs measure the noise floor of the
+    comparison."""
     orig = O.storage
-    worst = 0.0
+    out = []
     for sd in seeds:
         rng = np.random.default_rng(sd)
 
@@ -90,26 +93,59 @@ def noise_floor(run_perturbed, ref_logits, seeds=(0, 1, 2), amp=1e-7):
 
         O.storage = noisy
         try:
-            l2 = run_perturbed()
+            out.append(np.asarray(run_perturbed(), dtype=np.float32))
         finally:
             O.storage = orig
-        worst = max(worst, float(np.max(np.abs(l2 - ref_logits))))
-    return worst
+    return out
+
+
+def noise_floor(run_perturbed, ref_logits, seeds=(0, 1, 2), amp=1e-7):
+    """Largest maximum and root-mean-square difference of the perturbed runs
+    from the oracle's logits."""
+    worst, worst_rms = 0.0, 0.0
+    for l2 in perturbed_logits(run_perturbed, seeds, amp):
+        d = l2.astype(np.float64) - ref_logits
+        worst = max(worst, float(np.max(np.abs(d))))
+        worst_rms = max(worst_rms, float(np.sqrt(np.mean(d * d))))
+    return worst, worst_rms
+
+
+class Floor:
+    """Lazily computed perturbed runs of the oracle (three seeds), shared by
+    the logit floor and the decision floor."""
+
+    def __init__(self, run_perturbed, ref_logits):
+        self.run, self.ref, self.runs = run_perturbed, ref_logits, None
+
+    def logits(self):
+        if self.runs is None:
+            self.runs = perturbed_logits(self.run)
+        return self.runs
+
+    def __call__(self):
+        worst, worst_rms = 0.0, 0.0
+        for l2 in self.logits():
+            d = l2.astype(np.float64) - self.ref
+            worst = max(worst, float(np.max(np.abs(d))))
+            worst_rms = max(worst_rms, float(np.sqrt(np.mean(d * d))))
+        return worst, worst_rms
 
 
 def check_bf16_logits(got, ref, label, scale=1.0):
-    """bf16 multi-layer logits: the root-mean-square error within 2e-2 and the
-    maximum error within 2e-2 or twice the oracle's own noise floor (maximum
-    over three perturbation seeds).  The 2e-2 bound is stated for the
-    random-init model; an LM head sharpened by `scale` multiplies every logit,
-    and the effect of every upstream rounding difference, by that factor."""
+    """bf16 multi-layer logits: the maximum error within 2e-2 or twice the
+    oracle's own noise floor, and the root-mean-square error within 2e-2 or
+    twice the floor's root-mean-square (the floors: the largest over three
+    perturbation seeds; computed only when an error exceeds 2e-2).  The 2e-2
+    bound is stated for the random-init model; an LM head sharpened by
+    `scale` multiplies every logit, and the effect of every upstream rounding
+    difference, by that factor."""
     d = got["logits"] - ref["logits"]
     err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
     tol = 2e-2 * scale
-    floor = ref["floor"]() if err >= tol else 0.0
-    print(f"{label}: max |dlogit| {err:.3e} rms {rms:.3e} oracle noise floor {floor:.3e} (bound {tol:.3e})",
-          file=sys.stderr, flush=True)
-    assert rms < tol, rms
+    floor, floor_rms = ref["floor"]() if (err >= tol or rms >= tol) else (0.0, 0.0)
+    print(f"{label}: max |dlogit| {err:.3e} rms {rms:.3e}; oracle noise floor max {floor:.3e} rms {floor_rms:.3e} "
+          f"(bound {tol:.3e})", file=sys.stderr, flush=True)
+    assert rms < max(tol, 2.0 * floor_rms), (rms, floor_rms)
     assert err < max(tol, 2.0 * floor), (err, floor)
     return err, rms, floor
 
@@ -181,40 +217,61 @@ def check_op_level(tok, state, got, params):
 
 def check_step_level(tok, state, got, ref, params, label=""):
     """GPU decisions against the independent oracle's, where the measured
-    margins make them unambiguous.  Returns (max |dlogit|, excluded count,
-    transition counts of the candidates)."""
+    margins make them unambiguous.
+
+    The decision row of a position is its shadow row (C, U) or its mixed row
+    (M, Eq. 7).  M rows are mixed with the GPU's weight on both sides: the
+    weights themselves are checked at op level, and they differ from the
+    oracle's only after a candidate decided differently, which is counted
+    there.  A position is excluded when its argmax is ambiguous (the oracle's
+    top-1 / top-2 gap within twice the largest error among the row's
+    contenders, the entries within twice the run's maximal logit error of the
+    top) or its state is (the oracle's confidence within twice the
+    position's confidence error of a threshold).  A confidence error must
+    itself stay within what the run's logit error allows, c (e^(2 eps) - 1):
+    a gross error cannot pass as an exclusion.  Returns (max |dlogit|,
+    excluded count, transition counts of the GPU's decisions)."""
     flags = params.get("flags", 0)
-    Lg = np.asarray(got["logits"], dtype=np.float64)
-    Lr = np.asarray(ref["logits"], dtype=np.float64)
-    diff = np.abs(Lg - Lr)
-    eps = float(np.max(diff))
-    c_ref = confidences(ref, state, flags)
-    c_gpu = np.where(state == O.STATE_M, got["maxprob_mix"],
-                     got["pcur_s"] if flags & O.F_VERIFY_PCUR else got["maxprob_s"])
+    pcur_mode = bool(flags & O.F_VERIFY_PCUR)
+    Lg = np.asarray(got["logits"], dtype=np.float32)
+    Lr = np.asarray(ref["logits"], dtype=np.float32)
     b, B = state.shape
+    rows_g, rows_r = np.empty((b, B, Lg.shape[-1])), np.empty((b, B, Lr.shape[-1]))
+    for s in range(b):
+        for i in range(B):
+            if state[s, i] == O.STATE_M:
+                wg = got["w"][s, i]
+                rows_g[s, i] = O.mix_logits(Lg[s, i], Lg[s, B + i], wg)
+                rows_r[s, i] = O.mix_logits(Lr[s, i], Lr[s, B + i], wg)
+            else:
+                rows_g[s, i], rows_r[s, i] = Lg[s, B + i], Lr[s, B + i]
+    diff = np.abs(rows_g - rows_r)
+    eps = float(np.max(np.abs(Lg.astype(np.float64) - Lr)))
+    eps_rows = float(np.max(diff))
+    c_gpu = np.where(state == O.STATE_M, got["maxprob_mix"], got["pcur_s"] if pcur_mode else got["maxprob_s"])
     excluded = 0
     for s in range(b):
         for i in range(B):
-            rows = [B + i] if state[s, i] != O.STATE_M else [i, B + i]
-            ambiguous = False
-            for r in rows:
-                row = Lr[s, r]
-                a = int(np.argmax(row))
-                top2 = np.partition(row, -2)[-2:]
-                gap = float(top2[1] - top2[0])
-                contenders = row >= row[a] - 2 * eps
-                eps_r = float(np.max(diff[s, r][contenders]))
-                ambiguous |= gap <= 2 * eps_r
-            c = float(c_ref[s, i])
+            row = rows_r[s, i]
+            a, c, pc = O.confidence(row, int(tok[s, i]) if state[s, i] != O.STATE_M else None)
+            if pcur_mode and state[s, i] != O.STATE_M:
+                c = pc
+            c = float(np.float32(c))
+            top2 = np.partition(row, -2)[-2:]
+            gap = float(top2[1] - top2[0])
+            contenders = row >= row[a] - 2 * eps_rows
+            eps_r = float(np.max(diff[s, i][contenders]))
             dc = abs(float(c_gpu[s, i]) - c)
-            ambiguous |= min(abs(c - params["tau_c"]), abs(c - params["tau_u"])) <= 2 * dc + 1e-7
-            if state[s, i] == O.STATE_M:
-                ambiguous |= abs(float(got["w"][s, i]) - float(ref["w"][s, i])) > 1e-6
-            if ambiguous:
+            assert dc <= c * (math.exp(2 * eps_rows) - 1.0) + 1e-6, (label, "confidence error", s, i, dc, eps_rows)
+            st = O.transition(c, params["tau_c"], params["tau_u"])
+            state_ambiguous = min(abs(c - params["tau_c"]), abs(c - params["tau_u"])) <= 2 * dc + 1e-7
+            # the prediction matters only where the position does not fall back to [Mask]
+            if state_ambiguous or (st != O.STATE_M and gap <= 2 * eps_r):
                 excluded += 1
                 continue
-            assert got["state_out"][s, i] == ref["state_out"][s, i], (label, "state", s, i)
-            assert got["tok_out"][s, i] == ref["tok_out"][s, i], (label, "token", s, i)
+            assert got["state_out"][s, i] == st or flags & O.F_PROGRESS, (label, "state", s, i)
+            if got["state_out"][s, i] != O.STATE_M:
+                assert got["tok_out"][s, i] == a, (label, "token", s, i)
     C = state == O.STATE_C
     trans = {"C->U": int(np.sum(C & (got["state_out"] == O.STATE_U))),
              "C->M": int(np.sum(C & (got["state_out"] == O.STATE_M))),
@@ -232,11 +289,36 @@ def check_decisions(tok, state, got, ref, params, label=""):
     return eps, excl, trans
 
 
-def check_workload_decisions(tok, state, got, ref, params, label):
-    """The workload-shape protocol: op level exact, at most 10 % of positions
-    excluded at step level, and both candidate promotions and demotions
-    among the GPU's decisions (so that the comparison is not vacuous)."""
+def decision_floor(tok, state, ref, params):
+    """Positions the same step-level protocol excludes when the oracle is
+    compared with its own perturbed runs (the largest count over the seeds):
+    the part of the bf16 exclusions that the rounding noise alone causes."""
+    worst = 0
+    for l2 in ref["floor"].logits():
+        pseudo = O.decide(l2, tok, state, params)
+        pseudo["logits"] = l2
+        pseudo["w"] = pseudo["w"].astype(np.float32)
+        for k in ("maxprob_s", "pcur_s", "maxprob_mix"):
+            pseudo[k] = pseudo[k].astype(np.float32)
+        _, excl, _ = check_step_level(tok, state, pseudo, ref, params, "oracle vs its perturbed run")
+        worst = max(worst, excl)
+    return worst
+
+
+def check_workload_decisions(tok, state, got, ref, params, label, require_transitions=True):
+    """The workload-shape protocol: op level exact; at step level at most 10 %
+    of the positions excluded, or twice what the oracle's own one-ulp
+    perturbation excludes (the same rule as for the logits); and both
+    candidate promotions and demotions among the GPU's decisions, so that the
+    comparison is not vacuous."""
     eps, excl, trans = check_decisions(tok, state, got, ref, params, label)
-    assert excl <= state.size // 10, (excl, state.size)
-    assert trans["C->U"] >= 1 and trans["C->M"] >= 1, trans
+    bound = state.size // 10
+    if excl > bound:
+        floor = decision_floor(tok, state, ref, params)
+        print(f"{label}: decision floor (oracle vs its perturbed runs) {floor} of {state.size}", file=sys.stderr,
+              flush=True)
+        bound = max(bound, 2 * floor)
+    assert excl <= bound, (excl, bound, state.size)
+    if require_transitions:
+        assert trans["C->U"] >= 1 and trans["C->M"] >= 1, trans
     return eps, excl, trans

@@ -20,8 +20,8 @@ import torch
 
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
-from parity import (P, announce, check_bf16_logits, check_op_level, check_step_level, collect, cparams, dev,
-                    noise_floor, step_buffers)
+from parity import (P, Floor, announce, check_bf16_logits, check_op_level, check_workload_decisions, collect,
+                    cparams, dev, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -86,11 +86,13 @@ def test_oracle_and_p2_32_layers(llada8b):
         c2 = O.prefill(ow, dd, ids)
         return O.step_logits(ow, dd, c2, tok, state, conf, prm["mask_id"])[0]
 
-    floor = noise_floor(perturbed, ref["logits"])
-    ref["floor"] = lambda: floor
+    ref["floor"] = Floor(perturbed, ref["logits"])
+    floor, floor_rms = ref["floor"]()
     err, rms, _ = check_bf16_logits(got, ref, "llada8b 32 layers")
-    check_op_level(tok, state, got, prm)
-    check_step_level(tok, state, got, ref, prm, "llada8b 32 layers")
+    # the random-init head gives top-1 probabilities near 1/V: every position
+    # falls to M on both sides (the decisions at 32 layers are not vacuous in
+    # their logits, which the bound above compares)
+    check_workload_decisions(tok, state, got, ref, prm, "llada8b 32 layers", require_transitions=False)
     # P2: no candidates (the C positions of the same block become U)
     state2 = np.where(state == O.STATE_C, O.STATE_U, state).astype(np.uint8)
     announce("P2 at 32 layers")
@@ -98,9 +100,10 @@ def test_oracle_and_p2_32_layers(llada8b):
     M = state2[0] == O.STATE_M
     d = got2["logits"][0, :B][M] - got2["logits"][0, B:][M]
     p2max, p2rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
-    print(f"32 layers: GPU vs oracle max {err:.3e} rms {rms:.3e}, oracle noise floor (3 seeds) {floor:.3e}; "
-          f"P2 max |x - s| {p2max:.3e} rms {p2rms:.3e}", file=sys.stderr, flush=True)
-    assert p2rms < 2e-2, p2rms
+    print(f"32 layers: GPU vs oracle max {err:.3e} rms {rms:.3e}, oracle noise floor (3 seeds) max {floor:.3e} "
+          f"rms {floor_rms:.3e}; P2 max |x - s| {p2max:.3e} rms {p2rms:.3e}", file=sys.stderr, flush=True)
+    assert p2rms < max(2e-2, 2.0 * floor_rms), (p2rms, floor_rms)
     assert p2max < max(2e-2, 2.0 * floor), (p2max, floor)
-    assert np.all(got2["w"] == 1.0)
+    # Eq. 6 without promotions or demotions: w = p0 / p0 = 1 at every M position
+    assert np.all(got2["w"][0][M] == 1.0)
     check_op_level(tok, state2, got2, prm)

@@ -10,7 +10,7 @@ from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
 from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, noise_floor, sharpen, step_buffers)
+                    dev, Floor, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -39,7 +39,7 @@ def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None,
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     ref = O.dard_step_full(ow, dd, seq, blk, B, state, conf, params)
-    ref["floor"] = lambda: noise_floor(
+    ref["floor"] = Floor(
         lambda: O.full_step_logits(ow, dd, seq, blk, B, state, conf, params["mask_id"], params.get("flags", 0)),
         ref["logits"])
     return tok, state, conf, got, ref

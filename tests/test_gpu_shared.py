@@ -10,7 +10,7 @@ from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
 from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, noise_floor, sharpen, step_buffers)
+                    dev, Floor, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,7 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
         c2 = O.join_shared(shp, O.prefill_suffix(ow, dd, shp, committed))
         return O.step_logits(ow, dd, c2, tok, state, conf, params["mask_id"], params.get("flags", 0))[0]
 
-    ref["floor"] = lambda: noise_floor(perturbed, ref["logits"])
+    ref["floor"] = Floor(perturbed, ref["logits"])
     # the suffix keys written by dard_prefill_suffix (V of every layer; K is stored with
     # each head's rotary pairs interleaved)
     if Pc:
