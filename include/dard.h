@@ -218,6 +218,23 @@ dard_status dard_confidence(const float* logits_s, const float* logits_x, const 
                             float* entropy, float* margin,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* dard_confidence for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and results, with the chunk partials in
+ * a scratch array the library keeps in device memory (4 MiB per GPU, held
+ * until the process ends) instead of a caller workspace.  It calls no
+ * hipMalloc / hipFree.  Needs rows * ceil(V / 8192) * k <= 1048576 (k = 5
+ * when entropy or margin is asked for, else 3): about 11000 rows at
+ * V = 152064 with k = 5; larger sizes return DARD_ERR_SHAPE and launch
+ * nothing.  Every call on one GPU uses that GPU's one array, so calls that
+ * overlap on one GPU (other streams, other threads) race; calls ordered on
+ * one stream do not.  Each call writes every partial it reads, so nothing
+ * carries over from the previous call. */
+dard_status dard_confidence_noalloc(const float* logits_s, const float* logits_x, const float* w,
+                                    const int32_t* cur_tok, int rows, int V, int64_t ld,
+                                    int32_t* argmax, float* maxprob, float* pcur,
+                                    float* entropy, float* margin, void* stream);
+
 /* ------------------------------------------------------------ a6/a8: decisions
  * Decision part of Algorithm 1 for b sequences of block length B.
  * phase DARD_PHASE_VERIFY (after the shadow confidences of the candidates):

@@ -293,23 +293,56 @@ size_t dard_confidence_workspace_bytes(int rows, int V) {
     return align256((size_t)rows * conf_chunks(V) * kConfStatsStride * 4);
 }
 
-dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w, const int32_t* cur_tok,
-                            int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur,
-                            float* entropy, float* margin, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+
+int check_confidence_args(const float* logits_s, const float* logits_x, const float* w, const int32_t* cur_tok,
+                          int rows, int V, int64_t ld, const int32_t* argmax, const float* maxprob,
+                          const float* pcur) {
     if (!logits_s || !argmax || !maxprob) return fail(DARD_ERR_ARG, "NULL pointer");
     if (logits_x && !w) return fail(DARD_ERR_ARG, "mixing needs w");
     if (pcur && (!cur_tok || logits_x)) return fail(DARD_ERR_ARG, "pcur needs cur_tok and no mixing");
     if (rows < 1 || V < 1 || ld < V || ld % 4) return fail(DARD_ERR_SHAPE, "need rows, V >= 1, ld >= V, ld %% 4 == 0");
-    const size_t need = dard_confidence_workspace_bytes(rows, V);
-    if (!ws || ws_bytes < need) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", need);
+    return DARD_OK;
+}
+
+// The two kernels of the confidence reduction with chunk partials at `part`.
+int run_confidence(float* part, const float* logits_s, const float* logits_x, const float* w,
+                   const int32_t* cur_tok, int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur,
+                   float* entropy, float* margin, hipStream_t s) {
     ConfArgs a{};
     a.ls = logits_s; a.lx = logits_x; a.w = w; a.ld_s = ld; a.ld_x = ld;
-    a.rows = rows; a.V = V; a.part = (float*)ws; a.state = nullptr; a.phase = 0; a.step_B = 0;
-    hipStream_t s = (hipStream_t)stream;
+    a.rows = rows; a.V = V; a.part = part; a.state = nullptr; a.phase = 0; a.step_B = 0;
     HIPOK(launch_conf_partial(a, entropy || margin, s));
-    HIPOK(launch_conf_combine((float*)ws, rows, conf_chunks(V), V, logits_s, ld, cur_tok, argmax, maxprob, pcur,
-                              entropy, margin, s));
+    HIPOK(launch_conf_combine(part, rows, conf_chunks(V), V, logits_s, ld, cur_tok, argmax, maxprob, pcur, entropy,
+                              margin, s));
     return DARD_OK;
+}
+
+}  // namespace
+
+dard_status dard_confidence(const float* logits_s, const float* logits_x, const float* w, const int32_t* cur_tok,
+                            int rows, int V, int64_t ld, int32_t* argmax, float* maxprob, float* pcur,
+                            float* entropy, float* margin, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_confidence_args(logits_s, logits_x, w, cur_tok, rows, V, ld, argmax, maxprob, pcur)) return rc;
+    const size_t need = dard_confidence_workspace_bytes(rows, V);
+    if (!ws || ws_bytes < need) return fail(DARD_ERR_WORKSPACE, "workspace needs %zu bytes", need);
+    return run_confidence((float*)ws, logits_s, logits_x, w, cur_tok, rows, V, ld, argmax, maxprob, pcur, entropy,
+                          margin, (hipStream_t)stream);
+}
+
+dard_status dard_confidence_noalloc(const float* logits_s, const float* logits_x, const float* w,
+                                    const int32_t* cur_tok, int rows, int V, int64_t ld, int32_t* argmax,
+                                    float* maxprob, float* pcur, float* entropy, float* margin, void* stream) {
+    if (int rc = check_confidence_args(logits_s, logits_x, w, cur_tok, rows, V, ld, argmax, maxprob, pcur)) return rc;
+    const size_t stride = (entropy || margin) ? kConfStatsStride : kConfStride;
+    const size_t need = (size_t)rows * conf_chunks(V) * stride;
+    if (need > conf_scratch_floats())
+        return fail(DARD_ERR_SHAPE, "rows x ceil(V / 8192) x %zu = %zu partial floats exceed the %zu of the "
+                    "preallocated scratch", stride, need, conf_scratch_floats());
+    float* part = nullptr;
+    HIPOK(conf_scratch(&part));
+    return run_confidence(part, logits_s, logits_x, w, cur_tok, rows, V, ld, argmax, maxprob, pcur, entropy, margin,
+                          (hipStream_t)stream);
 }
 
 // ---------------------------------------------------------------- decisions

@@ -12,6 +12,8 @@
 // the entropy is ln(s) - t / s, and the second-largest logit m2, so that the
 // margin p_(1) - p_(2) is (1 - exp(m2 - max)) / s.  Moving a partial to a
 // larger maximum M scales s and t by e = exp(m - M) and adds (m - M) s e to t.
+#include <mutex>
+
 #include "common.h"
 #include "launch.h"
 
@@ -217,6 +219,37 @@ __global__ void conf_combine_kernel(const float* __restrict__ part, int rows, in
 }
 
 }  // namespace
+
+// Chunk partials of dard_confidence_noalloc: a fixed array in device memory
+// (each GPU holds its own copy for the life of the process).  Its device
+// address comes from hipGetSymbolAddress, once per device; the host-side
+// name `scratch` is not a device address and is never passed to a kernel.
+constexpr size_t kScratchFloats = size_t(1) << 20;   // 4 MiB
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch[kMaxDevices];
+}  // namespace
+
+size_t conf_scratch_floats() { return kScratchFloats; }
+
+hipError_t conf_scratch(float** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch[dev] = static_cast<float*>(p);
+    }
+    *out = g_scratch[dev];
+    return hipSuccess;
+}
 
 int conf_chunks(int V) { return (V + kChunk - 1) / kChunk; }
 

@@ -133,6 +133,10 @@ struct ConfArgs {
 };
 constexpr int kConfStride = 3, kConfStatsStride = 5;
 int conf_chunks(int V);
+// The device-resident partials array of dard_confidence_noalloc on the
+// current device (looked up on first use per device) and its size in floats.
+hipError_t conf_scratch(float** out);
+size_t conf_scratch_floats();
 // stats: also form the entropy / margin terms (partials of kConfStatsStride)
 hipError_t launch_conf_partial(const ConfArgs& a, bool stats, hipStream_t s);
 // entropy or margin != NULL reads statistics partials

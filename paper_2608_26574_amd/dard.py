@@ -29,7 +29,7 @@ PHASE_VERIFY, PHASE_FINAL = 0, 1
 
 EXPORTS = [
     "dard_last_error", "dard_version", "dard_check_states", "dard_build_state_mask", "dard_attention_workspace_bytes",
-    "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence",
+    "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence", "dard_confidence_noalloc",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
     "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_prefill_suffix",
     "dard_step_shared", "dard_pack_matrix", "dard_linear", "dard_gemm_plan",
@@ -83,6 +83,7 @@ def lib():
                                             u32, vp, vp, sz, vp]),
             "dard_confidence_workspace_bytes": (sz, [i32, i32]),
             "dard_confidence": (i32, [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "dard_confidence_noalloc": (i32, [vp, vp, vp, vp, i32, i32, i64, vp, vp, vp, vp, vp, vp]),
             "dard_commit_remask": (i32, [i32, vp, i32, i32] + [vp] * 14),
             "dard_packed_weight_bytes": (sz, [vp]),
             "dard_pack_weights": (i32, [vp, vp, i32, vp, sz, vp]),
@@ -203,6 +204,15 @@ def dard_confidence(logits_s, argmax, maxprob, logits_x=None, w=None, cur_tok=No
     _check(lib().dard_confidence(_p(logits_s), _p(logits_x), _p(w), _p(cur_tok), rows, V, logits_s.stride(0),
                                  _p(argmax), _p(maxprob), _p(pcur), _p(entropy), _p(margin), _p(ws), nbytes,
                                  _stream(stream)))
+
+
+def dard_confidence_noalloc(logits_s, argmax, maxprob, logits_x=None, w=None, cur_tok=None, pcur=None,
+                            stream=None, entropy=None, margin=None):
+    """dard_confidence with the library's preallocated scratch (no workspace)."""
+    rows, V = logits_s.shape
+    _check(lib().dard_confidence_noalloc(_p(logits_s), _p(logits_x), _p(w), _p(cur_tok), rows, V,
+                                         logits_s.stride(0), _p(argmax), _p(maxprob), _p(pcur), _p(entropy),
+                                         _p(margin), _stream(stream)))
 
 
 def dard_commit_remask(phase, params, state_in, maxprob_s=None, pcur_s=None, argmax_s=None, maxprob_mix=None,
