@@ -43,6 +43,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the 7B GQA and multimodal full-step lines")
     ap.add_argument("--layers", type=int, default=32, help=argparse.SUPPRESS)
+    ap.add_argument("--profile", choices=("ops", "traffic"), default=None,
+                    help="run a fixed workload for a profiler pass instead of the benchmark: 'ops' (isolated "
+                         "attention, confidence reduction, 7B GQA large-tile steps, a 1 GiB copy) or 'traffic' "
+                         "(three 8B-shape steps and a 1 GiB copy, for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the DARD step is data-parallel "
@@ -53,6 +57,11 @@ def main():
     import torch
 
     from paper_2608_26574_amd import dard, synth
+
+    if args.profile == "ops":
+        return profile_ops()
+    if args.profile == "traffic":
+        return profile_traffic()
 
     dims = synth.LLADA8B if args.layers == 32 else synth.truncated(synth.LLADA8B, args.layers)
     b, B, prompt, gen, frac = 1, 32, 512, 256, 0.25
@@ -585,7 +594,8 @@ def op_measurements(reps=20):
         return ms / n
 
     res = {"attention": [], "confidence": []}
-    shapes = [("8B MHA", bsz, 32, 32, 32, 512, 0.25) for bsz in (1, 4, 16)] + \
+    # the isolated-attention workload: batch 1 / 4 / 16 x candidate fraction 0.1 / 0.25 / 0.5
+    shapes = [("8B MHA", bsz, 32, 32, 32, 512, frac) for bsz in (1, 4, 16) for frac in (0.1, 0.25, 0.5)] + \
              [("7B GQA", 8, 28, 4, 64, P, 0.3) for P in (1024, 1472)]
     dh = 128
     for label, bsz, H, Hkv, B, P, frac in shapes:
@@ -609,6 +619,7 @@ def op_measurements(reps=20):
         flops = 4 * dh * H * 2 * B * (P + B) * bsz
         nbytes = 2 * bsz * Hkv * (P + 2 * B) * dh * 2 + 2 * q.numel() * 2
         res["attention"].append({"shape": label, "batch": bsz, "heads": [H, Hkv], "block": B, "prefix": P,
+                                 "cand_frac": frac,
                                  "us": round(ms * 1e3, 2), "kernel_us": round(kms * 1e3, 2),
                                  "tflops": round(flops / (kms * 1e-3) / 1e12, 2),
                                  "mfma_frac": round(flops / (kms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
@@ -710,12 +721,129 @@ def cpu_baseline(dims, b, B, P, frac, layers_sampled=2, min_s=10.0):
     per_layer = max((t_s - t_0) / layers_sampled, 1e-9)
     t_step = t_0 + dims.n_layers * per_layer
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(1.0 / t_step, 5), "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model,
             "sample": f"{n_s} oracle DARD steps with {layers_sampled} of {dims.n_layers} layers plus LM head and "
                       f"decisions ({el_s:.1f} s) and {n_0} with no layers ({el_0:.1f} s); per-layer time "
                       f"{per_layer:.3f} s scaled to {dims.n_layers} layers",
             "host_cpus": os.cpu_count()}
 
 
+# ---------------------------------------------------------------- profiler workloads
+COPY_BYTES = 1 << 30
+
+
+def _copy_calibration(tag):
+    """One plain device-to-device copy of COPY_BYTES: its kernel calibrates the
+    byte counters (a copy of S bytes reads S and writes S bytes of HBM)."""
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[{tag}] copied {COPY_BYTES} bytes")
+
+
+def profile_traffic():
+    """Three DARD steps at the 8B shape (32 layers, batch 1, block 32, prompt
+    512) and one 1 GiB copy, for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE."""
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+    dims = synth.LLADA8B
+    b, B, P, cap = 1, 32, 512, 800
+    log("[traffic] packing weights")
+    w = synth.make_weights(dims, seed=1, device="cuda")
+    eng = dard.Engine(dims, w, b, B, cap)
+    del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    eng.dard_prefill(torch.from_numpy(synth.prompt_ids(b, P, dims.vocab, seed=2)).cuda())
+    tok, state, conf = (torch.from_numpy(a).cuda() for a in synth.workload_block(b, B, 0.25, dims.vocab, seed=1000))
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, 0)
+    t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    c_out = torch.empty(b, B, device="cuda")
+    done = torch.empty(b, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        eng.dard_step(P, params, tok, state, conf, t_out, s_out, c_out, done)
+    torch.cuda.synchronize()
+    log("[traffic] 3 steps done")
+    _copy_calibration("traffic")
+    return 0
+
+
+def profile_ops():
+    """The isolated operations for counter passes, inputs rotated through
+    copies larger than the 256 MB MALL: 10 attention calls at the 7B GQA
+    shape (28/4 heads x 128, batch 8, block 64, prefix 1024, candidate
+    fraction 0.3), 10 at the 8B MHA shape (32 x 128, batch 16, prefix 512,
+    block 32, fraction 0.25), 10 confidence reductions over 696 x 152064
+    fp32 logits, 3 steps of the 7B GQA model truncated to 2 layers at batch 8
+    (1024 token rows: the large-tile GEMMs), then a 1 GiB copy."""
+    import torch
+
+    from paper_2608_26574_amd import dard, synth
+
+    def attention(b, Hq, Hkv, B, P, frac, calls, seed):
+        dh, cap = 128, P + 2 * B
+        g = torch.Generator(device="cuda").manual_seed(seed)
+        ncopy = max(2, -(-600 * 2**20 // (2 * b * Hkv * cap * dh * 2)))
+        q = torch.randn(b, 2 * B, Hq, dh, generator=g, device="cuda").bfloat16()
+        ks = [torch.randn(b, Hkv, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        vs = [torch.randn(b, Hkv, dh, cap, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        _, state, conf = synth.workload_block(b, B, frac, 100, seed=seed)
+        state, conf = torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()
+        out = torch.empty_like(q)
+        ws = torch.empty(max(dard.dard_attention_workspace_bytes(1, b, B, Hq, dh, P), 1), dtype=torch.uint8,
+                         device="cuda")
+        for i in range(calls):
+            dard.dard_masked_attention(q, ks[i % ncopy], vs[i % ncopy], P, state, conf, dh ** -0.5, 0, out, ws)
+        torch.cuda.synchronize()
+
+    def confidence(rows, V, calls):
+        ncopy = max(2, -(-600 * 2**20 // (rows * V * 4)))
+        g = torch.Generator(device="cuda").manual_seed(4)
+        ls = [torch.randn(rows, V, generator=g, device="cuda") for _ in range(ncopy)]
+        am = torch.empty(rows, dtype=torch.int32, device="cuda")
+        mp = torch.empty(rows, device="cuda")
+        ws = torch.empty(dard.dard_confidence_workspace_bytes(rows, V), dtype=torch.uint8, device="cuda")
+        for i in range(calls):
+            dard.dard_confidence(ls[i % ncopy], am, mp, ws=ws)
+        torch.cuda.synchronize()
+
+    attention(8, 28, 4, 64, 1024, 0.3, 10, seed=1)
+    log("[ops] GQA attention done")
+    attention(16, 32, 32, 32, 512, 0.25, 10, seed=2)
+    log("[ops] MHA attention done")
+    confidence(8 * 87, 152064, 10)
+    log("[ops] confidence done")
+    dims = synth.truncated(synth.DREAM7B, 2)
+    b, B, P = 8, 64, 1024
+    w = synth.make_weights(dims, seed=1, device="cuda")
+    eng = dard.Engine(dims, w, b, B, P + 2 * B)
+    del w
+    eng.dard_prefill(torch.from_numpy(synth.prompt_ids(b, P, dims.vocab, seed=2)).cuda())
+    tok, state, conf = (torch.from_numpy(a).cuda() for a in synth.workload_block(b, B, 0.3, dims.vocab, seed=3))
+    params = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, 0)
+    t_out = torch.empty(b, B, dtype=torch.int32, device="cuda")
+    s_out = torch.empty(b, B, dtype=torch.uint8, device="cuda")
+    c_out = torch.empty(b, B, device="cuda")
+    for _ in range(3):
+        eng.dard_step(P, params, tok, state, conf, t_out, s_out, c_out)
+    torch.cuda.synchronize()
+    log("[ops] 7B GQA steps done")
+    _copy_calibration("ops")
+    return 0
+
+
 if __name__ == "__main__":
-    main()
+    sys.exit(main() or 0)

@@ -88,6 +88,16 @@ typedef int dard_status;
  *                 probabilities, largest first: the carried key is the margin;
  *   FIXED_W       every masked token mixes its logits with the constant
  *                 params.w_fixed instead of the weight of Eq. 5-6.
+ * An evaluation order (the steps only; other entry points ignore it):
+ *   HIDDEN_MIX    Eq. 7 applied to the final normalised hidden state instead
+ *                 of the logits: the LM head has no bias, so
+ *                 W (w x + (1 - w) s) = w W x + (1 - w) W s in exact
+ *                 arithmetic; the mixed row is rounded to the storage type
+ *                 before the head, so results differ from logit mixing by
+ *                 that rounding.  The head then runs twice, over the
+ *                 candidates' shadow rows (their verification gives w) and
+ *                 over the U shadow rows plus one mixed row per M position:
+ *                 B rows per sequence instead of B + |M|.
  * Validation:
  *   CHECK_STATES  the steps (dard_step, dard_step_full, dard_step_shared) and
  *                 the FINAL phase of dard_commit_remask check every state
@@ -105,9 +115,10 @@ typedef int dard_status;
 #define DARD_F_ORDER_MARGIN   (1u << 7)
 #define DARD_F_FIXED_W        (1u << 8)
 #define DARD_F_CHECK_STATES   (1u << 9)
+#define DARD_F_HIDDEN_MIX     (1u << 10)
 #define DARD_F_ORDERS (DARD_F_C_BIDIR | DARD_F_ORDER_L2R | DARD_F_ORDER_ENTROPY | DARD_F_ORDER_MARGIN)
 #define DARD_F_ALL    (DARD_F_XSELF_SHADOW | DARD_F_MKEYS_SHADOW | DARD_F_VERIFY_PCUR | DARD_F_PROGRESS | \
-                       DARD_F_ORDERS | DARD_F_FIXED_W | DARD_F_CHECK_STATES)
+                       DARD_F_ORDERS | DARD_F_FIXED_W | DARD_F_CHECK_STATES | DARD_F_HIDDEN_MIX)
 
 /* block_done value of a sequence whose state_in held a code outside {0,1,2}
  * (only with DARD_F_CHECK_STATES). */
@@ -312,7 +323,14 @@ dard_status dard_prefill(const dard_dims* dims, const void* packed, void* kv, in
  *   conf_in/conf_out [b][B] float32 (the ordering key: c_i, or -entropy /
  *   margin under ORDER_ENTROPY / ORDER_MARGIN), block_done [b] int32.
  * Outputs may alias the matching inputs.  `dbg`, when not NULL, receives
- * copies of intermediate results (any member may be NULL). */
+ * copies of intermediate results (any member may be NULL).
+ * Rows of the LM head: with at most 64 rows per step (b * 2B <= 64, logit
+ * mixing) the head runs over all of them; otherwise only over the rows the
+ * decisions read -- the shadow row of every position and the x row of every
+ * M position (with HIDDEN_MIX: the shadow rows of C and U positions and the
+ * mixed row of every M position, which takes the M position's shadow slot).
+ * dbg->logits receives exactly the rows the head ran over; the others are
+ * left as they were. */
 typedef struct {
     float* logits;       /* [b][2B][V]: x rows then s rows                  */
     float* w;            /* [b][B] guidance weights (0 at C/U)              */

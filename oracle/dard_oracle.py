@@ -74,6 +74,8 @@ F_ORDER_L2R = 1 << 5      # candidates ordered by position, left first
 F_ORDER_ENTROPY = 1 << 6  # ... by entropy of the prediction, lowest first
 F_ORDER_MARGIN = 1 << 7   # ... by top-1 minus top-2 probability, largest first
 F_FIXED_W = 1 << 8        # every M token mixes with the constant w_fixed
+F_CHECK_STATES = 1 << 9   # library-side validation of state codes (no effect on the arithmetic)
+F_HIDDEN_MIX = 1 << 10    # library-side evaluation order of Eq. 7 (the oracle mixes logits)
 F_ORDERS = F_C_BIDIR | F_ORDER_L2R | F_ORDER_ENTROPY | F_ORDER_MARGIN
 
 LAMBDA_DEFAULT = 0.5 ** (1.0 / 8.0)   # App. A.2: lambda = 0.917, i.e. 0.5^(1/8)

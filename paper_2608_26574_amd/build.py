@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(CSRC, "_build")
 LIB = os.path.join(HERE, "libdard.so")
 SOURCES = ["mask.hip", "attention.hip", "gemm.hip", "elementwise.hip", "confidence.hip", "decide.hip",
-           "api.cpp"]
+           "lmhead.hip", "api.cpp"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -92,7 +92,9 @@ Layout layout_of(const dard_dims* d) {
 
 // Workspace of dard_step / dard_prefill.
 struct WsLayout {
-    size_t h, xn, q, attn, act, sel, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, ids, tok, total;
+    size_t h, xn, q, attn, act, sel, part, part_ml, part_slots, gpart, logits, cpart_v, cpart_m, w, ids, tok;
+    size_t hx, rowmap, lmcount, lpart;   // the LM head on listed rows (lmhead.hip)
+    size_t total;
 };
 
 WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
@@ -131,6 +133,14 @@ WsLayout ws_layout(const dard_dims* d, int b, int B, int cap) {
     // rows (streaming GEMM) or 4 splits of all rows (pipelined and large-tile GEMMs)
     const size_t prow = rows * 4 > 8 * 64 ? rows * 4 : 8 * 64;
     W.gpart = o; o = align256(o + prow * d->d_model * 4);
+    // listed LM-head rows: the compact input (whole 64-row blocks), two row
+    // lists, their device counts, and the fused column-tile partials (tiles of
+    // 128 columns or more)
+    const size_t lrows = (step_rows + 63) / 64 * 64;
+    W.hx = o; o = align256(o + lrows * d->d_model * es);
+    W.rowmap = o; o = align256(o + 2 * step_rows * 4);
+    W.lmcount = o; o = align256(o + 4 * 4);
+    W.lpart = o; o = align256(o + step_rows * (((size_t)d->vocab + 127) / 128) * 3 * 4);
     W.total = o;
     return W;
 }
@@ -595,53 +605,124 @@ dard_status dard_prefill(const dard_dims* d, const void* packed, void* kv, int c
 
 namespace {
 
-// The end of a step, shared by both modes: LM head over the final-normalised
-// rows xrows (x then s rows of each sequence, b * 2B rows), the shadow
-// confidences of the candidates, verification and guidance weights, the
-// mixed confidences and the transitions (a4-a8).
+// The end of a step, shared by every step mode (a4-a8): the LM head over the
+// final-normalised rows xrows (x then s rows of each sequence, b * 2B rows),
+// the shadow confidences of the candidates, verification and guidance
+// weights, the mixed confidences of the M positions and the transitions.
+//   - With at most 64 rows (the weight-streaming LM head, which reads every
+//     token slot of its 64 anyway) the head runs over all 2B rows.
+//   - Otherwise it runs only on the rows the decisions read (lmhead.hip):
+//     B + |M| rows per sequence with logit mixing; with hidden-state mixing
+//     (DARD_F_HIDDEN_MIX, Eq. 7 applied to the final hidden state) the
+//     candidates' shadow rows first, then, once their verification has given
+//     the guidance weights, the U shadow rows and one mixed row per M
+//     position: B rows per sequence.
+//   - When the large-tile GEMM runs the head (and neither the entropy /
+//     margin statistics nor the current-token probability are asked for),
+//     its epilogue forms the (max, argmax, sum) partials of the C and U
+//     shadow rows itself and their logits are never written.
 int step_tail(const Fwd& f, const dard_params* params, int b, int B, const void* xrows, const int32_t* tok_in,
               const uint8_t* state_in, int32_t* tok_out, uint8_t* state_out, float* conf_out, int32_t* block_done,
               const dard_step_debug* dbg) {
     const dard_dims* d = f.d;
-    const int rows = b * 2 * B, V = d->vocab;
+    const int rows = b * 2 * B, V = d->vocab, D = d->d_model, dt = d->dtype;
     float* logits = (float*)(f.ws + f.W.logits);
-    EpiArgs e{};
-    e.kind = EPI_STORE_F32; e.y = logits; e.ldy = V;
-    HIPOK(launch_gemm(d->dtype, xrows, rows, d->d_model, d->d_model, f.pk + f.L.lm_head, V, e,
-                      DARD_K_GEMM_HEAD, f.s, frag_rows(d->dtype, rows)));
+    float* cpv = (float*)(f.ws + f.W.cpart_v);
+    float* cpm = (float*)(f.ws + f.W.cpart_m);
+    float* wbuf = (float*)(f.ws + f.W.w);
+    const uint32_t flags = params->flags;
+    const bool stats = needs_stats(flags);
+    const bool hidden = (flags & DARD_F_HIDDEN_MIX) != 0;
+    const bool frag = frag_rows(dt, rows);
+    const void* head_w = f.pk + f.L.lm_head;
 
     ConfArgs c{};
     c.ls = logits; c.ld_s = V; c.ld_x = V; c.rows = b * B; c.V = V; c.state = state_in; c.step_B = B;
-    c.phase = 0; c.part = (float*)(f.ws + f.W.cpart_v);
-    const bool stats = needs_stats(params->flags);
-    HIPOK(launch_conf_partial(c, stats, f.s));
-
     DecideArgs a{};
     a.b = b; a.B = B; a.tau_c = params->tau_c; a.tau_u = params->tau_u; a.lambda = params->lambda;
-    a.p0 = params->p0; a.mask_id = params->mask_id; a.flags = params->flags; a.w_fixed = params->w_fixed;
+    a.p0 = params->p0; a.mask_id = params->mask_id; a.flags = flags; a.w_fixed = params->w_fixed;
     a.state_in = state_in; a.tok_in = tok_in; a.stride = stats ? kConfStatsStride : kConfStride;
-    a.part_v = (const float*)(f.ws + f.W.cpart_v); a.part_m = (const float*)(f.ws + f.W.cpart_m);
+    a.part_v = cpv; a.part_m = cpm;
     a.logits = logits; a.ld = V; a.nchunk = conf_chunks(V);
-    a.w_out = (float*)(f.ws + f.W.w);
-    a.phase = DARD_PHASE_VERIFY;
-    HIPOK(launch_decide(a, f.s));
+    a.w_out = wbuf;
+    auto verify = [&]() -> int {
+        a.phase = DARD_PHASE_VERIFY;
+        HIPOK(launch_decide(a, f.s));
+        return DARD_OK;
+    };
+    auto final_phase = [&]() -> int {
+        a.phase = DARD_PHASE_FINAL;
+        a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out; a.block_done = block_done;
+        if (dbg) {
+            a.dbg_maxprob_s = dbg->maxprob_s; a.dbg_argmax_s = dbg->argmax_s; a.dbg_pcur_s = dbg->pcur_s;
+            a.dbg_maxprob_mix = dbg->maxprob_mix; a.dbg_argmax_mix = dbg->argmax_mix;
+            if (stats) { a.dbg_entropy = dbg->entropy; a.dbg_margin = dbg->margin; }
+        }
+        HIPOK(launch_decide(a, f.s));
+        if (dbg && dbg->w) HIPOK(hipMemcpyAsync(dbg->w, wbuf, (size_t)b * B * 4, hipMemcpyDeviceToDevice, f.s));
+        return DARD_OK;
+    };
 
-    c.phase = 1; c.w = (const float*)(f.ws + f.W.w); c.part = (float*)(f.ws + f.W.cpart_m);
-    HIPOK(launch_conf_partial(c, stats, f.s));
-
-    a.phase = DARD_PHASE_FINAL;
-    a.state_out = state_out; a.tok_out = tok_out; a.conf_out = conf_out; a.block_done = block_done;
-    if (dbg) {
-        a.dbg_maxprob_s = dbg->maxprob_s; a.dbg_argmax_s = dbg->argmax_s; a.dbg_pcur_s = dbg->pcur_s;
-        a.dbg_maxprob_mix = dbg->maxprob_mix; a.dbg_argmax_mix = dbg->argmax_mix;
-        if (stats) { a.dbg_entropy = dbg->entropy; a.dbg_margin = dbg->margin; }
+    const int max_rows = hidden ? b * B : rows;
+    int32_t plan[4];
+    gemm_plan(dt, max_rows, V, D, false, frag, plan, true);
+    if (!hidden && plan[0] == DARD_GEMM_STREAM) {
+        EpiArgs e{};
+        e.kind = EPI_STORE_F32; e.y = logits; e.ldy = V;
+        HIPOK(launch_gemm(dt, xrows, rows, D, D, head_w, V, e, DARD_K_GEMM_HEAD, f.s, frag));
+        c.phase = 0; c.part = cpv;
+        HIPOK(launch_conf_partial(c, stats, f.s));
+        if (int rc = verify()) return rc;
+        c.phase = 1; c.w = wbuf; c.part = cpm;
+        HIPOK(launch_conf_partial(c, stats, f.s));
+        if (int rc = final_phase()) return rc;
+        if (dbg && dbg->logits)
+            HIPOK(hipMemcpyAsync(dbg->logits, logits, (size_t)rows * V * 4, hipMemcpyDeviceToDevice, f.s));
+        return DARD_OK;
     }
-    HIPOK(launch_decide(a, f.s));
-    if (dbg && dbg->logits)
-        HIPOK(hipMemcpyAsync(dbg->logits, logits, (size_t)rows * V * 4, hipMemcpyDeviceToDevice, f.s));
-    if (dbg && dbg->w)
-        HIPOK(hipMemcpyAsync(dbg->w, f.ws + f.W.w, (size_t)b * B * 4, hipMemcpyDeviceToDevice, f.s));
-    return DARD_OK;
+
+    const bool fused = dt == DARD_DTYPE_BF16 && plan[0] == DARD_GEMM_BIG && !stats &&
+                       !(flags & DARD_F_VERIFY_PCUR);
+    int32_t* rm0 = (int32_t*)(f.ws + f.W.rowmap);
+    int32_t* rm1 = rm0 + rows;
+    int32_t* cnt = (int32_t*)(f.ws + f.W.lmcount);
+    void* hx = f.ws + f.W.hx;
+    float* lpart = (float*)(f.ws + f.W.lpart);
+    const int tile_cols = 32 * plan[2];
+    HIPOK(launch_lm_select(state_in, b, B, hidden ? 1 : 0, fused, rm0, rm1, cnt, f.s));
+    auto head = [&](const int32_t* rm, const int32_t* count) -> int {
+        HIPOK(launch_lm_gather(dt, xrows, D, frag, rm, count, max_rows, wbuf, B, hx, f.s));
+        EpiArgs e{};
+        e.kind = EPI_LMHEAD; e.y = logits; e.ldy = V; e.rowmap = rm; e.rows_dev = count;
+        e.y2 = dbg ? dbg->logits : nullptr;
+        if (fused) { e.lpart = lpart; e.ntile = (V + tile_cols - 1) / tile_cols; }
+        HIPOK(launch_gemm(dt, hx, max_rows, D, D, head_w, V, e, DARD_K_GEMM_HEAD, f.s, frag_rows(dt, max_rows)));
+        if (fused) {
+            TraceScope ts(DARD_K_CONFIDENCE, f.s);
+            HIPOK(launch_lm_merge(lpart, e.ntile, tile_cols, rm, count, max_rows, B, V, cpv, cpm, f.s));
+        }
+        return DARD_OK;
+    };
+    // the candidates' shadow rows (and, with logit mixing, every other listed row)
+    if (int rc = head(rm0, cnt)) return rc;
+    if (!fused) {
+        c.phase = 0; c.part = cpv;
+        HIPOK(launch_conf_partial(c, stats, f.s));
+    }
+    if (int rc = verify()) return rc;
+    if (hidden) {
+        // U shadow rows and the mixed rows of the M positions (guidance weights from verify)
+        if (int rc = head(rm1, cnt + 1)) return rc;
+        if (!fused) {
+            c.phase = 1; c.no_mix = 1; c.part = cpm;
+            HIPOK(launch_conf_partial(c, stats, f.s));
+        }
+    } else {
+        // logit mixing of the M positions (Eq. 7); with the fused head the U rows' partials are already there
+        c.phase = 1; c.w = wbuf; c.part = cpm; c.m_only = fused;
+        HIPOK(launch_conf_partial(c, stats, f.s));
+    }
+    return final_phase();
 }
 
 int check_step_args(const dard_dims* d, const dard_params* params, const void* tok, const uint8_t* state_in,

@@ -95,6 +95,30 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// ---------------------------------------------------------------- softmax partials
+// (max, first argmax, sum of exp(l - max)) of a run of logits (Eq. 1 needs the
+// first two and the sum), and the merge of two runs: the larger maximum wins,
+// ties go to the lower index, the sums are rescaled to the common maximum.
+// Evaluated without contraction, so merge(x, y) == merge(y, x) bit for bit.
+struct SmPart {
+    float m;
+    int a;
+    float s;
+};
+
+__device__ __forceinline__ SmPart smpart_merge(SmPart x, SmPart y) {
+#pragma clang fp contract(off)
+    constexpr float kL2e = 1.4426950408889634f;
+    SmPart r;
+    const bool take_y = (y.m > x.m) || (y.m == x.m && y.a < x.a);
+    r.a = take_y ? y.a : x.a;
+    r.m = fmaxf(x.m, y.m);
+    const float ex = x.m == -INFINITY ? 0.f : exp2f((x.m - r.m) * kL2e);
+    const float ey = y.m == -INFINITY ? 0.f : exp2f((y.m - r.m) * kL2e);
+    r.s = x.s * ex + y.s * ey;
+    return r;
+}
+
 // ---------------------------------------------------------------- DARD mask
 // Does query row (stream, position i) read the ORIGINAL key x^j (true) or the
 // shadow key s^j (false)?  Sec. 3.2: U queries read U tokens from x and the

@@ -21,7 +21,7 @@ namespace dard {
 
 namespace {
 
-constexpr int kChunk = 8192;
+constexpr int kChunk = kConfChunk;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct Acc {
@@ -72,9 +72,10 @@ __global__ __launch_bounds__(256) void conf_partial_kernel(ConfArgs a, int step_
         // rows are block positions; logits hold [b][2B][V] (x rows then s rows)
         const int st = a.state[row];
         if (a.phase == 0 ? st != DARD_STATE_C : st == DARD_STATE_C) return;
+        if (a.phase == 1 && a.m_only && st != DARD_STATE_M) return;
         const int s = row / step_B, i = row % step_B;
         ls = a.ls + ((size_t)s * 2 * step_B + step_B + i) * a.ld_s;
-        if (a.phase == 1 && st == DARD_STATE_M) {
+        if (a.phase == 1 && st == DARD_STATE_M && !a.no_mix) {
             lx = a.ls + ((size_t)s * 2 * step_B + i) * a.ld_s;
             w = a.w[row];
         }

@@ -81,6 +81,7 @@ __device__ __forceinline__ void with_kind(int kind, F&& f) {
     case EPI_RESID: f(Kind<EPI_RESID>{}); break;
     case EPI_SWIGLU: f(Kind<EPI_SWIGLU>{}); break;
     case EPI_QKV: f(Kind<EPI_QKV>{}); break;
+    case EPI_LMHEAD: f(Kind<EPI_LMHEAD>{}); break;
     default: break;
     }
 }
@@ -131,6 +132,13 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx
         // interleaved rows: (gate, up) pairs at (n, n+1) and (n+2, n+3)
         T* a = reinterpret_cast<T*>(e.act) + (e.act_frag ? frag_off(m, n / 2, e.ld_act) : (size_t)m * e.ld_act + n / 2);
         store2<T>(a, silu(v[0]) * v[1], silu(v[2]) * v[3]);
+    } else if constexpr (EK == EPI_LMHEAD) {
+        // a listed row of the LM head: stored at its logit row when its code says so
+        const int code = e.rowmap[m];
+        const size_t o = (size_t)(code & kLmRowMask) * e.ldy + n;
+        const float4 val = make_float4(v[0], v[1], v[2], v[3]);
+        if (code & kLmStore) *reinterpret_cast<float4*>(e.y + o) = val;
+        if (e.y2) *reinterpret_cast<float4*>(e.y2 + o) = val;
     } else if constexpr (EK == EPI_QKV) {
         const QkvRow row = qkv_row(e, m);
         const int qd = e.Hq * e.dh, kd = e.Hkv * e.dh;
@@ -154,6 +162,12 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx
             for (int i = 0; i < 4; ++i) St<T>::st(vc + (size_t)i * e.cap, v[i]);
         }
     }
+}
+
+// Rows of the launch whose results are kept: all M, or the device count of
+// an LM-head launch over listed rows.
+__device__ __forceinline__ int valid_rows(const EpiArgs& e, int M) {
+    return e.rows_dev ? min(M, __builtin_amdgcn_readfirstlane(*e.rows_dev)) : M;
 }
 
 __device__ __forceinline__ bf16x8 ld_nt(const bf16_t* p) {
@@ -256,6 +270,7 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
     }
     EpiArgs ee = e;
     if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
+    const int Mv = valid_rows(e, M);
     with_kind(e.kind, [&](auto kind) {
         constexpr int EK = decltype(kind)::value;
         float4 pre[NW][NQ];
@@ -264,14 +279,14 @@ __global__ __launch_bounds__(64 * KSPLIT) void gemm_stream_bf16(const bf16_t* __
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
-                pre[j][q] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                pre[j][q] = (m < Mv && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
             }
 #pragma unroll
         for (int j = 0; j < NW; ++j)
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int n = 16 * (nb0 + j) + 4 * g, m = 16 * (mb0 + q) + lr;
-                if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, res[j][q], pre[j][q]);
+                if (m < Mv && n < N) epi_store<bf16_t, EK>(ee, m, n, res[j][q], pre[j][q]);
             }
     });
 }
@@ -314,6 +329,8 @@ __global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf1
     int bid = blockIdx.x;
     if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
     const int tm = bid % tiles_m, tn = bid / tiles_m;
+    const int Mv = valid_rows(e, M);
+    if (tm * PBM >= Mv) return;   // the whole row tile is past the kept rows
     const int KU = K / 64, NB = N / 16, MB = (M + 15) / 16;
     const int split = blockIdx.y, nsplit = gridDim.y;
     const int u_begin = (int)((long)KU * split / nsplit), u_end = (int)((long)KU * (split + 1) / nsplit);
@@ -412,14 +429,14 @@ __global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf1
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
-                    pre[j][i] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                    pre[j][i] = (m < Mv && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
                 }
 #pragma unroll
             for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int n = 16 * (nb0 + 2 * jh + j) + 4 * g, m = m0 + 16 * i + lr;
-                    if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, acc[2 * jh + j][i], pre[j][i]);
+                    if (m < Mv && n < N) epi_store<bf16_t, EK>(ee, m, n, acc[2 * jh + j][i], pre[j][i]);
                 }
         }
     });
@@ -474,6 +491,8 @@ void gemm_big_bf16(const bf16_t* __restrict__ X, int M, int K, const bf16_t* __r
     int bid = blockIdx.x;
     if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
     const int tm = bid % tiles_m, tn = bid / tiles_m;
+    const int Mv = valid_rows(e, M);
+    if (tm * 32 * TI >= Mv) return;   // the whole row tile is past the kept rows
     const int KU = K / 64, NB = N / 16, MB = (M + 15) / 16;
     const int split = blockIdx.y, nsplit = gridDim.y;
     const int u_begin = (int)((long)KU * split / nsplit), u_end = (int)((long)KU * (split + 1) / nsplit);
@@ -550,9 +569,16 @@ void gemm_big_bf16(const bf16_t* __restrict__ X, int M, int K, const bf16_t* __r
     EpiArgs ee = e;
     if (e.kind == EPI_PARTIAL) ee.y = e.y + (size_t)split * M * e.ldy;
     const int nb0 = tn * WB + wn * TJ, m0 = tm * 32 * TI + wm * 16 * TI;
-    floatx4* park = reinterpret_cast<floatx4*>(smem) + wave * (TJ / 2) * TI * 64 + lane;
+    constexpr int kPark = (TJ / 2) * TI * 64;       // floatx4 slots of one wave's parking region
+    floatx4* park = reinterpret_cast<floatx4*>(smem) + wave * kPark + lane;
     with_kind(e.kind, [&](auto kind) {
         constexpr int EK = decltype(kind)::value;
+        // LM head with fused confidence partials: per row, (max, first argmax,
+        // sum of exp(l - max)) over the tile's columns (Eq. 1)
+        const bool parts = EK == EPI_LMHEAD && e.lpart != nullptr;
+        SmPart pt[TI];
+#pragma unroll
+        for (int i = 0; i < TI; ++i) pt[i] = SmPart{-INFINITY, 0x7fffffff, 0.f};
         // the halves are separate instances (compile-time indices into acc,
         // which must stay in registers)
         auto half = [&](auto hjc) __attribute__((always_inline)) {
@@ -569,17 +595,93 @@ void gemm_big_bf16(const bf16_t* __restrict__ X, int M, int K, const bf16_t* __r
 #pragma unroll
                 for (int i = 0; i < TI; ++i) {
                     const int m = m0 + 16 * i + lr;
-                    pre[i] = (m < M && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                    pre[i] = (m < Mv && n < N) ? epi_fetch<EK>(ee, m, n) : make_float4(0.f, 0.f, 0.f, 0.f);
                 }
 #pragma unroll
                 for (int i = 0; i < TI; ++i) {
                     const int m = m0 + 16 * i + lr;
-                    if (m < M && n < N) epi_store<bf16_t, EK>(ee, m, n, park[(j * TI + i) * 64], pre[i]);
+                    if (m < Mv && n < N) epi_store<bf16_t, EK>(ee, m, n, park[(j * TI + i) * 64], pre[i]);
+                }
+            }
+            if constexpr (EK == EPI_LMHEAD) {
+                if (parts) {
+                    // this half's columns: the maximum and its first column, then
+                    // the sum of exp2(l log2e - mb) (mb = max log2e rounded once;
+                    // its rounding error, common to every term, is corrected at the end)
+                    constexpr float kL2e = 1.4426950408889634f;
+#pragma unroll
+                    for (int i = 0; i < TI; ++i) {
+                        SmPart h{-INFINITY, 0x7fffffff, 0.f};
+#pragma unroll
+                        for (int j = 0; j < TJ / 2; ++j) {
+                            const int n = 16 * (nb0 + hj * (TJ / 2) + j) + 4 * g;
+                            if (n < N) {
+                                const floatx4 v = park[(j * TI + i) * 64];
+#pragma unroll
+                                for (int q = 0; q < 4; ++q)
+                                    if (v[q] > h.m) { h.m = v[q]; h.a = n + q; }
+                            }
+                        }
+                        const float mb = h.m * kL2e;
+#pragma unroll
+                        for (int j = 0; j < TJ / 2; ++j) {
+                            const int n = 16 * (nb0 + hj * (TJ / 2) + j) + 4 * g;
+                            if (n < N) {
+                                const floatx4 v = park[(j * TI + i) * 64];
+#pragma unroll
+                                for (int q = 0; q < 4; ++q) h.s += __builtin_amdgcn_exp2f(fmaf(v[q], kL2e, -mb));
+                            }
+                        }
+                        if (h.m != -INFINITY) h.s *= exp2f(-fmaf(h.m, kL2e, -mb));
+                        pt[i] = smpart_merge(pt[i], h);
+                    }
                 }
             }
         };
         half(Kind<0>{});
         half(Kind<1>{});
+        if constexpr (EK == EPI_LMHEAD) {
+            if (parts) {
+                // merge the four column groups of a row (lanes lr + 16 g), then the
+                // two waves that share the rows (wn = 0 holds the lower columns)
+#pragma unroll
+                for (int i = 0; i < TI; ++i)
+#pragma unroll
+                    for (int o = 16; o < 64; o <<= 1) {
+                        const SmPart y{__shfl_xor(pt[i].m, o, 64), __shfl_xor(pt[i].a, o, 64),
+                                       __shfl_xor(pt[i].s, o, 64)};
+                        pt[i] = smpart_merge(pt[i], y);
+                    }
+                // wave wn = 1 leaves its partials in its own (finished) parking region
+                float* mine = reinterpret_cast<float*>(reinterpret_cast<floatx4*>(smem) + wave * kPark);
+                if (wn == 1 && g == 0) {
+#pragma unroll
+                    for (int i = 0; i < TI; ++i) {
+                        mine[(i * 16 + lr) * 3 + 0] = pt[i].m;
+                        mine[(i * 16 + lr) * 3 + 1] = __int_as_float(pt[i].a);
+                        mine[(i * 16 + lr) * 3 + 2] = pt[i].s;
+                    }
+                }
+                __syncthreads();
+                if (wn == 0 && g == 0) {
+                    const float* other = reinterpret_cast<const float*>(reinterpret_cast<floatx4*>(smem) +
+                                                                        (wave + 1) * kPark);
+#pragma unroll
+                    for (int i = 0; i < TI; ++i) {
+                        const int m = m0 + 16 * i + lr;
+                        const SmPart y{other[(i * 16 + lr) * 3 + 0], __float_as_int(other[(i * 16 + lr) * 3 + 1]),
+                                       other[(i * 16 + lr) * 3 + 2]};
+                        const SmPart r = smpart_merge(pt[i], y);
+                        if (m < Mv) {
+                            float* o = e.lpart + ((size_t)m * e.ntile + tn) * 3;
+                            o[0] = r.m;
+                            o[1] = __int_as_float(r.a);
+                            o[2] = r.s;
+                        }
+                    }
+                }
+            }
+        }
     });
 }
 
@@ -681,6 +783,8 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
     const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
     const int m = blockIdx.y * 16 + ty;
     const int n = blockIdx.x * 64 + tx * 4;
+    const int Mv = valid_rows(e, M);
+    if (blockIdx.y * 16 >= Mv) return;   // the whole row block is past the kept rows
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < K; k0 += 32) {
         for (int t = threadIdx.x; t < 16 * 32; t += 256) {
@@ -701,7 +805,7 @@ __global__ __launch_bounds__(256) void gemm_f32(const float* __restrict__ X, int
         }
         __syncthreads();
     }
-    if (m < M && n < N)
+    if (m < Mv && n < N)
         with_kind(e.kind, [&](auto kind) {
             constexpr int EK = decltype(kind)::value;
             epi_store<float, EK>(e, m, n, floatx4{acc[0], acc[1], acc[2], acc[3]}, epi_fetch<EK>(e, m, n));
@@ -814,14 +918,14 @@ int pipe_split(int M, int N, int K) {
 struct BigCfg {
     int ti, tj, split;   // ti == 0: use the pipelined kernel
 };
-BigCfg big_cfg(int M, int N, int K, bool partial) {
+BigCfg big_cfg(int M, int N, int K, bool partial, bool no192 = false) {
     if (M < 256) return BigCfg{0, 0, 1};
     const int cand[4][2] = {{8, 4}, {4, 8}, {4, 4}, {4, 6}};
     const double eff[4] = {1.0, M >= 4096 ? 1.2 : 0.97, 0.72, 0.9};
     BigCfg best{0, 0, 1};
     double best_t = 0.0;
     for (int v = 0; v < 4; ++v) {
-        if (v == 3 && partial) continue;
+        if (v == 3 && (partial || no192)) continue;
         const int ti = cand[v][0], tj = cand[v][1];
         const long tiles = (long)((M + 32 * ti - 1) / (32 * ti)) * ((N + 32 * tj - 1) / (32 * tj));
         int S = 1;
@@ -836,7 +940,7 @@ BigCfg big_cfg(int M, int N, int K, bool partial) {
     return best;
 }
 
-void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan) {
+void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan, bool fused_head) {
     plan[1] = plan[2] = 0;
     plan[3] = 1;
     if (dtype == DARD_DTYPE_F32) {
@@ -857,7 +961,7 @@ void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t
         plan[2] = TBN / 32;
         return;
     }
-    const BigCfg c = big_cfg(M, N, K, partial);
+    const BigCfg c = big_cfg(M, N, K, partial, fused_head);
     if (c.ti) {
         plan[0] = DARD_GEMM_BIG;
         plan[1] = c.ti;
@@ -883,6 +987,10 @@ int gemm_split(int dtype, int M, int N, int K) {
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
                        const EpiArgs& e, int kernel_class, hipStream_t s, bool xfrag) {
     TraceScope ts(kernel_class, s);
+    if (e.kind == EPI_LMHEAD && (!e.rowmap || !e.rows_dev || !e.y)) return hipErrorInvalidValue;
+    // fused LM-head partials: only the large-tile kernel forms them
+    if (e.kind == EPI_LMHEAD && e.lpart && (dtype != DARD_DTYPE_BF16 || M <= 64 || !xfrag))
+        return hipErrorInvalidValue;
     if (dtype == DARD_DTYPE_F32) {
         dim3 grid((N + 63) / 64, (M + 15) / 16);
         launch(gemm_f32, grid, dim3(256), 0, s, reinterpret_cast<const float*>(X), M, K, ldx,
@@ -913,7 +1021,10 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
         return hipGetLastError();
     }
     if (xfrag) {
-        const BigCfg c = big_cfg(M, N, K, e.kind == EPI_PARTIAL);
+        // the fused LM-head partials need tile widths that divide the 8192-logit chunks
+        const BigCfg c = big_cfg(M, N, K, e.kind == EPI_PARTIAL, e.kind == EPI_LMHEAD && e.lpart);
+        if (c.ti && e.kind == EPI_LMHEAD && e.lpart && e.ntile != (N + 32 * c.tj - 1) / (32 * c.tj))
+            return hipErrorInvalidValue;
         if (c.ti) {
             const int tiles_m = (M + 32 * c.ti - 1) / (32 * c.ti), tiles_n = (N + 32 * c.tj - 1) / (32 * c.tj);
             const dim3 grid(tiles_m * tiles_n, c.split);
@@ -927,6 +1038,7 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
                 launch(gemm_big_bf16<4, 4, 5, 2>, grid, dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);
             return hipGetLastError();
         }
+        if (e.kind == EPI_LMHEAD && e.lpart) return hipErrorInvalidValue;   // partials need the large tiles
         const int tiles_m = (M + PBM - 1) / PBM, tiles_n = (N + PipeTile<4>::BN - 1) / PipeTile<4>::BN;
         const int S = e.kind == EPI_PARTIAL ? pipe_split(M, N, K) : 1;
         launch(gemm_pipe_bf16<4>, dim3(tiles_m * tiles_n, S), dim3(256), 0, s, x, M, K, w, N, e, tiles_m, tiles_n);

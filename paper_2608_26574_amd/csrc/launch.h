@@ -58,9 +58,29 @@ size_t attention_partial_slots(int dtype, int b, int R, int Hq, int Hkv, int nti
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 
 // ---- gemm.hip
-enum EpiKind { EPI_STORE_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PARTIAL = 4 };
+enum EpiKind { EPI_STORE_F32 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_PARTIAL = 4, EPI_LMHEAD = 5 };
+
+// Code of a listed LM-head row (lmhead.hip): its logit row (sequence * 2B +
+// row) and what becomes of its logits.
+constexpr int kLmRowMask = (1 << 24) - 1;
+constexpr int kLmStore = 1 << 24;   // stored at the logit row
+constexpr int kLmToV = 1 << 25;     // merged partial of a candidate's shadow row (verification)
+constexpr int kLmToM = 1 << 26;     // merged partial of a U shadow row or of a mixed M row
+constexpr int kLmMix = 1 << 27;     // the row is w x + (1 - w) s of an M position (hidden-state mixing)
+
 struct EpiArgs {
     int kind;
+    // LMHEAD: the rows are listed rows (rowmap codes); rows at or past the
+    // device count *rows_dev are skipped (row tiles entirely past it exit
+    // before their K loop).  Stored rows go to y (ldy = V) at their logit
+    // row, every row also to y2 when it is set (debug capture); with lpart
+    // the large-tile kernel writes per-column-tile (max, argmax, sum)
+    // partials [M][ntile][3] of every row instead of needing its logits.
+    const int32_t* rowmap;
+    const int32_t* rows_dev;
+    float* y2;
+    float* lpart;
+    int ntile;
     float* y;  int ldy;             // STORE_F32 / RESID (fp32, RESID adds)
     void* act; int ld_act;          // SWIGLU output (dtype), columns N/2
     int act_frag;                   // 1: act fragment-major with K = ld_act
@@ -83,8 +103,10 @@ struct EpiArgs {
 hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const void* W, int N,
                        const EpiArgs& e, int kernel_class, hipStream_t s, bool xfrag = false);
 int gemm_split(int dtype, int M, int N, int K);
-// The kernel and tiling launch_gemm picks for these sizes (dard_gemm_plan).
-void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan);
+// The kernel and tiling launch_gemm picks for these sizes (dard_gemm_plan);
+// fused_head: the LM-head epilogue with column-tile partials (tile widths
+// that divide kConfChunk only).
+void gemm_plan(int dtype, int M, int N, int K, bool partial, bool xfrag, int32_t* plan, bool fused_head = false);
 // bf16 fragment-major packing (mode 0 plain, 1 rotary-pair rows, 2 gate/up interleave)
 hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N, int K, int mode, int dh,
                             hipStream_t s);
@@ -130,8 +152,11 @@ struct ConfArgs {
     const uint8_t* state;  // [rows] or NULL
     int phase;
     int step_B;            // >0: rows are block positions of [b][2B][V] logits
+    int m_only;            // phase 1: only M rows (the U rows' partials come from elsewhere)
+    int no_mix;            // phase 1: M rows already mixed (hidden-state mixing): plain shadow-slot rows
 };
 constexpr int kConfStride = 3, kConfStatsStride = 5;
+constexpr int kConfChunk = 8192;   // logits per confidence partial
 int conf_chunks(int V);
 // The device-resident partials array of dard_confidence_noalloc on the
 // current device (looked up on first use per device) and its size in floats.
@@ -144,6 +169,19 @@ hipError_t launch_conf_combine(const float* part, int rows, int nchunk, int V, c
                                int64_t ld, const int32_t* cur_tok, int32_t* argmax,
                                float* maxprob, float* pcur, float* entropy, float* margin,
                                hipStream_t s);
+
+// ---- lmhead.hip (the LM head on the rows the decisions read)
+// mode 0: logit mixing (one list); mode 1: hidden-state mixing (two passes).
+hipError_t launch_lm_select(const uint8_t* state, int b, int B, int mode, bool fused, int32_t* rowmap0,
+                            int32_t* rowmap1, int32_t* count, hipStream_t s);
+// Listed rows of xn ([b*2B][d], fragment-major when frag) into out (the same
+// layout, compact); mixed rows take w [b][B].
+hipError_t launch_lm_gather(int dtype, const void* xn, int d, bool frag, const int32_t* rowmap, const int32_t* count,
+                            int max_rows, const float* w, int B, void* out, hipStream_t s);
+// Column-tile partials (tile_cols columns each) into the chunk partials
+// [b*B][conf_chunks(V)][kConfStride] of part_v (candidates) / part_m.
+hipError_t launch_lm_merge(const float* lpart, int ntile, int tile_cols, const int32_t* rowmap, const int32_t* count,
+                           int max_rows, int B, int V, float* part_v, float* part_m, hipStream_t s);
 
 // ---- decide.hip
 struct DecideArgs {

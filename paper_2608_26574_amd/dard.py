@@ -21,6 +21,7 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR, F_PROGRESS = 1, 2, 4, 8
 F_C_BIDIR, F_ORDER_L2R, F_ORDER_ENTROPY, F_ORDER_MARGIN, F_FIXED_W = 16, 32, 64, 128, 256
 F_CHECK_STATES = 512
+F_HIDDEN_MIX = 1024
 BAD_STATE = -1
 GEMM_STREAM, GEMM_PIPE, GEMM_BIG, GEMM_TILED, GEMM_F32 = range(5)
 PHASE_VERIFY, PHASE_FINAL = 0, 1

@@ -63,7 +63,9 @@ def step_buffers(b, B, V):
     z = lambda dt=torch.float32: torch.zeros(b, B, dtype=dt, device="cuda")
     out = dict(tok_out=z(torch.int32), state_out=z(torch.uint8), conf_out=z(),
                block_done=torch.zeros(b, dtype=torch.int32, device="cuda"))
-    dbg = dict(logits=torch.zeros(b, 2 * B, V, device="cuda"), w=z(), maxprob_s=z(), argmax_s=z(torch.int32),
+    # rows the LM head does not run over stay NaN (the head skips the x rows of C and U positions)
+    dbg = dict(logits=torch.full((b, 2 * B, V), float("nan"), device="cuda"), w=z(), maxprob_s=z(),
+               argmax_s=z(torch.int32),
                pcur_s=z(), maxprob_mix=z(), argmax_mix=z(torch.int32), entropy=z(), margin=z())
     return out, dbg
 
@@ -131,6 +133,53 @@ class Floor:
         return worst, worst_rms
 
 
+def hidden_mix(params):
+    return bool(params.get("flags", 0) & O.F_HIDDEN_MIX)
+
+
+def reference_logits(got, ref, state, params):
+    """The oracle's values for the logit rows the GPU step computed: every
+    row as the oracle has it, except that with hidden-state mixing the shadow
+    slot of an M position holds the mixed row, compared with the oracle's
+    logit mixing (Eq. 7) under the GPU's guidance weight, and the x rows are
+    not computed."""
+    R = np.array(ref["logits"], dtype=np.float64)
+    if hidden_mix(params):
+        b, B = state.shape
+        for s_ in range(b):
+            for i in range(B):
+                if state[s_, i] == O.STATE_M:
+                    R[s_, B + i] = O.mix_logits(ref["logits"][s_, i], ref["logits"][s_, B + i], got["w"][s_, i])
+        R[:, :B] = np.nan
+    return R
+
+
+def needed_rows(state, params):
+    """[b][2B] bool: the logit rows the decisions read."""
+    b, B = state.shape
+    need = np.zeros((b, 2 * B), dtype=bool)
+    need[:, B:] = True
+    if not hidden_mix(params):
+        need[:, :B] = state == O.STATE_M
+    return need
+
+
+def logit_diff(got, ref, state, params):
+    """GPU minus oracle over the rows the GPU computed (flattened); every row
+    the decisions read must be among them."""
+    G = np.asarray(got["logits"], dtype=np.float64)
+    R = reference_logits(got, ref, state, params)
+    computed = np.all(np.isfinite(G), axis=-1)
+    need = needed_rows(state, params)
+    assert np.all(computed[need]), "a logit row the decisions read was not computed"
+    rows = computed & np.all(np.isfinite(R), axis=-1)
+    return (G - R)[rows]
+
+
+def logit_err(got, ref, state, params):
+    return float(np.max(np.abs(logit_diff(got, ref, state, params))))
+
+
 def check_bf16_logits(got, ref, label, scale=1.0):
     """bf16 multi-layer logits: the maximum error within 2e-2 or twice the
     oracle's own noise floor, and the root-mean-square error within 2e-2 or
@@ -139,7 +188,7 @@ def check_bf16_logits(got, ref, label, scale=1.0):
     bound is stated for the random-init model; an LM head sharpened by
     `scale` multiplies every logit, and the effect of every upstream rounding
     difference, by that factor."""
-    d = got["logits"] - ref["logits"]
+    d = logit_diff(got, ref, ref["state"], ref["params"])
     err, rms = float(np.max(np.abs(d))), float(np.sqrt(np.mean(d * d)))
     tol = 2e-2 * scale
     floor, floor_rms = ref["floor"]() if (err >= tol or rms >= tol) else (0.0, 0.0)
@@ -180,11 +229,15 @@ def check_op_level(tok, state, got, params):
         # Eq. 5-6 on the GPU's candidate confidences: w bit-exact
         _, _, _, w = O.verify_candidates(state[s], c_s, params)
         assert np.array_equal(w.astype(f32), got["w"][s]), ("w", s, w, got["w"][s])
-        # Eq. 7 with the GPU's w, on the GPU's rows: argmax exact
+        # Eq. 7 with the GPU's w, on the GPU's rows: argmax exact (with hidden-state
+        # mixing the GPU's mixed row sits in the shadow slot)
         for i in range(B):
             if state[s, i] != O.STATE_M:
                 continue
-            mixed = O.mix_logits(L[s, i], L[s, B + i], got["w"][s, i])
+            if hidden_mix(params):
+                mixed = L[s, B + i]
+            else:
+                mixed = O.mix_logits(L[s, i], L[s, B + i], got["w"][s, i])
             a, mp, _ = O.confidence(mixed)
             assert got["argmax_mix"][s, i] == a, ("argmax_mix", s, i)
             assert abs(got["maxprob_mix"][s, i] - mp) <= 1e-5 * mp, ("maxprob_mix", s, i)
@@ -241,12 +294,12 @@ def check_step_level(tok, state, got, ref, params, label=""):
         for i in range(B):
             if state[s, i] == O.STATE_M:
                 wg = got["w"][s, i]
-                rows_g[s, i] = O.mix_logits(Lg[s, i], Lg[s, B + i], wg)
+                rows_g[s, i] = Lg[s, B + i] if hidden_mix(params) else O.mix_logits(Lg[s, i], Lg[s, B + i], wg)
                 rows_r[s, i] = O.mix_logits(Lr[s, i], Lr[s, B + i], wg)
             else:
                 rows_g[s, i], rows_r[s, i] = Lg[s, B + i], Lr[s, B + i]
     diff = np.abs(rows_g - rows_r)
-    eps = float(np.max(np.abs(Lg.astype(np.float64) - Lr)))
+    eps = float(np.max(np.abs(logit_diff(got, ref, state, params))))
     eps_rows = float(np.max(diff))
     c_gpu = np.where(state == O.STATE_M, got["maxprob_mix"], got["pcur_s"] if pcur_mode else got["maxprob_s"])
     excluded = 0
@@ -294,13 +347,14 @@ def decision_floor(tok, state, ref, params):
     compared with its own perturbed runs (the largest count over the seeds):
     the part of the bf16 exclusions that the rounding noise alone causes."""
     worst = 0
+    prm = dict(params, flags=params.get("flags", 0) & ~O.F_HIDDEN_MIX)
     for l2 in ref["floor"].logits():
-        pseudo = O.decide(l2, tok, state, params)
+        pseudo = O.decide(l2, tok, state, prm)
         pseudo["logits"] = l2
         pseudo["w"] = pseudo["w"].astype(np.float32)
         for k in ("maxprob_s", "pcur_s", "maxprob_mix"):
             pseudo[k] = pseudo[k].astype(np.float32)
-        _, excl, _ = check_step_level(tok, state, pseudo, ref, params, "oracle vs its perturbed run")
+        _, excl, _ = check_step_level(tok, state, pseudo, ref, prm, "oracle vs its perturbed run")
         worst = max(worst, excl)
     return worst
 

@@ -80,6 +80,7 @@ def test_oracle_and_p2_32_layers(llada8b):
     announce("32-layer oracle prefill and step")
     cache = O.prefill(ow, dd, ids)
     ref = O.dard_step(ow, dd, cache, tok, state, conf, prm)
+    ref["state"], ref["params"] = state, prm
 
     def perturbed():
         announce("32-layer oracle, perturbed")

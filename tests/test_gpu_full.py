@@ -10,7 +10,7 @@ from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
 from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, Floor, sharpen, step_buffers)
+                    dev, Floor, logit_err, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -39,6 +39,7 @@ def full_case(dims, b, prompt, gen, B, blk_index, params, seed=1, lm_scale=None,
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     ref = O.dard_step_full(ow, dd, seq, blk, B, state, conf, params)
+    ref["state"], ref["params"] = state, params
     ref["floor"] = Floor(
         lambda: O.full_step_logits(ow, dd, seq, blk, B, state, conf, params["mask_id"], params.get("flags", 0)),
         ref["logits"])
@@ -54,7 +55,7 @@ def test_tiny_full_step_fp32(blk_index, flags):
     announce("tiny fp32 full step", blk_index, flags)
     prm = P(dims.mask_id, flags, w_fixed=0.5)
     tok, state, conf, got, ref = full_case(dims, 1, 40, 96, 32, blk_index, prm, seed=3, lm_scale=20.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 1e-4 * 20, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"tiny full step {blk_index} {flags}")
     assert excl <= 1
@@ -70,7 +71,7 @@ def test_small_full_step_bf16(case):
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = full_case(dims, case["b"], case["prompt"], case["gen"], case["B"], case["k"], prm,
                                            seed=4, lm_scale=8.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 2e-2 * 8, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step")
     assert excl <= state.size // 4
@@ -84,7 +85,7 @@ def test_block128_full_step_fp32():
     announce("block-128 fp32 full step")
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = full_case(dims, 1, 64, 256, 128, 0, prm, seed=4, lm_scale=8.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 1e-4 * 8, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step")
     assert excl <= state.size // 4
@@ -97,7 +98,7 @@ def test_block256_full_step_fp32():
     announce("block-256 fp32 full step")
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = full_case(dims, 1, 64, 256, 256, 0, prm, seed=6, lm_scale=8.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 1e-4 * 8, err
 
 

@@ -10,7 +10,7 @@ from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
 from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, Floor, sharpen, step_buffers)
+                    dev, Floor, logit_err, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -47,6 +47,7 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
     suffix = O.prefill_suffix(ow, dd, shared, committed)
     cache = O.join_shared(shared, suffix)
     ref = O.dard_step(ow, dd, cache, tok, state, conf, params)
+    ref["state"], ref["params"] = state, params
 
     def perturbed():
         shp = O.prefill(ow, dd, prompt, None if embeds is None else embeds.double().numpy())
@@ -74,7 +75,7 @@ def test_tiny_shared_step_fp32(b, Ps, Pc, flags):
     announce("tiny fp32 shared step", b, Ps, Pc, flags)
     prm = P(dims.mask_id, flags)
     tok, state, conf, got, ref = shared_case(dims, b, Ps, Pc, 32, prm, seed=3, lm_scale=20.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 1e-4 * 20, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, "tiny shared step")
     assert excl <= 1
@@ -85,7 +86,7 @@ def test_small_shared_step_bf16_gqa():
     announce("small bf16 shared step")
     prm = P(dims.mask_id)
     tok, state, conf, got, ref = shared_case(dims, 4, 128, 64, 32, prm, seed=5, lm_scale=8.0)
-    err = np.max(np.abs(got["logits"] - ref["logits"]))
+    err = logit_err(got, ref, state, prm)
     assert err < 2e-2 * 8, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small shared step")
     assert excl <= state.size // 4
