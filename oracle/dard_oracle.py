@@ -15,7 +15,9 @@ precision, so values are accumulated in float64 and rounded to the storage type
 (bfloat16, round-to-nearest-even, or float32 in the fp32 configuration) exactly
 where a real implementation stores them: the embedding output, every RMSNorm
 output, Q/K/V after RoPE (the KV cache), the attention output and the SwiGLU
-output.  The residual stream and the logits are float32.  Decisions that turn
+output.  The FP8 KV-cache variant (the prefix-cache discussion of App. C.5
+names the KV cache's size as the shadow block's memory cost) rounds K and V
+to OCP FP8 E4M3 instead (``dims['kv_dtype'] = 'fp8'``); Q stays bf16.  The residual stream and the logits are float32.  Decisions that turn
 floats into integers (argmax, threshold tests of Eq. 8, logit mixing feeding an
 argmax) are taken on float32 values, the precision of the GPU kernels.
 
@@ -25,7 +27,12 @@ Parity pins (see ``tests/test_oracle_*.py``):
   * masked_attention        -- dense textbook evaluation with -inf and torch's
                                CPU scaled_dot_product_attention.
   * rmsnorm, rope, swiglu   -- closed forms (unit RMS, norm preservation,
-                               relative-position property, silu identities).
+                               relative-position property, silu identities);
+                               the FFN half of a layer against a closed form
+                               with one-hot gate / up / down rows.
+  * to_fp8                  -- the format's defining constants (448, 2^-6,
+                               2^-9, spacing), ties to even, saturation, and
+                               its relative error bound 2^-4 on normals.
   * confidence              -- closed forms (uniform row, single spike, shift
                                invariance), argmax tie rule.
   * guidance_weights        -- closed forms of Eq. 5-6 (lambda^8 = 1/2, a
@@ -104,12 +111,39 @@ def to_bf16(x):
     return u.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
+# The finite non-negative values of the OCP 8-bit floating-point format E4M3
+# (4 exponent bits, bias 7, 3 mantissa bits; no infinities, the all-ones
+# pattern is NaN): code c = 8 e + m is m/8 * 2^-6 for e = 0 (subnormal) and
+# (1 + m/8) * 2^(e-7) otherwise, for c = 0 .. 126.  The largest is 448.
+E4M3_VALUES = np.array([(m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+                        for e in range(16) for m in range(8)][:127])
+
+
+def to_fp8(x):
+    """Round to OCP FP8 E4M3 (round to nearest, ties to the even code, i.e. the
+    one whose last mantissa bit is 0; magnitudes beyond 448 saturate to 448),
+    after rounding to binary32 as a kernel holding a float32 value does.
+    Returns float64 values of the format."""
+    a = np.abs(np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64))
+    sign = np.sign(np.asarray(x, dtype=np.float64))
+    hi = np.clip(np.searchsorted(E4M3_VALUES, a), 1, 126)     # E4M3_VALUES[hi - 1] <= a <= E4M3_VALUES[hi]
+    lo = hi - 1
+    below, above = E4M3_VALUES[lo], E4M3_VALUES[hi]
+    take_hi = (a - below > above - a) | ((a - below == above - a) & (hi % 2 == 0))
+    code = np.where(take_hi, hi, lo)
+    code = np.where(a >= E4M3_VALUES[126], 126, code)           # saturation at 448
+    return sign * E4M3_VALUES[code]
+
+
 def storage(x, dtype):
-    """Round to the activation storage type: 'bf16' or 'f32'."""
+    """Round to a storage type: 'bf16', 'f32', or 'fp8' (OCP E4M3, the KV cache
+    format of the fp8 variant)."""
     if dtype == "bf16":
         return to_bf16(x)
     if dtype == "f32":
         return to_f32(x)
+    if dtype == "fp8":
+        return to_fp8(x)
     raise ValueError(dtype)
 
 
@@ -260,6 +294,7 @@ def _layer(w, dims, h, pos, kv_prefix, visible_fn, scale):
     Returns the new residual and this layer's (K, V) of the rows.
     """
     dt = dims["dtype"]
+    kvdt = dims.get("kv_dtype") or dt      # the KV cache's storage type (the fp8 variant: 'fp8')
     Hq, Hkv, dh = dims["n_heads"], dims["n_kv_heads"], dims["head_dim"]
     b, R, d = h.shape
     xn = storage(rmsnorm(h, w["attn_norm"], dims["norm_eps"]), dt)
@@ -267,8 +302,8 @@ def _layer(w, dims, h, pos, kv_prefix, visible_fn, scale):
     k = (xn @ w["wk"].T).reshape(b, R, Hkv, dh)
     v = (xn @ w["wv"].T).reshape(b, R, Hkv, dh)
     q = storage(rope(q, pos, dims["rope_theta"]), dt)
-    k = storage(rope(k, pos, dims["rope_theta"]), dt)
-    v = storage(v, dt)
+    k = storage(rope(k, pos, dims["rope_theta"]), kvdt)
+    v = storage(v, kvdt)
     att = np.zeros((b, R, Hq, dh))
     for bi in range(b):
         if kv_prefix is not None:

@@ -39,6 +39,7 @@ class Dims:
     dtype: str          # 'bf16' or 'f32'
     norm_eps: float = 1e-5
     rope_theta: float = 10000.0
+    kv_dtype: str = ""  # KV-cache storage: "" = dtype, "fp8" = OCP FP8 E4M3 (bf16 models)
 
     def as_dict(self):
         return asdict(self)
@@ -57,6 +58,12 @@ DREAM7B = Dims(28, 3584, 28, 4, 128, 18944, 152064, 4096, "bf16")
 def truncated(dims: Dims, n_layers: int) -> Dims:
     d = dims.as_dict()
     d["n_layers"] = n_layers
+    return Dims(**d)
+
+
+def with_fp8_kv(dims: Dims) -> Dims:
+    d = dims.as_dict()
+    d["kv_dtype"] = "fp8"
     return Dims(**d)
 
 

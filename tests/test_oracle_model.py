@@ -355,3 +355,67 @@ def test_ffn_closed_form_catches_a_missing_rounding():
     assert len(calls) == 9
     ref, _ = O.step_logits(w, dims, cache, tok, state, conf, V - 1)
     assert not np.allclose(logits, ref, rtol=0, atol=1e-6)
+
+
+def test_fp8_e4m3_constants():
+    """OCP FP8 E4M3: largest finite value 448 = 1.75 * 2^8, smallest normal
+    2^-6, smallest subnormal 2^-9; three mantissa bits, so the values in
+    [1, 2) are spaced by 1/8 and those in [2^-6, 2^-5) by 2^-9."""
+    V = O.E4M3_VALUES
+    assert len(V) == 127 and V[0] == 0.0
+    assert V[-1] == 448.0 and V[1] == 2.0 ** -9 and V[8] == 2.0 ** -6
+    assert np.all(np.diff(V) > 0)
+    ones = V[(V >= 1) & (V < 2)]
+    assert np.array_equal(ones, 1 + np.arange(8) / 8)
+    small = V[(V >= 2.0 ** -6) & (V < 2.0 ** -5)]
+    assert np.allclose(np.diff(small), 2.0 ** -9, rtol=0, atol=0)
+    # exactly representable values round to themselves, with either sign
+    assert np.array_equal(O.to_fp8(V), V) and np.array_equal(O.to_fp8(-V), -V)
+
+
+def test_fp8_rounding_ties_and_saturation():
+    # halfway between 1 and 1.125 (codes 56 and 57): the even code, 1.0
+    assert O.to_fp8(1.0625) == 1.0
+    # halfway between 1.125 and 1.25 (codes 57 and 58): 1.25
+    assert O.to_fp8(1.1875) == 1.25
+    # off-centre values go to the nearer one
+    assert O.to_fp8(1.07) == 1.125 and O.to_fp8(-1.05) == -1.0
+    # halfway between 0 and the smallest subnormal: 0 (even); just above: 2^-9
+    assert O.to_fp8(2.0 ** -10) == 0.0 and O.to_fp8(2.0 ** -10 * 1.01) == 2.0 ** -9
+    # beyond the largest finite value: saturation at +-448
+    assert O.to_fp8(1e6) == 448.0 and O.to_fp8(-470.0) == -448.0 and O.to_fp8(449.0) == 448.0
+
+
+def test_fp8_relative_error_bound():
+    """Round to nearest with 3 mantissa bits: relative error at most 2^-4 for
+    normal magnitudes (half the spacing 2^-3 of [1, 2)), absolute error at most
+    2^-10 (half the subnormal spacing) below 2^-6."""
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal(200000) * np.exp(rng.uniform(-6, 6, 200000))
+    x = x[np.abs(x) <= 448]
+    r = O.to_fp8(x)
+    normal = np.abs(x) >= 2.0 ** -6
+    assert np.all(np.abs(r - x)[normal] <= 2.0 ** -4 * np.abs(x[normal]) * (1 + 1e-9))
+    assert np.all(np.abs(r - x)[~normal] <= 2.0 ** -10 + 1e-15)
+    # and the nearest value: no representable value lies strictly closer
+    V = np.concatenate([-O.E4M3_VALUES[::-1], O.E4M3_VALUES])
+    near = V[np.argmin(np.abs(V[None, :] - x[:2000, None]), axis=1)]
+    assert np.all(np.abs(r[:2000] - x[:2000]) <= np.abs(near - x[:2000]))
+
+
+def test_fp8_kv_cache_storage_point():
+    """With kv_dtype = 'fp8' the prefix cache holds K and V rounded to E4M3
+    (every cached value is a member of the format) and the step's logits move
+    by a small amount relative to the bf16 cache."""
+    dims, w = _tiny(n_layers=2, dtype="bf16")
+    dims8 = dict(dims, kv_dtype="fp8")
+    ids = synth.prompt_ids(1, 12, dims["vocab"], seed=3)
+    cache8 = O.prefill(w, dims8, ids)
+    vals = np.unique(np.abs(np.concatenate([np.ravel(k) for kv in cache8 for k in kv])))
+    assert np.all(np.isin(vals, O.E4M3_VALUES))
+    cache = O.prefill(w, dims, ids)
+    tok, state, conf = _block(6, dims["vocab"], [2, 1, 0, 1, 2, 0])
+    l8, _ = O.step_logits(w, dims8, cache8, tok, state, conf, dims["vocab"] - 1)
+    l16, _ = O.step_logits(w, dims, cache, tok, state, conf, dims["vocab"] - 1)
+    assert not np.array_equal(l8, l16)
+    assert np.max(np.abs(l8 - l16)) < 0.25 * np.max(np.abs(l16))
