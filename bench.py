@@ -178,7 +178,7 @@ def main():
     variants = {}
     for vname, vflags in (("entropy_order", dard.F_ORDER_ENTROPY), ("margin_order", dard.F_ORDER_MARGIN),
                           ("bidirectional", dard.F_C_BIDIR), ("left_to_right", dard.F_ORDER_L2R),
-                          ("fixed_w_0.5", dard.F_FIXED_W)):
+                          ("fixed_w_0.5", dard.F_FIXED_W), ("hidden_mix", dard.F_HIDDEN_MIX)):
         vp = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, vflags, 0.5)
 
         def vstep(t):
@@ -359,8 +359,30 @@ def full_step_configs(eng8b, steps=6):
                 res["gemm_mfma_frac"] = round(2 * params_n * rows / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
                 res["attention_tflops"] = round(att_fl / (bd["attention"] * 1e-3) / 1e12, 1)
                 res["attention_mfma_frac"] = round(att_fl / (bd["attention"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
-        # tokens committed / s over one generation (the middle candidate fraction's states)
+        # the same steps with Eq. 7 applied to the hidden state (two LM-head passes, B rows per sequence)
         frac = fracs[len(fracs) // 2]
+        hp = dard.make_params(0.4, 0.9, 0.5 ** 0.125, 0.1, dims.mask_id, dard.F_HIDDEN_MIX)
+        hins = [tuple(torch.from_numpy(a_).cuda() for a_ in synth.workload_block(b, B, frac, V, seed=2000 + t))
+                for t in range(steps + 1)]
+        Ph = [prompt + B * (t % nblocks) for t in range(steps + 1)]
+        eng.dard_step(Ph[steps], hp, *hins[steps], t_out, s_out, c_out, done)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(steps):
+            eng.dard_step(Ph[t], hp, *hins[t], t_out, s_out, c_out, done)
+        e1.record()
+        torch.cuda.synchronize()
+        res["hidden_mix_ms_per_step"] = round(e0.elapsed_time(e1) / steps, 3)
+        dard.dard_trace_reset()
+        dard.dard_trace_enable(1 << dard.K_GEMM_HEAD)
+        for t in range(steps):
+            eng.dard_step(Ph[t], hp, *hins[t], t_out, s_out, c_out, done)
+        torch.cuda.synchronize()
+        dard.dard_trace_enable(0)
+        res["hidden_mix_lm_head_ms_per_step"] = round(dard.dard_trace_read(dard.K_GEMM_HEAD)[1] / steps, 3)
+        dard.dard_trace_reset()
+        # tokens committed / s over one generation (the middle candidate fraction's states)
         ins = [tuple(torch.from_numpy(a_).cuda() for a_ in synth.workload_block(b, B, frac, V, seed=3000 + j))
                for j in range(S_b)]
         torch.cuda.synchronize()

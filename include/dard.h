@@ -56,9 +56,22 @@ typedef int dard_status;
 #define DARD_STATE_U 2
 
 /* Storage types of weights / activations / KV cache.  Logits, confidences
- * and the residual stream are always float32. */
+ * and the residual stream are always float32.  DARD_DTYPE_BF16_KV_FP8 is an
+ * operation type of dard_masked_attention only: bf16 q / out with K and V in
+ * OCP FP8 E4M3. */
 #define DARD_DTYPE_F32  0
 #define DARD_DTYPE_BF16 1
+#define DARD_DTYPE_BF16_KV_FP8 2
+
+/* KV-cache formats (dard_dims.kv_format): the model's storage dtype, or OCP
+ * FP8 E4M3 (4 exponent bits, 3 mantissa bits, largest finite 448; bf16
+ * models only).  FP8 halves the cache and the attention's key/value reads;
+ * K and V are rounded to nearest-even from fp32 once, when written, with
+ * magnitudes beyond 448 saturating, and widened to bf16 (exactly) before the
+ * matrix cores.  Prefix caching of the prompt (App. C.5) makes the cache the
+ * shadow block's memory cost; this is the variant that halves it. */
+#define DARD_KV_DTYPE 0
+#define DARD_KV_FP8   1
 
 /* Flags selecting alternative readings where the paper leaves a choice open
  * (the default, 0, is the reading the library documents as primary):
@@ -147,6 +160,7 @@ typedef struct {
     int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, max_pos;
     int32_t dtype;    /* DARD_DTYPE_F32 or DARD_DTYPE_BF16 */
     float norm_eps, rope_theta;
+    int32_t kv_format; /* DARD_KV_DTYPE or DARD_KV_FP8 */
 } dard_dims;
 
 /* ------------------------------------------------------------ library */
@@ -184,11 +198,12 @@ dard_status dard_build_state_mask(const uint8_t* state, const float* conf, int b
  * over the visible keys of row r: the prefix keys 0..P-1, and for every block
  * position j either x^j (cache index P+j) or s^j (cache index P+B+j) as the
  * mask of dard_build_state_mask says.
- *   q   [b][2B][Hq][dh]     dtype
- *   k   [b][Hkv][cap][dh]   dtype; keys P..P+2B-1 hold the block (x then s)
- *   v   [b][Hkv][dh][cap]   dtype, dims-major (the transpose of k's layout),
+ *   q   [b][2B][Hq][dh]     dtype (bf16 for DARD_DTYPE_BF16_KV_FP8)
+ *   k   [b][Hkv][cap][dh]   dtype (FP8 E4M3 codes for DARD_DTYPE_BF16_KV_FP8);
+ *                           keys P..P+2B-1 hold the block (x then s)
+ *   v   [b][Hkv][dh][cap]   as k, dims-major (the transpose of k's layout),
  *                           so a tile of V^T is contiguous per dim
- *   out [b][2B][Hq][dh]     dtype
+ *   out [b][2B][Hq][dh]     dtype (bf16 for DARD_DTYPE_BF16_KV_FP8)
  * Query head h reads KV head h / (Hq/Hkv).  Any permutation of the head_dim
  * axis applied to both q and k gives the same result.  Needs P >= 0,
  * P + 2B <= cap, dh in {64, 128}.
@@ -291,7 +306,8 @@ dard_status dard_commit_remask(int phase, const dard_params* params, int b, int 
  * which leaves every attention score unchanged.
  *
  * KV cache: per layer a K block [b][Hkv][cap][dh] then a V block
- * [b][Hkv][dh][cap] (dims-major), of the storage dtype, sized by
+ * [b][Hkv][dh][cap] (dims-major), of the storage dtype or, with
+ * kv_format = DARD_KV_FP8, one byte per value (E4M3 codes), sized by
  * dard_kv_bytes().  Keys 0..P-1 hold the prefix (dard_prefill); a step writes
  * its block keys at P..P+2B-1. */
 size_t dard_packed_weight_bytes(const dard_dims* dims);

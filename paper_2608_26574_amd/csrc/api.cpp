@@ -40,6 +40,8 @@ int fail(int code, const char* fmt, ...) {
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t esize(int dtype) { return dtype == DARD_DTYPE_BF16 ? 2 : 4; }
+// bytes per value of the KV cache
+size_t kv_esize(const dard_dims* d) { return d->kv_format == DARD_KV_FP8 ? 1 : esize(d->dtype); }
 
 int check_dims(const dard_dims* d) {
     if (!d) return fail(DARD_ERR_ARG, "dims is NULL");
@@ -57,6 +59,10 @@ int check_dims(const dard_dims* d) {
     if (d->dtype == DARD_DTYPE_F32 && (d->d_model % 4 || d->ffn_dim % 4 || d->vocab % 4))
         return fail(DARD_ERR_SHAPE, "f32 needs d_model, ffn_dim, vocab %% 4 == 0");
     if (!(d->norm_eps >= 0.f) || !(d->rope_theta > 0.f)) return fail(DARD_ERR_ARG, "bad norm_eps / rope_theta");
+    if (d->kv_format != DARD_KV_DTYPE && d->kv_format != DARD_KV_FP8)
+        return fail(DARD_ERR_ARG, "unknown kv_format %d", d->kv_format);
+    if (d->kv_format == DARD_KV_FP8 && d->dtype != DARD_DTYPE_BF16)
+        return fail(DARD_ERR_UNSUPPORTED, "the FP8 KV cache is a bf16-model format");
     return DARD_OK;
 }
 
@@ -261,8 +267,9 @@ AttnWs attn_ws(int dtype, int b, int B, int Hq, int dh, int P) {
 }  // namespace
 
 size_t dard_attention_workspace_bytes(int dtype, int b, int B, int Hq, int dh, int P) {
-    if (b < 1 || B < 1 || B > 256 || Hq < 1 || P < 0 || dtype != DARD_DTYPE_BF16 || (dh != 64 && dh != 128)) return 0;
-    return attn_ws(dtype, b, B, Hq, dh, P).total;
+    if (b < 1 || B < 1 || B > 256 || Hq < 1 || P < 0 || (dh != 64 && dh != 128)) return 0;
+    if (dtype != DARD_DTYPE_BF16 && dtype != DARD_DTYPE_BF16_KV_FP8) return 0;
+    return attn_ws(DARD_DTYPE_BF16, b, B, Hq, dh, P).total;
 }
 
 dard_status dard_masked_attention(int dtype, const void* q, const void* k, const void* v, int P, int cap,
@@ -270,7 +277,10 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
                                   float scale, uint32_t flags, void* out, void* ws, size_t ws_bytes,
                                   void* stream) {
     if (!q || !k || !v || !state || !conf || !out) return fail(DARD_ERR_ARG, "NULL pointer");
-    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16) return fail(DARD_ERR_ARG, "unknown dtype");
+    if (dtype != DARD_DTYPE_F32 && dtype != DARD_DTYPE_BF16 && dtype != DARD_DTYPE_BF16_KV_FP8)
+        return fail(DARD_ERR_ARG, "unknown dtype");
+    const bool kv8 = dtype == DARD_DTYPE_BF16_KV_FP8;
+    if (kv8) dtype = DARD_DTYPE_BF16;
     if (int rc = check_flags(flags)) return rc;
     if (b < 1 || B < 1 || B > 256 || P < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv || P + 2 * B > cap)
         return fail(DARD_ERR_SHAPE, "bad attention shape (b=%d B=%d P=%d cap=%d Hq=%d Hkv=%d)", b, B, P, cap, Hq, Hkv);
@@ -281,6 +291,7 @@ dard_status dard_masked_attention(int dtype, const void* q, const void* k, const
     a.q = q; a.k = k; a.v = v; a.out = out; a.state = state; a.conf = conf;
     a.b = b; a.R = 2 * B; a.Hq = Hq; a.Hkv = Hkv; a.dh = dh; a.cap = cap;
     a.P = P; a.B = B; a.nkeys = P + 2 * B; a.masked = 1; a.scale = scale; a.flags = flags;
+    a.kv_fp8 = kv8;
     hipStream_t s = (hipStream_t)stream;
     TraceScope ts(DARD_K_ATTENTION, s);
     if (dtype == DARD_DTYPE_BF16) {
@@ -401,7 +412,7 @@ size_t dard_packed_weight_bytes(const dard_dims* dims) {
 
 size_t dard_kv_bytes(const dard_dims* d, int b, int cap) {
     if (check_dims(d) || b < 1 || cap < 1) return 0;
-    return (size_t)d->n_layers * 2 * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+    return (size_t)d->n_layers * 2 * b * d->n_kv_heads * cap * d->head_dim * kv_esize(d);
 }
 
 dard_status dard_pack_weights(const dard_dims* d, const void* const* src, int n_src, void* packed,
@@ -489,16 +500,16 @@ struct Fwd {
 
     const void* layer(int l, size_t off) const { return pk + L.layer0 + L.layer_stride * l + off; }
     void* kc(int l) const {
-        return kv + (size_t)(2 * l) * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+        return kv + (size_t)(2 * l) * b * d->n_kv_heads * cap * d->head_dim * kv_esize(d);
     }
     void* vc(int l) const {
-        return kv + (size_t)(2 * l + 1) * b * d->n_kv_heads * cap * d->head_dim * esize(d->dtype);
+        return kv + (size_t)(2 * l + 1) * b * d->n_kv_heads * cap * d->head_dim * kv_esize(d);
     }
     const void* kc_sh(int l) const {
-        return kv_sh + (size_t)(2 * l) * d->n_kv_heads * cap_sh * d->head_dim * esize(d->dtype);
+        return kv_sh + (size_t)(2 * l) * d->n_kv_heads * cap_sh * d->head_dim * kv_esize(d);
     }
     const void* vc_sh(int l) const {
-        return kv_sh + (size_t)(2 * l + 1) * d->n_kv_heads * cap_sh * d->head_dim * esize(d->dtype);
+        return kv_sh + (size_t)(2 * l + 1) * d->n_kv_heads * cap_sh * d->head_dim * kv_esize(d);
     }
 };
 
@@ -529,7 +540,7 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         e.kind = EPI_QKV; e.q = q; e.ldq = qd; e.kc = f.kc(l); e.vc = f.vc(l);
         e.rope = (const float*)(f.pk + f.L.rope);
         e.rows_per_seq = R; e.P = P; e.B = B; e.cap = f.cap; e.Hq = d->n_heads; e.Hkv = d->n_kv_heads; e.dh = dh;
-        e.step = step; e.blk = blk;
+        e.step = step; e.blk = blk; e.kv_fp8 = d->kv_format == DARD_KV_FP8;
         HIPOK(launch_gemm(dt, xn, rows, D, D, f.layer(l, f.L.wqkv), qd + 2 * kd, e, DARD_K_GEMM_QKV, f.s, fr));
 
         AttnArgs a{};
@@ -546,6 +557,7 @@ int run_layers(const Fwd& f, int R, int P, int B, int step, const uint8_t* state
         a.flags = flags; a.part = (float*)(f.ws + f.W.part); a.part_ml = (float*)(f.ws + f.W.part_ml);
         a.part_slots = f.W.part_slots;
         a.out_frag = fr;
+        a.kv_fp8 = d->kv_format == DARD_KV_FP8;
         {
             TraceScope ts(DARD_K_ATTENTION, f.s);
             HIPOK(launch_attention(dt, a, f.s));
@@ -689,9 +701,15 @@ int step_tail(const Fwd& f, const dard_params* params, int b, int B, const void*
     void* hx = f.ws + f.W.hx;
     float* lpart = (float*)(f.ws + f.W.lpart);
     const int tile_cols = 32 * plan[2];
-    HIPOK(launch_lm_select(state_in, b, B, hidden ? 1 : 0, fused, rm0, rm1, cnt, f.s));
+    {
+        TraceScope ts(DARD_K_GEMM_HEAD, f.s);   // the row lists belong to the LM-head stage
+        HIPOK(launch_lm_select(state_in, b, B, hidden ? 1 : 0, fused, rm0, rm1, cnt, f.s));
+    }
     auto head = [&](const int32_t* rm, const int32_t* count) -> int {
-        HIPOK(launch_lm_gather(dt, xrows, D, frag, rm, count, max_rows, wbuf, B, hx, f.s));
+        {
+            TraceScope ts(DARD_K_GEMM_HEAD, f.s);
+            HIPOK(launch_lm_gather(dt, xrows, D, frag, rm, count, max_rows, wbuf, B, hx, f.s));
+        }
         EpiArgs e{};
         e.kind = EPI_LMHEAD; e.y = logits; e.ldy = V; e.rowmap = rm; e.rows_dev = count;
         e.y2 = dbg ? dbg->logits : nullptr;

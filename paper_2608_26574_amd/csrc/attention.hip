@@ -32,6 +32,8 @@
 // (o, m, l), merged in split order by a small combine kernel).
 //
 // fp32 path: one thread per (row, head), plain online softmax.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -110,7 +112,10 @@ __device__ __forceinline__ int tile_count(int t, int npre, int pre_end, int B2) 
 // Grid: x = row tile (row tile fastest, then KV head, then sequence), dealt to
 // the XCDs in contiguous runs so the workgroups reading one KV head share an
 // L2; y = key split.
-template <int DH, int WAVES, int G>
+// KV8: the cache holds OCP FP8 E4M3 codes; tiles go through registers (8
+// bytes per 8-key or 8-dim chunk), are widened to bf16 and written to LDS in
+// the same swizzled image the bf16 copies produce, so the MFMA code is shared.
+template <int DH, int WAVES, int G, bool KV8>
 __global__ __launch_bounds__(64 * WAVES * G) __attribute__((amdgpu_waves_per_eu(G)))
 void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     constexpr int TPG = 64 * WAVES, ROWS = 32 * WAVES;
@@ -145,11 +150,12 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     const int iters = (t_end - t_begin + G - 1) / G;   // tile steps of every group
     const int P = a.P, B2 = 2 * a.B, cap = a.cap;
 
-    const bf16_t* kbase = reinterpret_cast<const bf16_t*>(a.k) + ((size_t)s * a.Hkv + kvh) * cap * DH;
-    const bf16_t* vbase = reinterpret_cast<const bf16_t*>(a.v) + ((size_t)s * a.Hkv + kvh) * DH * cap;
+    using KVT = typename std::conditional<KV8, uint8_t, bf16_t>::type;
+    const KVT* kbase = reinterpret_cast<const KVT*>(a.k) + ((size_t)s * a.Hkv + kvh) * cap * DH;
+    const KVT* vbase = reinterpret_cast<const KVT*>(a.v) + ((size_t)s * a.Hkv + kvh) * DH * cap;
     // keys below P_sh (whole tiles) come from the cache the batch shares
-    const bf16_t* kbase_sh = a.P_sh ? reinterpret_cast<const bf16_t*>(a.k_sh) + (size_t)kvh * a.cap_sh * DH : kbase;
-    const bf16_t* vbase_sh = a.P_sh ? reinterpret_cast<const bf16_t*>(a.v_sh) + (size_t)kvh * DH * a.cap_sh : vbase;
+    const KVT* kbase_sh = a.P_sh ? reinterpret_cast<const KVT*>(a.k_sh) + (size_t)kvh * a.cap_sh * DH : kbase;
+    const KVT* vbase_sh = a.P_sh ? reinterpret_cast<const KVT*>(a.v_sh) + (size_t)kvh * DH * a.cap_sh : vbase;
     char* gbase = smem + grp * L::GROUP;
 
     // ---- copy the K (or V^T) tile of key tile `tile` into LDS at `dst`:
@@ -159,28 +165,93 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     // held), V^T chunks past n are written as zeros (their probabilities are 0
     // and 0 * stale could be NaN), and a chunk that straddles n goes through
     // registers element by element.
-    auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
+    // FP8 cache: this thread's chunks of the next K and V tiles, held in
+    // registers between their loads (early in a step) and their conversion
+    // into LDS (at the end of the step, before its barrier)
+    uint2 kreg[NI], vreg[NI];
+    auto load_k8 = [&](int tile) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
-        const bf16_t* kb = k0 < a.P_sh ? kbase_sh : kbase;
+        const KVT* kb = k0 < a.P_sh ? kbase_sh : kbase;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
             const int r = q / (DH / 8), sl = q % (DH / 8);
-            const bf16_t* src = kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
+            // a key row of DH bytes: every 8-byte chunk is aligned
             if (n == kKeys || r < n)
-                __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
+                kreg[j] = *reinterpret_cast<const uint2*>(kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1))));
         }
     };
-    auto issue_v = [&](int tile, char* dst) __attribute__((always_inline)) {
+    auto commit_k8 = [&](int tile, char* dst) __attribute__((always_inline)) {
+        const int n = tile_count(tile, npre, pre_end, B2);
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            if (n == kKeys || q / (DH / 8) < n) *reinterpret_cast<uint4*>(dst + 16 * q) = e4m3x8_to_bf16x8(kreg[j]);
+        }
+    };
+    auto load_v8 = [&](int tile) __attribute__((always_inline)) {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
         const bool sh = k0 < a.P_sh;
-        const bf16_t* vb = sh ? vbase_sh : vbase;
+        const KVT* vb = sh ? vbase_sh : vbase;
         const int vcap = sh ? a.cap_sh : cap;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
             const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
-            const bf16_t* src = vb + (size_t)d * vcap + k0 + 8 * c;
+            const KVT* src = vb + (size_t)d * vcap + k0 + 8 * c;
+            const int cnt = n == kKeys ? 8 : max(0, min(8, n - 8 * c));   // keys of the chunk inside the tile
+            uint2 w = make_uint2(0u, 0u);                                    // code 0 is +0
+            if (cnt == 8 && ((reinterpret_cast<uintptr_t>(src) & 7) == 0)) {
+                w = *reinterpret_cast<const uint2*>(src);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (e < cnt) {
+                        const uint32_t bt = (uint32_t)src[e] << (8 * (e & 3));
+                        if (e < 4) w.x |= bt; else w.y |= bt;
+                    }
+            }
+            vreg[j] = w;
+        }
+    };
+    auto commit_v8 = [&](char* dst) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            *reinterpret_cast<uint4*>(dst + 16 * q) = e4m3x8_to_bf16x8(vreg[j]);
+        }
+    };
+    auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
+        if constexpr (KV8) {
+            load_k8(tile);
+            commit_k8(tile, dst);
+        } else {
+        const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
+        const KVT* kb = k0 < a.P_sh ? kbase_sh : kbase;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            const int r = q / (DH / 8), sl = q % (DH / 8);
+            const KVT* src = kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
+            if (n == kKeys || r < n)
+                __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
+        }
+        }
+    };
+    auto issue_v = [&](int tile, char* dst) __attribute__((always_inline)) {
+        if constexpr (KV8) {
+            load_v8(tile);
+            commit_v8(dst);
+        } else {
+        const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
+        const bool sh = k0 < a.P_sh;
+        const KVT* vb = sh ? vbase_sh : vbase;
+        const int vcap = sh ? a.cap_sh : cap;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int q = (wave * NI + j) * 64 + lane;
+            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
+            const KVT* src = vb + (size_t)d * vcap + k0 + 8 * c;
             if (n == kKeys || 8 * c + 8 <= n) {
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
             } else {
@@ -192,6 +263,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
                 }
                 *reinterpret_cast<bf16x8*>(dst + 16 * q) = vv;
             }
+        }
         }
     };
     // stage addresses by arithmetic on the LDS array (an indexed table of
@@ -344,30 +416,52 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     __syncthreads();
     if (!late) {
         for (int it = 0; it < iters; ++it) {         // iters is uniform across the workgroup
-            if (mine(it + 1)) issue_v(tile_of(it + 1), vst(it + 1));
-            const bool ahead = mine(it + 2);
-            if (ahead) issue_k(tile_of(it + 2), kst(it + 2));
+            const bool nextv = mine(it + 1), ahead = mine(it + 2);
+            if constexpr (KV8) {
+                if (nextv) load_v8(tile_of(it + 1));
+                if (ahead) load_k8(tile_of(it + 2));
+            } else {
+                if (nextv) issue_v(tile_of(it + 1), vst(it + 1));
+                if (ahead) issue_k(tile_of(it + 2), kst(it + 2));
+            }
             if (mine(it)) {
                 floatx16 sc[2];
                 scores(kst(it), sc);
                 softmax_pv(sc, tile_of(it), vst(it));
             }
-            if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
-            else __builtin_amdgcn_s_waitcnt(0);
+            if constexpr (KV8) {
+                if (nextv) commit_v8(vst(it + 1));
+                if (ahead) commit_k8(tile_of(it + 2), kst(it + 2));
+                __builtin_amdgcn_s_waitcnt(0);
+            } else {
+                if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+                else __builtin_amdgcn_s_waitcnt(0);
+            }
             wg_barrier();
         }
     } else {
         floatx16 sc[2];
         if (mine(0)) scores(kst(0), sc);
         for (int it = 0; it < iters; ++it) {
-            if (mine(it + 1)) issue_v(tile_of(it + 1), vst(it + 1));
-            const bool ahead = mine(it + 3);
-            if (ahead) issue_k(tile_of(it + 3), kst(it + 3));
+            const bool nextv = mine(it + 1), ahead = mine(it + 3);
+            if constexpr (KV8) {
+                if (nextv) load_v8(tile_of(it + 1));
+                if (ahead) load_k8(tile_of(it + 3));
+            } else {
+                if (nextv) issue_v(tile_of(it + 1), vst(it + 1));
+                if (ahead) issue_k(tile_of(it + 3), kst(it + 3));
+            }
             if (mine(it)) softmax_pv(sc, tile_of(it), vst(it));
             __builtin_amdgcn_sched_barrier(0);
             if (mine(it + 1)) scores(kst(it + 1), sc);
-            if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
-            else __builtin_amdgcn_s_waitcnt(0);
+            if constexpr (KV8) {
+                if (nextv) commit_v8(vst(it + 1));
+                if (ahead) commit_k8(tile_of(it + 3), kst(it + 3));
+                __builtin_amdgcn_s_waitcnt(0);
+            } else {
+                if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+                else __builtin_amdgcn_s_waitcnt(0);
+            }
             wg_barrier();
         }
     }
@@ -585,10 +679,14 @@ AttnCfg attention_cfg(int b, int R, int Hq, int Hkv, int ntiles) {
 
 using AttnKernel = void (*)(AttnArgs, int, int);
 
-template <int DH>
+template <int DH, bool KV8>
 AttnKernel attention_kernel(const AttnCfg& c) {
-    if (c.g == 2) return c.waves == 2 ? attn_mfma_kernel<DH, 2, 2> : attn_mfma_kernel<DH, 4, 2>;
-    return c.waves == 2 ? attn_mfma_kernel<DH, 2, 1> : attn_mfma_kernel<DH, 4, 1>;
+    // the fp8 cache's staging registers do not fit the two-group 4-wave
+    // kernel (it would spill), so that shape runs one group with fp8
+    if (c.g == 2 && c.waves == 2) return attn_mfma_kernel<DH, 2, 2, KV8>;
+    if constexpr (!KV8)
+        if (c.g == 2) return attn_mfma_kernel<DH, 4, 2, false>;
+    return c.waves == 2 ? attn_mfma_kernel<DH, 2, 1, KV8> : attn_mfma_kernel<DH, 4, 1, KV8>;
 }
 
 }  // namespace
@@ -611,6 +709,7 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
         if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
         const int ntiles = attention_tiles(a.masked, a.P, a.B, a.nkeys);
         AttnCfg c = attention_cfg(a.b, a.R, a.Hq, a.Hkv, ntiles);
+        if (a.kv_fp8 && c.waves == 4) c.g = 1;   // see attention_kernel: one key group with the fp8 cache
         // a split needs room for its partials; without it one workgroup walks every key
         const size_t nrow = (size_t)a.b * a.R * a.Hq;
         if (c.ns > 1 && (!a.part || !a.part_ml || (size_t)c.ns * nrow > a.part_slots)) {
@@ -620,7 +719,8 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
         const size_t tiles = (size_t)a.b * a.Hkv * c.rowtiles;
         if (tiles == 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
         dim3 grid((unsigned)tiles, c.ns);
-        const AttnKernel k = a.dh == 128 ? attention_kernel<128>(c) : attention_kernel<64>(c);
+        const AttnKernel k = a.kv_fp8 ? (a.dh == 128 ? attention_kernel<128, true>(c) : attention_kernel<64, true>(c))
+                                      : (a.dh == 128 ? attention_kernel<128, false>(c) : attention_kernel<64, false>(c));
         launch(k, grid, dim3(64 * c.waves * c.g), 0, s, a, c.rowtiles, c.tps);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess || c.ns == 1) return e;
@@ -633,6 +733,7 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
                    nrow, a.Hq, a.out_frag, reinterpret_cast<bf16_t*>(a.out));
         return hipGetLastError();
     }
+    if (a.kv_fp8) return hipErrorInvalidValue;   // the fp8 cache is a bf16-model variant
     const size_t total = (size_t)a.b * a.R * a.Hq;
     dim3 grid((total + 63) / 64);
     if (a.dh == 128)

@@ -24,6 +24,41 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
     return (bf16_t)(u >> 16);
 }
 
+// ---------------------------------------------------------------- FP8 (OCP E4M3)
+// float -> E4M3 code (sign in bit 7): round to nearest, ties to the even code;
+// magnitudes from 448 (the largest finite value) up, and non-finite inputs,
+// give +-448.  Below 2^-6 the format steps by 2^-9 (subnormals).
+__device__ __forceinline__ uint32_t f2e4m3(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t sign = (u >> 24) & 0x80u;
+    const uint32_t a = u & 0x7FFFFFFFu;
+    uint32_t code;
+    if (a >= 0x43E00000u) {                 // |f| >= 448
+        code = 0x7Eu;
+    } else if (a < 0x3C800000u) {           // |f| < 2^-6: multiples of 2^-9, 8 = the smallest normal
+        code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    } else {                                // keep 3 mantissa bits (ties to even on bit 20), rebias 127 -> 7
+        const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+        code = (r >> 20) - (120u << 3);
+        code = code > 0x7Eu ? 0x7Eu : code;
+    }
+    return sign | code;
+}
+
+// Eight E4M3 codes (little-endian in w) -> eight bf16 values.  The hardware
+// conversion gives the exact value in fp32; E4M3 values have at most 4
+// significant bits and exponents within bf16's, so keeping the upper half of
+// each fp32 is exact.
+template <bool HI>   // HI: the codes in bits 16..31, else bits 0..15
+__device__ __forceinline__ uint32_t e4m3x2_to_bf16x2(uint32_t x) {
+    const auto f = __builtin_amdgcn_cvt_pk_f32_fp8((int)x, HI);
+    return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xFFFF0000u);
+}
+__device__ __forceinline__ uint4 e4m3x8_to_bf16x8(uint2 w) {
+    return make_uint4(e4m3x2_to_bf16x2<false>(w.x), e4m3x2_to_bf16x2<true>(w.x), e4m3x2_to_bf16x2<false>(w.y),
+                      e4m3x2_to_bf16x2<true>(w.y));
+}
+
 // Storage-type traits: activations and weights are either float or bf16.
 template <typename T> struct St;
 template <> struct St<float> {

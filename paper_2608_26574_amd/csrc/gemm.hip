@@ -151,15 +151,26 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, int m, int n, floatx
                 store4<T>(reinterpret_cast<T*>(e.q) + (size_t)m * e.ldq + n, a0, b0, a1, b1);
             } else {
                 const int nk = n - qd, kvh = nk >> sh, ein = nk & (e.dh - 1);
-                T* kc = reinterpret_cast<T*>(e.kc) + (((size_t)row.s * e.Hkv + kvh) * e.cap + row.cidx) * e.dh + ein;
-                store4<T>(kc, a0, b0, a1, b1);
+                const size_t ko = (((size_t)row.s * e.Hkv + kvh) * e.cap + row.cidx) * e.dh + ein;
+                if (e.kv_fp8)
+                    *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(e.kc) + ko) =
+                        f2e4m3(a0) | (f2e4m3(b0) << 8) | (f2e4m3(a1) << 16) | (f2e4m3(b1) << 24);
+                else
+                    store4<T>(reinterpret_cast<T*>(e.kc) + ko, a0, b0, a1, b1);
             }
         } else {
             // the V cache is dims-major ([dh][cap] per KV head): four strided stores
             const int nv = n - qd - kd, kvh = nv >> sh, ein = nv & (e.dh - 1);
-            T* vc = reinterpret_cast<T*>(e.vc) + (((size_t)row.s * e.Hkv + kvh) * e.dh + ein) * e.cap + row.cidx;
+            const size_t vo = (((size_t)row.s * e.Hkv + kvh) * e.dh + ein) * e.cap + row.cidx;
+            if (e.kv_fp8) {
+                uint8_t* vc = reinterpret_cast<uint8_t*>(e.vc) + vo;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) St<T>::st(vc + (size_t)i * e.cap, v[i]);
+                for (int i = 0; i < 4; ++i) vc[(size_t)i * e.cap] = (uint8_t)f2e4m3(v[i]);
+            } else {
+                T* vc = reinterpret_cast<T*>(e.vc) + vo;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) St<T>::st(vc + (size_t)i * e.cap, v[i]);
+            }
         }
     }
 }

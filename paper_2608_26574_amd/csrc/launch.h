@@ -50,6 +50,7 @@ struct AttnArgs {
     float* part_ml;     // [nsplit][b][R][Hq][2]: running max (log2 units) and sum
     size_t part_slots;  // capacity of part / part_ml in (split, row, head) slots
     int out_frag;       // 1: out is fragment-major [b*R][Hq*dh] (bf16 only)
+    int kv_fp8;         // 1: k, v (and k_sh, v_sh) hold OCP FP8 E4M3 codes (bf16 q / out)
 };
 // 64-key tiles of a launch: the prefix (or all keys when unmasked), then the block.
 int attention_tiles(int masked, int P, int B, int nkeys);
@@ -90,6 +91,7 @@ struct EpiArgs {
     const float* rope;              // [max_pos][dh/2][2] (cos, sin)
     int rows_per_seq;               // R
     int P, B, cap, Hq, Hkv, dh;
+    int kv_fp8;                     // 1: K and V are written to the cache as OCP FP8 E4M3 codes
     int step;                       // 1: row r -> pos P + r%B, cache P + r; 0: pos = cache = r;
                                     // 2 (full sequence): cache r, pos r (r < blk), r + B (blk <= r < P),
                                     //   blk + (r - P) % B (block rows r >= P);

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libdard.so")
 
 DARD_OK = 0
 STATE_M, STATE_C, STATE_U = 0, 1, 2
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_BF16_KV_FP8 = 0, 1, 2
+KV_DTYPE, KV_FP8 = 0, 1
 F_XSELF_SHADOW, F_MKEYS_SHADOW, F_VERIFY_PCUR, F_PROGRESS = 1, 2, 4, 8
 F_C_BIDIR, F_ORDER_L2R, F_ORDER_ENTROPY, F_ORDER_MARGIN, F_FIXED_W = 16, 32, 64, 128, 256
 F_CHECK_STATES = 512
@@ -54,7 +55,7 @@ class dard_params(ctypes.Structure):
 class dard_dims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "d_model", "n_heads", "n_kv_heads", "head_dim",
                                               "ffn_dim", "vocab", "max_pos", "dtype")] + \
-               [("norm_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+               [("norm_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("kv_format", ctypes.c_int32)]
 
 
 class dard_step_debug(ctypes.Structure):
@@ -152,8 +153,12 @@ def make_params(tau_c=0.4, tau_u=0.9, lam=0.5 ** (1 / 8), p0=0.1, mask_id=0, fla
 
 def make_dims(d):
     """From a synth.Dims (or anything with the same attributes)."""
+    kv = getattr(d, "kv_dtype", "")
+    if kv not in ("", "fp8", d.dtype):
+        raise ValueError(f"unknown kv_dtype {kv!r}")
     return dard_dims(d.n_layers, d.d_model, d.n_heads, d.n_kv_heads, d.head_dim, d.ffn_dim, d.vocab, d.max_pos,
-                     DTYPE_BF16 if d.dtype == "bf16" else DTYPE_F32, d.norm_eps, d.rope_theta)
+                     DTYPE_BF16 if d.dtype == "bf16" else DTYPE_F32, d.norm_eps, d.rope_theta,
+                     KV_FP8 if kv == "fp8" else KV_DTYPE)
 
 
 # ------------------------------------------------------------------ entry points
@@ -184,13 +189,15 @@ def dard_attention_workspace_bytes(dtype, b, B, Hq, dh, P):
 
 
 def dard_masked_attention(q, k, v, P, state, conf, scale, flags, out, ws=None, stream=None):
-    """q [b][2B][Hq][dh], k [b][Hkv][cap][dh], v [b][Hkv][dh][cap] (dims-major)."""
+    """q [b][2B][Hq][dh], k [b][Hkv][cap][dh], v [b][Hkv][dh][cap] (dims-major);
+    uint8 k / v hold OCP FP8 E4M3 codes (bf16 q / out)."""
     b, R, Hq, dh = q.shape
     _, Hkv, cap, _ = k.shape
     if tuple(v.shape) != (b, Hkv, dh, cap):
         raise ValueError(f"v must be [b][Hkv][dh][cap] = {(b, Hkv, dh, cap)}, got {tuple(v.shape)}")
     nbytes = ws.numel() * ws.element_size() if ws is not None else 0
-    _check(lib().dard_masked_attention(_dt(q), _p(q), _p(k), _p(v), P, cap, _p(state), _p(conf), b, R // 2, Hq,
+    dt = DTYPE_BF16_KV_FP8 if k.dtype == torch.uint8 else _dt(q)
+    _check(lib().dard_masked_attention(dt, _p(q), _p(k), _p(v), P, cap, _p(state), _p(conf), b, R // 2, Hq,
                                        Hkv, dh, scale, flags, _p(out), _p(ws), nbytes, _stream(stream)))
 
 
@@ -296,7 +303,8 @@ class Engine:
 
     def kv_view(self, dtype):
         """KV cache as (K, V) tensors [layers][b][Hkv][cap][dh] (V read out of
-        its dims-major storage [layers][b][Hkv][dh][cap] as a transposed view)."""
+        its dims-major storage [layers][b][Hkv][dh][cap] as a transposed view);
+        dtype torch.uint8 for an FP8 cache (E4M3 codes)."""
         d = self.dims
         n = d.n_layers * 2 * self.b * d.n_kv_heads * self.cap * d.head_dim
         kv = self.kv.view(dtype)[:n].view(d.n_layers, 2, self.b, d.n_kv_heads, self.cap * d.head_dim)

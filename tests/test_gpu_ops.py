@@ -419,3 +419,56 @@ def test_check_states():
     st[4999] = 3
     dard.dard_check_states(st, status)
     assert status.cpu().tolist() == [2, 4097]
+
+
+# ---------------------------------------------------------------- FP8 KV cache
+def fp8_codes(x):
+    """OCP FP8 E4M3 codes (uint8) of the values O.to_fp8 rounds x to."""
+    r = O.to_fp8(x)
+    code = np.searchsorted(O.E4M3_VALUES, np.abs(r)).astype(np.uint8)
+    return code | np.where(r < 0, 0x80, 0).astype(np.uint8)
+
+
+def _attn_case_fp8(b, B, P, Hq, Hkv, dh, cand_frac, seed, cap_extra=3):
+    """bf16 Q against K and V held as E4M3 codes (DARD_DTYPE_BF16_KV_FP8); the
+    reference attends over the codes' values in float64."""
+    cap = P + 2 * B + cap_extra
+    q, k, v = synth.qkv(b, 2 * B, Hq, Hkv, dh, cap, seed=seed, dtype=torch.bfloat16)
+    kc = fp8_codes(k.double().numpy())
+    vc = fp8_codes(v.double().numpy())
+    kf, vf = O.to_fp8(k.double().numpy()), O.to_fp8(v.double().numpy())
+    if cand_frac is None:
+        _, state, conf = synth.tiny_block(b, B, 100, seed=seed)
+    else:
+        _, state, conf = synth.workload_block(b, B, cand_frac, 100, seed=seed)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device="cuda")
+    scale = 1.0 / math.sqrt(dh)
+    ws = torch.empty(max(dard.dard_attention_workspace_bytes(dard.DTYPE_BF16_KV_FP8, b, B, Hq, dh, P), 1),
+                     dtype=torch.uint8, device="cuda")
+    dard.dard_masked_attention(q.cuda(), dev(kc), dev(np.ascontiguousarray(vc.transpose(0, 1, 3, 2))), P, dev(state),
+                               dev(conf), scale, 0, out, ws)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    qn = q.double().numpy()
+    worst = 0.0
+    for s in range(b):
+        vis = O.visible_keys(state[s], conf[s], P)
+        ref = O.masked_attention(qn[s], kf[s, :, :P + 2 * B].transpose(1, 0, 2),
+                                 vf[s, :, :P + 2 * B].transpose(1, 0, 2), vis, scale, Hkv)
+        worst = max(worst, float(np.max(np.abs(got[s] - ref))))
+    return worst
+
+
+@pytest.mark.parametrize("case", [
+    dict(b=1, B=32, P=512, Hq=32, Hkv=32, dh=128, frac=0.25),   # 8B MHA, batch 1 (key splits)
+    dict(b=4, B=32, P=512, Hq=32, Hkv=32, dh=128, frac=0.1),    # batch 4 (two key groups)
+    dict(b=16, B=32, P=512, Hq=32, Hkv=32, dh=128, frac=0.5),   # batch 16
+    dict(b=8, B=64, P=1024, Hq=28, Hkv=4, dh=128, frac=0.3),    # 7B GQA (one key group with fp8)
+    dict(b=2, B=5, P=70, Hq=4, Hkv=2, dh=128, frac=None),       # ragged block and prefix: unaligned V chunks
+    dict(b=3, B=32, P=100, Hq=4, Hkv=4, dh=64, frac=None),      # head_dim 64
+    dict(b=1, B=256, P=100, Hq=2, Hkv=1, dh=128, frac=None),    # maximum block
+])
+def test_attention_fp8_kv(case):
+    announce("attention fp8 kv", case)
+    err = _attn_case_fp8(case["b"], case["B"], case["P"], case["Hq"], case["Hkv"], case["dh"], case["frac"], seed=9)
+    assert err < 2e-2, err

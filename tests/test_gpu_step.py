@@ -64,7 +64,28 @@ def run_case(dims, b, B, P_, params, seed=1, lm_scale=None, frac=None, wdevice="
     dd = dims.as_dict()
     emb_np = None if embeds is None else embeds.double().numpy()
     cache = O.prefill(ow, dd, ids, emb_np)
-    if check_kv:
+    if check_kv and dims.kv_dtype == "fp8":
+        # the cache holds E4M3 codes: decoded, every value is within one code
+        # (relative step 2^-3) of the oracle's, and in the first layer, whose
+        # inputs agree up to fp32 rounding order, almost every one is equal
+        # (deeper layers see the earlier layers' bf16 rounding differences,
+        # which move values across E4M3 midpoints)
+        kc, vc = eng.kv_view(torch.uint8)
+        vals = np.concatenate([-O.E4M3_VALUES[::-1], O.E4M3_VALUES])
+
+        def decode(c):
+            c = c.cpu().numpy().astype(np.int64)
+            mag = O.E4M3_VALUES[np.minimum(c & 0x7F, 126)]
+            return np.where(c & 0x80, -mag, mag)
+        for layer in range(dims.n_layers):
+            k_gpu = unpermute_k(decode(kc[layer, :, :, :P_]), dims.head_dim).transpose(0, 2, 1, 3)
+            v_gpu = decode(vc[layer, :, :, :P_]).transpose(0, 2, 1, 3)
+            for g, r in ((k_gpu, cache[layer][0]), (v_gpu, cache[layer][1])):
+                assert np.all(np.isin(g, vals))
+                if layer == 0:
+                    assert np.mean(g == r) > 0.97, (layer, np.mean(g == r))
+                assert np.all(np.abs(g - r) <= 0.13 * np.abs(r) + 2e-2 + 2.0 ** -9), layer
+    elif check_kv:
         tol = 2e-2 if dims.dtype == "bf16" else 1e-4
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
         kc, vc = eng.kv_view(kvd)
@@ -321,3 +342,35 @@ def test_hidden_mix(case):
     check_workload_decisions(tok, state, got, ref, prm, f"hidden mix {case['name']}")
     # the x rows never ran through the head
     assert np.all(np.isnan(got["logits"][:, :case["B"]]))
+
+
+@pytest.mark.parametrize("case", [
+    dict(name="small bf16", dims=(256, 4, 2, 64, 512, 1024, 2), b=2, B=16, P=41, frac=None, scale=8.0),
+    dict(name="llada8b 2 layers", dims=("llada8b", 2), b=1, B=32, P=512, frac=0.25, scale=WORKLOAD_LM_SCALE),
+    dict(name="dream7b b8 1 layer", dims=("dream7b", 1), b=8, B=64, P=160, frac=0.3, scale=WORKLOAD_LM_SCALE),
+    dict(name="multimodal b32 1 layer", dims=("llada8b", 1), b=32, B=32, P=96, frac=0.3, scale=WORKLOAD_LM_SCALE,
+         n_image=64),
+])
+def test_fp8_kv_cache(case):
+    """The FP8 KV cache (OCP E4M3) against the oracle with K and V rounded to
+    E4M3 at the cache's storage point: the prefix cache's codes (decoded), the
+    logits under the bf16 rule and the decisions by the protocol."""
+    if case["dims"][0] == "llada8b":
+        dims = synth.truncated(synth.LLADA8B, case["dims"][1])
+    elif case["dims"][0] == "dream7b":
+        dims = synth.truncated(synth.DREAM7B, case["dims"][1])
+    else:
+        d, H, Hkv, dh, F, V, L = case["dims"]
+        dims = synth.Dims(L, d, H, Hkv, dh, F, V, 1024, "bf16")
+    dims = synth.with_fp8_kv(dims)
+    announce("fp8 kv cache", case["name"])
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = run_case(dims, case["b"], case["B"], case["P"], prm, seed=21,
+                                          frac=case["frac"], wdevice="cuda", check_kv=True,
+                                          n_image=case.get("n_image", 0), lm_scale=case["scale"])
+    check_bf16_logits(got, ref, f"fp8 kv {case['name']}", scale=case["scale"])
+    if case["frac"] is None:
+        eps, excl, _ = check_decisions(tok, state, got, ref, prm, f"fp8 kv {case['name']}")
+        assert excl <= state.size // 4
+    else:
+        check_workload_decisions(tok, state, got, ref, prm, f"fp8 kv {case['name']}")
