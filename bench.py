@@ -193,6 +193,33 @@ def main():
         torch.cuda.synchronize()
         variants[vname + "_ms_per_step"] = round(ev0.elapsed_time(ev1) / args.steps, 4)
 
+    # ---- the same steps with the FP8 (E4M3) KV cache (the packed weights shared)
+    d8 = synth.with_fp8_kv(dims)
+    eng8 = dard.Engine(d8, None, b, B, cap, packed=eng.packed)
+    eng8.dard_prefill(ids)
+
+    def step8(t):
+        tok, state, conf = inputs[t]
+        eng8.dard_step(Ps[t], params, tok, state, conf, t_out, s_out, c_out, done)
+    step8(args.warmup)
+    torch.cuda.synchronize()
+    ev0.record()
+    for t in range(args.warmup, total):
+        step8(t)
+    ev1.record()
+    torch.cuda.synchronize()
+    variants["fp8_kv_ms_per_step"] = round(ev0.elapsed_time(ev1) / args.steps, 4)
+    dard.dard_trace_reset()
+    dard.dard_trace_enable(1 << dard.K_ATTENTION)
+    for t in range(args.warmup, total):
+        step8(t)
+    torch.cuda.synchronize()
+    dard.dard_trace_enable(0)
+    variants["fp8_kv_attention_ms_per_step"] = round(dard.dard_trace_read(dard.K_ATTENTION)[1] / args.steps, 4)
+    dard.dard_trace_reset()
+    del eng8
+    torch.cuda.empty_cache()
+
     # ---- tokens committed / s: 8 blocks of prefill + ceil(B / 6) steps each
     def generation():
         for k in range(nblocks):
@@ -427,7 +454,15 @@ def full_step_configs(eng8b, steps=6):
     out["multimodal_8b"] = {"workload": "llada8b-like full DARD step with a multimodal prefix: 576 image-embedding "
                                         "positions N(0, 1) + 256 prompt ids; batch 32, generation 128, block 32, "
                                         "candidate fraction 0.1 / 0.3 / 0.5, prefix KV cache", **rm}
-    del engm, ids, embeds
+    del engm
+    torch.cuda.empty_cache()
+    # the same workload with the FP8 (E4M3) KV cache
+    d8f = synth.with_fp8_kv(d8)
+    engf = dard.Engine(d8f, None, b, B, prompt + gen + B, packed=eng8b.packed)
+    rf = run(engf, d8f, b, B, prompt, gen, [0.3], 8.8, ids, embeds, "multimodal, FP8 KV")
+    out["multimodal_8b_fp8_kv"] = {"workload": "as multimodal_8b with the KV cache in OCP FP8 E4M3, candidate "
+                                               "fraction 0.3", **rf}
+    del engf, ids, embeds
     torch.cuda.empty_cache()
     out["multimodal_8b_shared_prompt"] = shared_prompt_workload(eng8b, steps)
     out["paper_latency_8b"] = paper_latency_workload(eng8b, steps)
@@ -618,28 +653,39 @@ def op_measurements(reps=20):
     res = {"attention": [], "confidence": []}
     # the isolated-attention workload: batch 1 / 4 / 16 x candidate fraction 0.1 / 0.25 / 0.5
     shapes = [("8B MHA", bsz, 32, 32, 32, 512, frac) for bsz in (1, 4, 16) for frac in (0.1, 0.25, 0.5)] + \
-             [("7B GQA", 8, 28, 4, 64, P, 0.3) for P in (1024, 1472)]
+             [("7B GQA", 8, 28, 4, 64, P, 0.3) for P in (1024, 1472)] + \
+             [("8B MHA, FP8 KV", bsz, 32, 32, 32, 512, 0.25) for bsz in (1, 4, 16)] + \
+             [("7B GQA, FP8 KV", 8, 28, 4, 64, 1024, 0.3)]
     dh = 128
     for label, bsz, H, Hkv, B, P, frac in shapes:
+        fp8 = "FP8" in label
+        kvb = 1 if fp8 else 2                       # bytes per cached value
         cap = P + 2 * B
-        kv_bytes = bsz * Hkv * cap * dh * 2
+        kv_bytes = bsz * Hkv * cap * dh * kvb
         ncopy = max(4, -(-600 * 2**20 // (2 * kv_bytes)))
         g = torch.Generator(device="cuda").manual_seed(2)
         q = torch.randn(bsz, 2 * B, H, dh, generator=g, device="cuda").bfloat16()
-        ks = [torch.randn(bsz, Hkv, cap, dh, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
-        vs = [torch.randn(bsz, Hkv, dh, cap, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+
+        def kvt(shape):
+            x = torch.randn(shape, generator=g, device="cuda").bfloat16()
+            # FP8: random E4M3 codes of magnitude below 16 (exponent field < 11), either sign
+            return torch.randint(0, 88, shape, generator=g, device="cuda", dtype=torch.int32).to(torch.uint8) | \
+                (torch.randint(0, 2, shape, generator=g, device="cuda", dtype=torch.int32) * 128).to(torch.uint8) \
+                if fp8 else x
+        ks = [kvt((bsz, Hkv, cap, dh)) for _ in range(ncopy)]
+        vs = [kvt((bsz, Hkv, dh, cap)) for _ in range(ncopy)]
         _, state, conf = synth.workload_block(bsz, B, frac, 100, seed=3)
         state, conf = torch.from_numpy(state).cuda(), torch.from_numpy(conf).cuda()
         out = torch.empty_like(q)
-        ws = torch.empty(max(dard.dard_attention_workspace_bytes(1, bsz, B, H, dh, P), 1), dtype=torch.uint8,
-                         device="cuda")
+        ws = torch.empty(max(dard.dard_attention_workspace_bytes(2 if fp8 else 1, bsz, B, H, dh, P), 1),
+                         dtype=torch.uint8, device="cuda")
 
         def att(i):
             dard.dard_masked_attention(q, ks[i % ncopy], vs[i % ncopy], P, state, conf, dh ** -0.5, 0, out, ws)
         ms = timed(att, reps)
         kms = traced(att, reps, dard.K_ATTENTION)
         flops = 4 * dh * H * 2 * B * (P + B) * bsz
-        nbytes = 2 * bsz * Hkv * (P + 2 * B) * dh * 2 + 2 * q.numel() * 2
+        nbytes = 2 * bsz * Hkv * (P + 2 * B) * dh * kvb + 2 * q.numel() * 2
         res["attention"].append({"shape": label, "batch": bsz, "heads": [H, Hkv], "block": B, "prefix": P,
                                  "cand_frac": frac,
                                  "us": round(ms * 1e3, 2), "kernel_us": round(kms * 1e3, 2),

@@ -871,7 +871,9 @@ hipError_t launch_pack_frag(const void* src0, const void* src1, void* dst, int N
 // that over more weight columns: the widest of 8, 6, 4, 3 column blocks whose
 // grid still covers the 256 CUs; otherwise the tile that fills the CUs most
 // evenly, with 4 waves per workgroup.  The O and down projections, whose
-// 4096-wide output has too few column tiles, split K 4 ways instead.
+// 4096-wide output has too few column tiles, split K 4 ways instead, with 4
+// waves per workgroup splitting K again (3 k units in flight for the long K
+// of the down projection).
 struct StreamCfg {
     int nw, ks, depth, split;
 };
@@ -881,7 +883,7 @@ StreamCfg stream_cfg(int N, int K, bool partial) {
     if (partial) {
         int S = 4;
         while (S > 1 && KU / S < 8) S /= 2;
-        if (N % 64 == 0) return K > 4096 ? StreamCfg{4, 4, 2, S} : StreamCfg{4, 2, 3, S};
+        if (N % 64 == 0) return K > 4096 ? StreamCfg{4, 4, 3, S} : StreamCfg{4, 4, 2, S};
         return StreamCfg{1, 4, 2, S};
     }
     for (int c : {8, 6}) {
@@ -1021,8 +1023,8 @@ hipError_t launch_gemm(int dtype, const void* X, int M, int K, int ldx, const vo
     } while (0)
         if (c.nw == 8) DARD_GS(8, 2, 3);
         else if (c.nw == 6) DARD_GS(6, 4, 3);
+        else if (c.nw == 4 && c.ks == 4 && c.depth == 3) DARD_GS(4, 4, 3);
         else if (c.nw == 4 && c.ks == 4) DARD_GS(4, 4, 2);
-        else if (c.nw == 4 && c.depth == 3) DARD_GS(4, 2, 3);
         else if (c.nw == 4) DARD_GS(4, 2, 2);
         else if (c.nw == 3 && c.ks == 4) DARD_GS(3, 4, 3);
         else if (c.nw == 3) DARD_GS(3, 2, 2);

@@ -77,28 +77,30 @@ def collect(out, dbg):
     return got
 
 
-def perturbed_logits(run_perturbed, seeds=(0, 1, 2), amp=1e-7):
-    """The oracle's logits with every value perturbed by one float32 ulp
-    (relative `amp`) just before each storage rounding, once per seed:
-    run_perturbed() recomputes the logits while O.storage is replaced.  Any
-    implementation whose accumulation order differs from the oracle's flips
-    some of those roundings, so these runs measure the noise floor of the
-    comparison."""
+def under_perturbation(run, seed, amp=1e-7):
+    """run() with every value the oracle computes perturbed by about one
+    float32 ulp (relative `amp`) just before each storage rounding (O.storage
+    is replaced meanwhile).  Any implementation whose accumulation order
+    differs from the oracle's flips some of those roundings, so such runs
+    measure the noise floor of a comparison."""
     orig = O.storage
-    out = []
-    for sd in seeds:
-        rng = np.random.default_rng(sd)
+    rng = np.random.default_rng(seed)
 
-        def noisy(x, dt, rng=rng):
-            x = np.asarray(x, dtype=np.float64)
-            return orig(x * (1.0 + amp * rng.standard_normal(x.shape)), dt)
+    def noisy(x, dt):
+        x = np.asarray(x, dtype=np.float64)
+        return orig(x * (1.0 + amp * rng.standard_normal(x.shape)), dt)
 
-        O.storage = noisy
-        try:
-            out.append(np.asarray(run_perturbed(), dtype=np.float32))
-        finally:
-            O.storage = orig
-    return out
+    O.storage = noisy
+    try:
+        return run()
+    finally:
+        O.storage = orig
+
+
+def perturbed_logits(run_perturbed, seeds=(0, 1, 2), amp=1e-7):
+    """The oracle's logits recomputed by run_perturbed() under the one-ulp
+    perturbation, once per seed."""
+    return [np.asarray(under_perturbation(run_perturbed, sd, amp), dtype=np.float32) for sd in seeds]
 
 
 def noise_floor(run_perturbed, ref_logits, seeds=(0, 1, 2), amp=1e-7):

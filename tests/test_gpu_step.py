@@ -65,11 +65,16 @@ def run_case(dims, b, B, P_, params, seed=1, lm_scale=None, frac=None, wdevice="
     emb_np = None if embeds is None else embeds.double().numpy()
     cache = O.prefill(ow, dd, ids, emb_np)
     if check_kv and dims.kv_dtype == "fp8":
-        # the cache holds E4M3 codes: decoded, every value is within one code
-        # (relative step 2^-3) of the oracle's, and in the first layer, whose
-        # inputs agree up to fp32 rounding order, almost every one is equal
-        # (deeper layers see the earlier layers' bf16 rounding differences,
-        # which move values across E4M3 midpoints)
+        # The cache holds E4M3 codes, compared in code steps (signed code
+        # ordinals).  In the first layer, whose inputs agree with the oracle's
+        # up to fp32 rounding order, almost every code is equal and none is
+        # more than one step away.  Deeper layers inherit the first layer's
+        # flipped E4M3 roundings (each a whole code step) through attention:
+        # the oracle's own prefill, perturbed by 1e-6 relative before every
+        # storage rounding, changes 3-8 % of the second layer's codes in a
+        # d = 256 model and 16.5 % at the 8B shape (3 % by more than one step).
+        # There the bound only rules out gross errors (a layer offset, a scale
+        # or a sign), which change 98 % of the codes or more.
         kc, vc = eng.kv_view(torch.uint8)
         vals = np.concatenate([-O.E4M3_VALUES[::-1], O.E4M3_VALUES])
 
@@ -77,14 +82,22 @@ def run_case(dims, b, B, P_, params, seed=1, lm_scale=None, frac=None, wdevice="
             c = c.cpu().numpy().astype(np.int64)
             mag = O.E4M3_VALUES[np.minimum(c & 0x7F, 126)]
             return np.where(c & 0x80, -mag, mag)
+
+        def ordinal(v):
+            m = np.searchsorted(O.E4M3_VALUES, np.abs(v))
+            return np.where(v < 0, -m, m)
         for layer in range(dims.n_layers):
             k_gpu = unpermute_k(decode(kc[layer, :, :, :P_]), dims.head_dim).transpose(0, 2, 1, 3)
             v_gpu = decode(vc[layer, :, :, :P_]).transpose(0, 2, 1, 3)
-            for g, r in ((k_gpu, cache[layer][0]), (v_gpu, cache[layer][1])):
+            for j, g in enumerate((k_gpu, v_gpu)):
                 assert np.all(np.isin(g, vals))
+                dg = np.abs(ordinal(g) - ordinal(cache[layer][j]))
+                print(f"fp8 cache layer {layer} {'KV'[j]}: codes differing {np.mean(dg > 0):.4f}, by more than one "
+                      f"step {np.mean(dg > 1):.4f}", file=sys.stderr, flush=True)
                 if layer == 0:
-                    assert np.mean(g == r) > 0.97, (layer, np.mean(g == r))
-                assert np.all(np.abs(g - r) <= 0.13 * np.abs(r) + 2e-2 + 2.0 ** -9), layer
+                    assert np.mean(dg == 0) > 0.97 and dg.max() <= 1, (layer, j, np.mean(dg == 0), dg.max())
+                else:
+                    assert np.mean(dg > 0) < 0.35 and np.mean(dg > 1) < 0.08, (layer, j)
     elif check_kv:
         tol = 2e-2 if dims.dtype == "bf16" else 1e-4
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
@@ -317,9 +330,12 @@ def test_step_reports_bad_state_codes():
     dict(name="llada8b b1", dims=("llada8b", 2), b=1, B=32, P=256, frac=0.5, seed=12),
     # 7B GQA shape, batch 8: 512 rows per pass, the large-tile head with fused partials
     dict(name="dream7b b8", dims=("dream7b", 1), b=8, B=64, P=160, frac=0.3, seed=13),
-    # small bf16 model, 144 rows per pass: the pipelined head
-    # (a head sharpened x12: its d = 512 leaves the x6 head's top probabilities below tau_u)
-    dict(name="small bf16", dims=(512, 4, 2, 128, 1024, 2048, 2), b=6, B=24, P=40, frac=0.4, seed=14, scale=12.0),
+    # small bf16 model, 144 rows per pass: the pipelined head (a head
+    # sharpened x12: its d = 512 leaves the x6 head's top probabilities below
+    # tau_u).  Weights drawn on the host, where the oracle alone shows that
+    # this step has 11 C->U and 10 C->M decisions (none at scale 10)
+    dict(name="small bf16", dims=(512, 4, 2, 128, 1024, 2048, 2), b=6, B=24, P=40, frac=0.4, seed=14, scale=12.0,
+         wdevice="cpu"),
 ])
 def test_hidden_mix(case):
     """DARD_F_HIDDEN_MIX (Eq. 7 applied to the final hidden state; two LM-head
@@ -337,7 +353,8 @@ def test_hidden_mix(case):
     prm = P(dims.mask_id, O.F_HIDDEN_MIX)
     scale = case.get("scale", WORKLOAD_LM_SCALE)
     tok, state, conf, got, ref = run_case(dims, case["b"], case["B"], case["P"], prm, seed=case["seed"],
-                                          frac=case["frac"], wdevice="cuda", check_kv=False, lm_scale=scale)
+                                          frac=case["frac"], wdevice=case.get("wdevice", "cuda"), check_kv=False,
+                                          lm_scale=scale)
     check_bf16_logits(got, ref, f"hidden mix {case['name']}", scale=scale)
     check_workload_decisions(tok, state, got, ref, prm, f"hidden mix {case['name']}")
     # the x rows never ran through the head
