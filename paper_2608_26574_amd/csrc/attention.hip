@@ -57,12 +57,29 @@ struct Lds {
     static constexpr int GROUP = ((5 * TILE > MERGE ? 5 * TILE : MERGE) + 15) / 16 * 16;
 };
 
-// 16-byte chunk slots: K row r keeps its chunk c (dims 8c..8c+7) in slot
-// c ^ (r % (DH/8)); V^T row d (a dim) keeps its chunk c (keys 8c..8c+7) in
-// slot c ^ (d % 8).
+// 16-byte chunk slots.  The LDS serves a 16-byte read 16 consecutive lanes
+// per cycle over 64 banks (256 bytes; measured: an image that separates only
+// groups of 8 lanes within 128 bytes kept its conflicts), and each group must
+// hit 16 different 4-bank groups; the swizzles below also keep every 8 lanes
+// within 128 bytes apart.  With x ^ (x >> 3) a value x in [0, 16) and its
+// neighbour x ^ 8 differ in their low three bits.
+//   K row r keeps its chunk c (dims 8c..8c+7) in slot c ^ kswz(r): with
+//   x = pi(r) % 16, pi swapping bits 2 and 3, kswz = x for DH = 128 (a row
+//   is 256 bytes) and (x ^ (x >> 3)) % 8 for DH = 64.  The S^T operand read
+//   of lane l takes key row pi(l % 32), so x is l % 16.
+//   V^T row d (a dim, 128 bytes) keeps its chunk c (keys 8c..8c+7) in slot
+//   c ^ vswz(d), vswz(d) = (d ^ (d >> 3)) % 8; the V^T read of lane l takes
+//   row 32j + l % 32.
+__device__ __forceinline__ int swap23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 template <int DH>
-__device__ __forceinline__ int kslot(int r, int c) { return r * (DH / 8) + (c ^ (r & (DH / 8 - 1))); }
-__device__ __forceinline__ int vslot(int d, int c) { return d * (kKeys / 8) + (c ^ (d & 7)); }
+__device__ __forceinline__ int kswz(int r) {
+    const int x = swap23(r) & 15;   // rows 32 apart share their swizzle
+    return DH == 128 ? x : ((x ^ (x >> 3)) & (DH / 8 - 1));
+}
+template <int DH>
+__device__ __forceinline__ int kslot(int r, int c) { return r * (DH / 8) + (c ^ kswz<DH>(r)); }
+__device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 3)) & 7; }
+__device__ __forceinline__ int vslot(int d, int c) { return d * (kKeys / 8) + (c ^ vswz(d)); }
 
 // The 2B-bit block visibility of a row, x^j for the set bits j of its take-x
 // value X (B <= 256 bits, zero above B), s^j for the clear ones: bits [0, B)
@@ -178,7 +195,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             const int r = q / (DH / 8), sl = q % (DH / 8);
             // a key row of DH bytes: every 8-byte chunk is aligned
             if (n == kKeys || r < n)
-                kreg[j] = *reinterpret_cast<const uint2*>(kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1))));
+                kreg[j] = *reinterpret_cast<const uint2*>(kb + (size_t)(k0 + r) * DH + 8 * (sl ^ kswz<DH>(r)));
         }
     };
     auto commit_k8 = [&](int tile, char* dst) __attribute__((always_inline)) {
@@ -197,7 +214,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
-            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
+            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ vswz(d);
             const KVT* src = vb + (size_t)d * vcap + k0 + 8 * c;
             const int cnt = n == kKeys ? 8 : max(0, min(8, n - 8 * c));   // keys of the chunk inside the tile
             uint2 w = make_uint2(0u, 0u);                                    // code 0 is +0
@@ -221,6 +238,16 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
             *reinterpret_cast<uint4*>(dst + 16 * q) = e4m3x8_to_bf16x8(vreg[j]);
         }
     };
+    // byte offsets of this thread's chunks inside a K tile and inside a V^T
+    // tile of the sequence's own cache (the same for every tile)
+    uint32_t koff[NI], voff[NI];
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+        const int q = (wave * NI + j) * 64 + lane;
+        const int r = q / (DH / 8), d = q / (kKeys / 8);
+        koff[j] = (uint32_t)(r * DH + 8 * ((q % (DH / 8)) ^ kswz<DH>(r))) * sizeof(KVT);
+        voff[j] = (uint32_t)(d * cap + 8 * ((q % (kKeys / 8)) ^ vswz(d))) * sizeof(KVT);
+    }
     auto issue_k = [&](int tile, char* dst) __attribute__((always_inline)) {
         if constexpr (KV8) {
             load_k8(tile);
@@ -228,12 +255,20 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
         } else {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
         const KVT* kb = k0 < a.P_sh ? kbase_sh : kbase;
+        if (n == kKeys) {   // a full tile: the common case, no per-chunk test
+            const char* kt = reinterpret_cast<const char*>(kb + (size_t)k0 * DH);
+#pragma unroll
+            for (int j = 0; j < NI; ++j)
+                __builtin_amdgcn_global_load_lds((glb_ptr)(kt + koff[j]), (lds_ptr)(dst + (wave * NI + j) * 1024),
+                                                 16, 0, 0);
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
             const int r = q / (DH / 8), sl = q % (DH / 8);
-            const KVT* src = kb + (size_t)(k0 + r) * DH + 8 * (sl ^ (r & (DH / 8 - 1)));
-            if (n == kKeys || r < n)
+            const KVT* src = kb + (size_t)(k0 + r) * DH + 8 * (sl ^ kswz<DH>(r));
+            if (r < n)
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
         }
         }
@@ -245,12 +280,20 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
         } else {
         const int k0 = tile_first(tile, npre, P), n = tile_count(tile, npre, pre_end, B2);
         const bool sh = k0 < a.P_sh;
+        if (n == kKeys && !sh) {   // a full tile of the own cache: no per-chunk test
+            const char* vt = reinterpret_cast<const char*>(vbase + k0);
+#pragma unroll
+            for (int j = 0; j < NI; ++j)
+                __builtin_amdgcn_global_load_lds((glb_ptr)(vt + voff[j]), (lds_ptr)(dst + (wave * NI + j) * 1024),
+                                                 16, 0, 0);
+            return;
+        }
         const KVT* vb = sh ? vbase_sh : vbase;
         const int vcap = sh ? a.cap_sh : cap;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int q = (wave * NI + j) * 64 + lane;
-            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ (d & 7);
+            const int d = q / (kKeys / 8), c = (q % (kKeys / 8)) ^ vswz(d);
             const KVT* src = vb + (size_t)d * vcap + k0 + 8 * c;
             if (n == kKeys || 8 * c + 8 <= n) {
                 __builtin_amdgcn_global_load_lds((glb_ptr)src, (lds_ptr)(dst + (wave * NI + j) * 1024), 16, 0, 0);
@@ -309,8 +352,17 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
         }
     }
     const float sl2 = a.scale * kLog2e;
-    // K row this lane supplies to the S^T MFMAs: key pi(lr) of each 32-key block
-    const int krow = (lr & ~12) | ((lr & 4) << 1) | ((lr & 8) >> 1);
+    // K row this lane supplies to the S^T MFMAs: key pi(lr) of each 32-key
+    // block.  Operand addresses inside a stage: K chunk 2c + eta of key block
+    // kb is at kaddr0 ^ 32c, plus kb * 32 rows (kswz repeats every 32 rows);
+    // V^T chunk 2st + eta of dim block d at (vaddr0 ^ 32 (st ^ 2 (d & 1))) +
+    // d * 32 rows (vswz(32 + x) = vswz(x) ^ 4 for x < 32).  The XOR touches
+    // bits 5-6 (5-7) only, below a row and above the eta chunk, and the stage
+    // bases are multiples of 16 KB, so base + (addr0 ^ m) = (base + addr0) ^ m:
+    // a step adds the stage base once per operand and XORs per chunk, and the
+    // block steps are immediate offsets.
+    const int krow = swap23(lr);
+    const uint32_t kaddr0 = 16 * kslot<DH>(krow, eta), vaddr0 = 16 * vslot(lr, eta);
 
     floatx16 o[DH / 32];
 #pragma unroll
@@ -325,12 +377,13 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     // (left to itself the compiler waits for each read right before its MFMA).
     auto scores = [&](const char* ks, floatx16 (&sc)[2]) __attribute__((always_inline)) {
         constexpr int NC = DH / 16;
+        const uint32_t kb0 = (uint32_t)(ks - smem) + kaddr0;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             bf16x8 kf[NC];
 #pragma unroll
             for (int c = 0; c < NC; ++c)
-                kf[c] = *reinterpret_cast<const bf16x8*>(ks + 16 * kslot<DH>(32 * kb + krow, 2 * c + eta));
+                kf[c] = *reinterpret_cast<const bf16x8*>(smem + ((kb0 ^ (32u * c)) + kb * 32 * DH * 2));
 #pragma unroll
             for (int v = 0; v < 16; ++v) sc[kb][v] = 0.f;
 #pragma unroll
@@ -387,12 +440,14 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
         l_run += psum;
         // O^T += V^T * P^T: step st = 2kb + hh covers keys 16st + [0, 16); the
         // lane's 8 probabilities are keys 16st + 8eta + [0, 8), V^T chunk 2st + eta
+        const uint32_t vb0 = (uint32_t)(vs - smem) + vaddr0;
 #pragma unroll
         for (int d = 0; d < DH / 32; ++d) {
             bf16x8 vf[4];
 #pragma unroll
             for (int st = 0; st < 4; ++st)
-                vf[st] = *reinterpret_cast<const bf16x8*>(vs + 16 * vslot(32 * d + lr, 2 * st + eta));
+                vf[st] = *reinterpret_cast<const bf16x8*>(
+                    smem + ((vb0 ^ (32u * (st ^ (2 * (d & 1))))) + d * 32 * kKeys * 2));
 #pragma unroll
             for (int st = 0; st < 4; ++st) o[d] = mfma32x32x16(vf[st], pb[st >> 1][st & 1], o[d]);
             __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
