@@ -425,6 +425,45 @@ def full_step_configs(eng8b, steps=6):
         res["tokens_committed_note"] = f"{nblocks} blocks x (prefill + {S_b} steps), {r_tok} tokens/step as reported"
         return res
 
+    def library_gemm_us(M, N, K, reps=20):
+        """torch.matmul (hipBLASLt) of bf16 [M, K] x [K, N], weight copies
+        rotated through >= 600 MB so that no launch finds its weights cached."""
+        g = torch.Generator(device="cuda").manual_seed(7)
+        x = torch.randn(M, K, generator=g, device="cuda").bfloat16()
+        ncopy = max(2, -(-600 * 2**20 // (N * K * 2)))
+        ws = [torch.randn(K, N, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        y = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+        for i in range(3):
+            torch.matmul(x, ws[i % ncopy], out=y)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(reps):
+            torch.matmul(x, ws[i % ncopy], out=y)
+        e1.record()
+        torch.cuda.synchronize()
+        del ws
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    def versus_library(dims, rows, bd):
+        """Each projection's kernel time per launch in the step (its traced
+        class time over the layers; QKV with RoPE and the cache writes, O and
+        down as split-K partials, gate/up with SwiGLU) beside a plain library
+        GEMM of the same shape."""
+        qd, kd = dims.n_heads * dims.head_dim, dims.n_kv_heads * dims.head_dim
+        shapes = {"gemm_qkv": (qd + 2 * kd, dims.d_model), "gemm_o": (dims.d_model, qd),
+                  "gemm_gate_up": (2 * dims.ffn_dim, dims.d_model), "gemm_down": (dims.d_model, dims.ffn_dim)}
+        res = []
+        for nm, (N, K) in shapes.items():
+            ours = bd[nm] / dims.n_layers * 1e3
+            lib = library_gemm_us(rows, N, K)
+            fl = 2.0 * rows * N * K
+            res.append({"gemm": nm[5:], "M": rows, "N": N, "K": K, "ours_us": round(ours, 1),
+                        "hipblaslt_us": round(lib, 1), "ours_over_hipblaslt": round(ours / lib, 3),
+                        "ours_mfma_frac": round(fl / (ours * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                        "hipblaslt_mfma_frac": round(fl / (lib * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4)})
+        return res
+
     out = {}
     # ---- 7B GQA shape
     d7 = synth.DREAM7B
@@ -441,6 +480,7 @@ def full_step_configs(eng8b, steps=6):
                                       "candidate fraction 0.3, prefix KV cache", **r7}
     del eng7, ids
     torch.cuda.empty_cache()
+    vs_lib = {"dream7b_gqa_1024_rows": versus_library(d7, 8 * 2 * 64, r7["breakdown_ms_per_step"])}
     # ---- multimodal prefix at the 8B shape (weights shared with the headline engine)
     d8 = synth.LLADA8B
     b, B, n_img, n_txt, gen = 32, 32, 576, 256, 128
@@ -456,6 +496,8 @@ def full_step_configs(eng8b, steps=6):
                                         "candidate fraction 0.1 / 0.3 / 0.5, prefix KV cache", **rm}
     del engm
     torch.cuda.empty_cache()
+    vs_lib["multimodal_8b_2048_rows"] = versus_library(d8, 32 * 2 * 32, rm["breakdown_ms_per_step"])
+    out["gemm_vs_hipblaslt"] = vs_lib
     # the same workload with the FP8 (E4M3) KV cache
     d8f = synth.with_fp8_kv(d8)
     engf = dard.Engine(d8f, None, b, B, prompt + gen + B, packed=eng8b.packed)
@@ -856,7 +898,8 @@ def profile_ops():
     fraction 0.3), 10 at the 8B MHA shape (32 x 128, batch 16, prefix 512,
     block 32, fraction 0.25), 10 confidence reductions over 696 x 152064
     fp32 logits, 3 steps of the 7B GQA model truncated to 2 layers at batch 8
-    (1024 token rows: the large-tile GEMMs), then a 1 GiB copy."""
+    (1024 token rows: the large-tile GEMMs), 3 library GEMMs (torch.matmul) of
+    each of its four projection shapes at 1024 rows, then a 1 GiB copy."""
     import torch
 
     from paper_2608_26574_amd import dard, synth
@@ -909,6 +952,21 @@ def profile_ops():
         eng.dard_step(P, params, tok, state, conf, t_out, s_out, c_out)
     torch.cuda.synchronize()
     log("[ops] 7B GQA steps done")
+    del eng
+    torch.cuda.empty_cache()
+    # the library's GEMMs (torch.matmul, hipBLASLt) on the same step shapes
+    # (1024 rows), weight copies rotated through >= 600 MB, 3 calls each
+    g = torch.Generator(device="cuda").manual_seed(7)
+    for N, K in ((4608, 3584), (3584, 3584), (37888, 3584), (3584, 18944)):
+        x = torch.randn(1024, K, generator=g, device="cuda").bfloat16()
+        ncopy = max(2, -(-600 * 2**20 // (N * K * 2)))
+        ws = [torch.randn(K, N, generator=g, device="cuda").bfloat16() for _ in range(ncopy)]
+        y = torch.empty(1024, N, device="cuda", dtype=torch.bfloat16)
+        for i in range(3):
+            torch.matmul(x, ws[i % ncopy], out=y)
+        torch.cuda.synchronize()
+        del ws
+    log("[ops] library GEMMs done")
     _copy_calibration("ops")
     return 0
 
