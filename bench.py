@@ -239,7 +239,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: seeded random-init weights N(0, 0.02), uniform prompt ids, drawn token states",
-        "config": {"workload": "llada8b-like full DARD step: 32 layers, d 4096, 32x128 MHA, FFN 12288, "
+        "config": {"workload": f"llada8b-like full DARD step: {dims.n_layers} layers, d 4096, 32x128 MHA, FFN 12288, "
                                "vocab 126464, bf16; batch 1, prompt 512, generation 256, block 32, "
                                "candidate fraction 0.25, prefix KV cache",
                    "batch": b, "block": B, "prompt": prompt, "gen_len": gen, "cand_frac": frac,
