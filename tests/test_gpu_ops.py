@@ -71,7 +71,8 @@ def test_state_mask_bit_exact(B, flags):
 
 
 # ---------------------------------------------------------------- attention
-def _attn_case(b, B, P, Hq, Hkv, dh, dtype, cand_frac, seed, flags=0, cap_extra=3):
+def _attn_case(b, B, P, Hq, Hkv, dh, dtype, cand_frac, seed, flags=0, cap_extra=3, sample=None):
+    """Max |GPU - oracle| over the sequences in `sample` (all by default)."""
     cap = P + 2 * B + cap_extra
     td = torch.bfloat16 if dtype == "bf16" else torch.float32
     q, k, v = synth.qkv(b, 2 * B, Hq, Hkv, dh, cap, seed=seed, dtype=td)
@@ -88,12 +89,12 @@ def _attn_case(b, B, P, Hq, Hkv, dh, dtype, cand_frac, seed, flags=0, cap_extra=
                                scale, flags, out, ws)
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
-    qn, kn, vn = q.double().numpy(), k.double().numpy(), v.double().numpy()
     worst = 0.0
-    for s in range(b):
+    for s in (range(b) if sample is None else sample):
+        qn, kn, vn = q[s].double().numpy(), k[s].double().numpy(), v[s].double().numpy()
         vis = O.visible_keys(state[s], conf[s], P, flags)
-        ref = O.masked_attention(qn[s], kn[s, :, :P + 2 * B].transpose(1, 0, 2),
-                                 vn[s, :, :P + 2 * B].transpose(1, 0, 2), vis, scale, Hkv)
+        ref = O.masked_attention(qn, kn[:, :P + 2 * B].transpose(1, 0, 2),
+                                 vn[:, :P + 2 * B].transpose(1, 0, 2), vis, scale, Hkv)
         worst = max(worst, float(np.max(np.abs(got[s] - ref))))
     return worst
 
@@ -104,6 +105,25 @@ def test_attention_llada_shape(b, frac):
     """The isolated attention workload: 32 heads x 128, prompt 512, block 32."""
     announce("attention 8B-shape", b, frac)
     err = _attn_case(b, 32, 512, 32, 32, 128, "bf16", frac, seed=b * 10 + int(frac * 100))
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("P", [608, 736])
+def test_attention_headline_step_prefixes(P):
+    """The 8B step's attention at the longer prefixes of its generation (batch 1,
+    32 heads x 128, block 32): 11 and 13 key tiles, split 4 and 5 ways."""
+    announce("attention 8B step prefix", P)
+    err = _attn_case(1, 32, P, 32, 32, 128, "bf16", 0.25, seed=P)
+    assert err < 2e-2, err
+
+
+@pytest.mark.parametrize("P", [832, 928])
+def test_attention_multimodal_batch32(P):
+    """The multimodal step's attention (batch 32, 32 heads x 128, block 32,
+    576 image + 256 text prefix positions and committed blocks), compared on
+    sampled sequences (the first, a middle and the last)."""
+    announce("attention multimodal batch 32", P)
+    err = _attn_case(32, 32, P, 32, 32, 128, "bf16", 0.3, seed=P, sample=(0, 13, 31))
     assert err < 2e-2, err
 
 
