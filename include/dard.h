@@ -340,8 +340,10 @@ dard_status dard_prefill(const dard_dims* dims, const void* packed, void* kv, in
  *   margin under ORDER_ENTROPY / ORDER_MARGIN), block_done [b] int32.
  * Outputs may alias the matching inputs.  `dbg`, when not NULL, receives
  * copies of intermediate results (any member may be NULL).
- * Rows of the LM head: with at most 64 rows per step (b * 2B <= 64, logit
- * mixing) the head runs over all of them; otherwise only over the rows the
+ * Rows of the LM head: for a bf16 model with at most 64 rows per step
+ * (b * 2B <= 64) and logit mixing, the head runs over all of them (its
+ * weight-streaming kernel reads the weights once either way); otherwise
+ * (fp32 models included) only over the rows the
  * decisions read -- the shadow row of every position and the x row of every
  * M position (with HIDDEN_MIX: the shadow rows of C and U positions and the
  * mixed row of every M position, which takes the M position's shadow slot).
