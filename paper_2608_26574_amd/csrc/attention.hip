@@ -314,6 +314,13 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
     auto kst = [&](int i) __attribute__((always_inline)) { return gbase + (i % 3) * L::TILE; };
     auto vst = [&](int i) __attribute__((always_inline)) { return gbase + (3 + (i & 1)) * L::TILE; };
     auto tile_of = [&](int it) __attribute__((always_inline)) { return t_begin + grp + G * it; };
+    // A ragged K tile's copies skip the rows past its end, so a wave may issue
+    // fewer than NI of them; the end-of-step wait then counts on the newest K
+    // tile's NI copies only when that tile is full, and otherwise waits for
+    // every copy (an older copy must never be left in flight at the barrier).
+    auto full_tile = [&](int tile) __attribute__((always_inline)) {
+        return tile_count(tile, npre, pre_end, B2) == kKeys;
+    };
     auto mine = [&](int it) __attribute__((always_inline)) { return it < iters && tile_of(it) < t_end; };
     if (mine(0)) {
         issue_k(tile_of(0), kst(0));
@@ -489,7 +496,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
                 if (ahead) commit_k8(tile_of(it + 2), kst(it + 2));
                 __builtin_amdgcn_s_waitcnt(0);
             } else {
-                if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+                if (ahead && full_tile(tile_of(it + 2))) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
                 else __builtin_amdgcn_s_waitcnt(0);
             }
             wg_barrier();
@@ -514,7 +521,7 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
                 if (ahead) commit_k8(tile_of(it + 3), kst(it + 3));
                 __builtin_amdgcn_s_waitcnt(0);
             } else {
-                if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
+                if (ahead && full_tile(tile_of(it + 3))) __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));
                 else __builtin_amdgcn_s_waitcnt(0);
             }
             wg_barrier();
