@@ -154,8 +154,11 @@ typedef struct {
  * embedding of the rotate-half form (rope_theta), multi-head / grouped-query
  * attention, SwiGLU feed-forward, no biases, untied LM head.
  * Supported: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
- * d_model == n_heads * head_dim; bf16 needs d_model, ffn_dim % 64 == 0 and
- * vocab % 16 == 0; max_pos bounds prefix + block positions. */
+ * d_model == n_heads * head_dim; d_model <= 8192; bf16 needs d_model,
+ * ffn_dim % 64 == 0, vocab % 16 == 0 and every weight matrix under 4 GiB
+ * (vocab * d_model, 2 * ffn_dim * d_model and (n_heads + 2 n_kv_heads) *
+ * head_dim * d_model values of 2 bytes); max_pos bounds prefix + block
+ * positions.  Other shapes are refused with DARD_ERR_SHAPE. */
 typedef struct {
     int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, max_pos;
     int32_t dtype;    /* DARD_DTYPE_F32 or DARD_DTYPE_BF16 */

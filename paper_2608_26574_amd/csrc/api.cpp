@@ -56,6 +56,17 @@ int check_dims(const dard_dims* d) {
     if (d->dtype == DARD_DTYPE_BF16 && (d->d_model % 64 || d->ffn_dim % 64 || d->vocab % 16))
         return fail(DARD_ERR_SHAPE, "bf16 needs d_model, ffn_dim %% 64 == 0 and vocab %% 16 == 0");
     if (d->d_model > 8192) return fail(DARD_ERR_SHAPE, "d_model must be <= 8192");
+    if (d->dtype == DARD_DTYPE_BF16) {
+        // the pipelined GEMM (65-255 rows) addresses a weight matrix through a
+        // buffer descriptor: 32-bit byte offsets, so every matrix stays under 4 GiB
+        const size_t D = d->d_model, F = d->ffn_dim, V = d->vocab;
+        const size_t qkv = (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim;
+        size_t most = V * D;
+        most = 2 * F * D > most ? 2 * F * D : most;
+        most = qkv * D > most ? qkv * D : most;
+        if (most * 2 > 0xFFFFFFFFull)
+            return fail(DARD_ERR_SHAPE, "bf16 weight matrices must be under 4 GiB (largest: %zu bytes)", most * 2);
+    }
     if (d->dtype == DARD_DTYPE_F32 && (d->d_model % 4 || d->ffn_dim % 4 || d->vocab % 4))
         return fail(DARD_ERR_SHAPE, "f32 needs d_model, ffn_dim, vocab %% 4 == 0");
     if (!(d->norm_eps >= 0.f) || !(d->rope_theta > 0.f)) return fail(DARD_ERR_ARG, "bad norm_eps / rope_theta");

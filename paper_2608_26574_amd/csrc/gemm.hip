@@ -353,10 +353,12 @@ __global__ __launch_bounds__(256, WN <= 4 ? 2 : 1) void gemm_pipe_bf16(const bf1
     // Loads go through buffer descriptors (base and size in scalar registers,
     // 32-bit byte offsets per lane; the hardware returns 0 past the size).
     static_assert(T::CHW % 256 == 0, "a thread's chunks are all weight or all activation");
-    const __amdgpu_buffer_rsrc_t rw =
-        __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, (int)((size_t)NB * KU * 2048), 0x00020000);
-    const __amdgpu_buffer_rsrc_t rx =
-        __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, (int)((size_t)MB * KU * 2048), 0x00020000);
+    // (the library rejects bf16 weight matrices of 4 GiB or more, so the byte
+    // counts fit the descriptors' 32-bit record field)
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)W, (short)0, (int)(uint32_t)((size_t)NB * KU * 2048), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)X, (short)0, (int)(uint32_t)((size_t)MB * KU * 2048), 0x00020000);
     uint32_t off[T::PER];
 #pragma unroll
     for (int i = 0; i < T::PER; ++i) {

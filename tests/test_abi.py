@@ -108,6 +108,13 @@ def test_dims_validation_and_sizes():
     assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
     bad = dard.make_dims(synth.Dims(2, 4096, 32, 32, 128, 12288, 126460, 64, "bf16"))
     assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
+    # a bf16 weight matrix of 4 GiB or more (LM head 262144 x 8192) is refused:
+    # the pipelined GEMM addresses weights with 32-bit byte offsets
+    bad = dard.make_dims(synth.Dims(2, 8192, 64, 8, 128, 28672, 262144, 64, "bf16"))
+    assert L.dard_packed_weight_bytes(ctypes.byref(bad)) == 0
+    assert b"4 GiB" in L.dard_last_error()
+    ok = dard.make_dims(synth.Dims(2, 8192, 64, 8, 128, 28672, 131072, 64, "bf16"))
+    assert L.dard_packed_weight_bytes(ctypes.byref(ok)) > 0
 
 
 def test_attention_workspace_sizing():
