@@ -9,9 +9,9 @@ the GPU committed (the prefix-cache reading of App. C.5).  The oracle runs
 each step on the same inputs the GPU step received, so the comparison covers
 the GPU's own trajectory through several blocks, including the re-prefill
 with decoded tokens; every step goes through the decision-parity protocol
-(op level exact, step level exact wherever the margins decide).  Tiny fp32
-model with the LM head sharpened so that confidences pass tau_u and blocks
-complete."""
+(op level exact, step level exact wherever the margins decide).  The tiny
+fp32 model and a small bf16 one, each with the LM head sharpened so that
+confidences pass tau_u and blocks complete."""
 import numpy as np
 import pytest
 import torch
@@ -23,19 +23,28 @@ from parity import P, announce, check_decisions, collect, cparams, dev, logit_er
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("flags", [O.F_PROGRESS, O.F_PROGRESS | O.F_ORDER_ENTROPY, O.F_PROGRESS | O.F_HIDDEN_MIX])
-def test_decoding_loop_tiny_fp32(flags):
-    dims = synth.TINY
-    b, B, P0, nblocks, lm_scale = 2, 16, 24, 3, 40.0
-    announce("decoding loop, tiny fp32", flags)
-    w = sharpen(synth.make_weights(dims, seed=31), lm_scale)
+SMALL_BF16 = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 512, "bf16")
+
+
+@pytest.mark.parametrize("dims,lm_scale,flags,seed", [
+    (synth.TINY, 40.0, O.F_PROGRESS, 31),
+    (synth.TINY, 40.0, O.F_PROGRESS | O.F_ORDER_ENTROPY, 31),
+    (synth.TINY, 40.0, O.F_PROGRESS | O.F_HIDDEN_MIX, 31),
+    # bf16, grouped-query heads (4 on 2), head_dim 128
+    (SMALL_BF16, 48.0, O.F_PROGRESS, 41),
+])
+def test_decoding_loop(dims, lm_scale, flags, seed):
+    b, B, P0, nblocks = 2, 16, 24, 3
+    announce("decoding loop", dims.dtype, lm_scale, flags)
+    fp32 = dims.dtype == "f32"
+    w = sharpen(synth.make_weights(dims, seed=seed), lm_scale)
     cap = P0 + B * nblocks + 2 * B
     eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, cap)
     ow = synth.OracleWeights(dims, w)
     dd = dims.as_dict()
     prm = P(dims.mask_id, flags)
-    seq = synth.prompt_ids(b, P0, dims.vocab, seed=32)
-    steps, done_blocks, excluded, committed_u = [], 0, 0, 0
+    seq = synth.prompt_ids(b, P0, dims.vocab, seed=seed + 1)
+    steps, done_blocks, excluded, committed_u, total = [], 0, 0, 0, 0
     for k in range(nblocks):
         Pk = seq.shape[1]
         eng.dard_prefill(dev(seq))
@@ -52,9 +61,11 @@ def test_decoding_loop_tiny_fp32(flags):
             ref = O.dard_step(ow, dd, cache, tok, state, conf, prm)
             err = logit_err(got, ref, state, prm)
             # the sharpened head multiplies every upstream rounding difference by lm_scale
-            assert err < 1e-4 * lm_scale, (k, n, err)
+            assert err < (1e-4 if fp32 else 2e-2) * lm_scale, (k, n, err)
             _, excl, _ = check_decisions(tok, state, got, ref, prm, f"loop block {k} step {n}")
+            assert fp32 or excl <= state.size // 4, (k, n, excl)
             excluded += excl
+            total += state.size
             n += 1
             tok, state, conf = got["tok_out"], got["state_out"], got["conf_out"]
             if np.all(got["block_done"] == 1) or n >= 2 * B:
@@ -68,11 +79,14 @@ def test_decoding_loop_tiny_fp32(flags):
           f"excluded positions {excluded}", flush=True)
     # the loop really decodes: blocks finish and commit their tokens
     assert done_blocks >= 1 and committed_u >= B, (steps, done_blocks, committed_u)
-    assert excluded <= 2, excluded
+    # fp32: at most two positions left to the margins over the whole loop; bf16:
+    # at most 10 % (the per-step bound of the workload shapes)
+    assert excluded <= (2 if fp32 else total // 10), (excluded, total)
     if excluded == 0:
         # no decision was left to the margins: the oracle decoding on its own
         # produces the same sequence in the same number of steps
-        ref_seq, ref_steps = oracle_loop(ow, dd, prm, synth.prompt_ids(b, P0, dims.vocab, seed=32), B, nblocks)
+        ref_seq, ref_steps = oracle_loop(ow, dd, prm, synth.prompt_ids(b, P0, dims.vocab, seed=seed + 1), B,
+                                         nblocks)
         assert ref_steps == steps, (ref_steps, steps)
         assert np.array_equal(ref_seq, seq)
 
