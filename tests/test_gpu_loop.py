@@ -112,3 +112,64 @@ def oracle_loop(ow, dd, prm, seq, B, nblocks):
         steps.append(n)
         seq = np.concatenate([seq, tok.astype(seq.dtype)], axis=1)
     return seq, steps
+
+
+@pytest.mark.parametrize("flags", [O.F_PROGRESS, O.F_PROGRESS | O.F_ORDER_L2R])
+def test_decoding_loop_full_sequence(flags):
+    """The loop in full-sequence mode (no prefix cache; the setting of the
+    paper's latency table): the sequence holds the prompt, the blocks decoded
+    so far, the current block's tokens and [Mask] after it; each step runs on
+    the whole sequence and writes the block's new tokens back into it."""
+    dims, lm_scale, seed = synth.TINY, 40.0, 31
+    b, B, P0, nblocks = 2, 16, 24, 3
+    announce("decoding loop, full sequence", flags)
+    w = sharpen(synth.make_weights(dims, seed=seed), lm_scale)
+    N = P0 + nblocks * B
+    eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, N + B)
+    ow = synth.OracleWeights(dims, w)
+    dd = dims.as_dict()
+    prm = P(dims.mask_id, flags)
+    seq = np.full((b, N), dims.mask_id, dtype=np.int32)
+    seq[:, :P0] = synth.prompt_ids(b, P0, dims.vocab, seed=seed + 1)
+    start = seq.copy()
+    steps, excluded = [], 0
+    for k in range(nblocks):
+        blk = P0 + k * B
+        state = np.zeros((b, B), dtype=np.uint8)
+        conf = np.zeros((b, B), dtype=np.float32)
+        n = 0
+        while True:
+            out, dbg = step_buffers(b, B, dims.vocab)
+            eng.dard_step_full(blk, cparams(dard, prm), dev(seq), dev(state), dev(conf), out["tok_out"],
+                               out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+            got = collect(out, dbg)
+            ref = O.dard_step_full(ow, dd, seq, blk, B, state, conf, prm)
+            err = logit_err(got, ref, state, prm)
+            assert err < 1e-4 * lm_scale, (k, n, err)
+            _, excl, _ = check_decisions(seq[:, blk:blk + B], state, got, ref, prm, f"full loop block {k} step {n}")
+            excluded += excl
+            n += 1
+            seq[:, blk:blk + B] = got["tok_out"]
+            state, conf = got["state_out"], got["conf_out"]
+            if np.all(got["block_done"] == 1) or n >= 2 * B:
+                break
+        steps.append(n)
+    print(f"full-sequence loop flags {flags}: steps per block {steps}, excluded positions {excluded}", flush=True)
+    assert excluded <= 2, excluded
+    if excluded == 0:
+        ref_seq, ref_steps = start.copy(), []
+        for k in range(nblocks):
+            blk = P0 + k * B
+            state = np.zeros((b, B), dtype=np.uint8)
+            conf = np.zeros((b, B), dtype=np.float32)
+            n = 0
+            while True:
+                ref = O.dard_step_full(ow, dd, ref_seq, blk, B, state, conf, prm)
+                n += 1
+                ref_seq[:, blk:blk + B] = ref["tok_out"]
+                state, conf = ref["state_out"].astype(np.uint8), ref["conf_out"].astype(np.float32)
+                if np.all(ref["block_done"] == 1) or n >= 2 * B:
+                    break
+            ref_steps.append(n)
+        assert ref_steps == steps, (ref_steps, steps)
+        assert np.array_equal(ref_seq, seq)
