@@ -173,3 +173,53 @@ def test_decoding_loop_full_sequence(flags):
             ref_steps.append(n)
         assert ref_steps == steps, (ref_steps, steps)
         assert np.array_equal(ref_seq, seq)
+
+
+def test_decoding_loop_shared_prompt():
+    """The loop with one prompt cached for the whole batch: at every block
+    boundary only each sequence's decoded blocks are prefilled after the
+    shared prompt (dard_prefill_suffix), and the steps read the shared cache
+    in place (dard_step_shared)."""
+    dims, lm_scale, seed = synth.TINY, 24.0, 37
+    b, B, Ps, nblocks = 2, 16, 64, 3
+    flags = O.F_PROGRESS
+    announce("decoding loop, shared prompt")
+    w = sharpen(synth.make_weights(dims, seed=seed), lm_scale)
+    sh = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, 1, B, Ps)
+    eng = dard.Engine(dims, None, b, B, Ps + nblocks * B + 2 * B, packed=sh.packed)
+    ow = synth.OracleWeights(dims, w)
+    dd = dims.as_dict()
+    prm = P(dims.mask_id, flags)
+    prompt = synth.prompt_ids(1, Ps, dims.vocab, seed=seed + 1)
+    sh.dard_prefill(dev(prompt))
+    shared = O.prefill(ow, dd, prompt)
+    committed = np.zeros((b, 0), dtype=np.int32)
+    steps, excluded = [], 0
+    for k in range(nblocks):
+        Pc = committed.shape[1]
+        if Pc:
+            eng.dard_prefill_suffix(sh, Ps, dev(committed))
+        cache = O.join_shared(shared, O.prefill_suffix(ow, dd, shared, committed))
+        tok = np.full((b, B), dims.mask_id, dtype=np.int32)
+        state = np.zeros((b, B), dtype=np.uint8)
+        conf = np.zeros((b, B), dtype=np.float32)
+        n = 0
+        while True:
+            out, dbg = step_buffers(b, B, dims.vocab)
+            eng.dard_step_shared(sh, Ps, Ps + Pc, cparams(dard, prm), dev(tok), dev(state), dev(conf),
+                                 out["tok_out"], out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+            got = collect(out, dbg)
+            ref = O.dard_step(ow, dd, cache, tok, state, conf, prm)
+            err = logit_err(got, ref, state, prm)
+            assert err < 1e-4 * lm_scale, (k, n, err)
+            _, excl, _ = check_decisions(tok, state, got, ref, prm, f"shared loop block {k} step {n}")
+            excluded += excl
+            n += 1
+            tok, state, conf = got["tok_out"], got["state_out"], got["conf_out"]
+            if np.all(got["block_done"] == 1) or n >= 2 * B:
+                break
+        steps.append(n)
+        committed = np.concatenate([committed, tok.astype(np.int32)], axis=1)
+    print(f"shared-prompt loop: steps per block {steps}, excluded positions {excluded}", flush=True)
+    assert excluded <= 2, excluded
+    assert sum(s < 2 * B for s in steps) >= 1, steps   # at least one block finishes
