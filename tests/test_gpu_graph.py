@@ -1,0 +1,76 @@
+"""A DARD step captured in a HIP graph (torch.cuda.CUDAGraph over the
+library's launches) and replayed: dard_step makes no host synchronisation,
+allocation or memset, so the captured step must reproduce the eager step
+exactly.  The replays alternate two sets of inputs written into the captured
+input tensors, with eager steps, zeroed outputs and synchronisations between
+them, and every replay is compared bit for bit with the eager step on the same
+inputs."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_26574_amd import dard, synth
+from parity import P, announce, cparams, dev, sharpen
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("case", [
+    # 8B shape, 2 layers, batch 1: weight-streaming GEMMs, split-key attention and its combine
+    dict(dims=("llada8b", 2), b=1, B=32, P=544, frac=0.25, scale=6.0),
+    # 7B GQA shape, 1 layer, batch 4 (256 step rows): large-tile GEMMs, the fused LM-head partials
+    dict(dims=("dream7b", 1), b=4, B=64, P=160, frac=0.3, scale=6.0),
+])
+def test_step_graph_replay(case):
+    name, layers = case["dims"]
+    dims = synth.truncated(synth.LLADA8B if name == "llada8b" else synth.DREAM7B, layers)
+    b, B, P_ = case["b"], case["B"], case["P"]
+    announce("graph replay", name, layers, b, B, P_)
+    w = sharpen(synth.make_weights(dims, seed=51, device="cuda"), case["scale"])
+    eng = dard.Engine(dims, w, b, B, P_ + 2 * B)
+    del w
+    eng.dard_prefill(dev(synth.prompt_ids(b, P_, dims.vocab, seed=52)))
+    params = cparams(dard, P(dims.mask_id))
+    inputs = [tuple(dev(a) for a in synth.workload_block(b, B, case["frac"], dims.vocab, seed=53 + k))
+              for k in range(2)]
+
+    def outputs():
+        return (torch.zeros(b, B, dtype=torch.int32, device="cuda"), torch.zeros(b, B, dtype=torch.uint8, device="cuda"),
+                torch.zeros(b, B, device="cuda"), torch.zeros(b, dtype=torch.int32, device="cuda"))
+
+    # eager reference of each input set
+    ref = []
+    for tok, st, cf in inputs:
+        o = outputs()
+        eng.dard_step(P_, params, tok, st, cf, *o)
+        ref.append(o)
+    torch.cuda.synchronize()
+    # the two input sets must lead to different decisions, or the replays would prove nothing
+    assert not all(torch.equal(x, y) for x, y in zip(ref[0][:3], ref[1][:3]))
+
+    # capture one step on static tensors
+    s_tok, s_st, s_cf = (t.clone() for t in inputs[0])
+    s_out = outputs()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        eng.dard_step(P_, params, s_tok, s_st, s_cf, *s_out)
+    torch.cuda.synchronize()
+
+    scratch = outputs()
+    for r, k in enumerate((0, 1, 1, 0, 1)):
+        # eager work between replays: a step on the other inputs, the outputs zeroed
+        tok, st, cf = inputs[1 - k]
+        eng.dard_step(P_, params, tok, st, cf, *scratch)
+        for t in s_out:
+            t.zero_()
+        for dst, src in zip((s_tok, s_st, s_cf), inputs[k]):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want, what in zip(s_out, ref[k], ("tok_out", "state_out", "conf_out", "block_done")):
+            assert torch.equal(got, want), (r, k, what)
+        for got, want in zip(scratch, ref[1 - k]):
+            assert torch.equal(got, want), (r, "eager step between replays")
+    print(f"graph replay {name} x{layers}: 5 replays equal the eager steps", flush=True)
