@@ -74,3 +74,43 @@ def test_step_graph_replay(case):
         for got, want in zip(scratch, ref[1 - k]):
             assert torch.equal(got, want), (r, "eager step between replays")
     print(f"graph replay {name} x{layers}: 5 replays equal the eager steps", flush=True)
+
+
+def test_steps_on_two_streams():
+    """Two engines stepping on two streams at once (default priority) give the
+    same results as each engine alone: a step keeps all of its state in the
+    caller's workspace and KV cache, none in the library."""
+    dims = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 512, "bf16")
+    b, B, P_ = 2, 32, 96
+    announce("two streams")
+    engines, inputs = [], []
+    for k in range(2):
+        w = sharpen(synth.make_weights(dims, seed=61 + k, device="cuda"), 12.0)
+        eng = dard.Engine(dims, w, b, B, P_ + 2 * B)
+        eng.dard_prefill(dev(synth.prompt_ids(b, P_, dims.vocab, seed=63 + k)))
+        engines.append(eng)
+        inputs.append(tuple(dev(a) for a in synth.workload_block(b, B, 0.3, dims.vocab, seed=65 + k)))
+    params = cparams(dard, P(dims.mask_id))
+
+    def outputs():
+        return (torch.zeros(b, B, dtype=torch.int32, device="cuda"), torch.zeros(b, B, dtype=torch.uint8, device="cuda"),
+                torch.zeros(b, B, device="cuda"), torch.zeros(b, dtype=torch.int32, device="cuda"))
+
+    alone = []
+    for eng, inp in zip(engines, inputs):
+        o = outputs()
+        eng.dard_step(P_, params, *inp, *o)
+        torch.cuda.synchronize()
+        alone.append(o)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    together = [[outputs() for _ in range(4)] for _ in range(2)]
+    torch.cuda.synchronize()
+    for r in range(4):
+        for k in range(2):
+            with torch.cuda.stream(streams[k]):
+                engines[k].dard_step(P_, params, *inputs[k], *together[k][r])
+    torch.cuda.synchronize()
+    for k in range(2):
+        for r in range(4):
+            for got, want in zip(together[k][r], alone[k]):
+                assert torch.equal(got, want), (k, r)
