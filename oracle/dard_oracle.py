@@ -384,6 +384,32 @@ def prefill_suffix(weights, dims, shared, ids, embeds=None):
     return cache
 
 
+def prefill_extend(weights, dims, cache, ids):
+    """Extend-only refresh of a per-sequence prefix cache at a block boundary
+    (an approximation of the refresh at a block start, whose exact form is
+    ``prefill`` over the prompt and the committed blocks; prefix caching is
+    App. C.5, attention overhead): only the new positions P..P+Pn-1 of each
+    sequence go through the model, each of their rows seeing the sequence's
+    P cached keys and the new positions, bidirectionally among those; the
+    cached keys are kept as they are.
+
+    cache: per layer (K, V) of the prefix, each [b, P, Hkv, dh].  ids: [b, Pn].
+    Returns per layer (K, V) of the extended prefix, each [b, P + Pn, Hkv, dh].
+    """
+    ids = np.asarray(ids)
+    b, Pn = ids.shape
+    P = cache[0][0].shape[1] if dims["n_layers"] > 0 else 0
+    h = to_f32(embed_rows(weights, dims, ids))
+    pos = P + np.arange(Pn)
+    scale = 1.0 / math.sqrt(dims["head_dim"])
+    allvis = np.ones((Pn, P + Pn), dtype=bool)
+    out = []
+    for layer in range(dims["n_layers"]):
+        h, (k, v) = _layer(weights["layers"][layer], dims, h, pos, cache[layer], lambda bi: allvis, scale)
+        out.append((np.concatenate([cache[layer][0], k], axis=1), np.concatenate([cache[layer][1], v], axis=1)))
+    return out
+
+
 def join_shared(shared, suffix):
     """Per-sequence prefix cache [b, Ps + Pc] from the shared prompt's cache
     (broadcast over the batch) followed by each sequence's suffix."""
