@@ -330,6 +330,23 @@ dard_status dard_prefill(const dard_dims* dims, const void* packed, void* kv, in
                          int b, int P, const int32_t* ids, const void* embeds,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* Extend-only refresh of the prefix cache at a block boundary (an
+ * approximation; the exact refresh runs dard_prefill over the prompt and the
+ * committed blocks again): only the Pn new positions P..P+Pn-1 of each
+ * sequence -- the block just committed -- are run through the model, each of
+ * their rows seeing the P cached keys of its own sequence and the Pn new
+ * positions (bidirectionally among the new ones), and their K/V are written
+ * at P..P+Pn-1 of every layer.  Keys 0..P-1 are read as they are, although a
+ * recompute would change them from the first layer's output on (every
+ * prefix position also attends to the new block); layer-0 keys are the same
+ * either way.  The cost is a forward over Pn rows instead of P + Pn.
+ *   ids [b][Pn] int32 token ids (no embedding rows).
+ * Needs P >= 0, Pn >= 1, P + Pn <= min(cap, max_pos); kv and ws as for
+ * dard_prefill with the same b and cap (ws sized by dard_workspace_bytes). */
+dard_status dard_prefill_extend(const dard_dims* dims, const void* packed, void* kv, int cap,
+                                int P, int b, int Pn, const int32_t* ids, void* ws, size_t ws_bytes,
+                                void* stream);
+
 /* ------------------------------------------------------------ a1-a8: one step
  * One DARD step (one loop iteration of Algorithm 1) for b sequences whose
  * current block has B positions after a prefix of P cached keys:

@@ -854,6 +854,21 @@ dard_status dard_prefill_suffix(const dard_dims* d, const void* packed, void* kv
     return run_layers(f, Pc, Ps, 0, 3, nullptr, nullptr, 0, 0, Ps);
 }
 
+dard_status dard_prefill_extend(const dard_dims* d, const void* packed, void* kv, int cap, int P, int b, int Pn,
+                                const int32_t* ids, void* ws, size_t ws_bytes, void* stream) {
+    Fwd f;
+    int rc = fwd_setup(f, d, packed, kv, cap, b, 1, ws, ws_bytes, stream);
+    if (rc) return rc;
+    if (!ids) return fail(DARD_ERR_ARG, "NULL ids");
+    if (P < 0 || Pn < 1 || P + Pn > cap || P + Pn > d->max_pos)
+        return fail(DARD_ERR_SHAPE, "need P >= 0, Pn >= 1, P + Pn <= min(cap, max_pos)");
+    const void* gain0 = d->n_layers > 0 ? f.layer(0, f.L.attn_norm) : f.pk + f.L.final_norm;
+    HIPOK(launch_embed_norm(d->dtype, ids, nullptr, f.pk + f.L.embed, gain0, b * Pn, d->d_model, d->vocab, d->norm_eps,
+                            0, 0, (float*)(f.ws + f.W.h), f.ws + f.W.xn, frag_rows(d->dtype, b * Pn), f.s));
+    // the new rows at positions P.., keys 0..P+Pn-1 of the sequence's own cache
+    return run_layers(f, Pn, P, 0, 3, nullptr, nullptr, 0, 0, 0);
+}
+
 dard_status dard_step_shared(const dard_dims* d, const void* packed, void* kv, int cap, const void* kv_shared,
                              int cap_shared, int Ps, int P, const dard_params* params, int b, int B,
                              const int32_t* tok_in, const uint8_t* state_in, const float* conf_in, int32_t* tok_out,

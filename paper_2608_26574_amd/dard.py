@@ -33,7 +33,7 @@ EXPORTS = [
     "dard_last_error", "dard_version", "dard_check_states", "dard_build_state_mask", "dard_attention_workspace_bytes",
     "dard_masked_attention", "dard_confidence_workspace_bytes", "dard_confidence", "dard_confidence_noalloc",
     "dard_commit_remask", "dard_packed_weight_bytes", "dard_pack_weights", "dard_kv_bytes",
-    "dard_workspace_bytes", "dard_prefill", "dard_step", "dard_step_full", "dard_prefill_suffix",
+    "dard_workspace_bytes", "dard_prefill", "dard_prefill_extend", "dard_step", "dard_step_full", "dard_prefill_suffix",
     "dard_step_shared", "dard_pack_matrix", "dard_linear", "dard_gemm_plan",
     "dard_trace_enable",
     "dard_trace_read", "dard_trace_reset", "dard_trace_sample",
@@ -96,6 +96,7 @@ def lib():
             "dard_step_full": (i32, [vp, vp, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                      vp]),
             "dard_prefill_suffix": (i32, [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp, sz, vp]),
+            "dard_prefill_extend": (i32, [vp, vp, vp, i32, i32, i32, i32, vp, vp, sz, vp]),
             "dard_step_shared": (i32, [vp, vp, vp, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
                                        vp, vp, sz, vp]),
             "dard_pack_matrix": (i32, [i32, vp, i32, i32, vp, vp]),
@@ -326,6 +327,13 @@ class Engine:
                                ctypes.byref(params), b, B, _p(tok_in), _p(state_in), _p(conf_in), _p(tok_out),
                                _p(state_out), _p(conf_out), _p(block_done), _ref(dbg), _p(self.ws),
                                self.ws.numel(), _stream(stream)))
+
+    def dard_prefill_extend(self, P, ids, stream=None):
+        """Extend-only refresh: positions P..P+Pn-1 of each sequence (ids
+        [b][Pn]) see the cached keys 0..P-1 and each other."""
+        b, Pn = ids.shape
+        _check(lib().dard_prefill_extend(ctypes.byref(self.cdims), _p(self.packed), _p(self.kv), self.cap, P, b, Pn,
+                                         _p(ids), _p(self.ws), self.ws.numel(), _stream(stream)))
 
     def dard_prefill_suffix(self, shared, Ps, ids, stream=None):
         """Positions Ps.. of each sequence after the prompt cached in `shared`
