@@ -223,3 +223,49 @@ def test_decoding_loop_shared_prompt():
     print(f"shared-prompt loop: steps per block {steps}, excluded positions {excluded}", flush=True)
     assert excluded <= 2, excluded
     assert sum(s < 2 * B for s in steps) >= 1, steps   # at least one block finishes
+
+
+def test_decoding_loop_extend_only_refresh():
+    """The loop with the extend-only refresh at block boundaries: the prompt
+    is prefilled once, and each finished block is appended to the cache with
+    dard_prefill_extend (its rows see the cached keys and each other) instead
+    of re-encoding the whole prefix."""
+    dims, lm_scale, seed = synth.TINY, 40.0, 31
+    b, B, P0, nblocks = 2, 16, 24, 3
+    flags = O.F_PROGRESS
+    announce("decoding loop, extend-only refresh")
+    w = sharpen(synth.make_weights(dims, seed=seed), lm_scale)
+    eng = dard.Engine(dims, {k: v.cuda() for k, v in w.items()}, b, B, P0 + nblocks * B + 2 * B)
+    ow = synth.OracleWeights(dims, w)
+    dd = dims.as_dict()
+    prm = P(dims.mask_id, flags)
+    prompt = synth.prompt_ids(b, P0, dims.vocab, seed=seed + 1)
+    eng.dard_prefill(dev(prompt))
+    cache = O.prefill(ow, dd, prompt)
+    Pk, steps, excluded = P0, [], 0
+    for k in range(nblocks):
+        tok = np.full((b, B), dims.mask_id, dtype=np.int32)
+        state = np.zeros((b, B), dtype=np.uint8)
+        conf = np.zeros((b, B), dtype=np.float32)
+        n = 0
+        while True:
+            out, dbg = step_buffers(b, B, dims.vocab)
+            eng.dard_step(Pk, cparams(dard, prm), dev(tok), dev(state), dev(conf), out["tok_out"],
+                          out["state_out"], out["conf_out"], out["block_done"], debug=dbg)
+            got = collect(out, dbg)
+            ref = O.dard_step(ow, dd, cache, tok, state, conf, prm)
+            assert logit_err(got, ref, state, prm) < 1e-4 * lm_scale, (k, n)
+            _, excl, _ = check_decisions(tok, state, got, ref, prm, f"extend loop block {k} step {n}")
+            excluded += excl
+            n += 1
+            tok, state, conf = got["tok_out"], got["state_out"], got["conf_out"]
+            if np.all(got["block_done"] == 1) or n >= 2 * B:
+                break
+        steps.append(n)
+        # append the block to the cache
+        eng.dard_prefill_extend(Pk, dev(tok))
+        cache = O.prefill_extend(ow, dd, cache, tok)
+        Pk += B
+    print(f"extend-only loop: steps per block {steps}, excluded positions {excluded}", flush=True)
+    assert excluded <= 2, excluded
+    assert sum(s < 2 * B for s in steps) >= 1, steps
