@@ -86,8 +86,10 @@ typedef int dard_status;
  *                 confidences eventually pass tau_u): if no position of an
  *                 unfinished block entered U in this step, the most confident
  *                 position that is not U after the transitions (ties: lowest
- *                 position) becomes U with its prediction, so a block of B
- *                 positions finishes within B steps.
+ *                 position) becomes U with its prediction, so every step
+ *                 of an unfinished block commits at least one position (U
+ *                 positions are re-verified and may fall back, so a
+ *                 decoding loop still bounds its steps per block).
  * Variants of the design-choice analysis (Sec. 5.1, mask-design and
  * logit-mixing ablations); at most one of the four ordering flags is allowed:
  *   C_BIDIR       a candidate's queries see every candidate in x (no order;
