@@ -10,7 +10,9 @@ token states drawn at candidate fraction 0.25, thresholds (0.4, 0.9).
 A step is one dard_step call: the augmented-block forward through all 32
 layers, the LM head, both confidence passes and both decision phases.  The
 timed region runs K steps with inputs resident in HBM, cycling the prefix
-length over the 8 blocks of the generation.  Prints one JSON line.
+length over the 8 blocks of the generation, after one second of untimed
+steps that brings the GPU to its steady step time (the first pass from the
+start of sustained load is reported beside it).  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -40,6 +42,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=24)
     ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--burn-in", type=float, default=1.0,
+                    help="seconds of untimed steps before the warm-up steps (the first 0.5 s of sustained load "
+                         "runs about 3%% slower; the first window of steps is reported as cold_ms_per_step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the 7B GQA and multimodal full-step lines")
     ap.add_argument("--layers", type=int, default=32, help=argparse.SUPPRESS)
@@ -103,6 +108,27 @@ def main():
         tok, state, conf = inputs[t]
         eng.dard_step(Ps[t], params, tok, state, conf, t_out, s_out, c_out, done)
 
+    # ---- burn-in: from the start of sustained load the GPU takes about half a
+    # second to reach its steady step time (4.26 ms per step during the first
+    # 0.5 s, 4.14 ms after; idle gaps of up to 3 s do not undo it), so untimed
+    # steps run for --burn-in seconds before the warm-up steps.  The first pass
+    # over the K steps is timed on its own and reported as the cold-start figure.
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for t in range(args.warmup, total):
+        step(t)
+    ev1.record()
+    torch.cuda.synchronize()
+    cold_ms = ev0.elapsed_time(ev1) / args.steps
+    tb = time.perf_counter()
+    n_burn = 0
+    while time.perf_counter() - tb < args.burn_in:
+        for t in range(args.warmup, total):
+            step(t)
+        torch.cuda.synchronize()
+        n_burn += args.steps
+    log(f"[bench] cold start: {cold_ms:.3f} ms/step; burn-in of {n_burn} steps")
+
     for t in range(args.warmup):
         step(t)
     torch.cuda.synchronize()
@@ -114,7 +140,6 @@ def main():
     dard.dard_trace_reset()
     dard.dard_trace_sample(TRACE_PERIOD)
     dard.dard_trace_enable(1 << dard.K_GEMM_GU)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record()
     tw = time.perf_counter()
@@ -256,6 +281,9 @@ def main():
     out = {
         "metric": METRIC, "value": round(1e3 / ms_per_step, 2), "unit": "steps/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "cold_ms_per_step": round(cold_ms, 4),
+        "burn_in": f"{n_burn} untimed steps ({args.burn_in:g} s) before the warm-up; cold_ms_per_step is the "
+                   f"first pass over the same {args.steps} steps from the start of sustained load",
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: seeded random-init weights N(0, 0.02), uniform prompt ids, drawn token states",
         "config": {"workload": f"llada8b-like full DARD step: {dims.n_layers} layers, d 4096, 32x128 MHA, FFN 12288, "
