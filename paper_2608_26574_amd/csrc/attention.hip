@@ -25,9 +25,13 @@
 // built once per step) widened to 2B bits: x^j where the bit is set, s^j
 // where it is clear; so one aligned 64-bit word per block tile says which
 // keys a row sees, and full prefix tiles need no test at all.
-// The softmax runs in the log2 domain with a running maximum that may lag the
-// true one by up to kSlack (probabilities <= 2^kSlack), so the accumulators
-// are rescaled only when some row's maximum grows by more than that.
+// The softmax runs in the log2 domain against a running maximum that may lag
+// the true one: a tile's probabilities are taken against the running maximum
+// as it stands, and only when a lane's sum of them exceeds kBig = 2^32 (always
+// on a row's first visible tile, where the running maximum is still the
+// floor) is the tile's maximum taken, the accumulators rescaled and the
+// probabilities recomputed.  bf16 probabilities and fp32 sums have the range
+// for values up to 2^32, and a tile needs no maximum reduction otherwise.
 // Long key ranges may also be split across workgroups (fp32 partials of
 // (o, m, l), merged in split order by a small combine kernel).
 //
@@ -45,7 +49,7 @@ constexpr int kKeys = 64;      // keys per tile
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinLog2 = -1e30f;   // running-max floor (log2 units): exp2 of anything below it is 0
-constexpr float kSlack = 8.f;        // a row's running max may trail its true max by this (log2 units)
+constexpr float kBig = 4294967296.f; // 2^32: a lane's probability sum over a tile that moves the running max
 
 // LDS of one group of TPG threads: three K stages [64 keys][DH] and two V^T
 // stages [DH][64 keys], unpadded and XOR-swizzled in 16-byte chunks, or, at
@@ -418,22 +422,11 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
                 for (int v = 0; v < 16; ++v)
                     if (!((ww >> (32 * kb + 16 * (v >> 3) + (v & 7))) & 1ull)) sc[kb][v] = -INFINITY;
         }
-        // online softmax in the log2 domain
-        float mt = sc[0][0];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb][v]);
-        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-        const float m_new = fmaxf(m_run, mt * sl2);     // sl2 > 0: the max commutes with the scale
-        if (__ballot(m_new > m_run + kSlack)) {        // some row's max outgrew the slack
-            // arguments are <= 0: the hardware exp2 (v_exp_f32) needs no range handling
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-#pragma unroll
-            for (int d = 0; d < DH / 32; ++d) o[d] *= alpha;
-            l_run *= alpha;
-            m_run = m_new;
-        }
+        // online softmax in the log2 domain, against the running maximum as
+        // it stands; a tile with a row whose probabilities grow large (sum over
+        // the lane's keys above kBig, also the first visible tile, where the
+        // running maximum is still the floor) is recomputed after moving the
+        // running maximum to the tile's maximum
         float psum = 0.f;
         bf16x8 pb[2][2];
 #pragma unroll
@@ -444,6 +437,29 @@ void attn_mfma_kernel(AttnArgs a, int rowtiles, int tps) {
                 psum += p;
                 pb[kb][v >> 3][v & 7] = (__bf16)p;
             }
+        if (__ballot(psum > kBig)) {
+            float mt = sc[0][0];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb][v]);
+            mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+            const float m_new = fmaxf(m_run, mt * sl2);     // sl2 > 0: the max commutes with the scale
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+            for (int d = 0; d < DH / 32; ++d) o[d] *= alpha;
+            l_run *= alpha;
+            m_run = m_new;
+            psum = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb][v], sl2, -m_run));
+                    psum += p;
+                    pb[kb][v >> 3][v & 7] = (__bf16)p;
+                }
+        }
         l_run += psum;
         // O^T += V^T * P^T: step st = 2kb + hh covers keys 16st + [0, 16); the
         // lane's 8 probabilities are keys 16st + 8eta + [0, 8), V^T chunk 2st + eta
