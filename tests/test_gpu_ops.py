@@ -138,6 +138,51 @@ def test_attention_dream_gqa_shape(P):
 
 
 @pytest.mark.parametrize("case", [
+    # batch-1 shape (key splits and their merge): scores grow tile by tile
+    dict(b=1, B=32, P=736, Hq=4, Hkv=4, profile=(0.05, 1.0, 3.0, 6.0, 10.0)),
+    # 7B GQA shape (two key groups merged in the workgroup): large scores first, then small
+    dict(b=2, B=64, P=1024, Hq=14, Hkv=2, profile=(10.0, 0.2, 6.0, 0.05)),
+    # block keys far above the prefix
+    dict(b=2, B=32, P=200, Hq=4, Hkv=2, profile=(0.1, 0.1, 0.1, 0.1, 12.0)),
+])
+def test_attention_score_jumps(case):
+    """Keys scaled tile by tile, so that a row's scores rise above its running
+    maximum by 2^5 to 2^60 (log2 units 5 to 60) in later tiles: those within
+    2^32 are taken against the running maximum as it stands, larger ones move
+    it.  The outputs must match the oracle as for ordinary inputs."""
+    announce("attention score jumps", case)
+    b, B, P, Hq, Hkv, dh = case["b"], case["B"], case["P"], case["Hq"], case["Hkv"], 128
+    cap = P + 2 * B + 3
+    q, k, v = synth.qkv(b, 2 * B, Hq, Hkv, dh, cap, seed=17, dtype=torch.bfloat16)
+    prof = case["profile"]
+    tile_scale = torch.tensor([prof[(j // 64) % len(prof)] for j in range(cap)], dtype=torch.float32)
+    k = (k.float() * tile_scale[None, None, :, None]).bfloat16()
+    _, state, conf = synth.workload_block(b, B, 0.3, 100, seed=18)
+    out = torch.empty_like(q).cuda()
+    scale = 1.0 / math.sqrt(dh)
+    ws = torch.empty(max(dard.dard_attention_workspace_bytes(1, b, B, Hq, dh, P), 1), dtype=torch.uint8, device="cuda")
+    dard.dard_masked_attention(q.cuda(), k.cuda(), v.transpose(-1, -2).contiguous().cuda(), P, dev(state), dev(conf),
+                               scale, 0, out, ws)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy()
+    assert np.isfinite(got).all()
+    worst, span = 0.0, 0.0
+    for s in range(b):
+        qn, kn, vn = q[s].double().numpy(), k[s].double().numpy(), v[s].double().numpy()
+        vis = O.visible_keys(state[s], conf[s], P, 0)
+        ref = O.masked_attention(qn, kn[:, :P + 2 * B].transpose(1, 0, 2), vn[:, :P + 2 * B].transpose(1, 0, 2),
+                                 vis, scale, Hkv)
+        worst = max(worst, float(np.max(np.abs(got[s] - ref))))
+        # spread of the rows' scores in log2 units (how far above a first tile's maximum they rise)
+        kk = kn[np.arange(Hq) // (Hq // Hkv), :P + 2 * B]
+        sc = np.einsum("rhd,hkd->rhk", qn, kk) * scale / math.log(2)
+        span = max(span, float(np.max(sc.max(axis=2) - sc[..., :64].max(axis=2))))
+    print(f"score jumps: max |GPU - oracle| {worst:.3e}, scores rise up to {span:.1f} log2 units past the first tile", flush=True)
+    assert span > 32.0, span
+    assert worst < 2e-2, worst
+
+
+@pytest.mark.parametrize("case", [
     dict(b=1, B=1, P=0, Hq=2, Hkv=2, dh=128),       # smallest block, no prefix
     dict(b=2, B=5, P=70, Hq=4, Hkv=2, dh=128),      # ragged block, ragged prefix, GQA
     dict(b=1, B=64, P=1024, Hq=7, Hkv=1, dh=128),   # two row tiles, 7:1 GQA
