@@ -27,11 +27,11 @@
 // keys a row sees, and full prefix tiles need no test at all.
 // The softmax runs in the log2 domain against a running maximum that may lag
 // the true one: a tile's probabilities are taken against the running maximum
-// as it stands, and only when a lane's sum of them exceeds kBig = 2^32 (always
+// as it stands, and only when a lane's sum of them exceeds kBig = 256 (always
 // on a row's first visible tile, where the running maximum is still the
-// floor) is the tile's maximum taken, the accumulators rescaled and the
-// probabilities recomputed.  bf16 probabilities and fp32 sums have the range
-// for values up to 2^32, and a tile needs no maximum reduction otherwise.
+// floor; and whenever a score exceeds the running maximum by more than 8) is
+// the tile's maximum taken, the accumulators rescaled and the probabilities
+// recomputed.  A tile needs no maximum reduction otherwise.
 // Long key ranges may also be split across workgroups (fp32 partials of
 // (o, m, l), merged in split order by a small combine kernel).
 //
@@ -49,7 +49,7 @@ constexpr int kKeys = 64;      // keys per tile
 constexpr int kMaxSplit = 16;  // key splits across workgroups
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinLog2 = -1e30f;   // running-max floor (log2 units): exp2 of anything below it is 0
-constexpr float kBig = 4294967296.f; // 2^32: a lane's probability sum over a tile that moves the running max
+constexpr float kBig = 256.f;        // a lane's probability sum over a tile that moves the running max
 
 // LDS of one group of TPG threads: three K stages [64 keys][DH] and two V^T
 // stages [DH][64 keys], unpadded and XOR-swizzled in 16-byte chunks, or, at
