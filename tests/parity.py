@@ -135,6 +135,41 @@ class Floor:
         return worst, worst_rms
 
 
+def e4m3_decode(codes):
+    """Values of OCP FP8 E4M3 codes (a uint8 tensor or array), from the
+    oracle's table of the format's magnitudes."""
+    c = (codes.cpu().numpy() if hasattr(codes, "cpu") else np.asarray(codes)).astype(np.int64)
+    mag = O.E4M3_VALUES[np.minimum(c & 0x7F, 126)]
+    return np.where(c & 0x80, -mag, mag)
+
+
+def e4m3_steps(a, b):
+    """Distance in code steps between two arrays of E4M3 values (signed code
+    ordinals)."""
+    def ordinal(v):
+        m = np.searchsorted(O.E4M3_VALUES, np.abs(v))
+        return np.where(v < 0, -m, m)
+    return np.abs(ordinal(a) - ordinal(b))
+
+
+def check_fp8_cache_layers(pairs, label):
+    """Per layer (GPU values, oracle values) of K or V held as E4M3: in the
+    first layer, whose inputs agree with the oracle's up to fp32 rounding
+    order, nearly every code is equal and none more than one step away;
+    deeper layers inherit the first layer's flipped roundings (each a whole
+    code step) through attention, so there the bound only rules out gross
+    errors (a layer offset, a scale or a sign change 98 % of the codes or
+    more)."""
+    for layer, j, g, r in pairs:
+        dg = e4m3_steps(g, r)
+        print(f"{label} fp8 cache layer {layer} {'KV'[j]}: codes differing {np.mean(dg > 0):.4f}, "
+              f"by more than one step {np.mean(dg > 1):.4f}", file=sys.stderr, flush=True)
+        if layer == 0:
+            assert np.mean(dg == 0) > 0.97 and dg.max() <= 1, (label, layer, j, np.mean(dg == 0), dg.max())
+        else:
+            assert np.mean(dg > 0) < 0.35 and np.mean(dg > 1) < 0.08, (label, layer, j)
+
+
 def hidden_mix(params):
     return bool(params.get("flags", 0) & O.F_HIDDEN_MIX)
 

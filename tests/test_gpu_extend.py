@@ -9,8 +9,8 @@ import torch
 
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
-from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, Floor, logit_err, sharpen, step_buffers)
+from parity import (P, announce, check_bf16_logits, check_decisions, check_fp8_cache_layers, check_workload_decisions,
+                    collect, cparams, dev, e4m3_decode, Floor, logit_err, sharpen, step_buffers)
 from test_gpu_step import unpermute_k
 
 pytestmark = pytest.mark.gpu
@@ -34,31 +34,13 @@ def extend_case(dims, b, P0, blocks, B, seed, lm_scale, frac=None):
         P_ += n
     # the extended cache, every layer
     if dims.kv_dtype == "fp8":
-        # E4M3 codes, compared in code steps (signed code ordinals): in the
-        # first layer, whose inputs agree with the oracle's up to fp32 rounding
-        # order, nearly every code is equal and none more than one step away;
-        # deeper layers inherit flipped roundings through attention
         kc, vc = eng.kv_view(torch.uint8)
-
-        def decode(c):
-            c = c.cpu().numpy().astype(np.int64)
-            mag = O.E4M3_VALUES[np.minimum(c & 0x7F, 126)]
-            return np.where(c & 0x80, -mag, mag)
-
-        def ordinal(v):
-            m = np.searchsorted(O.E4M3_VALUES, np.abs(v))
-            return np.where(v < 0, -m, m)
+        pairs = []
         for layer in range(dims.n_layers):
-            k_gpu = unpermute_k(decode(kc[layer, :, :, :P_]), dims.head_dim).transpose(0, 2, 1, 3)
-            v_gpu = decode(vc[layer, :, :, :P_]).transpose(0, 2, 1, 3)
-            for j, g in enumerate((k_gpu, v_gpu)):
-                dg = np.abs(ordinal(g) - ordinal(cache[layer][j]))
-                print(f"extended fp8 cache layer {layer} {'KV'[j]}: codes differing {np.mean(dg > 0):.4f}, "
-                      f"by more than one step {np.mean(dg > 1):.4f}", flush=True)
-                if layer == 0:
-                    assert np.mean(dg == 0) > 0.97 and dg.max() <= 1, (layer, j)
-                else:
-                    assert np.mean(dg > 0) < 0.35 and np.mean(dg > 1) < 0.08, (layer, j)
+            k_gpu = unpermute_k(e4m3_decode(kc[layer, :, :, :P_]), dims.head_dim).transpose(0, 2, 1, 3)
+            v_gpu = e4m3_decode(vc[layer, :, :, :P_]).transpose(0, 2, 1, 3)
+            pairs += [(layer, 0, k_gpu, cache[layer][0]), (layer, 1, v_gpu, cache[layer][1])]
+        check_fp8_cache_layers(pairs, "extended")
     else:
         tol = 1e-4 if dims.dtype == "f32" else 8e-2
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16

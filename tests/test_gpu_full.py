@@ -77,6 +77,18 @@ def test_small_full_step_bf16(case):
     assert excl <= state.size // 4
 
 
+def test_small_full_step_bf16_fp8_kv():
+    """The full-sequence step with the KV cache in OCP FP8 E4M3: every row's K
+    and V are rounded to E4M3 where they are written and read back as codes."""
+    dims = synth.with_fp8_kv(synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16"))
+    announce("small bf16 full step, fp8 kv")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = full_case(dims, 2, 40, 96, 32, 1, prm, seed=6, lm_scale=8.0)
+    check_bf16_logits(got, ref, "full step, fp8 kv", scale=8.0)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step, fp8 kv")
+    assert excl <= state.size // 4
+
+
 def test_block128_full_step_fp32():
     """Block 128 (the paper's default block length) as the first of two
     generation blocks after a 64-token prompt; fp32, so that the decision

@@ -9,8 +9,8 @@ import torch
 from oracle import dard_oracle as O
 from paper_2608_26574_amd import dard, synth
 
-from parity import (P, announce, check_bf16_logits, check_decisions, check_workload_decisions, collect, cparams,
-                    dev, Floor, logit_err, sharpen, step_buffers)
+from parity import (P, announce, check_bf16_logits, check_decisions, check_fp8_cache_layers, check_workload_decisions,
+                    collect, cparams, dev, e4m3_decode, Floor, logit_err, sharpen, step_buffers)
 
 pytestmark = pytest.mark.gpu
 
@@ -57,7 +57,11 @@ def shared_case(dims, b, Ps, Pc, B, params, seed=1, lm_scale=None, frac=None, wd
     ref["floor"] = Floor(perturbed, ref["logits"])
     # the suffix keys written by dard_prefill_suffix (V of every layer; K is stored with
     # each head's rotary pairs interleaved)
-    if Pc:
+    if Pc and dims.kv_dtype == "fp8":
+        _, vc = eng.kv_view(torch.uint8)
+        check_fp8_cache_layers([(layer, 1, e4m3_decode(vc[layer, :, :, Ps:Ps + Pc]).transpose(0, 2, 1, 3),
+                                 suffix[layer][1]) for layer in range(dims.n_layers)], "suffix")
+    elif Pc:
         kvd = torch.float32 if dims.dtype == "f32" else torch.bfloat16
         _, vc = eng.kv_view(kvd)
         vc = vc.float().cpu().numpy()
@@ -89,6 +93,18 @@ def test_small_shared_step_bf16_gqa():
     err = logit_err(got, ref, state, prm)
     assert err < 2e-2 * 8, err
     eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small shared step")
+    assert excl <= state.size // 4
+
+
+def test_small_shared_step_bf16_gqa_fp8_kv():
+    """The shared prompt cache, the sequences' suffixes and the step with the
+    KV caches in OCP FP8 E4M3."""
+    dims = synth.with_fp8_kv(synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16"))
+    announce("small bf16 shared step, fp8 kv")
+    prm = P(dims.mask_id)
+    tok, state, conf, got, ref = shared_case(dims, 4, 128, 64, 32, prm, seed=7, lm_scale=8.0)
+    check_bf16_logits(got, ref, "small shared step, fp8 kv", scale=8.0)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small shared step, fp8 kv")
     assert excl <= state.size // 4
 
 
