@@ -89,6 +89,19 @@ def test_small_full_step_bf16_fp8_kv():
     assert excl <= state.size // 4
 
 
+def test_small_full_step_bf16_hidden_mix():
+    """The full-sequence step with DARD_F_HIDDEN_MIX (Eq. 7 on the final hidden
+    rows, two LM-head passes) against the oracle's logit mixing."""
+    dims = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16")
+    announce("small bf16 full step, hidden mix")
+    prm = P(dims.mask_id, O.F_HIDDEN_MIX)
+    tok, state, conf, got, ref = full_case(dims, 2, 40, 96, 32, 1, prm, seed=8, lm_scale=8.0)
+    check_bf16_logits(got, ref, "full step, hidden mix", scale=8.0)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "full step, hidden mix")
+    assert excl <= state.size // 4
+    assert np.all(np.isnan(got["logits"][:, :32]))   # the x rows never ran through the head
+
+
 def test_block128_full_step_fp32():
     """Block 128 (the paper's default block length) as the first of two
     generation blocks after a 64-token prompt; fp32, so that the decision

@@ -108,6 +108,19 @@ def test_small_shared_step_bf16_gqa_fp8_kv():
     assert excl <= state.size // 4
 
 
+def test_small_shared_step_bf16_hidden_mix():
+    """The shared-prompt step with DARD_F_HIDDEN_MIX against the oracle's
+    logit mixing."""
+    dims = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16")
+    announce("small bf16 shared step, hidden mix")
+    prm = P(dims.mask_id, O.F_HIDDEN_MIX)
+    tok, state, conf, got, ref = shared_case(dims, 3, 64, 32, 32, prm, seed=9, lm_scale=8.0)
+    check_bf16_logits(got, ref, "small shared step, hidden mix", scale=8.0)
+    eps, excl, _ = check_decisions(tok, state, got, ref, prm, "small shared step, hidden mix")
+    assert excl <= state.size // 4
+    assert np.all(np.isnan(got["logits"][:, :32]))
+
+
 def test_multimodal_shared_prompt_two_layers():
     """8B shape, two layers: one 576-embedding image + 256-id prompt shared by
     a batch of 4, one committed block of 32 per sequence, block 32, candidate
