@@ -114,3 +114,69 @@ def test_steps_on_two_streams():
         for r in range(4):
             for got, want in zip(together[k][r], alone[k]):
                 assert torch.equal(got, want), (k, r)
+
+
+@pytest.mark.parametrize("mode", ["full", "shared"])
+def test_full_and_shared_steps_graph_replay(mode):
+    """dard_step_full and dard_step_shared captured in a HIP graph and
+    replayed on alternating inputs, every replay equal to the eager step."""
+    dims = synth.Dims(2, 512, 4, 2, 128, 1024, 2048, 1024, "bf16")
+    b, B = 2, 32
+    announce("graph replay", mode)
+    w = sharpen(synth.make_weights(dims, seed=71, device="cuda"), 8.0)
+    params = cparams(dard, P(dims.mask_id))
+    if mode == "full":
+        prompt, gen = 40, 96
+        N, blk = prompt + gen, prompt + B
+        eng = dard.Engine(dims, w, b, B, N + B)
+        inputs = []
+        for k in range(2):
+            tok, state, conf = synth.workload_block(b, B, 0.3, dims.vocab, seed=74 + k)
+            seq = synth.prompt_ids(b, N, dims.vocab, seed=72 + k)
+            seq[:, blk:blk + B] = tok
+            seq[:, blk + B:] = dims.mask_id
+            inputs.append((dev(seq), dev(state), dev(conf)))
+
+        def step(inp, o):
+            eng.dard_step_full(blk, params, inp[0], inp[1], inp[2], *o)
+    else:
+        Ps, Pc = 64, 32
+        sh = dard.Engine(dims, w, 1, B, Ps)
+        eng = dard.Engine(dims, None, b, B, Ps + Pc + 2 * B, packed=sh.packed)
+        sh.dard_prefill(dev(synth.prompt_ids(1, Ps, dims.vocab, seed=76)))
+        eng.dard_prefill_suffix(sh, Ps, dev(synth.prompt_ids(b, Pc, dims.vocab, seed=77)))
+        inputs = [tuple(dev(a) for a in synth.workload_block(b, B, 0.3, dims.vocab, seed=78 + k)) for k in range(2)]
+
+        def step(inp, o):
+            eng.dard_step_shared(sh, Ps, Ps + Pc, params, *inp, *o)
+    del w
+
+    def outputs():
+        return (torch.zeros(b, B, dtype=torch.int32, device="cuda"), torch.zeros(b, B, dtype=torch.uint8, device="cuda"),
+                torch.zeros(b, B, device="cuda"), torch.zeros(b, dtype=torch.int32, device="cuda"))
+
+    ref = []
+    for inp in inputs:
+        o = outputs()
+        step(inp, o)
+        ref.append(o)
+    torch.cuda.synchronize()
+    assert not all(torch.equal(x, y) for x, y in zip(ref[0][:3], ref[1][:3]))
+    s_in = tuple(t.clone() for t in inputs[0])
+    s_out = outputs()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(s_in, s_out)
+    torch.cuda.synchronize()
+    for r, k in enumerate((1, 0, 1)):
+        for t in s_out:
+            t.zero_()
+        for dst, src in zip(s_in, inputs[k]):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want, what in zip(s_out, ref[k], ("tok_out", "state_out", "conf_out", "block_done")):
+            assert torch.equal(got, want), (mode, r, k, what)
+    print(f"graph replay {mode}: 3 replays equal the eager steps", flush=True)
