@@ -165,3 +165,43 @@ def test_state_check_validation():
     assert L.dard_commit_remask(1, ctypes.byref(p), 1, 4, fake, fake, None, fake, fake, fake, None, None,
                                 None, fake, fake, fake, None, None) == -1
     assert b"block_done" in L.dard_last_error()
+
+
+def test_model_call_validation():
+    """Host-side argument checks of the whole-model calls (nothing enqueued):
+    the prefix refreshes and the three steps."""
+    L = dard.lib()
+    fake = ctypes.c_void_p(0x1000)
+    d = dard.make_dims(synth.Dims(2, 256, 4, 2, 64, 512, 2048, 256, "bf16"))
+    b, B, cap = 2, 16, 128
+    ws = L.dard_workspace_bytes(ctypes.byref(d), b, B, cap)
+    assert ws > 0
+    dp = ctypes.byref(d)
+    # extend-only refresh: NULL ids, Pn < 1, P + Pn past cap or max_pos, P < 0, workspace too small
+    assert L.dard_prefill_extend(dp, fake, fake, cap, 10, b, 8, None, fake, ws, None) == -1
+    assert L.dard_prefill_extend(dp, fake, fake, cap, 10, b, 0, fake, fake, ws, None) == -2
+    assert L.dard_prefill_extend(dp, fake, fake, cap, 120, b, 9, fake, fake, ws, None) == -2
+    assert L.dard_prefill_extend(dp, fake, fake, cap, -1, b, 8, fake, fake, ws, None) == -2
+    assert L.dard_prefill_extend(dp, fake, fake, cap, 10, b, 8, fake, fake, 16, None) == -5
+    # prefill: P outside [1, min(cap, max_pos)]
+    assert L.dard_prefill(dp, fake, fake, cap, b, 0, fake, None, fake, ws, None) == -2
+    assert L.dard_prefill(dp, fake, fake, cap, b, cap + 1, fake, None, fake, ws, None) == -2
+    p = _params(mask_id=2047)
+    pp = ctypes.byref(p)
+    # step: P + 2B past cap; NULL outputs
+    assert L.dard_step(dp, fake, fake, cap, cap - 2 * B + 1, pp, b, B, fake, fake, fake, fake, fake, fake, fake,
+                       None, fake, ws, None) == -2
+    assert L.dard_step(dp, fake, fake, cap, 8, pp, b, B, fake, fake, fake, None, fake, fake, fake,
+                       None, fake, ws, None) == -1
+    # full-sequence step: the block must lie inside the sequence, N + B <= cap
+    assert L.dard_step_full(dp, fake, fake, cap, 64, 60, pp, b, B, fake, fake, fake, fake, fake, fake, fake,
+                            None, fake, ws, None) == -2
+    assert L.dard_step_full(dp, fake, fake, cap, cap - B + 1, 0, pp, b, B, fake, fake, fake, fake, fake, fake, fake,
+                            None, fake, ws, None) == -2
+    # shared-prompt step: the shared prompt is whole 64-key tiles and no longer than P
+    assert L.dard_step_shared(dp, fake, fake, cap, fake, 128, 60, 64, pp, b, B, fake, fake, fake, fake, fake, fake,
+                              fake, None, fake, ws, None) == -2
+    assert L.dard_step_shared(dp, fake, fake, cap, fake, 128, 128, 64, pp, b, B, fake, fake, fake, fake, fake, fake,
+                              fake, None, fake, ws, None) == -2
+    assert L.dard_step_shared(dp, fake, fake, cap, None, 128, 64, 64, pp, b, B, fake, fake, fake, fake, fake, fake,
+                              fake, None, fake, ws, None) == -1
