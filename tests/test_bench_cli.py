@@ -19,5 +19,5 @@ def test_bench_help_names_the_profile_modes():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"], capture_output=True, text=True,
                        timeout=120)
     assert r.returncode == 0
-    for flag in ("--gpus", "--steps", "--warmup", "--profile"):
+    for flag in ("--gpus", "--steps", "--warmup", "--burn-in", "--profile"):
         assert flag in r.stdout
