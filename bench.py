@@ -312,6 +312,19 @@ def main():
         out["configs"] = full_step_configs(eng)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(dims, b, B, prompt, frac)
+    # attention against the bf16 MFMA peak per workload (kernel time): the
+    # headline decode step (64 query rows per MHA head, about 55 flop per K/V
+    # byte: bound by HBM and latency, not by the matrix cores) and the
+    # isolated operations, of which the 7B GQA shape (7 query heads per KV
+    # head, block 64) is the MFMA-bound one
+    by_workload = {"8B step, batch 1 (in the step)": attention["mfma_frac"]}
+    for a in out["ops"]["attention"]:
+        key = f"{a['shape']}, batch {a['batch']}, prefix {a['prefix']}, cand {a.get('cand_frac')}"
+        by_workload[key] = a["mfma_frac"]
+    for name, cfg in out.get("configs", {}).items():
+        if "attention_mfma_frac" in cfg:
+            by_workload[f"{name} (in the step)"] = cfg["attention_mfma_frac"]
+    out["attention_mfma_frac_by_workload"] = by_workload
     print(json.dumps(out), flush=True)
 
 
